@@ -1,0 +1,262 @@
+"""Seeded synthetic Q/K/V shaped like a Llama-3.1-8B attention layer at long context.
+
+The paper measures on real prompts through Llama 3.1-8B-Instruct (Sec. 4.1); those
+weights and datasets are not available, so these generators stand in for the shape of
+that workload: grouped-query attention with 32 query and 8 key/value heads, head dim
+128, rotary position encoding with base 500000, and contexts up to 128K tokens.  The
+structure the sparse patterns exploit (attention sinks, vertical key columns, a local
+band, dispersed evidence spans) is planted explicitly so that each pattern family has
+something to find.
+
+Recipe (all draws from numpy PCG64, ``seed = 1000 * config + layer``):
+
+* base: Q, K, V ~ N(0, 1), float32, one independent stream per head
+  (``[seed, 1, h]`` for query head h, ``[seed, 2, g]`` / ``[seed, 3, g]`` for K / V of
+  key/value head g), so any subset of heads can be regenerated on its own;
+* local bias (before RoPE): a fixed unit vector ``c`` spread evenly over the rotary pairs
+  whose frequency lies in [1e-3, 1e-1] is added as ``sqrt(lam*sqrt(d)) * c`` to every
+  query and key, which after RoPE adds ``lam * mean_f cos(theta_f (i-j))`` to logit i,j;
+* RoPE, rotate-half convention: pair f = dims (f, f + d/2), theta_f = 500000^(-2f/d),
+  position = token index (no long-context frequency rescaling);
+* planted "+k sigma" boosts (after RoPE): direction u (orthonormal set drawn from the
+  structure stream ``[seed, 7]``), ``sqrt(k*sqrt(d)) * u`` added to the chosen keys and
+  to the chosen queries, so the logit rises by k background standard deviations;
+* cast: round-to-nearest-even to bf16 (configs 2-5); config 1 stays float32.
+"""
+from __future__ import annotations
+
+import math
+import os
+from concurrent.futures import ThreadPoolExecutor
+from dataclasses import dataclass, field
+
+import numpy as np
+
+ROPE_BASE = 500000.0
+
+# Five workloads: a single-head fp32 case, then GQA 32/8 d=128 bf16 layers of growing length.
+CONFIGS = {
+    1: dict(n=2048, hq=1, hkv=1, d=64, dtype="f32", layers=1),
+    2: dict(n=8192, hq=32, hkv=8, d=128, dtype="bf16", layers=1),
+    3: dict(n=32768, hq=32, hkv=8, d=128, dtype="bf16", layers=1),
+    4: dict(n=131072, hq=32, hkv=8, d=128, dtype="bf16", layers=1),
+    5: dict(n=131072, hq=32, hkv=8, d=128, dtype="bf16", layers=32),
+}
+
+REGIMES = ("local", "sink", "vertical", "diffuse")
+REGIME_P = (0.35, 0.30, 0.28, 0.07)
+
+
+def bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to bf16 (nearest, ties to even); return the 16-bit patterns."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    u = u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))
+    return (u >> np.uint32(16)).astype(np.uint16)
+
+
+def bits_to_f32(b: np.ndarray) -> np.ndarray:
+    """Widen bf16 bit patterns to float32 (exact)."""
+    return (b.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def bf16_round(x: np.ndarray) -> np.ndarray:
+    """float32 values rounded to the nearest bf16 value, still stored as float32."""
+    return bits_to_f32(bf16_bits(x))
+
+
+@dataclass
+class GroupPlants:
+    """Planted structure of one key/value head group (shared by its query heads)."""
+    regime: str
+    sink_k: float = 0.0          # logit boost of keys [0, sink_n), in background std units
+    sink_n: int = 4
+    vert_k: float = 0.0          # logit boost of the vertical key columns
+    vert_cols: np.ndarray = field(default_factory=lambda: np.zeros(0, np.int64))
+    local_lam: float = 0.0       # peak local-band logit bias
+
+
+@dataclass
+class LayerSpec:
+    cfg: int
+    layer: int
+    seed: int
+    n: int
+    hq: int
+    hkv: int
+    d: int
+    dtype: str
+    groups: list
+    dirs: np.ndarray             # [16, d] orthonormal planted directions
+    span_starts: np.ndarray      # [n_spans] evidence span starts (config 4)
+    span_len: int
+    span_k: float
+    chunk_span: np.ndarray       # [n // 1024] span id each 1024-row query chunk follows, -1 none
+
+    @property
+    def group_size(self) -> int:
+        return self.hq // self.hkv
+
+
+def _plant_amp(k: float, d: int) -> float:
+    return math.sqrt(k * math.sqrt(d))
+
+
+def layer_spec(cfg: int, layer: int = 0, n: int | None = None) -> LayerSpec:
+    """Structure of one layer: everything but the Gaussian background (cheap)."""
+    c = CONFIGS[cfg]
+    n = int(c["n"] if n is None else n)
+    hq, hkv, d = c["hq"], c["hkv"], c["d"]
+    seed = 1000 * cfg + layer
+    rs = np.random.default_rng([seed, 7])
+    g = rs.standard_normal((d, 16))
+    qmat, _ = np.linalg.qr(g)
+    dirs = qmat.T.astype(np.float64)          # rows orthonormal
+    groups = []
+    for _g in range(hkv):
+        if cfg == 5:
+            regime = REGIMES[int(rs.choice(4, p=REGIME_P))]
+        else:
+            regime = "mixed"
+        if regime == "mixed":
+            nv = 16
+            cols = np.sort(rs.choice(np.arange(4, n), size=min(nv, max(n - 4, 0)), replace=False))
+            lam = 0.0 if cfg == 1 else 4.0
+            groups.append(GroupPlants(regime, sink_k=4.0, vert_k=3.0, vert_cols=cols, local_lam=lam))
+        elif regime == "sink":
+            k = math.log(1.65 * n / 4) + 4.0
+            groups.append(GroupPlants(regime, sink_k=k))
+        elif regime == "vertical":
+            nv = 64
+            cols = np.sort(rs.choice(np.arange(4, n), size=min(nv, max(n - 4, 0)), replace=False))
+            k = math.log(1.65 * n / nv) + 4.0
+            groups.append(GroupPlants(regime, vert_k=k, vert_cols=cols))
+        elif regime == "local":
+            groups.append(GroupPlants(regime, local_lam=9.0))
+        else:
+            groups.append(GroupPlants(regime))
+    span_len = 512
+    if cfg == 4:
+        n_spans = 8
+        eighth = n // n_spans
+        starts = np.array([k * eighth + int(rs.integers(0, max(eighth - span_len, 1)))
+                           for k in range(n_spans)], dtype=np.int64)
+        nchunk = (n + 1023) // 1024
+        chunk_span = np.full(nchunk, -1, dtype=np.int64)
+        for ch in range(nchunk):
+            elig = np.nonzero(starts < ch * 1024)[0]
+            if elig.size:
+                chunk_span[ch] = int(elig[int(rs.integers(0, elig.size))])
+    else:
+        starts = np.zeros(0, dtype=np.int64)
+        chunk_span = np.full((n + 1023) // 1024, -1, dtype=np.int64)
+    return LayerSpec(cfg, layer, seed, n, hq, hkv, d, c["dtype"], groups, dirs, starts,
+                     span_len, 3.0, chunk_span)
+
+
+def _rope_tables(n: int, d: int):
+    half = d // 2
+    theta = ROPE_BASE ** (-2.0 * np.arange(half, dtype=np.float64) / d)
+    ang = np.arange(n, dtype=np.float64)[:, None] * theta[None, :]
+    return np.cos(ang).astype(np.float32), np.sin(ang).astype(np.float32), theta
+
+
+def _local_vec(d: int, theta: np.ndarray) -> np.ndarray:
+    half = d // 2
+    band = np.nonzero((theta >= 1e-3) & (theta <= 1e-1))[0]
+    c = np.zeros(d, dtype=np.float64)
+    c[band] = 1.0
+    c[band + half] = 1.0
+    return (c / np.linalg.norm(c)).astype(np.float32)
+
+
+def _rope(x: np.ndarray, cos: np.ndarray, sin: np.ndarray) -> np.ndarray:
+    half = x.shape[1] // 2
+    x1, x2 = x[:, :half], x[:, half:]
+    out = np.empty_like(x)
+    out[:, :half] = x1 * cos - x2 * sin
+    out[:, half:] = x2 * cos + x1 * sin
+    return out
+
+
+def _finish(x: np.ndarray, dtype: str) -> np.ndarray:
+    return bf16_round(x) if dtype == "bf16" else np.ascontiguousarray(x, dtype=np.float32)
+
+
+def _gen_q(spec: LayerSpec, h: int, tabs) -> np.ndarray:
+    cos, sin, theta = tabs
+    n, d = spec.n, spec.d
+    gp = spec.groups[h // spec.group_size]
+    x = np.random.default_rng([spec.seed, 1, h]).standard_normal((n, d), dtype=np.float32)
+    if gp.local_lam > 0:
+        x += _plant_amp(gp.local_lam, d) * _local_vec(d, theta)[None, :]
+    x = _rope(x, cos, sin)
+    if gp.sink_k > 0:
+        x += (_plant_amp(gp.sink_k, d) * spec.dirs[0]).astype(np.float32)[None, :]
+    if gp.vert_k > 0 and gp.vert_cols.size:
+        x += (_plant_amp(gp.vert_k, d) * spec.dirs[1]).astype(np.float32)[None, :]
+    if spec.span_starts.size:
+        amp = _plant_amp(spec.span_k, d)
+        for ch, sid in enumerate(spec.chunk_span):
+            if sid >= 0:
+                x[ch * 1024:(ch + 1) * 1024] += (amp * spec.dirs[2 + sid]).astype(np.float32)
+    return _finish(x, spec.dtype)
+
+
+def _gen_k(spec: LayerSpec, g: int, tabs) -> np.ndarray:
+    cos, sin, theta = tabs
+    n, d = spec.n, spec.d
+    gp = spec.groups[g]
+    x = np.random.default_rng([spec.seed, 2, g]).standard_normal((n, d), dtype=np.float32)
+    if gp.local_lam > 0:
+        x += _plant_amp(gp.local_lam, d) * _local_vec(d, theta)[None, :]
+    x = _rope(x, cos, sin)
+    if gp.sink_k > 0:
+        x[:gp.sink_n] += (_plant_amp(gp.sink_k, d) * spec.dirs[0]).astype(np.float32)
+    if gp.vert_k > 0 and gp.vert_cols.size:
+        x[gp.vert_cols] += (_plant_amp(gp.vert_k, d) * spec.dirs[1]).astype(np.float32)
+    if spec.span_starts.size:
+        amp = _plant_amp(spec.span_k, d)
+        for sid, st in enumerate(spec.span_starts):
+            x[st:st + spec.span_len] += (amp * spec.dirs[2 + sid]).astype(np.float32)
+    return _finish(x, spec.dtype)
+
+
+def _gen_v(spec: LayerSpec, g: int) -> np.ndarray:
+    x = np.random.default_rng([spec.seed, 3, g]).standard_normal((spec.n, spec.d), dtype=np.float32)
+    return _finish(x, spec.dtype)
+
+
+def make_layer(cfg: int, layer: int = 0, n: int | None = None, q_heads=None, kv_heads=None,
+               threads: int | None = None) -> dict:
+    """Generate Q [hq, n, d], K, V [hkv, n, d] (float32 arrays; bf16-exact for bf16 configs).
+
+    ``q_heads`` / ``kv_heads`` restrict generation to a subset of heads; the other heads
+    are left as zeros.  Values of a generated head do not depend on the subset chosen.
+    """
+    spec = layer_spec(cfg, layer, n)
+    n, d = spec.n, spec.d
+    q_heads = list(range(spec.hq)) if q_heads is None else list(q_heads)
+    kv_heads = list(range(spec.hkv)) if kv_heads is None else list(kv_heads)
+    tabs = _rope_tables(n, d)
+    q = np.zeros((spec.hq, n, d), dtype=np.float32)
+    k = np.zeros((spec.hkv, n, d), dtype=np.float32)
+    v = np.zeros((spec.hkv, n, d), dtype=np.float32)
+    nthreads = threads or min(16, os.cpu_count() or 1)
+
+    def job(item):
+        kind, h = item
+        if kind == 0:
+            q[h] = _gen_q(spec, h, tabs)
+        elif kind == 1:
+            k[h] = _gen_k(spec, h, tabs)
+        else:
+            v[h] = _gen_v(spec, h)
+
+    items = [(0, h) for h in q_heads] + [(1, g) for g in kv_heads] + [(2, g) for g in kv_heads]
+    if nthreads > 1 and len(items) > 1:
+        with ThreadPoolExecutor(nthreads) as ex:
+            list(ex.map(job, items))
+    else:
+        for it in items:
+            job(it)
+    return dict(q=q, k=k, v=v, spec=spec)
