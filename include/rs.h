@@ -1,0 +1,239 @@
+/*
+ * rs.h - C ABI of the routed pattern-sparse causal attention prefill library (librs.so).
+ *
+ * The operation (Sec. 2.1, Eq. 1): for one causal head with Q, K, V in R^{n x d},
+ *   O = softmax(Q K^T / sqrt(d) + C) V,
+ * and with a binary sparse mask M the logits outside M become minus infinity, so each
+ * output row is a softmax over its kept key set S_i, renormalised on that set.  The
+ * library computes this per (query head, prompt segment) "unit", choosing per unit one
+ * candidate of the pattern library of Sec. 3.1 (A-shape, vertical-slash, block-sparse,
+ * dense) with the shared probe of Sec. 3.2 (Eq. 3), the risk/certificate quantities of
+ * Sec. 3.3 (Eqs. 4-5) and the latency-constrained router of Sec. 3.4 (Eqs. 6-8).
+ *
+ * Conventions shared by every call
+ *  - Device pointers are caller-owned (e.g. allocated by torch) and must stay valid
+ *    until the work queued on `stream` has finished.  Host pointers are read before the
+ *    call returns.
+ *  - The library allocates no device memory: calls that need scratch space take a
+ *    caller-provided workspace whose size a *_workspace_size() query returns.
+ *  - GPU calls are asynchronous on `stream` (a hipStream_t; NULL = the null stream).
+ *    rs_route_layer is host-only, synchronous and pure.
+ *  - Every call returns an rs_status; on failure nothing has been launched and
+ *    rs_last_error() returns a message (thread-local, valid until the next call).
+ *  - Results are deterministic: identical inputs give bitwise-identical outputs.
+ *  - Layout: Q is [hq][n][d], K and V are [hkv][n][d], each with element strides
+ *    (head, token) and a contiguous last dimension; query head h reads key/value head
+ *    h / (hq / hkv).  O is bf16 [hq][n][d] with strides (so_h, so_t).
+ *  - A unit covers query rows [s0, s1) of one query head; its rows see keys [0, s1)
+ *    causally (key j visible to row i iff j <= i), as in chunked prefill.
+ *  - Supported: d in {64, 128}; hq a multiple of hkv; n <= 262144.
+ */
+#ifndef RS_H
+#define RS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef void *rs_stream; /* hipStream_t */
+
+typedef enum {
+  RS_OK = 0,
+  RS_ERR_INVALID_ARG = 1,      /* bad sizes, strides, pointers or unit bounds */
+  RS_ERR_UNSUPPORTED = 2,      /* valid but not implemented (e.g. d not in {64,128}) */
+  RS_ERR_HIP = 3,              /* a HIP runtime call failed */
+  RS_ERR_WORKSPACE = 4,        /* workspace missing or smaller than required */
+  RS_ERR_BUDGET_INFEASIBLE = 5 /* rs_route_layer: route returned but over budget */
+} rs_status;
+
+typedef enum { RS_BF16 = 0, RS_F32 = 1 /* rounded to bf16 on load */ } rs_dtype;
+
+/* Pattern families of the candidate library (Sec. 3.1). */
+typedef enum { RS_DENSE = 0, RS_ASHAPE = 1, RS_VSLASH = 2, RS_BSPARSE = 3 } rs_family;
+
+/* Q, K, V of one layer. */
+typedef struct rs_qkv {
+  const void *q, *k, *v;     /* device */
+  int32_t dtype;             /* rs_dtype, same for q, k, v */
+  int32_t n, hq, hkv, d;     /* sequence length, query heads, key/value heads, head dim */
+  int32_t _pad0;
+  int64_t sq_h, sq_t;        /* element strides of q (head, token) */
+  int64_t sk_h, sk_t;
+  int64_t sv_h, sv_t;
+  float scale;               /* logit scale; 0 => 1/sqrt(d) */
+  int32_t _pad1;
+} rs_qkv;
+
+/* One unit: rows [s0, s1) of query head `head`; `cand` indexes the candidate grid.
+ * `slot` is the unit's position in the unit list given to rs_probe / rs_build_indices,
+ * i.e. its row in rs_probe_out and rs_index_set (used by vertical-slash attention;
+ * those two calls ignore it and use the list position). */
+typedef struct rs_unit {
+  int32_t head, s0, s1, cand, slot, _pad[3];
+} rs_unit;
+
+/* One candidate (p, b) of the pattern-budget library (Sec. 3.1):
+ *   RS_ASHAPE  a = sink tokens, b = window width (keys (i-b, i] plus [0, a))
+ *   RS_VSLASH  a = n_v vertical columns, b = n_s slash diagonals
+ *   RS_BSPARSE a = k key blocks per query block (diagonal block included), b = block (64)
+ *   RS_DENSE   a = b = 0
+ * Within a family, candidates must appear in the grid in increasing budget order
+ * (both a and b non-decreasing); a candidate's budget rank is its position among the
+ * candidates of its family.  Budgets of one family are nested prefixes of one ranking. */
+typedef struct rs_candidate {
+  int32_t fam, a, b, _pad;
+} rs_candidate;
+
+/* Probe configuration (Sec. 3.2).  Sampled rows of a unit [s0, s1):
+ *   R  = [max(s0, s1 - r_rec), s1)                              (recent rows)
+ *   U  = { s0 + floor((2t+1)(s1-s0) / (2 r_uni)) : t < r_uni } \ R  (uniform rows)
+ *   Bd = { max(s0, 64) + t : t < r_bnd } within [s0, s1), \ (R u U) (boundary rows)
+ * Column and diagonal scores use R; descriptors and coverage use all sampled rows. */
+typedef struct rs_probe_cfg {
+  int32_t r_rec, r_uni, r_bnd;
+  int32_t bs_block;          /* block width of the block-mean estimator, must be 64 */
+  int32_t local_w;           /* local-band width of the local-mass descriptor */
+  uint32_t flags;            /* RS_PROBE_* */
+} rs_probe_cfg;
+
+#define RS_PROBE_ROWS 1u      /* sampled-row scores: stats, col, diag, descriptors */
+#define RS_PROBE_BLOCKMEAN 2u /* block-mean scores L_bs of every query head */
+
+/* Probe results, all device arrays allocated by the caller with these dimensions:
+ *   nunits, rmax = r_rec + r_uni + r_bnd, n, nb = ceil(n / 64), ncand. */
+typedef struct rs_probe_out {
+  int32_t nunits, rmax, n, nb, ncand, hq;
+  int32_t *rows;     /* [nunits][rmax] sampled rows ascending, -1 padded        (written) */
+  int32_t *subset;   /* [nunits][rmax] 0 = R, 1 = U, 2 = Bd, -1 padded           (written) */
+  int32_t *nsub;     /* [nunits][3] subset sizes                                 (written) */
+  float *row_max;    /* [nunits][rmax] max scaled logit of the row over keys <= i */
+  float *row_sum;    /* [nunits][rmax] sum_j exp(l_ij - row_max)                  */
+  float *col;        /* [nunits][n] col[j] = sum over R rows of a_ij (0 for j >= s1) */
+  float *diag;       /* [nunits][n] diag[t] = sum over R rows of a_{i,i-t}           */
+  float *entropy;    /* [nunits][rmax] 64-block entropy / log(#visible blocks)    */
+  float *local;      /* [nunits][rmax] attention mass within (i - local_w, i]      */
+  float *lbs;        /* [hq][nb*(nb+1)/2] pooled logits, row bq at bq*(bq+1)/2, or NULL */
+  float *cov_rows;   /* [nunits][ncand][rmax] m_i(c): mass of row i kept by candidate c */
+  float *cov;        /* [nunits][ncand][4] m_hat, m_R, m_U, m_B (subset means; 0 if empty) */
+} rs_probe_out;
+
+/* Index sets built from probe scores (Sec. 3.1), device arrays allocated by the caller.
+ * VS arrays are per unit and per vertical-slash candidate (in grid order); BS arrays per
+ * query head, per block-sparse candidate and per query block.  Sorted arrays list each
+ * candidate's set in ascending order; bs_rank lists key blocks by score (diagonal block
+ * first); -1 pads.  Budgets of a family are nested: each set is a prefix of one ranking. */
+typedef struct rs_index_set {
+  int32_t nunits, n, nb, hq;
+  int32_t nv_max, ns_max, k_max, nwords; /* nwords = ceil(n/32), nbw = ceil(nb/32) */
+  int32_t ncand_vs, ncand_bs, nbw, _pad;
+  int32_t *vs_vsorted; /* [nunits][ncand_vs][nv_max] */
+  int32_t *vs_dsorted; /* [nunits][ncand_vs][ns_max] */
+  int32_t *vs_count;   /* [nunits][ncand_vs][2]  |V|, |D| */
+  uint32_t *vs_vbits;  /* [nunits][ncand_vs][nwords] bit j set iff column j in V */
+  uint32_t *vs_dbits;  /* [nunits][ncand_vs][nwords] bit t set iff diagonal t in D */
+  int32_t *bs_rank;    /* [hq][nb][k_max]  diagonal block first */
+  int32_t *bs_sorted;  /* [hq][ncand_bs][nb][k_max] */
+  int32_t *bs_count;   /* [hq][ncand_bs][nb] */
+  uint32_t *bs_bits;   /* [hq][ncand_bs][nb][nbw] bit bk set iff key block bk selected */
+} rs_index_set;
+
+/* Routing inputs (host arrays), [nunits][ncand] row-major unless stated. */
+typedef struct rs_route_in {
+  int32_t nunits, ncand;
+  const rs_candidate *grid;  /* [ncand]; must contain one RS_DENSE candidate */
+  const float *cov;          /* [nunits][ncand][4] as in rs_probe_out.cov */
+  const int32_t *nsub;       /* [nunits][3] */
+  const float *e;            /* [nunits][ncand] calibrated error predictor, or NULL (0) */
+  const int32_t *s1;         /* [nunits] key length of each unit (latency bucket key) */
+  /* profiled kernel latency t_ker(p, b, n) in microseconds per unit:
+   * t_table[c * nbucket + k] for kv lengths up to bucket_edge[k] (ascending); a unit
+   * uses the first bucket whose edge is >= s1, else the last. */
+  const double *t_table;
+  const int32_t *bucket_edge;
+  int32_t nbucket, _pad;
+  double t_probe_us;         /* probe + index + routing overhead charged to the layer */
+} rs_route_in;
+
+typedef struct rs_route_cfg {
+  double T_layer_us; /* latency budget of the layer, T_l */
+  double tau;        /* lower-mass threshold of the expand/fallback step */
+  double alpha;      /* weight of the subset disagreement u */
+  double beta;       /* weight of the error predictor e (0: training-free) */
+  double delta_q;    /* calibrated residual quantile: m_lower = max(0, m_hat - delta_q) */
+} rs_route_cfg;
+
+typedef struct rs_route_out {
+  int32_t *choice;      /* [nunits] chosen candidate                          (host) */
+  int32_t *group_cand;  /* [ncand] candidate of group g                       (host) */
+  int32_t *group_start; /* [ncand+1] group g holds units group_units[start[g]..start[g+1]) */
+  int32_t *group_units; /* [nunits] unit indices, grouped, ascending within a group */
+  double *risk;         /* [nunits][ncand] risk R(c) per unit (dense 0)             */
+  double *m_lower;      /* [nunits][ncand] lower mass per unit (dense 1)            */
+  int32_t ngroups, n_fallback, over_budget, infeasible;
+  double total_us, total_risk;
+} rs_route_out;
+
+/* ---- probe (Sec. 3.2, Eq. 3; coverage of Sec. 3.2-3.3) -------------------------------
+ * Scores mode (idx == NULL): for each unit, samples rows as in rs_probe_cfg, computes
+ * exact softmax statistics of the sampled rows over keys [0, s1), the recent-row column
+ * and diagonal scores and the per-row descriptors (flag RS_PROBE_ROWS), and the
+ * block-mean pooled logits L_bs of every query head (flag RS_PROBE_BLOCKMEAN).
+ * Coverage mode (idx != NULL, after a scores call on the same `out`): for each unit,
+ * candidate and sampled row, m_i(c) = sum of a_ij over the candidate's key set, and the
+ * subset means.  `grid`/`ncand` give the candidates (ignored in scores mode). */
+size_t rs_probe_workspace_size(const rs_qkv *qkv, const rs_unit *units, int32_t nunits,
+                               const rs_probe_cfg *cfg);
+rs_status rs_probe(const rs_qkv *qkv, const rs_unit *units, int32_t nunits,
+                   const rs_probe_cfg *cfg, const rs_candidate *grid, int32_t ncand,
+                   const rs_index_set *idx, void *ws, size_t ws_bytes, rs_probe_out *out,
+                   rs_stream stream);
+
+/* ---- index construction (Sec. 3.1) ------------------------------------------------------
+ * Total order of every selection: score descending, -0.0 after +0.0, position ascending.
+ * VS per unit: V = top n_v columns of col over [0, s1); D = {0} + top (n_s - 1) diagonals
+ * of diag over [1, s1).  BS per query head and query block bq (nb blocks of 64):
+ * Sel(bq) = {bq} + top (k - 1) of L_bs[bq][0..bq).  Fewer candidates than the budget:
+ * all are taken.  Needs the probe output of a scores call with the matching flags. */
+size_t rs_build_indices_workspace_size(const rs_probe_out *scores, const rs_candidate *grid,
+                                       int32_t ncand);
+rs_status rs_build_indices(const rs_probe_out *scores, const rs_unit *units, int32_t nunits,
+                           const rs_candidate *grid, int32_t ncand, void *ws, size_t ws_bytes,
+                           rs_index_set *out, rs_stream stream);
+
+/* ---- routing (Sec. 3.4, Eqs. 6-8; inference-procedure steps 3-6) ------------------------
+ * Host only.  Risk R = (1 - m_hat) + alpha u + beta e with u = max - min of the
+ * non-empty subset means (dense: 0); greedy risk-per-microsecond substitutions from
+ * all-dense until t_probe + sum t <= T_layer; then each sparse choice with
+ * m_lower < tau takes the smallest larger budget of its family with m_lower >= tau, else
+ * dense; units grouped by candidate.  Returns RS_ERR_BUDGET_INFEASIBLE (route still
+ * filled in) when the final total exceeds T_layer. */
+rs_status rs_route_layer(const rs_route_in *in, const rs_route_cfg *cfg, rs_route_out *out);
+
+/* ---- attention (Sec. 2.1; kernels of Sec. 3.1) ------------------------------------------
+ * Every unit of one call must use the same candidate (one (pattern, budget) group).
+ * Writes rows [s0, s1) of O for each unit and, if lse != NULL, lse[head * n + i] =
+ * log sum over S_i of exp(l_ij) (natural log; -inf for an empty row).  Sparse calls read
+ * the index set built by rs_build_indices with the same grid (A-shape needs none and
+ * accepts idx == NULL).  Units of different calls may run concurrently only if they write
+ * disjoint rows. */
+size_t rs_attn_workspace_size(const rs_qkv *qkv, const rs_unit *units, int32_t nunits);
+rs_status rs_sparse_attn_prefill(const rs_qkv *qkv, const rs_unit *units, int32_t nunits,
+                                 const rs_candidate *grid, int32_t ncand,
+                                 const rs_index_set *idx, void *o, int64_t so_h, int64_t so_t,
+                                 float *lse, void *ws, size_t ws_bytes, rs_stream stream);
+rs_status rs_dense_attn_prefill(const rs_qkv *qkv, const rs_unit *units, int32_t nunits,
+                                void *o, int64_t so_h, int64_t so_t, float *lse, void *ws,
+                                size_t ws_bytes, rs_stream stream);
+
+/* Message describing the last failure of the calling thread ("" if none). */
+const char *rs_last_error(void);
+/* Library version string. */
+const char *rs_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* RS_H */

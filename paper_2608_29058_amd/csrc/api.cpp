@@ -1,0 +1,279 @@
+// C ABI entry points of librs: argument validation and dispatch to the HIP launchers.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <string>
+#include <vector>
+
+#include "common.h"
+
+namespace rs {
+
+static thread_local std::string g_err;
+
+void set_error(const std::string &msg) { g_err = msg; }
+
+rs_status fail(rs_status st, const std::string &msg) {
+  g_err = msg;
+  return st;
+}
+
+rs_status hip_check(hipError_t e, const char *what) {
+  g_err = std::string(what) + ": " + hipGetErrorString(e);
+  return RS_ERR_HIP;
+}
+
+static bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+rs_status check_qkv(const rs_qkv *qkv, float *scale) {
+  if (!qkv) return fail(RS_ERR_INVALID_ARG, "qkv is NULL");
+  if (!qkv->q || !qkv->k || !qkv->v) return fail(RS_ERR_INVALID_ARG, "q, k or v is NULL");
+  if (qkv->n < 1 || qkv->n > kMaxN) return fail(RS_ERR_INVALID_ARG, "n must be in [1, 262144]");
+  if (qkv->hq < 1 || qkv->hkv < 1 || qkv->hq % qkv->hkv != 0)
+    return fail(RS_ERR_INVALID_ARG, "hq must be a positive multiple of hkv");
+  if (qkv->dtype != RS_BF16 && qkv->dtype != RS_F32) return fail(RS_ERR_INVALID_ARG, "unknown dtype");
+  if (qkv->d != 64 && qkv->d != 128) return fail(RS_ERR_UNSUPPORTED, "head dim must be 64 or 128");
+  const int64_t vec = qkv->dtype == RS_BF16 ? 8 : 4;  // elements per 16 bytes
+  const size_t esz = qkv->dtype == RS_BF16 ? 2 : 4;
+  const int64_t s[6] = {qkv->sq_h, qkv->sq_t, qkv->sk_h, qkv->sk_t, qkv->sv_h, qkv->sv_t};
+  for (int i = 0; i < 6; ++i)
+    if (s[i] < 0 || s[i] % vec != 0)
+      return fail(RS_ERR_INVALID_ARG, "strides must be non-negative multiples of 16 bytes");
+  if (qkv->sq_t < qkv->d || qkv->sk_t < qkv->d || qkv->sv_t < qkv->d)
+    return fail(RS_ERR_INVALID_ARG, "token stride smaller than head dim");
+  if (!aligned(qkv->q, 16) || !aligned(qkv->k, 16) || !aligned(qkv->v, 16))
+    return fail(RS_ERR_INVALID_ARG, "q, k and v must be 16-byte aligned");
+  (void)esz;
+  float sc = qkv->scale;
+  if (sc == 0.f) sc = 1.f / std::sqrt((float)qkv->d);
+  if (!(sc > 0.f) || !std::isfinite(sc)) return fail(RS_ERR_INVALID_ARG, "scale must be positive and finite");
+  *scale = sc;
+  return RS_OK;
+}
+
+rs_status check_units(const rs_qkv *qkv, const rs_unit *units, int32_t nunits) {
+  if (nunits < 0) return fail(RS_ERR_INVALID_ARG, "nunits < 0");
+  if (nunits > 32767) return fail(RS_ERR_INVALID_ARG, "at most 32767 units per call");
+  if (nunits > 0 && !units) return fail(RS_ERR_INVALID_ARG, "units is NULL");
+  for (int i = 0; i < nunits; ++i) {
+    const rs_unit &u = units[i];
+    if (u.head < 0 || u.head >= qkv->hq) return fail(RS_ERR_INVALID_ARG, "unit " + std::to_string(i) + ": head out of range");
+    if (u.s0 < 0 || u.s1 <= u.s0 || u.s1 > qkv->n)
+      return fail(RS_ERR_INVALID_ARG, "unit " + std::to_string(i) + ": need 0 <= s0 < s1 <= n");
+  }
+  return RS_OK;
+}
+
+// defined in the .hip translation units
+size_t attn_ws_bytes(const rs_unit *units, int32_t nunits);
+rs_status attn_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int32_t nunits, int fam,
+                      const rs_candidate *cand, int cand_local, const rs_index_set *idx, void *o, int64_t so_h,
+                      int64_t so_t, float *lse, void *ws, size_t ws_bytes, hipStream_t st);
+size_t probe_ws_bytes(const rs_qkv *qkv, int32_t nunits, const rs_probe_cfg *cfg);
+rs_status probe_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int32_t nunits,
+                       const rs_probe_cfg *cfg, const rs_candidate *grid, int32_t ncand, const rs_index_set *idx,
+                       void *ws, size_t ws_bytes, rs_probe_out *out, hipStream_t st);
+rs_status build_indices_launch(const rs_probe_out *sc, const rs_unit *units, int32_t nunits,
+                               const rs_candidate *grid, int32_t ncand, rs_index_set *out, hipStream_t st, void *ws,
+                               size_t ws_bytes);
+
+static rs_status check_grid(const rs_candidate *grid, int32_t ncand) {
+  if (ncand < 1 || !grid) return fail(RS_ERR_INVALID_ARG, "empty candidate grid");
+  if (ncand > 16) return fail(RS_ERR_UNSUPPORTED, "at most 16 candidates");
+  int last_a[4] = {-1, -1, -1, -1}, last_b[4] = {-1, -1, -1, -1}, cnt[4] = {0, 0, 0, 0};
+  for (int c = 0; c < ncand; ++c) {
+    const rs_candidate &g = grid[c];
+    if (g.fam < RS_DENSE || g.fam > RS_BSPARSE) return fail(RS_ERR_INVALID_ARG, "unknown family");
+    if (g.a < 0 || g.b < 0) return fail(RS_ERR_INVALID_ARG, "negative budget");
+    if (g.fam == RS_ASHAPE && g.b < 1) return fail(RS_ERR_INVALID_ARG, "A-shape window must be >= 1");
+    if (g.fam == RS_BSPARSE && (g.b != 64 || g.a < 1 || g.a > 256))
+      return fail(RS_ERR_UNSUPPORTED, "block-sparse needs block 64 and 1 <= k <= 256");
+    if (g.fam == RS_VSLASH && (g.a > 4096 || g.b > 1 << 20))
+      return fail(RS_ERR_UNSUPPORTED, "vertical-slash needs n_v <= 4096");
+    if (g.a < last_a[g.fam] || g.b < last_b[g.fam])
+      return fail(RS_ERR_INVALID_ARG, "candidates of a family must be listed in increasing budget order");
+    last_a[g.fam] = g.a;
+    last_b[g.fam] = g.b;
+    if (++cnt[g.fam] > 8) return fail(RS_ERR_UNSUPPORTED, "at most 8 candidates per family");
+  }
+  return RS_OK;
+}
+
+static int cand_local_index(const rs_candidate *grid, int c) {
+  int k = 0;
+  for (int i = 0; i < c; ++i)
+    if (grid[i].fam == grid[c].fam) ++k;
+  return k;
+}
+
+static rs_status check_out(const void *o, int64_t so_h, int64_t so_t, int d) {
+  if (!o) return fail(RS_ERR_INVALID_ARG, "output is NULL");
+  if (!aligned(o, 8) || so_t % 4 != 0 || so_h % 4 != 0 || so_t < d || so_h < 0)
+    return fail(RS_ERR_INVALID_ARG, "output must be 8-byte aligned with strides multiple of 4 elements");
+  return RS_OK;
+}
+
+}  // namespace rs
+
+using namespace rs;
+
+extern "C" {
+
+const char *rs_last_error(void) { return g_err.c_str(); }
+const char *rs_version(void) { return "routesparse-mi355x 0.1 (gfx950)"; }
+
+size_t rs_attn_workspace_size(const rs_qkv *qkv, const rs_unit *units, int32_t nunits) {
+  (void)qkv;
+  if (nunits <= 0 || !units) return 256;
+  return attn_ws_bytes(units, nunits);
+}
+
+rs_status rs_dense_attn_prefill(const rs_qkv *qkv, const rs_unit *units, int32_t nunits, void *o, int64_t so_h,
+                                int64_t so_t, float *lse, void *ws, size_t ws_bytes, rs_stream stream) {
+  g_err.clear();
+  float scale;
+  rs_status st;
+  if ((st = check_qkv(qkv, &scale)) != RS_OK) return st;
+  if ((st = check_units(qkv, units, nunits)) != RS_OK) return st;
+  if ((st = check_out(o, so_h, so_t, qkv->d)) != RS_OK) return st;
+  return attn_launch(qkv, scale, units, nunits, RS_DENSE, nullptr, 0, nullptr, o, so_h, so_t, lse, ws, ws_bytes,
+                     (hipStream_t)stream);
+}
+
+rs_status rs_sparse_attn_prefill(const rs_qkv *qkv, const rs_unit *units, int32_t nunits, const rs_candidate *grid,
+                                 int32_t ncand, const rs_index_set *idx, void *o, int64_t so_h, int64_t so_t,
+                                 float *lse, void *ws, size_t ws_bytes, rs_stream stream) {
+  g_err.clear();
+  float scale;
+  rs_status st;
+  if ((st = check_qkv(qkv, &scale)) != RS_OK) return st;
+  if ((st = check_units(qkv, units, nunits)) != RS_OK) return st;
+  if ((st = check_grid(grid, ncand)) != RS_OK) return st;
+  if ((st = check_out(o, so_h, so_t, qkv->d)) != RS_OK) return st;
+  if (nunits == 0) return RS_OK;
+  const int c = units[0].cand;
+  if (c < 0 || c >= ncand) return fail(RS_ERR_INVALID_ARG, "unit candidate out of range");
+  for (int i = 1; i < nunits; ++i)
+    if (units[i].cand != c) return fail(RS_ERR_INVALID_ARG, "all units of one call must share a candidate");
+  const rs_candidate &g = grid[c];
+  const int cl = cand_local_index(grid, c);
+  if (g.fam == RS_VSLASH || g.fam == RS_BSPARSE) {
+    if (!idx) return fail(RS_ERR_INVALID_ARG, "index set required");
+    if (idx->n != qkv->n) return fail(RS_ERR_INVALID_ARG, "index set built for another sequence length");
+  }
+  if (g.fam == RS_VSLASH) {
+    if (!idx->vs_vsorted || !idx->vs_dsorted || !idx->vs_count || !idx->vs_vbits || !idx->vs_dbits)
+      return fail(RS_ERR_INVALID_ARG, "vertical-slash arrays missing");
+    if (cl >= idx->ncand_vs || idx->nwords != (qkv->n + 31) / 32 || idx->nv_max > 4096)
+      return fail(RS_ERR_INVALID_ARG, "index set does not match the grid");
+    for (int i = 0; i < nunits; ++i)
+      if (units[i].slot < 0 || units[i].slot >= idx->nunits)
+        return fail(RS_ERR_INVALID_ARG, "unit slot outside the index set");
+  }
+  if (g.fam == RS_BSPARSE) {
+    if (!idx->bs_sorted || !idx->bs_count) return fail(RS_ERR_INVALID_ARG, "block-sparse arrays missing");
+    if (cl >= idx->ncand_bs || idx->nb != (qkv->n + 63) / 64 || idx->hq != qkv->hq)
+      return fail(RS_ERR_INVALID_ARG, "index set does not match the grid");
+  }
+  return attn_launch(qkv, scale, units, nunits, g.fam, &g, cl, idx, o, so_h, so_t, lse, ws, ws_bytes,
+                     (hipStream_t)stream);
+}
+
+size_t rs_probe_workspace_size(const rs_qkv *qkv, const rs_unit *units, int32_t nunits, const rs_probe_cfg *cfg) {
+  (void)units;
+  if (!qkv || !cfg || nunits < 0) return 0;
+  return probe_ws_bytes(qkv, nunits, cfg);
+}
+
+rs_status rs_probe(const rs_qkv *qkv, const rs_unit *units, int32_t nunits, const rs_probe_cfg *cfg,
+                   const rs_candidate *grid, int32_t ncand, const rs_index_set *idx, void *ws, size_t ws_bytes,
+                   rs_probe_out *out, rs_stream stream) {
+  g_err.clear();
+  float scale;
+  rs_status st;
+  if ((st = check_qkv(qkv, &scale)) != RS_OK) return st;
+  if ((st = check_units(qkv, units, nunits)) != RS_OK) return st;
+  if (!cfg || !out) return fail(RS_ERR_INVALID_ARG, "cfg or out is NULL");
+  if (cfg->r_rec < 0 || cfg->r_uni < 0 || cfg->r_bnd < 0 || cfg->r_rec + cfg->r_uni + cfg->r_bnd > 256)
+    return fail(RS_ERR_INVALID_ARG, "sampled rows must be in [0, 256]");
+  if (cfg->bs_block != 64) return fail(RS_ERR_UNSUPPORTED, "block-mean block must be 64");
+  if (cfg->local_w < 1) return fail(RS_ERR_INVALID_ARG, "local_w must be >= 1");
+  const int rmax = cfg->r_rec + cfg->r_uni + cfg->r_bnd;
+  if (out->nunits != nunits || out->rmax != rmax || out->n != qkv->n || out->nb != (qkv->n + 63) / 64 ||
+      out->hq != qkv->hq)
+    return fail(RS_ERR_INVALID_ARG, "probe output dimensions do not match");
+  if (!out->rows || !out->subset || !out->nsub || !out->row_max || !out->row_sum)
+    return fail(RS_ERR_INVALID_ARG, "probe row arrays missing");
+  if (idx == nullptr) {
+    if ((cfg->flags & RS_PROBE_ROWS) && (!out->col || !out->diag || !out->entropy || !out->local))
+      return fail(RS_ERR_INVALID_ARG, "probe score arrays missing");
+    if ((cfg->flags & RS_PROBE_BLOCKMEAN) && !out->lbs) return fail(RS_ERR_INVALID_ARG, "lbs missing");
+  } else {
+    if ((st = check_grid(grid, ncand)) != RS_OK) return st;
+    if (out->ncand != ncand || !out->cov_rows || !out->cov) return fail(RS_ERR_INVALID_ARG, "coverage arrays missing");
+    if (idx->nunits != nunits || idx->n != qkv->n) return fail(RS_ERR_INVALID_ARG, "index set does not match");
+    for (int c = 0; c < ncand; ++c) {
+      if (grid[c].fam == RS_VSLASH && (!idx->vs_vbits || !idx->vs_dbits))
+        return fail(RS_ERR_INVALID_ARG, "vertical-slash bitmaps missing");
+      if (grid[c].fam == RS_BSPARSE && (!idx->bs_bits || idx->hq != qkv->hq))
+        return fail(RS_ERR_INVALID_ARG, "block-sparse bitmaps missing");
+    }
+  }
+  if (nunits == 0) return RS_OK;
+  return probe_launch(qkv, scale, units, nunits, cfg, grid, ncand, idx, ws, ws_bytes, out, (hipStream_t)stream);
+}
+
+size_t rs_build_indices_workspace_size(const rs_probe_out *scores, const rs_candidate *grid, int32_t ncand) {
+  (void)grid;
+  (void)ncand;
+  if (!scores) return 0;
+  return (size_t)scores->nunits * sizeof(int) + 512;
+}
+
+rs_status rs_build_indices(const rs_probe_out *scores, const rs_unit *units, int32_t nunits,
+                           const rs_candidate *grid, int32_t ncand, void *ws, size_t ws_bytes, rs_index_set *out,
+                           rs_stream stream) {
+  g_err.clear();
+  rs_status st;
+  if (!scores || !out) return fail(RS_ERR_INVALID_ARG, "scores or out is NULL");
+  if ((st = check_grid(grid, ncand)) != RS_OK) return st;
+  if (nunits < 0 || (nunits > 0 && !units)) return fail(RS_ERR_INVALID_ARG, "bad units");
+  if (scores->nunits != nunits || out->nunits != nunits) return fail(RS_ERR_INVALID_ARG, "unit count mismatch");
+  const int n = scores->n;
+  if (n < 1 || n > kMaxN) return fail(RS_ERR_INVALID_ARG, "bad n");
+  int nvs = 0, nbs = 0, nvm = 0, nsm = 0, km = 0;
+  for (int c = 0; c < ncand; ++c) {
+    if (grid[c].fam == RS_VSLASH) {
+      ++nvs;
+      nvm = std::max(nvm, grid[c].a);
+      nsm = std::max(nsm, grid[c].b);
+    }
+    if (grid[c].fam == RS_BSPARSE) {
+      ++nbs;
+      km = std::max(km, grid[c].a);
+    }
+  }
+  const int nb = (n + 63) / 64;
+  if (out->n != n || out->nb != nb || out->nwords != (n + 31) / 32 || out->nbw != (nb + 31) / 32)
+    return fail(RS_ERR_INVALID_ARG, "index set dimensions do not match n");
+  if (out->ncand_vs != nvs || out->ncand_bs != nbs) return fail(RS_ERR_INVALID_ARG, "index set family counts");
+  for (int u = 0; u < nunits; ++u)
+    if (units[u].s1 < 1 || units[u].s1 > n || units[u].s0 < 0 || units[u].s0 >= units[u].s1)
+      return fail(RS_ERR_INVALID_ARG, "bad unit bounds");
+  if (nvs > 0) {
+    if (out->nv_max < nvm || out->ns_max < nsm) return fail(RS_ERR_INVALID_ARG, "nv_max/ns_max below the grid");
+    if (!scores->col || !scores->diag) return fail(RS_ERR_INVALID_ARG, "probe scores missing");
+    if (!out->vs_vsorted || !out->vs_dsorted || !out->vs_count || !out->vs_vbits || !out->vs_dbits)
+      return fail(RS_ERR_INVALID_ARG, "vertical-slash arrays missing");
+  }
+  if (nbs > 0) {
+    if (out->k_max < km || out->k_max > 256) return fail(RS_ERR_INVALID_ARG, "k_max below the grid or above 256");
+    if (!scores->lbs || out->hq != scores->hq) return fail(RS_ERR_INVALID_ARG, "block-mean scores missing");
+    if (!out->bs_rank || !out->bs_sorted || !out->bs_count || !out->bs_bits)
+      return fail(RS_ERR_INVALID_ARG, "block-sparse arrays missing");
+  }
+  if (nunits == 0 && nbs == 0) return RS_OK;
+  return build_indices_launch(scores, units, nunits, grid, ncand, out, (hipStream_t)stream, ws, ws_bytes);
+}
+
+}  // extern "C"

@@ -1,0 +1,539 @@
+// Causal dense and pattern-sparse attention prefill for gfx950 (bf16 MFMA, fp32 softmax).
+//
+// Computes, for each unit (query head, rows [s0, s1)), O_i = sum_{j in S_i} softmax(l_i.)_j v_j
+// over the kept key set S_i of the unit's pattern (Sec. 2.1: masked logits are minus
+// infinity, rows renormalise on their kept set).  The sets are token-exact:
+//   dense      S_i = {j <= i}
+//   A-shape    S_i = {j <= i : j < sink or j > i - window}
+//   block      S_i = {j <= i : j / 64 in Sel(i / 64)}
+//   vert-slash S_i = {j in V, j <= i} u {i - t : t in D, t <= i}
+//
+// Work decomposition: one workgroup = one query tile of BM = 32 * NW rows of one unit;
+// each wave owns 32 rows.  Keys stream through LDS in tiles of 64 (contiguous, or
+// gathered vertical columns for vertical-slash).  Per wave and key tile:
+//   S^T[64 keys x 32 rows] = K_tile (A operand, LDS) x Q^T (B operand, registers)
+// with v_mfma_f32_32x32x16_bf16, so each lane holds one query row and 32 of its keys:
+// row max / row sum are in-lane plus one exchange with the other lane half.  Then
+//   O^T[d x 32 rows] += V^T (A operand, LDS, stored transposed) x P^T (B operand, the
+// softmax probabilities straight from the S^T accumulators, repacked to bf16).
+// Online softmax in the exp2 domain (logit * scale * log2 e), fp32 statistics.
+#include <algorithm>
+#include <cstring>
+#include <vector>
+
+#include "common.h"
+
+namespace rs {
+
+enum { P_DENSE = 0, P_ASHAPE = 1, P_VS = 2, P_BS = 3 };
+
+struct DevUnit {
+  int head, s0, s1, cl, slot, pad0, pad1, pad2;
+};
+
+struct AttnArgs {
+  const void *q, *k, *v;
+  long long sq_h, sq_t, sk_h, sk_t, sv_h, sv_t;
+  bf16 *o;
+  long long so_h, so_t;
+  float *lse;
+  int n, group;
+  float c, scale;
+  const DevUnit *units;
+  const int *order;
+  int sink, window;  // A-shape
+  const int *vs_vsorted, *vs_dsorted, *vs_count;
+  const uint32_t *vs_vbits, *vs_dbits;
+  int nv_max, ns_max, nwords, ncand_vs;
+  const int *bs_sorted, *bs_count;
+  int k_max, nb, ncand_bs;
+};
+
+constexpr int kMaxTiles = kMaxN / 64;  // key tiles of the longest supported sequence
+constexpr int kMaxGather = 4096;       // vertical columns gathered per query tile
+
+template <int D, int NW, int PAT, typename InT>
+__global__ void __launch_bounds__(NW * 64) attn_fwd_kernel(const AttnArgs a) {
+  constexpr int NT = NW * 64;
+  constexpr int BM = NW * 32;
+  constexpr int KS = D / 16;             // k-steps of the QK^T contraction
+  constexpr int DB = D / 32;             // 32-row blocks of O^T
+  constexpr int KSTR = D + 8;            // K row stride in LDS (bf16), padded
+  constexpr int VSTR = 64 + 4;           // V^T row stride in LDS (bf16), padded
+  constexpr int KCH_TOT = 64 * (D / 8);  // 16-byte chunks of a K tile
+  constexpr int KCH = (KCH_TOT + NT - 1) / NT;
+  constexpr int VBL_TOT = 16 * (D / 8);  // 4-key x 8-dim blocks of a V tile
+  constexpr int VBL = (VBL_TOT + NT - 1) / NT;
+
+  __shared__ __align__(16) bf16 sK[64 * KSTR];
+  __shared__ __align__(16) bf16 sV[D * VSTR];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int l32 = lane & 31, hh = lane >> 5;
+
+  const int item = a.order[blockIdx.x];
+  const DevUnit U = a.units[item >> 16];
+  const int qt = item & 0xffff;
+  const int head = U.head, s0 = U.s0, s1 = U.s1;
+  const int kvh = head / a.group;
+  const int base = (s0 / BM + qt) * BM;
+  const int r_lo = max(s0, base), r_hi = min(s1, base + BM);  // valid rows [r_lo, r_hi)
+  const int wbase = base + 32 * wave;
+  const int w_lo = max(r_lo, wbase), w_hi = min(r_hi, wbase + 32) - 1;
+  const bool wave_active = w_lo <= w_hi;
+  const int my_row = wbase + l32;
+
+  const InT *Qp = (const InT *)a.q + (long long)head * a.sq_h;
+  const InT *Kp = (const InT *)a.k + (long long)kvh * a.sk_h;
+  const InT *Vp = (const InT *)a.v + (long long)kvh * a.sv_h;
+
+  // ---- pattern state ---------------------------------------------------------------------
+  int ntiles = 0;
+  int ash_ns = 0, ash_start2 = 0;
+  const int *bs_list = nullptr;
+  const uint32_t *vbits = nullptr, *dbits = nullptr;
+  int n_contig = 0, n_gather = 0;
+  const int last_tile = (r_hi - 1) >> 6;
+
+  // vertical-slash planning storage (only instantiated for that pattern)
+  int *sTL = nullptr, *sG = nullptr;
+  if constexpr (PAT == P_VS) {
+    __shared__ uint32_t sTB[kMaxTiles / 32];
+    __shared__ int sTLbuf[kMaxTiles];
+    __shared__ int sGbuf[kMaxGather];
+    __shared__ int sScan[NW + 1];
+    __shared__ int sWordPre[kMaxTiles / 32 + 1];
+    sTL = sTLbuf;
+    sG = sGbuf;
+    const long long vsrow = (long long)U.slot * a.ncand_vs + U.cl;
+    const int *vsorted = a.vs_vsorted + vsrow * a.nv_max;
+    const int *dsorted = a.vs_dsorted + vsrow * a.ns_max;
+    const int nvc = a.vs_count[vsrow * 2 + 0];
+    const int ndc = a.vs_count[vsrow * 2 + 1];
+    vbits = a.vs_vbits + vsrow * a.nwords;
+    dbits = a.vs_dbits + vsrow * a.nwords;
+    const int nwt = (last_tile >> 5) + 1;
+    for (int w = tid; w < nwt; w += NT) sTB[w] = 0u;
+    __syncthreads();
+    // slash lines: diagonal t covers keys [r_lo - t, r_hi - 1 - t] of this tile's rows
+    for (int x = tid; x < ndc; x += NT) {
+      const int t = dsorted[x];
+      if (t < 0 || t > r_hi - 1) continue;
+      const int lo = max(0, r_lo - t) >> 6, hi = (r_hi - 1 - t) >> 6;
+      for (int kt = lo; kt <= hi; ++kt) atomicOr(&sTB[kt >> 5], 1u << (kt & 31));
+    }
+    __syncthreads();
+    if (tid == 0) {
+      int acc = 0;
+      for (int w = 0; w < nwt; ++w) {
+        sWordPre[w] = acc;
+        acc += __builtin_popcount(sTB[w]);
+      }
+      sWordPre[nwt] = acc;
+    }
+    __syncthreads();
+    for (int w = tid; w < nwt; w += NT) {
+      uint32_t b = sTB[w];
+      int p = sWordPre[w];
+      while (b) {
+        const int bit = __builtin_ctz(b);
+        b &= b - 1;
+        sTL[p++] = w * 32 + bit;
+      }
+    }
+    n_contig = sWordPre[nwt];
+    // vertical columns outside the slash tiles are gathered (ascending order kept)
+    int total = 0;
+    for (int x0 = 0; x0 < nvc; x0 += NT) {
+      const int x = x0 + tid;
+      int j = (x < nvc) ? vsorted[x] : 0x7fffffff;
+      bool f = false;
+      if (x < nvc && j <= r_hi - 1) {
+        const int kt = j >> 6;
+        f = !((sTB[kt >> 5] >> (kt & 31)) & 1u);
+      }
+      const uint64_t bal = __ballot(f);
+      const int before = __popcll(bal & ((1ull << lane) - 1ull));
+      if (lane == 0) sScan[wave] = __popcll(bal);
+      __syncthreads();
+      int woff = total;
+      for (int w = 0; w < wave; ++w) woff += sScan[w];
+      int blk = 0;
+      for (int w = 0; w < NW; ++w) blk += sScan[w];
+      if (f && woff + before < kMaxGather) sG[woff + before] = j;
+      total += blk;
+      __syncthreads();
+      if (x0 + NT <= nvc) {
+        const int jl = vsorted[min(x0 + NT - 1, nvc - 1)];
+        if (jl > r_hi - 1) break;  // sorted: later columns are all beyond the tile
+      }
+    }
+    n_gather = min(total, kMaxGather);
+    __syncthreads();
+    ntiles = n_contig + (n_gather + 63) / 64;
+  } else if constexpr (PAT == P_DENSE) {
+    ntiles = last_tile + 1;
+  } else if constexpr (PAT == P_ASHAPE) {
+    ash_ns = min((a.sink + 63) >> 6, last_tile + 1);
+    const int wlo = max(0, r_lo - a.window + 1) >> 6;
+    ash_start2 = max(wlo, ash_ns);
+    ntiles = ash_ns + max(0, last_tile - ash_start2 + 1);
+  } else {  // P_BS: one 64-row query block per workgroup
+    const int bq = base >> 6;
+    const long long brow = ((long long)head * a.ncand_bs + U.cl) * a.nb + bq;
+    bs_list = a.bs_sorted + brow * a.k_max;
+    ntiles = a.bs_count[brow];
+  }
+
+  // tile t -> first key (contiguous) or -(1 + gather offset) (gathered)
+  auto tile_key = [&](int t) -> int {
+    if constexpr (PAT == P_DENSE) return t * 64;
+    else if constexpr (PAT == P_ASHAPE) return (t < ash_ns ? t : ash_start2 + (t - ash_ns)) * 64;
+    else if constexpr (PAT == P_BS) return bs_list[t] * 64;
+    else return t < n_contig ? sTL[t] * 64 : -(1 + (t - n_contig) * 64);
+  };
+
+  // ---- Q fragment in registers (B operand of QK^T) ------------------------------------------
+  u32x4 qf[KS];
+  {
+    const bool ok = wave_active && my_row < a.n;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      qf[ks] = u32x4{0u, 0u, 0u, 0u};
+      if (ok) qf[ks] = load8<InT>(Qp + (long long)my_row * a.sq_t + 16 * ks + 8 * hh);
+    }
+  }
+
+  // ---- global -> register tile loader ----------------------------------------------------
+  u32x4 kr[KCH];
+  u32x4 vr[VBL][4];
+  auto key_of = [&](int key0, int kk) -> int {
+    if constexpr (PAT == P_VS) {
+      if (key0 < 0) {
+        const int g = -key0 - 1 + kk;
+        return g < n_gather ? sG[g] : -1;
+      }
+    }
+    const int j = key0 + kk;
+    return j < a.n ? j : -1;
+  };
+  auto load_tile = [&](int key0) {
+#pragma unroll
+    for (int i = 0; i < KCH; ++i) {
+      const int cidx = tid + i * NT;
+      kr[i] = u32x4{0u, 0u, 0u, 0u};
+      if (cidx < KCH_TOT) {
+        const int row = cidx / (D / 8), cc = cidx % (D / 8);
+        const int j = key_of(key0, row);
+        if (j >= 0) kr[i] = load8<InT>(Kp + (long long)j * a.sk_t + 8 * cc);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < VBL; ++i) {
+      const int b = tid + i * NT;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) vr[i][e] = u32x4{0u, 0u, 0u, 0u};
+      if (b < VBL_TOT) {
+        const int dg = b / 16, kg = b % 16;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int j = key_of(key0, 4 * kg + e);
+          if (j >= 0) vr[i][e] = load8<InT>(Vp + (long long)j * a.sv_t + 8 * dg);
+        }
+      }
+    }
+  };
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int i = 0; i < KCH; ++i) {
+      const int cidx = tid + i * NT;
+      if (cidx < KCH_TOT) {
+        const int row = cidx / (D / 8), cc = cidx % (D / 8);
+        *(u32x4 *)&sK[row * KSTR + 8 * cc] = kr[i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < VBL; ++i) {
+      const int b = tid + i * NT;
+      if (b < VBL_TOT) {
+        const int dg = b / 16, kg = b % 16;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const uint32_t e0 = vr[i][0][w], e1 = vr[i][1][w], e2 = vr[i][2][w], e3 = vr[i][3][w];
+          u32x2 lo, hi;
+          lo[0] = (e0 & 0xffffu) | (e1 << 16);
+          lo[1] = (e2 & 0xffffu) | (e3 << 16);
+          hi[0] = (e0 >> 16) | (e1 & 0xffff0000u);
+          hi[1] = (e2 >> 16) | (e3 & 0xffff0000u);
+          *(u32x2 *)&sV[(8 * dg + 2 * w) * VSTR + 4 * kg] = lo;
+          *(u32x2 *)&sV[(8 * dg + 2 * w + 1) * VSTR + 4 * kg] = hi;
+        }
+      }
+    }
+  };
+
+  // ---- main loop -------------------------------------------------------------------------
+  f32x16 oacc[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+  const float c = a.c;
+
+  int key_next = ntiles > 0 ? tile_key(0) : 0;
+  if (ntiles > 0) load_tile(key_next);
+
+  for (int t = 0; t < ntiles; ++t) {
+    __syncthreads();
+    store_tile();
+    __syncthreads();
+    const int key0 = key_next;
+    if (t + 1 < ntiles) {
+      key_next = tile_key(t + 1);
+      load_tile(key_next);
+    }
+    if (!wave_active) continue;
+
+    // wave-uniform skip / mask decisions
+    bool need_mask = true;
+    int g_cnt = 0;
+    if constexpr (PAT == P_VS) {
+      if (key0 < 0) {
+        const int g0 = -key0 - 1;
+        g_cnt = min(64, n_gather - g0);
+        if (sG[g0] > w_hi) continue;
+      } else if (key0 > w_hi) {
+        continue;
+      }
+    } else {
+      if (key0 > w_hi) continue;
+      if constexpr (PAT == P_ASHAPE) {
+        if (key0 >= a.sink && key0 + 63 < w_lo - a.window + 1) continue;
+        need_mask = !(key0 + 63 <= w_lo && (key0 + 63 < a.sink || key0 > w_hi - a.window));
+      } else {
+        need_mask = key0 + 63 > w_lo;
+      }
+    }
+
+    f32x16 sacc[2];
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[mb][r] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const u32x4 kf = *(const u32x4 *)&sK[(32 * mb + l32) * KSTR + 16 * ks + 8 * hh];
+        sacc[mb] = mfma32(kf, qf[ks], sacc[mb]);
+      }
+    }
+
+    if (need_mask) {
+      const int i = my_row;
+      uint64_t M;
+      if constexpr (PAT == P_VS) {
+        if (key0 < 0) {
+          const int g0 = -key0 - 1;
+          int lo = 0, hi = g_cnt;
+          while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if (sG[g0 + mid] <= i) lo = mid + 1;
+            else hi = mid;
+          }
+          M = prefix_mask(lo);
+        } else {
+          const uint64_t w = bits64_at(dbits, a.nwords, i - key0 - 63);
+          const uint64_t md = __builtin_bitreverse64(w);
+          const uint64_t mv = bits64_at(vbits, a.nwords, key0);
+          M = (md | mv) & prefix_mask(i - key0 + 1);
+        }
+      } else if constexpr (PAT == P_ASHAPE) {
+        const uint64_t keep = prefix_mask(a.sink - key0) | ~prefix_mask(i - a.window + 1 - key0);
+        M = keep & prefix_mask(i - key0 + 1);
+      } else {
+        M = prefix_mask(i - key0 + 1);
+      }
+      M >>= 4 * hh;
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int kk = 32 * mb + 8 * (r >> 2) + (r & 3);
+          if (!((M >> kk) & 1ull)) sacc[mb][r] = -INFINITY;
+        }
+    }
+
+    // online softmax (exp2 domain)
+    float mx = -INFINITY;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[mb][r]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m_run, mx);
+    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+    const float alpha = __builtin_amdgcn_exp2f((m_run - m_use) * c);
+    const float nmc = -m_use * c;
+    float psum = 0.f;
+    u32x4 pb[2][2];
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int s = 0; s < 2; ++s)
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[mb][8 * s + 2 * w], c, nmc));
+          const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[mb][8 * s + 2 * w + 1], c, nmc));
+          psum += p0 + p1;
+          pb[mb][s][w] = pack_bf16x2(p0, p1);
+        }
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+          const bf16 *vp = &sV[(32 * db + l32) * VSTR + 32 * mb + 16 * s + 4 * hh];
+          const u32x2 lo = *(const u32x2 *)vp;
+          const u32x2 hi = *(const u32x2 *)(vp + 8);
+          const u32x4 af = u32x4{lo[0], lo[1], hi[0], hi[1]};
+          oacc[db] = mfma32(af, pb[mb][s], oacc[db]);
+        }
+  }
+
+  // ---- epilogue ----------------------------------------------------------------------------
+  if (!wave_active) return;
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const int i = my_row;
+  if (i < r_lo || i >= r_hi) return;
+  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  bf16 *op = a.o + (long long)head * a.so_h + (long long)i * a.so_t;
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii) {
+      u32x2 w;
+      w[0] = pack_bf16x2(oacc[db][4 * ii + 0] * inv, oacc[db][4 * ii + 1] * inv);
+      w[1] = pack_bf16x2(oacc[db][4 * ii + 2] * inv, oacc[db][4 * ii + 3] * inv);
+      *(u32x2 *)(op + 32 * db + 8 * ii + 4 * hh) = w;
+    }
+  if (a.lse && hh == 0)
+    a.lse[(long long)head * a.n + i] = l_tot > 0.f ? m_run * a.scale + logf(l_tot) : -INFINITY;
+}
+
+// ---- host side ---------------------------------------------------------------------------
+
+static int family_bm(int fam) { return (fam == RS_DENSE || fam == RS_ASHAPE) ? 128 : 64; }
+
+static int tiles_of(const rs_unit &u, int bm) { return (u.s1 - 1) / bm - u.s0 / bm + 1; }
+
+size_t attn_ws_bytes(const rs_unit *units, int32_t nunits) {
+  size_t items = 0;
+  for (int i = 0; i < nunits; ++i) items += (size_t)tiles_of(units[i], 64);
+  Arena ar(nullptr, 0);
+  ar.take<DevUnit>((size_t)nunits);
+  ar.take<int>(items);
+  return ar.off + 256;
+}
+
+// Build the dispatch order: items bucketed by key/value head (round-robin workgroup
+// dispatch places workgroup b on XCD b % 8, so the query heads sharing one K/V stream
+// share one XCD's L2), longest query tiles first within a bucket.
+static void build_order(const rs_unit *units, int nunits, int group, int bm,
+                        std::vector<int> &order) {
+  std::vector<std::vector<std::pair<int, int>>> buckets(8);  // (neg cost, item)
+  for (int u = 0; u < nunits; ++u) {
+    const int t0 = units[u].s0 / bm, nt = tiles_of(units[u], bm);
+    const int b = (units[u].head / group) & 7;
+    for (int t = 0; t < nt; ++t) buckets[b].push_back({-(t0 + t), (u << 16) | t});
+  }
+  size_t mx = 0;
+  for (auto &b : buckets) {
+    std::stable_sort(b.begin(), b.end(),
+                     [](const std::pair<int, int> &x, const std::pair<int, int> &y) { return x.first < y.first; });
+    mx = std::max(mx, b.size());
+  }
+  order.clear();
+  for (size_t i = 0; i < mx; ++i)
+    for (int b = 0; b < 8; ++b)
+      if (i < buckets[b].size()) order.push_back(buckets[b][i].second);
+}
+
+template <int D, int NW, int PAT>
+static hipError_t launch_pat(int dtype, const AttnArgs &a, int nitems, hipStream_t st) {
+  if (dtype == RS_BF16)
+    hipLaunchKernelGGL((attn_fwd_kernel<D, NW, PAT, bf16>), dim3(nitems), dim3(NW * 64), 0, st, a);
+  else
+    hipLaunchKernelGGL((attn_fwd_kernel<D, NW, PAT, float>), dim3(nitems), dim3(NW * 64), 0, st, a);
+  return hipGetLastError();
+}
+
+template <int D>
+static hipError_t launch_d(int fam, int dtype, const AttnArgs &a, int nitems, hipStream_t st) {
+  switch (fam) {
+    case RS_DENSE: return launch_pat<D, 4, P_DENSE>(dtype, a, nitems, st);
+    case RS_ASHAPE: return launch_pat<D, 4, P_ASHAPE>(dtype, a, nitems, st);
+    case RS_VSLASH: return launch_pat<D, 2, P_VS>(dtype, a, nitems, st);
+    default: return launch_pat<D, 2, P_BS>(dtype, a, nitems, st);
+  }
+}
+
+// Shared entry of the dense and sparse calls (arguments validated by the caller).
+rs_status attn_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int32_t nunits,
+                      int fam, const rs_candidate *cand, int cand_local,
+                      const rs_index_set *idx, void *o, int64_t so_h, int64_t so_t, float *lse,
+                      void *ws, size_t ws_bytes, hipStream_t st) {
+  if (nunits == 0) return RS_OK;
+  const int bm = family_bm(fam);
+  const int group = qkv->hq / qkv->hkv;
+  std::vector<int> order;
+  build_order(units, nunits, group, bm, order);
+  const size_t need = attn_ws_bytes(units, nunits);
+  if (!ws || ws_bytes < need)
+    return fail(RS_ERR_WORKSPACE, "attention workspace too small: need " + std::to_string(need) +
+                                      " bytes, got " + std::to_string(ws_bytes));
+  // host staging: [DevUnit x nunits][order]
+  Arena ar(ws, ws_bytes);
+  DevUnit *d_units = ar.take<DevUnit>((size_t)nunits);
+  int *d_order = ar.take<int>(order.size());
+  const size_t off_order = (char *)d_order - (char *)ws;
+  std::vector<char> stage(off_order + order.size() * sizeof(int));
+  DevUnit *h_units = (DevUnit *)stage.data();
+  for (int u = 0; u < nunits; ++u) {
+    h_units[u] = DevUnit{units[u].head, units[u].s0, units[u].s1, cand_local, units[u].slot, 0, 0, 0};
+  }
+  memcpy(stage.data() + off_order, order.data(), order.size() * sizeof(int));
+  RS_HIP(hipMemcpyAsync(ws, stage.data(), stage.size(), hipMemcpyHostToDevice, st));
+
+  AttnArgs a{};
+  a.q = qkv->q; a.k = qkv->k; a.v = qkv->v;
+  a.sq_h = qkv->sq_h; a.sq_t = qkv->sq_t; a.sk_h = qkv->sk_h; a.sk_t = qkv->sk_t;
+  a.sv_h = qkv->sv_h; a.sv_t = qkv->sv_t;
+  a.o = (bf16 *)o; a.so_h = so_h; a.so_t = so_t; a.lse = lse;
+  a.n = qkv->n; a.group = group; a.scale = scale; a.c = scale * kLog2e;
+  a.units = d_units; a.order = d_order;
+  if (fam == RS_ASHAPE) { a.sink = cand->a; a.window = cand->b; }
+  if (fam == RS_VSLASH) {
+    a.vs_vsorted = idx->vs_vsorted; a.vs_dsorted = idx->vs_dsorted; a.vs_count = idx->vs_count;
+    a.vs_vbits = idx->vs_vbits; a.vs_dbits = idx->vs_dbits;
+    a.nv_max = idx->nv_max; a.ns_max = idx->ns_max; a.nwords = idx->nwords; a.ncand_vs = idx->ncand_vs;
+  }
+  if (fam == RS_BSPARSE) {
+    a.bs_sorted = idx->bs_sorted; a.bs_count = idx->bs_count;
+    a.k_max = idx->k_max; a.nb = idx->nb; a.ncand_bs = idx->ncand_bs;
+  }
+  hipError_t e = qkv->d == 128 ? launch_d<128>(fam, qkv->dtype, a, (int)order.size(), st)
+                               : launch_d<64>(fam, qkv->dtype, a, (int)order.size(), st);
+  if (e != hipSuccess) return hip_check(e, "attention kernel launch");
+  return RS_OK;
+}
+
+}  // namespace rs

@@ -1,0 +1,632 @@
+// Shared attention probe (Sec. 3.2, Eq. 3 with token-resolution sampled rows) and the
+// block-mean estimator of the block-sparse builder (Sec. 3.1), for gfx950.
+//
+// For each unit (query head h, rows [s0, s1)) the sampled rows I = R u U u Bd are scored
+// exactly against keys [0, s1):
+//   pass 1  row statistics: max_j l_ij and sum_j exp(l_ij - max) over j <= i;
+//   pass 2  normalised a_ij reduced into col[j] = sum_{i in R} a_ij,
+//           diag[t] = sum_{i in R} a_{i,i-t}, and per row the 64-key block entropy and
+//           the local-band mass;
+//   pass 3  (coverage) m_i(c) = sum_{j in S_i(c)} a_ij for every candidate c.
+// Logit tiles are bf16 MFMA products (S^T = K_tile x Q_rows^T, one lane per sampled row),
+// statistics fp32.  Every cross-workgroup reduction goes through per-chunk partials
+// summed in a fixed order, so results are deterministic.
+//
+// Block-mean estimator: qbar/kbar = means of 64-row blocks (last block over its actual
+// rows), L_bs[h][bq][bk] = qbar_bq . kbar_bk * scale for bk <= bq (packed lower triangle).
+#include <algorithm>
+#include <cstring>
+#include <vector>
+
+#include "common.h"
+
+namespace rs {
+
+constexpr int kProbeMaxRows = 256;  // sampled rows per unit
+constexpr int kChunk = 256;         // keys per workgroup in passes 2 and 3
+constexpr int kMaxCand = 16;
+
+struct ProbeUnit {
+  int head, s0, s1, nrows;  // nrows = sampled rows actually present
+  int r0;                   // first recent row (R = [r0, s1)), nR = s1 - r0
+  int nR, pad0, pad1;
+};
+
+struct CandDev {
+  int fam, a, b, cl;  // cl = index among candidates of the same family
+};
+
+struct ProbeArgs {
+  const void *q, *k;
+  long long sq_h, sq_t, sk_h, sk_t;
+  int n, group, rmax, nchunks;
+  float c, scale;
+  int local_w;
+  const ProbeUnit *units;
+  const int *rows, *subset;
+  float *row_max, *row_sum;
+  // pass 2 partials / outputs
+  float *col, *diag_part, *ent_part, *loc_part;
+  int diag_w;  // width of a diagonal partial row (kChunk + rmax)
+  // pass 3
+  int ncand;
+  CandDev cand[kMaxCand];
+  const uint32_t *vs_vbits, *vs_dbits;
+  int nwords, ncand_vs;
+  const uint32_t *bs_bits;
+  int nb, nbw, ncand_bs;
+  float *cov_part;
+};
+
+// K rows [k0 + 32 mb + l32] as MFMA A fragments, straight from global memory.
+template <int D, typename InT>
+__device__ __forceinline__ void load_k_frag(const InT *Kp, long long sk_t, int n, int k0, int l32,
+                                            int hh, u32x4 (&kf)[2][D / 16]) {
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb) {
+    const int j = k0 + 32 * mb + l32;
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) {
+      kf[mb][ks] = u32x4{0u, 0u, 0u, 0u};
+      if (j < n) kf[mb][ks] = load8<InT>(Kp + (long long)j * sk_t + 16 * ks + 8 * hh);
+    }
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void qk_tile(const u32x4 (&kf)[2][D / 16], const u32x4 (&qf)[D / 16],
+                                        f32x16 (&s)[2]) {
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s[mb][r] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) s[mb] = mfma32(kf[mb][ks], qf[ks], s[mb]);
+  }
+}
+
+// Orders this wave's LDS writes before its following LDS reads by other lanes.
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// key offset within a 64-key tile of accumulator element (mb, r) for lane half hh
+__device__ __forceinline__ int acc_key(int mb, int r, int hh) {
+  return 32 * mb + 8 * (r >> 2) + 4 * hh + (r & 3);
+}
+
+// ---- pass 1: row statistics -----------------------------------------------------------------
+// grid: (row block, unit); 4 waves split the key tiles of the unit round-robin.
+template <int D, typename InT>
+__global__ void __launch_bounds__(256) probe_stats_kernel(const ProbeArgs a) {
+  const int rb = blockIdx.x, u = blockIdx.y;
+  const ProbeUnit U = a.units[u];
+  if (32 * rb >= U.nrows) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, hh = lane >> 5;
+  const int ridx = 32 * rb + l32;
+  const int row = ridx < U.nrows ? a.rows[(long long)u * a.rmax + ridx] : -1;
+  int maxrow = 0;
+  for (int x = 32 * rb; x < min(U.nrows, 32 * rb + 32); ++x) maxrow = max(maxrow, a.rows[(long long)u * a.rmax + x]);
+  const InT *Qp = (const InT *)a.q + (long long)U.head * a.sq_h;
+  const InT *Kp = (const InT *)a.k + (long long)(U.head / a.group) * a.sk_h;
+  u32x4 qf[D / 16];
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) {
+    qf[ks] = u32x4{0u, 0u, 0u, 0u};
+    if (row >= 0) qf[ks] = load8<InT>(Qp + (long long)row * a.sq_t + 16 * ks + 8 * hh);
+  }
+  float m_run = -INFINITY, l_run = 0.f;
+  const int ntile = (maxrow >> 6) + 1;
+  for (int kt = wave; kt < ntile; kt += 4) {
+    u32x4 kf[2][D / 16];
+    load_k_frag<D, InT>(Kp, a.sk_t, a.n, 64 * kt, l32, hh, kf);
+    f32x16 s[2];
+    qk_tile<D>(kf, qf, s);
+    float mx = -INFINITY;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int j = 64 * kt + acc_key(mb, r, hh);
+        if (j > row) s[mb][r] = -INFINITY;
+        mx = fmaxf(mx, s[mb][r]);
+      }
+    const float m_new = fmaxf(m_run, mx);
+    const float m_use = m_new == -INFINITY ? 0.f : m_new;
+    float ps = 0.f;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) ps += __builtin_amdgcn_exp2f((s[mb][r] - m_use) * a.c);
+    l_run = l_run * __builtin_amdgcn_exp2f((m_run - m_use) * a.c) + ps;
+    m_run = m_new;
+  }
+  // combine the two lane halves, then the four waves
+  __shared__ float sm[4][32], sl[4][32];
+  {
+    const float mo = __shfl_xor(m_run, 32), lo = __shfl_xor(l_run, 32);
+    const float mm = fmaxf(m_run, mo);
+    const float mu = mm == -INFINITY ? 0.f : mm;
+    const float ll = l_run * __builtin_amdgcn_exp2f((m_run - mu) * a.c) + lo * __builtin_amdgcn_exp2f((mo - mu) * a.c);
+    if (hh == 0) {
+      sm[wave][l32] = mm;
+      sl[wave][l32] = ll;
+    }
+  }
+  __syncthreads();
+  if (tid < 32 && ridx < U.nrows) {
+    float M = -INFINITY;
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, sm[w][tid]);
+    float L = 0.f;
+    for (int w = 0; w < 4; ++w) L += sl[w][tid] * __builtin_amdgcn_exp2f((sm[w][tid] - M) * a.c);
+    a.row_max[(long long)u * a.rmax + ridx] = M * a.scale;
+    a.row_sum[(long long)u * a.rmax + ridx] = L;
+  }
+}
+
+// ---- passes 2 and 3: normalised probabilities over one 256-key chunk --------------------
+// grid: (chunk, unit); wave w handles row blocks w, w+4, ... against the chunk's 4 tiles.
+template <int D, typename InT, bool COVER>
+__global__ void __launch_bounds__(256) probe_chunk_kernel(const ProbeArgs a) {
+  const int ch = blockIdx.x, u = blockIdx.y;
+  const ProbeUnit U = a.units[u];
+  const int c0 = ch * kChunk;
+  if (c0 >= U.s1) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, hh = lane >> 5;
+  const InT *Qp = (const InT *)a.q + (long long)U.head * a.sq_h;
+  const InT *Kp = (const InT *)a.k + (long long)(U.head / a.group) * a.sk_h;
+  const int nrb = (U.nrows + 31) / 32;
+
+  __shared__ float sP[4][32][65];                // per-wave probability tile [row][key]
+  __shared__ int sRows[4][32];                   // sampled rows of each wave's block
+  __shared__ float sCol[4][kChunk];              // per-wave column sums
+  __shared__ float sDg[4][kChunk + kProbeMaxRows];  // per-wave diagonal partials
+  const int dw = kChunk + U.nR;                  // diagonals touched by R rows in this chunk
+  const int dbase = U.r0 - (c0 + kChunk - 1);    // smallest such diagonal
+  if constexpr (!COVER) {
+    for (int x = tid; x < 4 * kChunk; x += 256) (&sCol[0][0])[x] = 0.f;
+    for (int x = lane; x < dw; x += 64) sDg[wave][x] = 0.f;
+  }
+  __syncthreads();
+
+  for (int rb = wave; rb < nrb; rb += 4) {
+    const int ridx = 32 * rb + l32;
+    const bool rvalid = ridx < U.nrows;
+    const long long rofs = (long long)u * a.rmax + ridx;
+    const int row = rvalid ? a.rows[rofs] : -1;
+    const int sub = rvalid ? a.subset[rofs] : -1;
+    const float nmc = rvalid ? -a.row_max[rofs] * kLog2e : 0.f;
+    const float invl = rvalid ? 1.f / a.row_sum[rofs] : 0.f;
+    if (hh == 0) sRows[wave][l32] = row;
+    wave_sync();
+    const int rbmax = sRows[wave][min(31, U.nrows - 1 - 32 * rb)];  // rows ascending
+    // position within the block of its first recent row (recent rows are the last nR)
+    const int rfirst = max(0, (U.nrows - U.nR) - 32 * rb);
+    if (rbmax < c0) {  // no row of the block sees this chunk (wave-uniform)
+      wave_sync();
+      continue;
+    }
+    u32x4 qf[D / 16];
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) {
+      qf[ks] = u32x4{0u, 0u, 0u, 0u};
+      if (rvalid) qf[ks] = load8<InT>(Qp + (long long)row * a.sq_t + 16 * ks + 8 * hh);
+    }
+    float ent = 0.f, loc = 0.f;
+    float cov[kMaxCand];
+#pragma unroll
+    for (int c = 0; c < kMaxCand; ++c) cov[c] = 0.f;
+    const bool isR = sub == 0;
+    // does the block hold recent rows? (wave-uniform)
+    const bool blockR = __ballot(isR && hh == 0) != 0ull;
+
+    for (int tt = 0; tt < kChunk / 64; ++tt) {
+      const int k0 = c0 + 64 * tt;
+      if (k0 > rbmax) break;
+      u32x4 kf[2][D / 16];
+      load_k_frag<D, InT>(Kp, a.sk_t, a.n, k0, l32, hh, kf);
+      f32x16 s[2];
+      qk_tile<D>(kf, qf, s);
+      float p[2][16];
+      float bsum = 0.f, lsum = 0.f;
+      const int lo_local = row - a.local_w + 1;  // keys >= lo_local are in the local band
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int j = k0 + acc_key(mb, r, hh);
+          const float v = (rvalid && j <= row) ? __builtin_amdgcn_exp2f(fmaf(s[mb][r], a.c, nmc)) * invl : 0.f;
+          p[mb][r] = v;
+          bsum += v;
+          if (j >= lo_local) lsum += v;
+        }
+      if constexpr (!COVER) {
+        bsum += __shfl_xor(bsum, 32);
+        if (bsum > 0.f) ent -= bsum * logf(bsum);
+        loc += lsum;
+        if (blockR) {
+#pragma unroll
+          for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) sP[wave][l32][acc_key(mb, r, hh)] = isR ? p[mb][r] : 0.f;
+          wave_sync();
+          // column sums: lane = key
+          {
+            float cs = 0.f;
+            for (int rr = 0; rr < 32; ++rr) cs += sP[wave][rr][lane];
+            sCol[wave][64 * tt + lane] += cs;
+          }
+          // diagonal sums over the block's recent rows (consecutive, starting at i_first):
+          // diagonal t = i - j is stored at x = t - dbase
+          {
+            const int i_first = max(U.r0, sRows[wave][0]);
+            const int i_last = sRows[wave][min(31, U.nrows - 1 - 32 * rb)];
+            const int xlo = i_first - k0 - 63 - dbase;
+            const int xn = i_last - i_first + 64;
+            for (int xx = lane; xx < xn; xx += 64) {
+              const int x = xlo + xx;
+              const int t = x + dbase;
+              float ds = 0.f;
+              for (int i2 = i_first; i2 <= i_last; ++i2) {
+                const int kk = i2 - t - k0;
+                if (kk >= 0 && kk < 64) ds += sP[wave][i2 - i_first + rfirst][kk];
+              }
+              if (x >= 0 && x < dw) sDg[wave][x] += ds;
+            }
+          }
+          wave_sync();
+        }
+      } else {
+        const int bq = row >> 6;
+        const int kt = k0 >> 6;
+#pragma unroll
+        for (int c = 0; c < kMaxCand; ++c) {
+          if (c >= a.ncand) break;
+          const CandDev cd = a.cand[c];
+          if (cd.fam == RS_DENSE) continue;
+          uint64_t M;
+          if (cd.fam == RS_ASHAPE) {
+            M = prefix_mask(cd.a - k0) | ~prefix_mask(row - cd.b + 1 - k0);
+          } else if (cd.fam == RS_VSLASH) {
+            const long long vrow = ((long long)u * a.ncand_vs + cd.cl) * a.nwords;
+            const uint64_t md = __builtin_bitreverse64(bits64_at(a.vs_dbits + vrow, a.nwords, row - k0 - 63));
+            const uint64_t mv = bits64_at(a.vs_vbits + vrow, a.nwords, k0);
+            M = md | mv;
+          } else {
+            const long long brow = (((long long)U.head * a.ncand_bs + cd.cl) * a.nb + (rvalid ? bq : 0)) * a.nbw;
+            const bool in = rvalid && ((a.bs_bits[brow + (kt >> 5)] >> (kt & 31)) & 1u);
+            M = in ? ~0ull : 0ull;
+          }
+          M >>= 4 * hh;
+          float cs = 0.f;
+#pragma unroll
+          for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              if ((M >> (32 * mb + 8 * (r >> 2) + (r & 3))) & 1ull) cs += p[mb][r];
+          cov[c] += cs;
+        }
+      }
+    }
+    if constexpr (!COVER) {
+      loc += __shfl_xor(loc, 32);
+      if (rvalid && hh == 0) {
+        const long long o = ((long long)u * a.nchunks + ch) * a.rmax + ridx;
+        a.ent_part[o] = ent;
+        a.loc_part[o] = loc;
+      }
+    } else {
+      for (int c = 0; c < a.ncand; ++c) {
+        const float tot = cov[c] + __shfl_xor(cov[c], 32);
+        if (rvalid && hh == 0) a.cov_part[(((long long)u * a.nchunks + ch) * a.ncand + c) * a.rmax + ridx] = tot;
+      }
+    }
+  }
+  if constexpr (!COVER) {
+    __syncthreads();
+    for (int x = tid; x < kChunk; x += 256) {
+      const int j = c0 + x;
+      if (j < a.n) {
+        const float v = (j < U.s1) ? sCol[0][x] + sCol[1][x] + sCol[2][x] + sCol[3][x] : 0.f;
+        a.col[(long long)u * a.n + j] = v;
+      }
+    }
+    for (int x = tid; x < dw; x += 256)
+      a.diag_part[((long long)u * a.nchunks + ch) * a.diag_w + x] = sDg[0][x] + sDg[1][x] + sDg[2][x] + sDg[3][x];
+  }
+}
+
+// ---- finalisation of pass 2: diagonals, descriptors, zero tails -------------------------
+__global__ void probe_finish_kernel(const ProbeArgs a, float *diag, float *entropy, float *local) {
+  const int u = blockIdx.y;
+  const ProbeUnit U = a.units[u];
+  const int x = blockIdx.x * blockDim.x + threadIdx.x;
+  if (x < a.n) {
+    float v = 0.f;
+    if (x < U.s1 && U.nR > 0) {
+      // chunks whose diagonal range [r0 - c0 - 255, r0 + nR - 1 - c0] holds t = x
+      const int chi = min((U.r0 + U.nR - 1 - x) / kChunk, (U.s1 - 1) / kChunk);
+      const int clo_num = U.r0 - (kChunk - 1) - x;
+      const int clo = clo_num <= 0 ? 0 : (clo_num + kChunk - 1) / kChunk;
+      for (int ch = clo; ch <= chi; ++ch) {
+        const int dbase = U.r0 - (ch * kChunk + kChunk - 1);
+        const int xi = x - dbase;
+        if (xi >= 0 && xi < kChunk + U.nR) v += a.diag_part[((long long)u * a.nchunks + ch) * a.diag_w + xi];
+      }
+    }
+    diag[(long long)u * a.n + x] = v;
+    if (x >= U.s1) a.col[(long long)u * a.n + x] = 0.f;
+  }
+  if (x < U.nrows) {
+    const int row = a.rows[(long long)u * a.rmax + x];
+    const int nch = (row >> 8) + 1;  // chunks holding keys <= row
+    float e = 0.f, l = 0.f;
+    for (int ch = 0; ch < nch; ++ch) {
+      const long long o = ((long long)u * a.nchunks + ch) * a.rmax + x;
+      e += a.ent_part[o];
+      l += a.loc_part[o];
+    }
+    const int nvis = row / 64 + 1;
+    entropy[(long long)u * a.rmax + x] = nvis > 1 ? e / logf((float)nvis) : 0.f;
+    local[(long long)u * a.rmax + x] = l;
+  }
+}
+
+__global__ void cover_finish_kernel(const ProbeArgs a, float *cov_rows, float *cov) {
+  const int u = blockIdx.y, c = blockIdx.x;
+  const ProbeUnit U = a.units[u];
+  __shared__ float sm[kProbeMaxRows];
+  const int x = threadIdx.x;  // blockDim = kProbeMaxRows
+  float m = 0.f;
+  if (x < U.nrows) {
+    const int row = a.rows[(long long)u * a.rmax + x];
+    if (a.cand[c].fam == RS_DENSE) {
+      m = 1.f;
+    } else {
+      const int nch = (row >> 8) + 1;
+      for (int ch = 0; ch < nch; ++ch) m += a.cov_part[(((long long)u * a.nchunks + ch) * a.ncand + c) * a.rmax + x];
+    }
+    cov_rows[((long long)u * a.ncand + c) * a.rmax + x] = m;
+  }
+  sm[x] = m;
+  __syncthreads();
+  if (x == 0) {
+    float tot = 0.f, sub[3] = {0.f, 0.f, 0.f};
+    int cnt[3] = {0, 0, 0};
+    for (int r = 0; r < U.nrows; ++r) {
+      const int s = a.subset[(long long)u * a.rmax + r];
+      tot += sm[r];
+      if (s >= 0 && s < 3) {
+        sub[s] += sm[r];
+        cnt[s]++;
+      }
+    }
+    float *o = cov + ((long long)u * a.ncand + c) * 4;
+    o[0] = U.nrows ? tot / U.nrows : 0.f;
+    for (int s = 0; s < 3; ++s) o[1 + s] = cnt[s] ? sub[s] / cnt[s] : 0.f;
+  }
+}
+
+// ---- block-mean estimator ----------------------------------------------------------------
+template <typename InT>
+__global__ void block_pool_kernel(const InT *x, long long s_h, long long s_t, int n, int d, float *out) {
+  const int b = blockIdx.x, h = blockIdx.y;  // blockDim = d
+  const int t = threadIdx.x;
+  const int r0 = b * 64, r1 = min(n, r0 + 64);
+  const InT *p = x + (long long)h * s_h + t;
+  float acc = 0.f;
+  for (int r = r0; r < r1; ++r) acc += (float)p[(long long)r * s_t];
+  out[((long long)h * gridDim.x + b) * d + t] = acc / (float)(r1 - r0);
+}
+
+// L[h][bq][bk] = qbar . kbar * scale for bk <= bq; 64 x 64 output tiles, fp32 FMA.
+__global__ void __launch_bounds__(256) block_logits_kernel(const float *qbar, const float *kbar, int nb, int d,
+                                                           int group, float scale, float *lbs) {
+  const int h = blockIdx.y;
+  // decode lower-triangular tile index
+  int tq = 0;
+  int t = blockIdx.x;
+  while (t > tq) {
+    t -= tq + 1;
+    ++tq;
+  }
+  const int tk = t;
+  const int nbt = (nb + 63) / 64;
+  if (tq >= nbt) return;
+  __shared__ float sq[32][65], sk[32][65];
+  const int tid = threadIdx.x;
+  const int tx = tid % 16, ty = tid / 16;  // each thread: rows ty*4.., cols tx*4..
+  float acc[4][4] = {};
+  const float *qb = qbar + (long long)h * nb * d;
+  const float *kb = kbar + (long long)(h / group) * nb * d;
+  for (int d0 = 0; d0 < d; d0 += 32) {
+    for (int x = tid; x < 64 * 32; x += 256) {
+      const int r = x / 32, cc = x % 32;
+      const int bq = tq * 64 + r, bk = tk * 64 + r;
+      sq[cc][r] = bq < nb ? qb[(long long)bq * d + d0 + cc] : 0.f;
+      sk[cc][r] = bk < nb ? kb[(long long)bk * d + d0 + cc] : 0.f;
+    }
+    __syncthreads();
+    for (int cc = 0; cc < 32; ++cc) {
+      float qa[4], ka[4];
+      for (int i = 0; i < 4; ++i) qa[i] = sq[cc][ty * 4 + i];
+      for (int j = 0; j < 4; ++j) ka[j] = sk[cc][tx * 4 + j];
+      for (int i = 0; i < 4; ++i)
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(qa[i], ka[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+  float *lh = lbs + (long long)h * ((long long)nb * (nb + 1) / 2);
+  for (int i = 0; i < 4; ++i) {
+    const int bq = tq * 64 + ty * 4 + i;
+    if (bq >= nb) continue;
+    for (int j = 0; j < 4; ++j) {
+      const int bk = tk * 64 + tx * 4 + j;
+      if (bk > bq) continue;
+      lh[(long long)bq * (bq + 1) / 2 + bk] = acc[i][j] * scale;
+    }
+  }
+}
+
+// ---- host side ---------------------------------------------------------------------------
+
+// Sampled rows of one unit (ascending) with subset labels; see rs_probe_cfg.
+static void sample_rows(int s0, int s1, const rs_probe_cfg &cfg, std::vector<int> &rows,
+                        std::vector<int> &lab, int &r0) {
+  std::vector<std::pair<int, int>> v;
+  r0 = std::max(s0, s1 - cfg.r_rec);
+  for (int i = r0; i < s1; ++i) v.push_back({i, 0});
+  std::vector<int> uni;
+  const long long L = s1 - s0;
+  for (int t = 0; t < cfg.r_uni && L > 0; ++t) {
+    const int i = s0 + (int)(((2LL * t + 1) * L) / (2LL * cfg.r_uni));
+    if (i >= r0) continue;
+    if (!uni.empty() && uni.back() == i) continue;
+    uni.push_back(i);
+  }
+  for (int i : uni) v.push_back({i, 1});
+  for (int t = 0; t < cfg.r_bnd; ++t) {
+    const int i = std::max(s0, 64) + t;
+    if (i < s0 || i >= s1 || i >= r0) continue;
+    if (std::find(uni.begin(), uni.end(), i) != uni.end()) continue;
+    v.push_back({i, 2});
+  }
+  std::sort(v.begin(), v.end());
+  rows.clear();
+  lab.clear();
+  for (auto &p : v) {
+    rows.push_back(p.first);
+    lab.push_back(p.second);
+  }
+}
+
+static int rmax_of(const rs_probe_cfg *cfg) { return cfg->r_rec + cfg->r_uni + cfg->r_bnd; }
+
+size_t probe_ws_bytes(const rs_qkv *qkv, int32_t nunits, const rs_probe_cfg *cfg) {
+  const int rmax = rmax_of(cfg);
+  const long long nchunks = (qkv->n + kChunk - 1) / kChunk;
+  const int nb = (qkv->n + 63) / 64;
+  Arena ar(nullptr, 0);
+  ar.take<ProbeUnit>(nunits);
+  ar.take<float>((size_t)nunits * nchunks * (kChunk + rmax));     // diag partials
+  ar.take<float>((size_t)nunits * nchunks * rmax * 2);            // entropy / local partials
+  ar.take<float>((size_t)nunits * nchunks * rmax * kMaxCand);     // coverage partials
+  if (cfg->flags & RS_PROBE_BLOCKMEAN) {
+    ar.take<float>((size_t)qkv->hq * nb * qkv->d);
+    ar.take<float>((size_t)qkv->hkv * nb * qkv->d);
+  }
+  return ar.off + 256;
+}
+
+template <int D, typename InT>
+static hipError_t launch_rows(const ProbeArgs &pa, int nunits, int mode, float *diag, float *ent, float *loc,
+                              float *cov_rows, float *cov, hipStream_t st) {
+  if (mode == 0) {
+    hipLaunchKernelGGL((probe_stats_kernel<D, InT>), dim3((pa.rmax + 31) / 32, nunits), dim3(256), 0, st, pa);
+    hipLaunchKernelGGL((probe_chunk_kernel<D, InT, false>), dim3(pa.nchunks, nunits), dim3(256), 0, st, pa);
+    hipLaunchKernelGGL(probe_finish_kernel, dim3((std::max(pa.n, pa.rmax) + 255) / 256, nunits), dim3(256), 0, st,
+                       pa, diag, ent, loc);
+  } else {
+    hipLaunchKernelGGL((probe_chunk_kernel<D, InT, true>), dim3(pa.nchunks, nunits), dim3(256), 0, st, pa);
+    hipLaunchKernelGGL(cover_finish_kernel, dim3(pa.ncand, nunits), dim3(kProbeMaxRows), 0, st, pa, cov_rows, cov);
+  }
+  return hipGetLastError();
+}
+
+rs_status probe_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int32_t nunits,
+                       const rs_probe_cfg *cfg, const rs_candidate *grid, int32_t ncand,
+                       const rs_index_set *idx, void *ws, size_t ws_bytes, rs_probe_out *out, hipStream_t st) {
+  const int rmax = rmax_of(cfg);
+  const int nchunks = (qkv->n + kChunk - 1) / kChunk;
+  const int nb = (qkv->n + 63) / 64;
+  const size_t need = probe_ws_bytes(qkv, nunits, cfg);
+  if (!ws || ws_bytes < need)
+    return fail(RS_ERR_WORKSPACE, "probe workspace too small: need " + std::to_string(need));
+  Arena ar(ws, ws_bytes);
+  ProbeUnit *d_units = ar.take<ProbeUnit>(nunits);
+  float *diag_part = ar.take<float>((size_t)nunits * nchunks * (kChunk + rmax));
+  float *ent_part = ar.take<float>((size_t)nunits * nchunks * rmax);
+  float *loc_part = ar.take<float>((size_t)nunits * nchunks * rmax);
+  float *cov_part = ar.take<float>((size_t)nunits * nchunks * rmax * kMaxCand);
+  float *qbar = nullptr, *kbar = nullptr;
+  if (cfg->flags & RS_PROBE_BLOCKMEAN) {
+    qbar = ar.take<float>((size_t)qkv->hq * nb * qkv->d);
+    kbar = ar.take<float>((size_t)qkv->hkv * nb * qkv->d);
+  }
+  // sampled rows are computed here and uploaded (scores mode), or re-derived (coverage)
+  std::vector<ProbeUnit> hu(nunits);
+  std::vector<int> hrows((size_t)nunits * rmax, -1), hsub((size_t)nunits * rmax, -1), hn((size_t)nunits * 3, 0);
+  for (int u = 0; u < nunits; ++u) {
+    std::vector<int> rows, lab;
+    int r0;
+    sample_rows(units[u].s0, units[u].s1, *cfg, rows, lab, r0);
+    hu[u] = ProbeUnit{units[u].head, units[u].s0, units[u].s1, (int)rows.size(), r0, units[u].s1 - r0, 0, 0};
+    for (size_t x = 0; x < rows.size(); ++x) {
+      hrows[(size_t)u * rmax + x] = rows[x];
+      hsub[(size_t)u * rmax + x] = lab[x];
+      hn[(size_t)u * 3 + lab[x]]++;
+    }
+  }
+  RS_HIP(hipMemcpyAsync(d_units, hu.data(), hu.size() * sizeof(ProbeUnit), hipMemcpyHostToDevice, st));
+  const bool cover = idx != nullptr;
+  if (!cover) {
+    RS_HIP(hipMemcpyAsync(out->rows, hrows.data(), hrows.size() * 4, hipMemcpyHostToDevice, st));
+    RS_HIP(hipMemcpyAsync(out->subset, hsub.data(), hsub.size() * 4, hipMemcpyHostToDevice, st));
+    RS_HIP(hipMemcpyAsync(out->nsub, hn.data(), hn.size() * 4, hipMemcpyHostToDevice, st));
+  }
+  ProbeArgs pa{};
+  pa.q = qkv->q; pa.k = qkv->k;
+  pa.sq_h = qkv->sq_h; pa.sq_t = qkv->sq_t; pa.sk_h = qkv->sk_h; pa.sk_t = qkv->sk_t;
+  pa.n = qkv->n; pa.group = qkv->hq / qkv->hkv; pa.rmax = rmax; pa.nchunks = nchunks;
+  pa.c = scale * kLog2e; pa.scale = scale; pa.local_w = cfg->local_w;
+  pa.units = d_units; pa.rows = out->rows; pa.subset = out->subset;
+  pa.row_max = out->row_max; pa.row_sum = out->row_sum;
+  pa.col = out->col; pa.diag_part = diag_part; pa.ent_part = ent_part; pa.loc_part = loc_part;
+  pa.diag_w = kChunk + rmax;
+  pa.cov_part = cov_part;
+  if (cover) {
+    pa.ncand = ncand;
+    int nvs = 0, nbs = 0;
+    for (int c = 0; c < ncand; ++c) {
+      int cl = 0;
+      if (grid[c].fam == RS_VSLASH) cl = nvs++;
+      if (grid[c].fam == RS_BSPARSE) cl = nbs++;
+      pa.cand[c] = CandDev{grid[c].fam, grid[c].a, grid[c].b, cl};
+    }
+    pa.vs_vbits = idx->vs_vbits; pa.vs_dbits = idx->vs_dbits; pa.nwords = idx->nwords; pa.ncand_vs = idx->ncand_vs;
+    pa.bs_bits = idx->bs_bits; pa.nb = idx->nb; pa.nbw = idx->nbw; pa.ncand_bs = idx->ncand_bs;
+  }
+  if (cfg->flags & RS_PROBE_ROWS || cover) {
+    hipError_t e;
+    const int mode = cover ? 1 : 0;
+    if (qkv->d == 128)
+      e = qkv->dtype == RS_BF16 ? launch_rows<128, bf16>(pa, nunits, mode, out->diag, out->entropy, out->local, out->cov_rows, out->cov, st)
+                                : launch_rows<128, float>(pa, nunits, mode, out->diag, out->entropy, out->local, out->cov_rows, out->cov, st);
+    else
+      e = qkv->dtype == RS_BF16 ? launch_rows<64, bf16>(pa, nunits, mode, out->diag, out->entropy, out->local, out->cov_rows, out->cov, st)
+                                : launch_rows<64, float>(pa, nunits, mode, out->diag, out->entropy, out->local, out->cov_rows, out->cov, st);
+    if (e != hipSuccess) return hip_check(e, "probe kernels");
+  }
+  if (!cover && (cfg->flags & RS_PROBE_BLOCKMEAN)) {
+    if (qkv->dtype == RS_BF16) {
+      hipLaunchKernelGGL(block_pool_kernel<bf16>, dim3(nb, qkv->hq), dim3(qkv->d), 0, st, (const bf16 *)qkv->q,
+                         (long long)qkv->sq_h, (long long)qkv->sq_t, qkv->n, qkv->d, qbar);
+      hipLaunchKernelGGL(block_pool_kernel<bf16>, dim3(nb, qkv->hkv), dim3(qkv->d), 0, st, (const bf16 *)qkv->k,
+                         (long long)qkv->sk_h, (long long)qkv->sk_t, qkv->n, qkv->d, kbar);
+    } else {
+      hipLaunchKernelGGL(block_pool_kernel<float>, dim3(nb, qkv->hq), dim3(qkv->d), 0, st, (const float *)qkv->q,
+                         (long long)qkv->sq_h, (long long)qkv->sq_t, qkv->n, qkv->d, qbar);
+      hipLaunchKernelGGL(block_pool_kernel<float>, dim3(nb, qkv->hkv), dim3(qkv->d), 0, st, (const float *)qkv->k,
+                         (long long)qkv->sk_h, (long long)qkv->sk_t, qkv->n, qkv->d, kbar);
+    }
+    const int nbt = (nb + 63) / 64;
+    hipLaunchKernelGGL(block_logits_kernel, dim3(nbt * (nbt + 1) / 2, qkv->hq), dim3(256), 0, st, qbar, kbar, nb,
+                       qkv->d, qkv->hq / qkv->hkv, scale, out->lbs);
+    RS_HIP(hipGetLastError());
+  }
+  return RS_OK;
+}
+
+}  // namespace rs

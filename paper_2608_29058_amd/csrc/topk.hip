@@ -1,0 +1,283 @@
+// Candidate index construction (Sec. 3.1) for gfx950: deterministic top-k selection.
+//
+// Every selection uses one total order: score descending (scores mapped to
+// order-preserving 32-bit keys, so -0.0 ranks below +0.0), then position ascending.
+// The k-th key is found by a 4-pass radix select over 8-bit digits (LDS histograms with
+// integer atomics); elements above it are taken, and among elements equal to it the
+// lowest positions are taken through an ordered block scan.  Sets are emitted as bitmaps
+// and as ascending lists.
+//
+//   vertical-slash, per unit and candidate (n_v, n_s):
+//     V = top n_v columns of col[0, s1);  D = {0} + top (n_s - 1) diagonals of diag[1, s1)
+//   block-sparse, per query head and query block bq:
+//     ranking {bq} + blocks [0, bq) by pooled score; Sel_k(bq) = first k of the ranking
+#include <algorithm>
+#include <vector>
+
+#include "common.h"
+
+namespace rs {
+
+constexpr int kMaxCandFam = 8;
+
+// inclusive prefix sum of v over the workgroup; returns it, total in *tot
+template <int NT>
+__device__ int block_incl_scan(int v, int *sWave, int *tot) {
+  constexpr int NWV = NT / 64;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) sWave[wave] = x;
+  __syncthreads();
+  int off = 0, all = 0;
+  for (int w = 0; w < NWV; ++w) {
+    const int t = sWave[w];
+    if (w < wave) off += t;
+    all += t;
+  }
+  __syncthreads();
+  *tot = all;
+  return x + off;
+}
+
+// Radix select over keys of vals[0, len): finds the key T of rank K (1-based, descending)
+// and how many elements equal to T are taken.  Requires len > K >= 1.
+template <int NT>
+__device__ void radix_select(const float *vals, int len, int K, uint32_t *T_out, int *take_out, int *sHist,
+                             int *sBcast) {
+  uint32_t prefix = 0, maskhi = 0;
+  int krem = K;
+  for (int byte = 3; byte >= 0; --byte) {
+    for (int b = threadIdx.x; b < 256; b += NT) sHist[b] = 0;
+    __syncthreads();
+    for (int i = threadIdx.x; i < len; i += NT) {
+      const uint32_t key = float_key(vals[i]);
+      if ((key & maskhi) == prefix) atomicAdd(&sHist[(key >> (8 * byte)) & 255u], 1);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int cum = 0, sel = 0;
+      for (int b = 255; b >= 0; --b) {
+        if (cum + sHist[b] >= krem) {
+          sel = b;
+          break;
+        }
+        cum += sHist[b];
+      }
+      sBcast[0] = sel;
+      sBcast[1] = krem - cum;
+    }
+    __syncthreads();
+    prefix |= (uint32_t)sBcast[0] << (8 * byte);
+    maskhi |= 0xffu << (8 * byte);
+    krem = sBcast[1];
+    __syncthreads();
+  }
+  *T_out = prefix;
+  *take_out = krem;
+}
+
+// Calls emit(i) for each selected element index of vals[0, len) (top K in the total order).
+template <int NT, typename F>
+__device__ void select_top(const float *vals, int len, int K, int *sHist, int *sBcast, int *sWave, F emit) {
+  if (K <= 0) return;
+  if (len <= K) {
+    for (int i = threadIdx.x; i < len; i += NT) emit(i);
+    return;
+  }
+  uint32_t T;
+  int take;
+  radix_select<NT>(vals, len, K, &T, &take, sHist, sBcast);
+  for (int i = threadIdx.x; i < len; i += NT)
+    if (float_key(vals[i]) > T) emit(i);
+  // equal keys: lowest positions first
+  int seen = 0;
+  for (int i0 = 0; i0 < len && seen < take; i0 += NT) {
+    const int i = i0 + threadIdx.x;
+    const int f = (i < len && float_key(vals[i]) == T) ? 1 : 0;
+    int tot;
+    const int incl = block_incl_scan<NT>(f, sWave, &tot);
+    if (f && seen + incl - 1 < take) emit(i);
+    seen += tot;
+  }
+}
+
+// ascending list of set bits of bits[0, nwords) -> out, padded with -1 to cap; returns count
+template <int NT>
+__device__ int bits_to_list(const uint32_t *bits, int nwords, int *out, int cap, int *sWave) {
+  constexpr int WPT_MAX = 16;
+  const int wpt = (nwords + NT - 1) / NT;  // contiguous words per thread
+  const int w0 = threadIdx.x * wpt;
+  int cnt = 0;
+  for (int w = w0; w < min(nwords, w0 + wpt); ++w) cnt += __builtin_popcount(bits[w]);
+  int tot;
+  const int incl = block_incl_scan<NT>(cnt, sWave, &tot);
+  int p = incl - cnt;
+  for (int w = w0; w < min(nwords, w0 + wpt); ++w) {
+    uint32_t b = bits[w];
+    while (b) {
+      const int bit = __builtin_ctz(b);
+      b &= b - 1;
+      if (p < cap) out[p] = w * 32 + bit;
+      ++p;
+    }
+  }
+  (void)WPT_MAX;
+  for (int x = tot + threadIdx.x; x < cap; x += NT) out[x] = -1;
+  return tot;
+}
+
+struct VsArgs {
+  const float *col, *diag;
+  int n, nunits, ncand_vs;
+  const int *s1;  // [nunits]
+  int nv[kMaxCandFam], ns[kMaxCandFam];
+  int nv_max, ns_max, nwords;
+  int *vsorted, *dsorted, *count;
+  uint32_t *vbits, *dbits;
+};
+
+// grid: (2 * ncand_vs, nunits); blockIdx.x = array * ncand_vs + candidate (array 0: V, 1: D)
+__global__ void __launch_bounds__(1024) vs_select_kernel(const VsArgs a) {
+  constexpr int NT = 1024;
+  extern __shared__ uint32_t sBits[];  // nwords
+  __shared__ int sHist[256], sBcast[2], sWave[NT / 64];
+  const int arr = blockIdx.x / a.ncand_vs, cl = blockIdx.x % a.ncand_vs;
+  const int u = blockIdx.y;
+  const int s1 = a.s1[u];
+  for (int w = threadIdx.x; w < a.nwords; w += NT) sBits[w] = 0u;
+  __syncthreads();
+  const long long row = (long long)u * a.ncand_vs + cl;
+  if (arr == 0) {
+    const float *vals = a.col + (long long)u * a.n;
+    select_top<NT>(vals, s1, a.nv[cl], sHist, sBcast, sWave,
+                   [&](int i) { atomicOr(&sBits[i >> 5], 1u << (i & 31)); });
+  } else {
+    const float *vals = a.diag + (long long)u * a.n + 1;  // diagonal 0 is forced
+    const int ns = a.ns[cl];
+    if (ns >= 1 && threadIdx.x == 0) atomicOr(&sBits[0], 1u);
+    select_top<NT>(vals, s1 - 1, ns - 1, sHist, sBcast, sWave, [&](int i) {
+      const int t = i + 1;
+      atomicOr(&sBits[t >> 5], 1u << (t & 31));
+    });
+  }
+  __syncthreads();
+  uint32_t *gb = (arr == 0 ? a.vbits : a.dbits) + row * a.nwords;
+  for (int w = threadIdx.x; w < a.nwords; w += NT) gb[w] = sBits[w];
+  int *list = arr == 0 ? a.vsorted + row * a.nv_max : a.dsorted + row * a.ns_max;
+  const int cnt = bits_to_list<NT>(sBits, a.nwords, list, arr == 0 ? a.nv_max : a.ns_max, sWave);
+  if (threadIdx.x == 0) a.count[row * 2 + arr] = cnt;
+}
+
+struct BsArgs {
+  const float *lbs;
+  int nb, hq, ncand_bs, k_max, nbw;
+  int k[kMaxCandFam];
+  int *rank, *sorted, *count;
+  uint32_t *bits;
+};
+
+// grid: (nb, hq); one query block per workgroup
+__global__ void __launch_bounds__(256) bs_select_kernel(const BsArgs a) {
+  constexpr int NT = 256;
+  constexpr int SP = 256;  // sort capacity (k_max <= 256)
+  __shared__ int sHist[256], sBcast[2], sWave[NT / 64], sCnt;
+  __shared__ unsigned long long sKey[SP];
+  __shared__ uint32_t sB[kMaxN / 64 / 32];
+  const int bq = blockIdx.x, h = blockIdx.y;
+  const float *vals = a.lbs + (long long)h * ((long long)a.nb * (a.nb + 1) / 2) + (long long)bq * (bq + 1) / 2;
+  for (int x = threadIdx.x; x < SP; x += NT) sKey[x] = 0ull;
+  if (threadIdx.x == 0) sCnt = 0;
+  __syncthreads();
+  const int K = a.k_max - 1;
+  select_top<NT>(vals, bq, K, sHist, sBcast, sWave, [&](int i) {
+    const int p = atomicAdd(&sCnt, 1);
+    sKey[p] = ((unsigned long long)float_key(vals[i]) << 32) | (unsigned long long)(0xffffffffu - (uint32_t)i);
+  });
+  __syncthreads();
+  // bitonic sort, descending
+  for (int size = 2; size <= SP; size <<= 1)
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int x = threadIdx.x; x < SP / 2; x += NT) {
+        const int lo = 2 * x - (x & (stride - 1));
+        const int hi = lo + stride;
+        const bool desc = ((lo & size) == 0);
+        const unsigned long long A = sKey[lo], B = sKey[hi];
+        if ((A < B) == desc) {
+          sKey[lo] = B;
+          sKey[hi] = A;
+        }
+      }
+      __syncthreads();
+    }
+  const int nsel = min(K, bq);
+  int *rk = a.rank + ((long long)h * a.nb + bq) * a.k_max;
+  for (int x = threadIdx.x; x < a.k_max; x += NT) {
+    int v = -1;
+    if (x == 0) v = bq;
+    else if (x - 1 < nsel) v = (int)(0xffffffffu - (uint32_t)(sKey[x - 1] & 0xffffffffull));
+    rk[x] = v;
+  }
+  __syncthreads();
+  for (int c = 0; c < a.ncand_bs; ++c) {
+    for (int w = threadIdx.x; w < a.nbw; w += NT) sB[w] = 0u;
+    __syncthreads();
+    const int take = min(a.k[c], bq + 1);
+    for (int x = threadIdx.x; x < take; x += NT) {
+      const int blk = x == 0 ? bq : (int)(0xffffffffu - (uint32_t)(sKey[x - 1] & 0xffffffffull));
+      atomicOr(&sB[blk >> 5], 1u << (blk & 31));
+    }
+    __syncthreads();
+    const long long crow = ((long long)h * a.ncand_bs + c) * a.nb + bq;
+    for (int w = threadIdx.x; w < a.nbw; w += NT) a.bits[crow * a.nbw + w] = sB[w];
+    const int cnt = bits_to_list<NT>(sB, a.nbw, a.sorted + crow * a.k_max, a.k_max, sWave);
+    if (threadIdx.x == 0) a.count[crow] = cnt;
+    __syncthreads();
+  }
+}
+
+rs_status build_indices_launch(const rs_probe_out *sc, const rs_unit *units, int32_t nunits,
+                               const rs_candidate *grid, int32_t ncand, rs_index_set *out, hipStream_t st,
+                               void *ws, size_t ws_bytes) {
+  int nvs = 0, nbs = 0;
+  VsArgs va{};
+  BsArgs ba{};
+  for (int c = 0; c < ncand; ++c) {
+    if (grid[c].fam == RS_VSLASH) {
+      va.nv[nvs] = grid[c].a;
+      va.ns[nvs] = grid[c].b;
+      ++nvs;
+    } else if (grid[c].fam == RS_BSPARSE) {
+      ba.k[nbs++] = grid[c].a;
+    }
+  }
+  if (nvs > 0) {
+    // unit key lengths go to the workspace
+    Arena ar(ws, ws_bytes);
+    int *d_s1 = ar.take<int>(nunits);
+    if (!ws || !ar.ok()) return fail(RS_ERR_WORKSPACE, "index workspace too small");
+    std::vector<int> hs1(nunits);
+    for (int u = 0; u < nunits; ++u) hs1[u] = units[u].s1;
+    RS_HIP(hipMemcpyAsync(d_s1, hs1.data(), nunits * sizeof(int), hipMemcpyHostToDevice, st));
+    va.col = sc->col; va.diag = sc->diag; va.n = sc->n; va.nunits = nunits; va.ncand_vs = nvs;
+    va.s1 = d_s1; va.nv_max = out->nv_max; va.ns_max = out->ns_max; va.nwords = out->nwords;
+    va.vsorted = out->vs_vsorted; va.dsorted = out->vs_dsorted; va.count = out->vs_count;
+    va.vbits = out->vs_vbits; va.dbits = out->vs_dbits;
+    const size_t lds = (size_t)out->nwords * sizeof(uint32_t);
+    hipLaunchKernelGGL(vs_select_kernel, dim3(2 * nvs, nunits), dim3(1024), lds, st, va);
+    RS_HIP(hipGetLastError());
+  }
+  if (nbs > 0) {
+    ba.lbs = sc->lbs; ba.nb = out->nb; ba.hq = out->hq; ba.ncand_bs = nbs; ba.k_max = out->k_max; ba.nbw = out->nbw;
+    ba.rank = out->bs_rank; ba.sorted = out->bs_sorted; ba.count = out->bs_count; ba.bits = out->bs_bits;
+    hipLaunchKernelGGL(bs_select_kernel, dim3(out->nb, out->hq), dim3(256), 0, st, ba);
+    RS_HIP(hipGetLastError());
+  }
+  return RS_OK;
+}
+
+}  // namespace rs

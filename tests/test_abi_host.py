@@ -1,0 +1,154 @@
+"""CPU checks of the C ABI: the library loads, exports every declared entry point,
+rejects bad arguments before launching anything, and the host-only router agrees bit
+for bit with the oracle router (Sec. 3.4, Eqs. 6-8)."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2608_29058_amd import _rs
+from oracle import router as RT
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "rs.h")).read()
+    return sorted(set(re.findall(r"^\s*(?:rs_status|size_t|const char \*)\s*(rs_\w+)\s*\(", src, re.M)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = _rs.lib()
+    names = _declared()
+    assert set(names) >= {"rs_probe", "rs_build_indices", "rs_route_layer", "rs_sparse_attn_prefill",
+                          "rs_dense_attn_prefill"}
+    for nm in names:
+        assert hasattr(L, nm), nm
+    assert set(_rs.EXPORTS) == set(names)
+    assert b"gfx950" in L.rs_version()
+
+
+def test_struct_layouts_match_the_c_compiler(tmp_path):
+    """ctypes mirrors of every struct have the size and field offsets gcc gives rs.h."""
+    import shutil
+    import subprocess
+    if not shutil.which("gcc"):
+        pytest.skip("gcc not available")
+    structs = {"rs_qkv": _rs.RsQkv, "rs_unit": _rs.RsUnit, "rs_candidate": _rs.RsCandidate,
+               "rs_probe_cfg": _rs.RsProbeCfg, "rs_probe_out": _rs.RsProbeOut,
+               "rs_index_set": _rs.RsIndexSet, "rs_route_in": _rs.RsRouteIn,
+               "rs_route_cfg": _rs.RsRouteCfg, "rs_route_out": _rs.RsRouteOut}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "rs.h"', 'int main(void) {']
+    for cname, py in structs.items():
+        lines.append(f'printf("{cname} size %zu\\n", sizeof({cname}));')
+        for f in py._fields_:
+            if f[0].startswith("_pad"):
+                continue
+            lines.append(f'printf("{cname} {f[0]} %zu\\n", offsetof({cname}, {f[0]}));')
+    lines.append("return 0; }")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split("\n")
+    for line in out:
+        if not line:
+            continue
+        cname, field, val = line.split()
+        py = structs[cname]
+        if field == "size":
+            assert C.sizeof(py) == int(val), cname
+        else:
+            assert getattr(py, field).offset == int(val), (cname, field)
+
+
+def test_invalid_arguments_rejected_without_launch():
+    L = _rs.lib()
+    st = L.rs_dense_attn_prefill(None, None, 0, None, 0, 0, None, None, 0, None)
+    assert st == _rs.RS_ERR_INVALID_ARG and b"qkv" in L.rs_last_error()
+    q = _rs.RsQkv(q=16, k=16, v=16, dtype=0, n=128, hq=32, hkv=8, d=96, sq_h=128 * 96, sq_t=96,
+                  sk_h=128 * 96, sk_t=96, sv_h=128 * 96, sv_t=96)
+    st = L.rs_dense_attn_prefill(C.byref(q), _rs.make_units([(0, 0, 128)]), 1, C.c_void_p(16), 96, 96,
+                                 None, None, 0, None)
+    assert st == _rs.RS_ERR_UNSUPPORTED
+    q.d, q.sq_t, q.sk_t, q.sv_t = 128, 128, 128, 128
+    q.sq_h = q.sk_h = q.sv_h = 128 * 128
+    st = L.rs_dense_attn_prefill(C.byref(q), _rs.make_units([(0, 64, 200)]), 1, C.c_void_p(16), 128, 128,
+                                 None, None, 0, None)
+    assert st == _rs.RS_ERR_INVALID_ARG and b"s1" in L.rs_last_error()
+    q.hkv = 5
+    st = L.rs_dense_attn_prefill(C.byref(q), _rs.make_units([(0, 0, 64)]), 1, C.c_void_p(16), 128, 128,
+                                 None, None, 0, None)
+    assert st == _rs.RS_ERR_INVALID_ARG
+
+
+GRID = [(RT.DENSE, 0, 0), (RT.ASHAPE, 128, 1024), (RT.ASHAPE, 128, 4096), (RT.VSLASH, 500, 2048),
+        (RT.VSLASH, 1000, 6096), (RT.VSLASH, 2000, 12288), (RT.BSPARSE, 50, 64), (RT.BSPARSE, 100, 64),
+        (RT.BSPARSE, 200, 64)]
+
+
+def _brank(grid):
+    out = []
+    for c, g in enumerate(grid):
+        out.append(sum(1 for g2 in grid[:c] if g2[0] == g[0]))
+    return out
+
+
+def _random_instance(seed, U=64):
+    r = np.random.default_rng(seed)
+    C_ = len(GRID)
+    cov = np.zeros((U, C_, 4), np.float32)
+    base = r.uniform(0.85, 1.0, (U, C_)).astype(np.float32)
+    cov[:, :, 0] = base
+    for s in range(3):
+        cov[:, :, 1 + s] = np.clip(base + r.normal(0, 0.02, (U, C_)), 0, 1).astype(np.float32)
+    cov[:, 0, :] = 1.0
+    nsub = np.tile(np.array([64, 64, 32], np.int32), (U, 1))
+    nsub[r.random(U) < 0.2, 1] = 0
+    s1 = r.choice([16384 * k for k in range(1, 9)], U).astype(np.int32)
+    edges = np.array([16384 * k for k in range(1, 9)], np.int32)
+    tt = np.zeros((C_, 8))
+    for c, g in enumerate(GRID):
+        for k in range(8):
+            kv = float(edges[k])
+            tt[c, k] = {0: kv * kv / 2e7, 1: (g[1] + g[2]) * kv / 2e7 * 8, 2: (g[1] + g[2] / 2) * kv / 2e7 * 10,
+                        3: g[1] * 64 * kv / 2e7 * 2}[g[0]] + 5.0
+    return cov, nsub, s1, edges, tt
+
+
+def _t_of(s1, edges, tt):
+    U = len(s1)
+    t = np.zeros((U, tt.shape[0]))
+    for u in range(U):
+        k = next((i for i, e in enumerate(edges) if e >= s1[u]), len(edges) - 1)
+        t[u] = tt[:, k]
+    return t
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_router_matches_oracle_bit_for_bit(seed):
+    cov, nsub, s1, edges, tt = _random_instance(seed)
+    t = _t_of(s1, edges, tt)
+    dense_total = 30.0 + t[:, 0].sum()
+    frac = [1.2, 0.5, 1 / 6.5, 0.05][seed % 4]
+    tau = [0.95, 0.9, 0.0, 0.99][seed % 3]
+    alpha, beta, dq = 1.0, 0.3 * (seed % 2), 0.01 * (seed % 3)
+    e = np.random.default_rng(seed + 100).random(cov.shape[:2]).astype(np.float32)
+    st, got = _rs.rs_route_layer(GRID, cov, nsub, s1, tt, edges, 30.0, dense_total * frac, tau, alpha,
+                                 beta, dq, e=e)
+    ref = RT.route_layer(cov[:, :, 0], cov[:, :, 1:], nsub, e, t, [g[0] for g in GRID], _brank(GRID), 30.0,
+                         dense_total * frac, tau, alpha, beta, dq)
+    assert got["choice"] == ref["choice"]
+    assert got["groups"] == [(c, us) for c, us in ref["groups"]]
+    assert got["total"] == ref["total"] and got["risk"] == ref["risk"]
+    assert got["n_fallback"] == ref["n_fallback"] and got["over_budget"] == ref["over_budget"]
+    assert np.array_equal(got["R"], ref["R"]) and np.array_equal(got["ML"], ref["ML"])
+    assert (st == _rs.RS_ERR_BUDGET_INFEASIBLE) == ref["over_budget"]
+
+
+def test_router_rejects_grid_without_dense():
+    cov, nsub, s1, edges, tt = _random_instance(0, U=4)
+    with pytest.raises(_rs.RsError):
+        _rs.rs_route_layer(GRID[1:], cov[:, 1:], nsub, s1, tt[1:], edges, 1.0, 10.0, 0.9, 1.0, 0.0, 0.0)

@@ -1,0 +1,181 @@
+"""GPU parity of the dense and sparse attention kernels against the fp64 oracle
+(Sec. 2.1 Eq. 1 and the masked-softmax semantics; pattern sets of Sec. 3.1).
+
+Index sets are written host-side here so each kernel is checked on its own; the
+probe-built sets are covered by the probe tests.  Tolerance: max-abs 2e-2 and
+relative Frobenius 1e-2 (bf16 inputs, fp32 accumulation)."""
+import numpy as np
+import pytest
+
+from oracle import attention as A
+from oracle import patterns as P
+from paper_2608_29058_amd import _rs
+from synth import gen as G
+
+from gpu_helpers import check_close, dev, fill_bs, fill_vs, out_tensor
+
+pytestmark = pytest.mark.gpu
+
+
+def _inputs(n, hq, hkv, d, seed, dtype="bf16"):
+    r = np.random.default_rng(seed)
+    q = r.standard_normal((hq, n, d)).astype(np.float32)
+    k = r.standard_normal((hkv, n, d)).astype(np.float32)
+    v = r.standard_normal((hkv, n, d)).astype(np.float32)
+    k[:, :3] += 3.0 * q[:, -1:].mean(0)[:1] if hq else 0       # a mild sink
+    if dtype == "bf16":
+        q, k, v = G.bf16_round(q), G.bf16_round(k), G.bf16_round(v)
+    return q, k, v
+
+
+def _run_dense(q, k, v, units, dtype="bf16", lse=False):
+    import torch
+    hq, n, d = q.shape
+    qd, kd, vd = dev(q, dtype), dev(k, dtype), dev(v, dtype)
+    qkv = _rs.make_qkv(qd, kd, vd)
+    u = _rs.make_units(units)
+    ws = _rs.workspace(_rs.rs_attn_workspace_size(qkv, u, len(units)))
+    o = out_tensor(hq, n, d)
+    ls = torch.full((hq, n), float("nan"), dtype=torch.float32, device="cuda") if lse else None
+    _rs.rs_dense_attn_prefill(qkv, u, len(units), o, ls, ws)
+    torch.cuda.synchronize()
+    return o.float().cpu().numpy(), (ls.cpu().numpy() if lse else None)
+
+
+@pytest.mark.parametrize("n,hq,hkv,d,dtype", [(1000, 4, 2, 128, "bf16"), (4097, 2, 1, 128, "bf16"),
+                                              (700, 2, 2, 64, "bf16"), (2048, 1, 1, 64, "f32"),
+                                              (64, 1, 1, 128, "bf16"), (1, 1, 1, 128, "bf16")])
+def test_dense_matches_oracle(n, hq, hkv, d, dtype):
+    q, k, v = _inputs(n, hq, hkv, d, seed=n + d)
+    units = [(h, 0, n) for h in range(hq)]
+    o, lse = _run_dense(q, k, v, units, dtype, lse=True)
+    g = hq // hkv
+    for h in range(hq):
+        ref = A.dense_attention(q[h], k[h // g], v[h // g])
+        check_close(o[h], ref, f"dense h={h}")
+        lg = A.logits(q[h], k[h // g], np.arange(n), n)
+        lg = np.where(P.dense_mask(np.arange(n), n), lg, -np.inf)
+        from scipy.special import logsumexp
+        np.testing.assert_allclose(lse[h], logsumexp(lg, axis=1), atol=2e-3, rtol=1e-4)
+
+
+def test_dense_segments_write_only_their_rows():
+    n, hq, hkv, d = 1500, 2, 1, 128
+    q, k, v = _inputs(n, hq, hkv, d, seed=7)
+    units = [(0, 100, 700), (1, 640, 1500), (0, 1200, 1201)]
+    o, _ = _run_dense(q, k, v, units)
+    written = np.zeros((hq, n), bool)
+    for h, s0, s1 in units:
+        written[h, s0:s1] = True
+        rows = np.arange(s0, s1)
+        check_close(o[h, s0:s1], A.dense_attention(q[h], k[0], v[0], rows=rows), f"seg {h},{s0},{s1}")
+    assert np.isnan(o[~written]).all()
+
+
+def _run_sparse(q, k, v, units, grid, ib, dtype="bf16"):
+    import torch
+    hq, n, d = q.shape
+    qd, kd, vd = dev(q, dtype), dev(k, dtype), dev(v, dtype)
+    qkv = _rs.make_qkv(qd, kd, vd)
+    u = _rs.make_units(units)
+    g = _rs.make_grid(grid)
+    ws = _rs.workspace(_rs.rs_attn_workspace_size(qkv, u, len(units)))
+    o = out_tensor(hq, n, d)
+    lse = torch.full((hq, n), float("nan"), dtype=torch.float32, device="cuda")
+    _rs.rs_sparse_attn_prefill(qkv, u, len(units), g, len(grid), ib, o, lse, ws)
+    torch.cuda.synchronize()
+    return o.float().cpu().numpy(), lse.cpu().numpy()
+
+
+@pytest.mark.parametrize("n,sink,window", [(3000, 128, 1024), (2500, 0, 1), (1800, 100, 300),
+                                           (700, 4, 64), (5000, 130, 1000)])
+def test_ashape_matches_oracle(n, sink, window):
+    hq, hkv, d = 2, 1, 128
+    q, k, v = _inputs(n, hq, hkv, d, seed=sink + window)
+    grid = [(_rs.RS_DENSE, 0, 0), (_rs.RS_ASHAPE, sink, window)]
+    units = [(0, 0, n, 1), (1, 640, n, 1)]
+    o, lse = _run_sparse(q, k, v, units, grid, None)
+    for h, s0, s1, _ in units:
+        rows = np.arange(s0, s1)
+        ref, rl = A.masked_attention(q[h], k[0], v[0], rows, P.ashape_mask(rows, s1, sink, window))
+        check_close(o[h, s0:s1], ref, f"ashape h={h}")
+        np.testing.assert_allclose(lse[h, s0:s1], rl, atol=2e-3, rtol=1e-4)
+
+
+@pytest.mark.parametrize("n,k_blocks", [(2000, 5), (4096, 12), (1100, 40)])
+def test_block_sparse_matches_oracle(n, k_blocks):
+    hq, hkv, d = 4, 2, 128
+    q, k, v = _inputs(n, hq, hkv, d, seed=n)
+    nb = (n + 63) // 64
+    grid = [(_rs.RS_DENSE, 0, 0), (_rs.RS_BSPARSE, k_blocks, 64)]
+    ib = _rs.IndexBuffers(hq, n, hq, grid)
+    r = np.random.default_rng(3)
+    sels = {}
+    for h in range(hq):
+        sel = []
+        for bq in range(nb):
+            others = r.permutation(bq)[:k_blocks - 1]
+            sel.append(sorted(set(others.tolist()) | {bq}))
+        sels[h] = sel
+        fill_bs(ib, h, 0, sel)
+    units = [(h, 0 if h % 2 == 0 else 320, n, 1) for h in range(hq)]
+    o, _ = _run_sparse(q, k, v, units, grid, ib)
+    g = hq // hkv
+    for h, s0, s1, _ in units:
+        rows = np.arange(s0, s1)
+        mask = P.bs_mask(rows, s1, 64, lambda bq, h=h: sels[h][bq])
+        ref, _ = A.masked_attention(q[h], k[h // g], v[h // g], rows, mask)
+        check_close(o[h, s0:s1], ref, f"bs h={h}")
+
+
+@pytest.mark.parametrize("n,nv,ns,spread", [(3000, 40, 300, "local"), (2048, 64, 256, "scatter"),
+                                            (4100, 200, 1500, "mixed"), (900, 0, 1, "diag_only")])
+def test_vertical_slash_matches_oracle(n, nv, ns, spread):
+    hq, hkv, d = 2, 1, 128
+    q, k, v = _inputs(n, hq, hkv, d, seed=nv + ns)
+    grid = [(_rs.RS_DENSE, 0, 0), (_rs.RS_VSLASH, nv, ns)]
+    units = [(0, 0, n, 1, 0), (1, 500, n, 1, 1)]
+    ib = _rs.IndexBuffers(2, n, hq, grid)
+    r = np.random.default_rng(5)
+    sets = []
+    for slot, (h, s0, s1, _, _) in enumerate(units):
+        V = np.sort(r.choice(s1, min(nv, s1), replace=False))
+        if spread == "local":
+            D = np.arange(min(ns, s1))
+        elif spread == "scatter":
+            D = np.sort(np.unique(np.concatenate([[0], r.choice(s1, ns - 1, replace=False)])))[:ns]
+        elif spread == "mixed":
+            D = np.unique(np.concatenate([np.arange(ns // 2), r.choice(s1, ns - ns // 2, replace=False)]))[:ns]
+        else:
+            D = np.array([0])
+        fill_vs(ib, slot, 0, V, D)
+        sets.append((V, D))
+    o, _ = _run_sparse(q, k, v, units, grid, ib)
+    for slot, (h, s0, s1, _, _) in enumerate(units):
+        rows = np.arange(s0, s1)
+        V, D = sets[slot]
+        ref, _ = A.masked_attention(q[h], k[0], v[0], rows, P.vs_mask(rows, s1, V, D))
+        check_close(o[h, s0:s1], ref, f"vs slot={slot}")
+
+
+def test_empty_rows_give_zero_and_minus_inf_lse():
+    # vertical-slash with no diagonals and columns only late: early rows keep nothing
+    n, d = 300, 128
+    q, k, v = _inputs(n, 1, 1, d, seed=11)
+    grid = [(_rs.RS_DENSE, 0, 0), (_rs.RS_VSLASH, 2, 0)]
+    ib = _rs.IndexBuffers(1, n, 1, grid)
+    fill_vs(ib, 0, 0, [200, 250], [])
+    o, lse = _run_sparse(q, k, v, [(0, 0, n, 1, 0)], grid, ib)
+    assert np.all(o[0, :200] == 0) and np.all(np.isneginf(lse[0, :200]))
+    rows = np.arange(200, n)
+    ref, _ = A.masked_attention(q[0], k[0], v[0], rows, P.vs_mask(rows, n, [200, 250], []))
+    check_close(o[0, 200:], ref, "late rows")
+
+
+def test_deterministic_bitwise():
+    n, hq, hkv, d = 2000, 4, 1, 128
+    q, k, v = _inputs(n, hq, hkv, d, seed=19)
+    units = [(h, 0, n) for h in range(hq)]
+    a, _ = _run_dense(q, k, v, units)
+    b, _ = _run_dense(q, k, v, units)
+    assert np.array_equal(a, b)
