@@ -1,0 +1,353 @@
+"""Routed pattern-sparse causal prefill at 128K on one MI355X.
+
+Workload: 32 layers of a Llama-3.1-8B-shaped attention layer (GQA 32/8, d = 128, bf16,
+n = 131072 tokens), per-layer seeds and mixed head regimes (synthetic, see synth/gen.py).
+One step = one layer through the whole hot path: probe (sampled rows + block-mean),
+index construction, coverage, host routing under the latency budget, and one grouped
+sparse/dense attention launch per (pattern, budget) group.  Each head is split into 8
+segments of 16K rows (units).  The reported value is ms per layer (lower is better).
+
+Before timing (offline calibration, untimed): the kernel latency of every candidate is
+profiled per 16K key-length bucket on layer 0 (median of 3), the probe/route overhead is
+measured, and the layer budget is T = (dense time of the layer) / 6.5.
+
+    python bench.py [--steps K] [--warmup W] [--layers L] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "prefill attn ms/layer at 128K, GQA 32/8 d128 bf16; x vs dense; MFMA util"
+N, HQ, HKV, D, SEG = 131072, 32, 8, 128, 16384
+GRID = [(0, 0, 0), (1, 128, 1024), (1, 128, 4096), (2, 500, 2048), (2, 1000, 6096), (2, 2000, 12288),
+        (3, 50, 64), (3, 100, 64), (3, 200, 64)]
+FAM_NAME = {0: "dense", 1: "ashape", 2: "vslash", 3: "bsparse"}
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+# ---- algorithmic work: kept query-key pairs of one unit under one candidate --------------
+
+def pairs_dense(s0, s1):
+    return (s1 * (s1 + 1) - s0 * (s0 + 1)) // 2
+
+
+def pairs_ashape(s0, s1, sink, w):
+    i = np.arange(s0, s1, dtype=np.int64)
+    return int((np.minimum(i + 1, w) + np.clip(np.minimum(sink, i - w + 1), 0, None)).sum())
+
+
+def pairs_bs(s0, s1, counts):
+    tot = 0
+    for bq in range(s0 // 64, (s1 - 1) // 64 + 1):
+        ra, rb = max(s0, 64 * bq), min(s1, 64 * bq + 64)
+        c = int(counts[bq])
+        tot += (c - 1) * 64 * (rb - ra) + sum(i - 64 * bq + 1 for i in range(ra, rb))
+    return tot
+
+
+def pairs_vs(s0, s1, V, D):
+    n = s1
+    iv = np.zeros(n, np.float64)
+    iv[V] = 1
+    idd = np.zeros(n, np.float64)
+    idd[D] = 1
+    cv, cd = np.cumsum(iv), np.cumsum(idd)
+    L = 1 << int(np.ceil(np.log2(2 * n)))
+    conv = np.fft.irfft(np.fft.rfft(iv, L) * np.fft.rfft(idd, L), L)[:n]
+    rows = np.arange(s0, s1)
+    return int(round((cv[rows] + cd[rows] - conv[rows]).sum()))
+
+
+# ---- CPU baseline: the oracle on a bounded sample ------------------------------------------
+
+def cpu_baseline(q, k, v, route, t_table, edges, knobs, rows_per_unit=32):
+    """Oracle pipeline of query head 0 (its 8 units): probe, index rules, coverage,
+    routing, and masked attention on ``rows_per_unit`` rows per unit; scaled to a layer."""
+    from oracle import attention as A, coverage as CV, indices as IX, patterns as P, probe as PR
+    from oracle import router as RT
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    h = 0
+    qh = q[h].float().cpu().numpy().astype(np.float64)
+    kh = k[0].float().cpu().numpy().astype(np.float64)
+    vh = v[0].float().cpu().numpy().astype(np.float64)
+    t0 = time.perf_counter()
+    L = PR.block_mean_logits(qh, kh, 64)
+    bs_sel = {c: IX.bs_indices(L, GRID[c][1])[0] for c in range(len(GRID)) if GRID[c][0] == 3}
+    mhat, msub, nsub = [], [], []
+    units = [(h, s, s + SEG) for s in range(0, N, SEG)]
+    masks_of = []
+    for (hh, s0, s1) in units:
+        pu = PR.probe_unit(qh, kh, s0, s1, 64, 64, 32)
+        rows = pu["rows"]
+        ms = []
+        for c, g in enumerate(GRID):
+            if g[0] == 0:
+                m = P.dense_mask(rows, s1)
+            elif g[0] == 1:
+                m = P.ashape_mask(rows, s1, g[1], g[2])
+            elif g[0] == 2:
+                V, Dd, _, _ = IX.vs_indices(pu["col"], pu["diag"], s1, g[1], g[2])
+                m = P.vs_mask(rows, s1, V, Dd)
+            else:
+                m = P.bs_mask(rows, s1, 64, lambda bq, c=c: bs_sel[c][bq])
+            mi = CV.row_coverage(pu["a"], m)
+            mh, means, counts = CV.subset_means(mi, pu["subset"])
+            ms.append((mh, means, counts))
+        mhat.append([x[0] for x in ms])
+        msub.append([x[1] for x in ms])
+        nsub.append(ms[0][2])
+        masks_of.append(pu)
+    t_probe = time.perf_counter() - t0
+    tt = np.zeros((len(units), len(GRID)))
+    for ui, (_, s0, s1) in enumerate(units):
+        b = next((i for i, e in enumerate(edges) if e >= s1), len(edges) - 1)
+        tt[ui] = t_table[:, b]
+    t1 = time.perf_counter()
+    r = RT.route_layer(np.array(mhat), np.array(msub), np.array(nsub), np.zeros_like(tt), tt,
+                       [g[0] for g in GRID], [sum(1 for g2 in GRID[:c] if g2[0] == g[0]) for c in range(len(GRID))],
+                       0.0, knobs.T_layer_us / 32, knobs.tau, knobs.alpha, knobs.beta, knobs.delta_q)
+    t_route = time.perf_counter() - t1
+    t2 = time.perf_counter()
+    for ui, (_, s0, s1) in enumerate(units):
+        c = r["choice"][ui]
+        g = GRID[c]
+        rows = np.linspace(s0, s1 - 1, rows_per_unit).astype(np.int64)
+        if g[0] == 0:
+            m = P.dense_mask(rows, s1)
+        elif g[0] == 1:
+            m = P.ashape_mask(rows, s1, g[1], g[2])
+        elif g[0] == 2:
+            pu = masks_of[ui]
+            V, Dd, _, _ = IX.vs_indices(pu["col"], pu["diag"], s1, g[1], g[2])
+            m = P.vs_mask(rows, s1, V, Dd)
+        else:
+            m = P.bs_mask(rows, s1, 64, lambda bq, c=c: bs_sel[c][bq])
+        A.masked_attention(qh, kh, vh, rows, m)
+    t_attn = time.perf_counter() - t2
+    per_layer_s = (t_probe + t_route) * HQ + t_attn * (SEG / rows_per_unit) * HQ
+    return {"value": per_layer_s * 1e3, "unit": "ms/layer", "cores": int(cores), "kind": "oracle",
+            "sample": (f"fp64 oracle on query head 0 of layer 0 (8 units): probe, index rules, coverage, "
+                       f"route, and masked attention on {rows_per_unit} of 16384 rows per unit; probe part "
+                       f"scaled x32 heads, attention part x{SEG // rows_per_unit}x32 (extrapolated)"),
+            "measured_s": round(t_probe + t_route + t_attn, 2),
+            "phase_s": {"probe_index_coverage": round(t_probe, 2), "route": round(t_route, 4),
+                        "attention_sample": round(t_attn, 2)}}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=32)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--layers", type=int, default=32)
+    ap.add_argument("--dense-reps", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--json-out", default=None)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+
+    import torch
+    from paper_2608_29058_amd import _rs
+    from paper_2608_29058_amd.pipeline import RoutedLayer, RouteKnobs
+    from synth import gen as G
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    _rs.lib()
+    t_gen = time.perf_counter()
+    layers = []
+    for l in range(args.layers):
+        t = G.make_layer_torch(5, l, device=dev)
+        layers.append((t["q"], t["k"], t["v"], t["spec"]))
+        if l % 8 == 7 or l == args.layers - 1:
+            log(f"generated {l + 1}/{args.layers} layers ({time.perf_counter() - t_gen:.1f}s)")
+    torch.cuda.synchronize()
+    RL = RoutedLayer(N, HQ, HKV, D, SEG, GRID)
+    stream = torch.cuda.current_stream()
+
+    def ev():
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(stream)
+        return e
+
+    # ---- offline calibration: kernel latency table, probe overhead, budget -----------------
+    q0, k0, v0, _ = layers[0]
+    qkv0 = RL.qkv(q0, k0, v0)
+    RL.probe_and_index(qkv0)
+    torch.cuda.synchronize()
+    edges = np.array([SEG * (b + 1) for b in range(N // SEG)], np.int32)
+    t_table = np.zeros((len(GRID), len(edges)))
+    for c in range(len(GRID)):
+        for b in range(len(edges)):
+            us = [i for i, u in enumerate(RL.unit_list) if u[2] == edges[b]]
+            ts = []
+            for _ in range(3):
+                a = ev()
+                RL.run_group(qkv0, c, us)
+                z = ev()
+                z.synchronize()
+                ts.append(a.elapsed_time(z))
+            t_table[c, b] = float(np.median(ts)) * 1e3 / len(us)
+    log("t_ker (us/unit) dense:", np.round(t_table[0], 1).tolist())
+    # probe + index + coverage time, and the host routing overhead
+    tp = []
+    for _ in range(3):
+        a = ev()
+        RL.probe_and_index(qkv0)
+        z = ev()
+        z.synchronize()
+        tp.append(a.elapsed_time(z))
+    RL.t_table, RL.edges = t_table, edges
+    t_dense_layer_us = float(sum(t_table[0, int(np.searchsorted(edges, u[2]))] for u in RL.unit_list))
+    RL.knobs = RouteKnobs(T_layer_us=t_dense_layer_us / 6.5, tau=0.95, alpha=1.0, beta=0.0, delta_q=0.0)
+    t0 = time.perf_counter()
+    RL.route()
+    t_route_host_us = (time.perf_counter() - t0) * 1e6
+    RL.t_probe_us = float(np.median(tp)) * 1e3 + t_route_host_us
+    log(f"t_probe {RL.t_probe_us:.0f} us, T_layer {RL.knobs.T_layer_us:.0f} us")
+
+    # ---- warmup + timed steps ----------------------------------------------------------------
+    for s in range(args.warmup):
+        q, k, v, _ = layers[s % args.layers]
+        RL.run(q, k, v)
+    torch.cuda.synchronize()
+    records = []
+    t_wall0 = time.perf_counter()
+    e_start = ev()
+    for s in range(args.steps):
+        li = s % args.layers
+        q, k, v, _ = layers[li]
+        marks = []
+        route = RL.run(q, k, v, events=lambda name: marks.append((name, ev())))
+        records.append((li, route, marks))
+    e_end = ev()
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t_wall0) * 1e3
+    total_ms = e_start.elapsed_time(e_end)
+    ms_per_layer = total_ms / args.steps
+
+    # ---- per-phase / per-family accounting (after the timed region) -------------------------
+    fam_time = {f: 0.0 for f in FAM_NAME}
+    fam_flops = {f: 0.0 for f in FAM_NAME}
+    fam_launches = {f: 0 for f in FAM_NAME}
+    ph = {"probe_index_coverage": 0.0, "d2h_route": 0.0, "attention": 0.0}
+    n_units_fb = 0
+    n_units_dense = 0
+    routed_flops = 0.0
+    cache = {}
+    for li, route, marks in records:
+        names = [m[0] for m in marks]
+        evs = [m[1] for m in marks]
+        ph["probe_index_coverage"] += evs[0].elapsed_time(evs[1])
+        ph["d2h_route"] += evs[1].elapsed_time(evs[2])
+        ph["attention"] += evs[2].elapsed_time(evs[-1])
+        n_units_fb += route["n_fallback"]
+        if li not in cache:
+            q, k, v, _ = layers[li]
+            RL.probe_and_index(RL.qkv(q, k, v))
+            torch.cuda.synchronize()
+            cache[li] = dict(bs_count=RL.ib.bs_count.cpu().numpy(), vs_count=RL.ib.vs_count.cpu().numpy(),
+                             vs_v=RL.ib.vs_vsorted.cpu().numpy(), vs_d=RL.ib.vs_dsorted.cpu().numpy())
+        ic = cache[li]
+        for gi, (cand, us) in enumerate(route["groups"]):
+            fam, a_, b_ = GRID[cand]
+            dt = evs[2 + gi].elapsed_time(evs[3 + gi])
+            pairs = 0
+            cl = sum(1 for g in GRID[:cand] if g[0] == fam)
+            for u in us:
+                h, s0, s1 = RL.unit_list[u]
+                if fam == 0:
+                    pairs += pairs_dense(s0, s1)
+                    n_units_dense += 1
+                elif fam == 1:
+                    pairs += pairs_ashape(s0, s1, a_, b_)
+                elif fam == 3:
+                    pairs += pairs_bs(s0, s1, ic["bs_count"][h, cl])
+                else:
+                    cv, cdn = ic["vs_count"][u, cl]
+                    pairs += pairs_vs(s0, s1, ic["vs_v"][u, cl, :cv], ic["vs_d"][u, cl, :cdn])
+            fl = 4.0 * D * pairs
+            fam_time[fam] += dt
+            fam_flops[fam] += fl
+            fam_launches[fam] += 1
+            routed_flops += fl
+    # dense reference: the whole layer through the dense kernel, same run
+    qkv_d = RL.qkv(q0, k0, v0)
+    ud = _rs.make_units([(h, 0, N, 0, 0) for h in range(HQ)])
+    wsd = _rs.workspace(_rs.rs_attn_workspace_size(qkv_d, ud, HQ))
+    od = torch.empty_like(q0)
+    _rs.rs_dense_attn_prefill(qkv_d, ud, HQ, od, None, wsd)
+    torch.cuda.synchronize()
+    a = ev()
+    for _ in range(args.dense_reps):
+        _rs.rs_dense_attn_prefill(qkv_d, ud, HQ, od, None, wsd)
+    z = ev()
+    torch.cuda.synchronize()
+    dense_ms = a.elapsed_time(z) / args.dense_reps
+    dense_flops = 4.0 * D * HQ * pairs_dense(0, N)
+
+    dom = max(fam_time, key=lambda f: fam_time[f])
+    dom_avg_ms = fam_time[dom] / max(1, fam_launches[dom])
+    dom_tflops = fam_flops[dom] / (fam_time[dom] * 1e-3) / 1e12 if fam_time[dom] > 0 else 0.0
+    roofline = {"bound": "mfma", "achieved": round(dom_tflops, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(dom_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "kernel": f"attn_fwd_kernel[{FAM_NAME[dom]}]", "avg_launch_ms": round(dom_avg_ms, 4),
+                "launches": fam_launches[dom],
+                "flops_def": "4*d*(kept query-key pairs) per launch"}
+    res = {
+        "metric": METRIC, "value": round(ms_per_layer, 4), "unit": "ms/layer", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_layer, 4),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "routed prefill, 32 layers x GQA 32/8 d128 bf16, n=131072, 8 segments of 16384 "
+                               "per head, 9-candidate grid, tau=0.95, T_layer=dense/6.5",
+                   "layers": args.layers, "n": N, "heads": [HQ, HKV], "head_dim": D, "segment": SEG},
+        "roofline": roofline,
+        "dense_ms_per_layer": round(dense_ms, 3),
+        "dense_tflops": round(dense_flops / (dense_ms * 1e-3) / 1e12, 1),
+        "speedup_vs_dense": round(dense_ms / ms_per_layer, 3),
+        "routed_effective_tflops": round(routed_flops / args.steps / (ms_per_layer * 1e-3) / 1e12, 1),
+        "phase_ms_per_layer": {k2: round(v2 / args.steps, 4) for k2, v2 in ph.items()},
+        "family_ms_per_layer": {FAM_NAME[f]: round(fam_time[f] / args.steps, 4) for f in FAM_NAME},
+        "family_tflops": {FAM_NAME[f]: (round(fam_flops[f] / (fam_time[f] * 1e-3) / 1e12, 1) if fam_time[f] else None)
+                          for f in FAM_NAME},
+        "fallback_units_per_layer": round(n_units_fb / args.steps, 2),
+        "dense_units_per_layer": round(n_units_dense / args.steps, 2),
+        "wall_ms_timed": round(wall_ms, 1),
+        "t_layer_budget_ms": round(RL.knobs.T_layer_us / 1e3, 3),
+        "t_probe_ms": round(RL.t_probe_us / 1e3, 3),
+    }
+    if not args.no_cpu_baseline:
+        try:
+            res["cpu_baseline"] = cpu_baseline(q0, k0, v0, records[0][1], t_table, edges, RL.knobs)
+        except Exception as exc:  # reported, never fatal to the GPU measurement
+            res["cpu_baseline"] = {"error": repr(exc)}
+    line = json.dumps(res)
+    if args.json_out:
+        with open(args.json_out, "w") as f:
+            f.write(line + "\n")
+    print(line, flush=True)
+
+
+if __name__ == "__main__":
+    main()

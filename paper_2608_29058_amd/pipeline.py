@@ -1,0 +1,118 @@
+"""Sequencing of one routed layer through the C ABI (inference-procedure steps 1-6).
+
+No arithmetic happens here: this module allocates caller-owned buffers once and calls the
+library in the order of the per-layer procedure (Sec. 3.4 and its table):
+  1. rs_probe (scores: sampled rows, col/diag, descriptors, block-mean logits)
+  2. rs_build_indices, then rs_probe (coverage of every candidate)
+  3-5. coverage copied to the host, rs_route_layer (latency lookup, greedy solve,
+       expand/fallback, grouping)
+  6. one rs_sparse_attn_prefill / rs_dense_attn_prefill launch per (pattern, budget) group.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+from . import _rs
+
+
+@dataclass
+class RouteKnobs:
+    T_layer_us: float = 1e30
+    tau: float = 0.95
+    alpha: float = 1.0
+    beta: float = 0.0
+    delta_q: float = 0.0
+
+
+@dataclass
+class LayerTimes:
+    phases_ms: dict = field(default_factory=dict)
+    groups: list = field(default_factory=list)  # (cand, n_units, ms)
+
+
+class RoutedLayer:
+    """Buffers and call order of one routed layer for fixed shapes."""
+
+    def __init__(self, n, hq, hkv, d, seg_len, grid, r_rec=64, r_uni=64, r_bnd=32, local_w=1024,
+                 device="cuda"):
+        import torch
+        self.n, self.hq, self.hkv, self.d = n, hq, hkv, d
+        self.grid = list(grid)
+        self.g = _rs.make_grid(self.grid)
+        self.ncand = len(self.grid)
+        segs = [(s, min(n, s + seg_len)) for s in range(0, n, seg_len)]
+        self.unit_list = [(h, s0, s1) for (s0, s1) in segs for h in range(hq)]
+        self.nunits = len(self.unit_list)
+        self.units = _rs.make_units([(h, s0, s1, 0, i) for i, (h, s0, s1) in enumerate(self.unit_list)])
+        self.cfg = _rs.RsProbeCfg(r_rec=r_rec, r_uni=r_uni, r_bnd=r_bnd, bs_block=64, local_w=local_w,
+                                  flags=_rs.RS_PROBE_ROWS | _rs.RS_PROBE_BLOCKMEAN)
+        self.rmax = r_rec + r_uni + r_bnd
+        self.pb = _rs.ProbeBuffers(self.nunits, self.rmax, n, hq, self.ncand, blockmean=True, device=device)
+        self.ib = _rs.IndexBuffers(self.nunits, n, hq, self.grid, device=device)
+        self.o = torch.empty((hq, n, d), dtype=torch.bfloat16, device=device)
+        self.s1 = np.array([u[2] for u in self.unit_list], np.int32)
+        self.cov_host = torch.empty((self.nunits, self.ncand, 4), dtype=torch.float32, pin_memory=True)
+        self.nsub_host = torch.empty((self.nunits, 3), dtype=torch.int32, pin_memory=True)
+        self._ws = None
+        self.t_table = None
+        self.edges = None
+        self.t_probe_us = 0.0
+        self.knobs = RouteKnobs()
+
+    def qkv(self, q, k, v):
+        return _rs.make_qkv(q, k, v)
+
+    def workspace(self, qkv):
+        if self._ws is None:
+            need = max(_rs.rs_probe_workspace_size(qkv, self.units, self.nunits, self.cfg),
+                       _rs.rs_build_indices_workspace_size(self.pb, self.g, self.ncand),
+                       _rs.rs_attn_workspace_size(qkv, self.units, self.nunits))
+            self._ws = _rs.workspace(need)
+        return self._ws
+
+    # -- steps ---------------------------------------------------------------------------
+    def probe_and_index(self, qkv):
+        ws = self.workspace(qkv)
+        _rs.rs_probe(qkv, self.units, self.nunits, self.cfg, None, 0, None, ws, self.pb)
+        _rs.rs_build_indices(self.pb, self.units, self.nunits, self.g, self.ncand, ws, self.ib)
+        _rs.rs_probe(qkv, self.units, self.nunits, self.cfg, self.g, self.ncand, self.ib, ws, self.pb)
+
+    def route(self):
+        import torch
+        self.cov_host.copy_(self.pb.cov, non_blocking=True)
+        self.nsub_host.copy_(self.pb.nsub, non_blocking=True)
+        torch.cuda.current_stream().synchronize()
+        k = self.knobs
+        st, out = _rs.rs_route_layer(self.grid, self.cov_host.numpy(), self.nsub_host.numpy(), self.s1,
+                                     self.t_table, self.edges, self.t_probe_us, k.T_layer_us, k.tau,
+                                     k.alpha, k.beta, k.delta_q)
+        return out
+
+    def group_units(self, cand, unit_idx):
+        return _rs.make_units([(self.unit_list[u][0], self.unit_list[u][1], self.unit_list[u][2], cand, u)
+                               for u in unit_idx])
+
+    def run_group(self, qkv, cand, unit_idx, lse=None):
+        ws = self.workspace(qkv)
+        us = self.group_units(cand, unit_idx)
+        if self.grid[cand][0] == _rs.RS_DENSE:
+            _rs.rs_dense_attn_prefill(qkv, us, len(unit_idx), self.o, lse, ws)
+        else:
+            _rs.rs_sparse_attn_prefill(qkv, us, len(unit_idx), self.g, self.ncand, self.ib, self.o, lse, ws)
+
+    def run(self, q, k, v, events=None):
+        """One routed layer; returns the route.  ``events`` (optional) is a callable
+        ``mark(name)`` used to record stream events between phases."""
+        qkv = self.qkv(q, k, v)
+        mark = events or (lambda name: None)
+        mark("start")
+        self.probe_and_index(qkv)
+        mark("probe")
+        route = self.route()
+        mark("route")
+        for ci, (cand, us) in enumerate(route["groups"]):
+            self.run_group(qkv, cand, us)
+            mark(f"group{ci}")
+        return route

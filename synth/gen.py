@@ -131,7 +131,7 @@ def layer_spec(cfg: int, layer: int = 0, n: int | None = None) -> LayerSpec:
             k = math.log(1.65 * n / nv) + 4.0
             groups.append(GroupPlants(regime, vert_k=k, vert_cols=cols))
         elif regime == "local":
-            groups.append(GroupPlants(regime, local_lam=9.0))
+            groups.append(GroupPlants(regime, local_lam=17.0))
         else:
             groups.append(GroupPlants(regime))
     span_len = 512
@@ -153,11 +153,20 @@ def layer_spec(cfg: int, layer: int = 0, n: int | None = None) -> LayerSpec:
                      span_len, 3.0, chunk_span)
 
 
-def _rope_tables(n: int, d: int):
-    half = d // 2
-    theta = ROPE_BASE ** (-2.0 * np.arange(half, dtype=np.float64) / d)
-    ang = np.arange(n, dtype=np.float64)[:, None] * theta[None, :]
-    return np.cos(ang).astype(np.float32), np.sin(ang).astype(np.float32), theta
+_TABLES = {}
+
+
+def _rope_tables(n: int, d: int, device="cpu"):
+    import torch
+    key = (n, d, str(device))
+    if key not in _TABLES:
+        half = d // 2
+        theta = ROPE_BASE ** (-2.0 * np.arange(half, dtype=np.float64) / d)
+        ang = np.arange(n, dtype=np.float64)[:, None] * theta[None, :]
+        _TABLES.clear()
+        _TABLES[key] = (torch.from_numpy(np.cos(ang).astype(np.float32)).to(device),
+                        torch.from_numpy(np.sin(ang).astype(np.float32)).to(device), theta)
+    return _TABLES[key]
 
 
 def _local_vec(d: int, theta: np.ndarray) -> np.ndarray:
@@ -169,94 +178,119 @@ def _local_vec(d: int, theta: np.ndarray) -> np.ndarray:
     return (c / np.linalg.norm(c)).astype(np.float32)
 
 
-def _rope(x: np.ndarray, cos: np.ndarray, sin: np.ndarray) -> np.ndarray:
+def _rope(x, cos, sin):
+    """Rotate-half RoPE on a [n, d] float32 torch tensor (elementwise float32 ops)."""
+    import torch
     half = x.shape[1] // 2
     x1, x2 = x[:, :half], x[:, half:]
-    out = np.empty_like(x)
+    out = torch.empty_like(x)
     out[:, :half] = x1 * cos - x2 * sin
     out[:, half:] = x2 * cos + x1 * sin
     return out
 
 
-def _finish(x: np.ndarray, dtype: str) -> np.ndarray:
-    return bf16_round(x) if dtype == "bf16" else np.ascontiguousarray(x, dtype=np.float32)
+_DEV = ["cpu"]
 
 
-def _gen_q(spec: LayerSpec, h: int, tabs) -> np.ndarray:
+def _vec(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(_DEV[0])
+
+
+def _finish(x, dtype: str):
+    """bf16 configs: round to nearest even and return the bf16 tensor; else float32."""
+    import torch
+    return x.to(torch.bfloat16) if dtype == "bf16" else x.contiguous()
+
+
+def _normals(seed_key, n, d):
+    return np.random.default_rng(seed_key).standard_normal((n, d), dtype=np.float32)
+
+
+def _gen_q(spec: LayerSpec, h: int, tabs, base):
+    import torch
     cos, sin, theta = tabs
-    n, d = spec.n, spec.d
+    d = spec.d
     gp = spec.groups[h // spec.group_size]
-    x = np.random.default_rng([spec.seed, 1, h]).standard_normal((n, d), dtype=np.float32)
+    x = torch.from_numpy(base).to(_DEV[0])
     if gp.local_lam > 0:
-        x += _plant_amp(gp.local_lam, d) * _local_vec(d, theta)[None, :]
+        x += _vec(_plant_amp(gp.local_lam, d) * _local_vec(d, theta))[None, :]
     x = _rope(x, cos, sin)
     if gp.sink_k > 0:
-        x += (_plant_amp(gp.sink_k, d) * spec.dirs[0]).astype(np.float32)[None, :]
+        x += _vec(_plant_amp(gp.sink_k, d) * spec.dirs[0])[None, :]
     if gp.vert_k > 0 and gp.vert_cols.size:
-        x += (_plant_amp(gp.vert_k, d) * spec.dirs[1]).astype(np.float32)[None, :]
+        x += _vec(_plant_amp(gp.vert_k, d) * spec.dirs[1])[None, :]
     if spec.span_starts.size:
         amp = _plant_amp(spec.span_k, d)
         for ch, sid in enumerate(spec.chunk_span):
             if sid >= 0:
-                x[ch * 1024:(ch + 1) * 1024] += (amp * spec.dirs[2 + sid]).astype(np.float32)
+                x[ch * 1024:(ch + 1) * 1024] += _vec(amp * spec.dirs[2 + sid])
     return _finish(x, spec.dtype)
 
 
-def _gen_k(spec: LayerSpec, g: int, tabs) -> np.ndarray:
+def _gen_k(spec: LayerSpec, g: int, tabs, base):
     cos, sin, theta = tabs
-    n, d = spec.n, spec.d
+    d = spec.d
     gp = spec.groups[g]
-    x = np.random.default_rng([spec.seed, 2, g]).standard_normal((n, d), dtype=np.float32)
+    import torch
+    x = torch.from_numpy(base).to(_DEV[0])
     if gp.local_lam > 0:
-        x += _plant_amp(gp.local_lam, d) * _local_vec(d, theta)[None, :]
+        x += _vec(_plant_amp(gp.local_lam, d) * _local_vec(d, theta))[None, :]
     x = _rope(x, cos, sin)
     if gp.sink_k > 0:
-        x[:gp.sink_n] += (_plant_amp(gp.sink_k, d) * spec.dirs[0]).astype(np.float32)
+        x[:gp.sink_n] += _vec(_plant_amp(gp.sink_k, d) * spec.dirs[0])
     if gp.vert_k > 0 and gp.vert_cols.size:
-        x[gp.vert_cols] += (_plant_amp(gp.vert_k, d) * spec.dirs[1]).astype(np.float32)
+        x[torch.from_numpy(gp.vert_cols).to(_DEV[0])] += _vec(_plant_amp(gp.vert_k, d) * spec.dirs[1])
     if spec.span_starts.size:
         amp = _plant_amp(spec.span_k, d)
         for sid, st in enumerate(spec.span_starts):
-            x[st:st + spec.span_len] += (amp * spec.dirs[2 + sid]).astype(np.float32)
+            x[st:st + spec.span_len] += _vec(amp * spec.dirs[2 + sid])
     return _finish(x, spec.dtype)
 
 
-def _gen_v(spec: LayerSpec, g: int) -> np.ndarray:
-    x = np.random.default_rng([spec.seed, 3, g]).standard_normal((spec.n, spec.d), dtype=np.float32)
-    return _finish(x, spec.dtype)
+def _gen_v(spec: LayerSpec, g: int, base):
+    import torch
+    return _finish(torch.from_numpy(base).to(_DEV[0]), spec.dtype)
 
 
-def make_layer(cfg: int, layer: int = 0, n: int | None = None, q_heads=None, kv_heads=None,
-               threads: int | None = None) -> dict:
-    """Generate Q [hq, n, d], K, V [hkv, n, d] (float32 arrays; bf16-exact for bf16 configs).
-
-    ``q_heads`` / ``kv_heads`` restrict generation to a subset of heads; the other heads
-    are left as zeros.  Values of a generated head do not depend on the subset chosen.
-    """
+def make_layer_torch(cfg: int, layer: int = 0, n: int | None = None, q_heads=None, kv_heads=None,
+                     threads: int | None = None, device="cpu") -> dict:
+    """Like make_layer, but returns torch tensors on ``device`` (bf16 for bf16 configs):
+    q [hq, n, d], k, v [hkv, n, d].  Heads not requested are zero.  The Gaussian background
+    is always drawn on the host (PCG64); the elementwise float32 transforms (bias, RoPE,
+    plants, rounding) are single IEEE operations, so every device gives the same bits."""
+    import torch
     spec = layer_spec(cfg, layer, n)
     n, d = spec.n, spec.d
     q_heads = list(range(spec.hq)) if q_heads is None else list(q_heads)
     kv_heads = list(range(spec.hkv)) if kv_heads is None else list(kv_heads)
-    tabs = _rope_tables(n, d)
-    q = np.zeros((spec.hq, n, d), dtype=np.float32)
-    k = np.zeros((spec.hkv, n, d), dtype=np.float32)
-    v = np.zeros((spec.hkv, n, d), dtype=np.float32)
-    nthreads = threads or min(16, os.cpu_count() or 1)
-
-    def job(item):
-        kind, h = item
-        if kind == 0:
-            q[h] = _gen_q(spec, h, tabs)
-        elif kind == 1:
-            k[h] = _gen_k(spec, h, tabs)
-        else:
-            v[h] = _gen_v(spec, h)
-
+    _DEV[0] = device
+    tabs = _rope_tables(n, d, device)
+    tdt = torch.bfloat16 if spec.dtype == "bf16" else torch.float32
+    q = torch.zeros((spec.hq, n, d), dtype=tdt, device=device)
+    k = torch.zeros((spec.hkv, n, d), dtype=tdt, device=device)
+    v = torch.zeros((spec.hkv, n, d), dtype=tdt, device=device)
     items = [(0, h) for h in q_heads] + [(1, g) for g in kv_heads] + [(2, g) for g in kv_heads]
-    if nthreads > 1 and len(items) > 1:
-        with ThreadPoolExecutor(nthreads) as ex:
-            list(ex.map(job, items))
-    else:
-        for it in items:
-            job(it)
+    keys = {0: 1, 1: 2, 2: 3}
+    nthreads = threads or min(16, os.cpu_count() or 1)
+    # Gaussian background: one PCG64 stream per head, drawn in parallel threads
+    with ThreadPoolExecutor(nthreads) as ex:
+        bases = list(ex.map(lambda it: _normals([spec.seed, keys[it[0]], it[1]], n, d), items))
+    for (kind, h), base in zip(items, bases):
+        if kind == 0:
+            q[h] = _gen_q(spec, h, tabs, base)
+        elif kind == 1:
+            k[h] = _gen_k(spec, h, tabs, base)
+        else:
+            v[h] = _gen_v(spec, h, base)
     return dict(q=q, k=k, v=v, spec=spec)
+
+
+def make_layer(cfg: int, layer: int = 0, n: int | None = None, q_heads=None, kv_heads=None,
+               threads: int | None = None) -> dict:
+    """Generate Q [hq, n, d], K, V [hkv, n, d] as float32 numpy arrays (bf16-exact for bf16
+    configs).  ``q_heads`` / ``kv_heads`` restrict generation to a subset of heads; the other
+    heads are zeros.  Values of a generated head do not depend on the subset chosen."""
+    t = make_layer_torch(cfg, layer, n, q_heads, kv_heads, threads)
+    return dict(q=t["q"].float().numpy(), k=t["k"].float().numpy(), v=t["v"].float().numpy(),
+                spec=t["spec"])
