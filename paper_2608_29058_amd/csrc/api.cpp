@@ -88,8 +88,8 @@ static rs_status check_grid(const rs_candidate *grid, int32_t ncand) {
     if (g.fam == RS_ASHAPE && g.b < 1) return fail(RS_ERR_INVALID_ARG, "A-shape window must be >= 1");
     if (g.fam == RS_BSPARSE && (g.b != 64 || g.a < 1 || g.a > 256))
       return fail(RS_ERR_UNSUPPORTED, "block-sparse needs block 64 and 1 <= k <= 256");
-    if (g.fam == RS_VSLASH && (g.a > 4096 || g.b > 1 << 20))
-      return fail(RS_ERR_UNSUPPORTED, "vertical-slash needs n_v <= 4096");
+    if (g.fam == RS_VSLASH && (g.a > 2048 || g.b > 1 << 20))
+      return fail(RS_ERR_UNSUPPORTED, "vertical-slash needs n_v <= 2048");
     if (g.a < last_a[g.fam] || g.b < last_b[g.fam])
       return fail(RS_ERR_INVALID_ARG, "candidates of a family must be listed in increasing budget order");
     last_a[g.fam] = g.a;
@@ -164,7 +164,7 @@ rs_status rs_sparse_attn_prefill(const rs_qkv *qkv, const rs_unit *units, int32_
   if (g.fam == RS_VSLASH) {
     if (!idx->vs_vsorted || !idx->vs_dsorted || !idx->vs_count || !idx->vs_vbits || !idx->vs_dbits)
       return fail(RS_ERR_INVALID_ARG, "vertical-slash arrays missing");
-    if (cl >= idx->ncand_vs || idx->nwords != (qkv->n + 31) / 32 || idx->nv_max > 4096)
+    if (cl >= idx->ncand_vs || idx->nwords != (qkv->n + 31) / 32 || idx->nv_max > 2048)
       return fail(RS_ERR_INVALID_ARG, "index set does not match the grid");
     for (int i = 0; i < nunits; ++i)
       if (units[i].slot < 0 || units[i].slot >= idx->nunits)

@@ -8,15 +8,22 @@
 //   block      S_i = {j <= i : j / 64 in Sel(i / 64)}
 //   vert-slash S_i = {j in V, j <= i} u {i - t : t in D, t <= i}
 //
-// Work decomposition: one workgroup = one query tile of BM = 32 * NW rows of one unit;
-// each wave owns 32 rows.  Keys stream through LDS in tiles of 64 (contiguous, or
-// gathered vertical columns for vertical-slash).  Per wave and key tile:
-//   S^T[64 keys x 32 rows] = K_tile (A operand, LDS) x Q^T (B operand, registers)
+// Work decomposition: one workgroup = one 128-row query tile of one unit, 4 waves of 32
+// rows each; two workgroups share a CU (<= 256 VGPRs, 64 KB LDS each), so one's softmax
+// overlaps the other's matrix work.  Keys stream through two LDS buffers in tiles of 64
+// (contiguous keys, or gathered vertical columns for vertical-slash): the next tile is
+// copied global -> LDS directly (global_load_lds_dwordx4, no registers) while the current
+// one is computed, with one barrier per tile.  K and V tiles are row-major with an XOR
+// swizzle of the 16-byte chunks.  Per wave and key tile:
+//   S^T[64 keys x 32 rows] = K_tile (A operand) x Q^T (B operand, registers)
 // with v_mfma_f32_32x32x16_bf16, so each lane holds one query row and 32 of its keys:
 // row max / row sum are in-lane plus one exchange with the other lane half.  Then
-//   O^T[d x 32 rows] += V^T (A operand, LDS, stored transposed) x P^T (B operand, the
-// softmax probabilities straight from the S^T accumulators, repacked to bf16).
-// Online softmax in the exp2 domain (logit * scale * log2 e), fp32 statistics.
+//   O^T[d x 32 rows] += V^T (A operand, read transposed with ds_read_b64_tr_b16) x P^T
+// (B operand: the probabilities straight from the S^T accumulators, packed to bf16).
+// Online softmax in the exp2 domain (logit * scale * log2 e), fp32 statistics; the running
+// max is raised only when it grows by more than 2^8, so the O rescale is rare.
+// Block-sparse: the workgroup's two 64-row query blocks walk the union of their block
+// lists; each pair of waves computes only the blocks its own query block selected.
 #include <algorithm>
 #include <cstring>
 #include <vector>
@@ -50,23 +57,40 @@ struct AttnArgs {
 };
 
 constexpr int kMaxTiles = kMaxN / 64;  // key tiles of the longest supported sequence
-constexpr int kMaxGather = 4096;       // vertical columns gathered per query tile
+constexpr int kMaxGather = 2048;       // vertical columns gathered per query tile
 
-template <int D, int NW, int PAT, typename InT>
-__global__ void __launch_bounds__(NW * 64) attn_fwd_kernel(const AttnArgs a) {
-  constexpr int NT = NW * 64;
-  constexpr int BM = NW * 32;
+// XOR swizzle of the 16-byte chunk index of LDS row r.  K fragment reads (8 consecutive
+// rows, one chunk) and transposed V reads (4 consecutive rows, 2 adjacent chunks) then hit
+// 8 distinct chunk positions, i.e. distinct banks.
+__device__ __forceinline__ int swz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void lds_fence_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Per-tile description produced ahead of its use (the next tile is issued while the
+// current one is computed).
+struct TileRef {
+  int key0;  // first key of a contiguous tile, or -(1 + gather offset)
+  int tag;   // bit 0: rows of waves 0-1 use it, bit 1: rows of waves 2-3 (block-sparse)
+};
+
+template <int D, int PAT, typename InT>
+__global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const AttnArgs a) {
+  constexpr int NW = 4, NT = 256, BM = 128;
   constexpr int KS = D / 16;             // k-steps of the QK^T contraction
   constexpr int DB = D / 32;             // 32-row blocks of O^T
-  constexpr int KSTR = D + 8;            // K row stride in LDS (bf16), padded
-  constexpr int VSTR = 64 + 4;           // V^T row stride in LDS (bf16), padded
-  constexpr int KCH_TOT = 64 * (D / 8);  // 16-byte chunks of a K tile
-  constexpr int KCH = (KCH_TOT + NT - 1) / NT;
-  constexpr int VBL_TOT = 16 * (D / 8);  // 4-key x 8-dim blocks of a V tile
-  constexpr int VBL = (VBL_TOT + NT - 1) / NT;
+  constexpr int CPR = D / 8;             // 16-byte chunks per K/V row
+  constexpr int RPI = 64 / CPR;          // rows covered by one wave-wide 16-byte load
+  constexpr int LPT = 64 / RPI / NW;     // loads per thread per K (or V) tile
+  constexpr int TE = 64 * D;             // elements of one K or V tile
 
-  __shared__ __align__(16) bf16 sK[64 * KSTR];
-  __shared__ __align__(16) bf16 sV[D * VSTR];
+  __shared__ __align__(16) bf16 sKV0[2 * TE];  // [K tile | V tile], row-major, swizzled
+  __shared__ __align__(16) bf16 sKV1[2 * TE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -83,28 +107,27 @@ __global__ void __launch_bounds__(NW * 64) attn_fwd_kernel(const AttnArgs a) {
   const int w_lo = max(r_lo, wbase), w_hi = min(r_hi, wbase + 32) - 1;
   const bool wave_active = w_lo <= w_hi;
   const int my_row = wbase + l32;
+  const int last_tile = (r_hi - 1) >> 6;
 
   const InT *Qp = (const InT *)a.q + (long long)head * a.sq_h;
   const InT *Kp = (const InT *)a.k + (long long)kvh * a.sk_h;
   const InT *Vp = (const InT *)a.v + (long long)kvh * a.sv_h;
 
-  // ---- pattern state ---------------------------------------------------------------------
+  // ---- tile enumeration state ----------------------------------------------------------
   int ntiles = 0;
-  int ash_ns = 0, ash_start2 = 0;
-  const int *bs_list = nullptr;
+  int st0 = 0, st1 = 0;  // pattern cursors
+  const int *bs_a = nullptr, *bs_b = nullptr;
+  int bs_na = 0, bs_nb = 0;
   const uint32_t *vbits = nullptr, *dbits = nullptr;
   int n_contig = 0, n_gather = 0;
-  const int last_tile = (r_hi - 1) >> 6;
+  uint32_t *sTB = nullptr;
+  int *sG = nullptr;
 
-  // vertical-slash planning storage (only instantiated for that pattern)
-  int *sTL = nullptr, *sG = nullptr;
   if constexpr (PAT == P_VS) {
-    __shared__ uint32_t sTB[kMaxTiles / 32];
-    __shared__ int sTLbuf[kMaxTiles];
+    __shared__ uint32_t sTBbuf[kMaxTiles / 32];
     __shared__ int sGbuf[kMaxGather];
     __shared__ int sScan[NW + 1];
-    __shared__ int sWordPre[kMaxTiles / 32 + 1];
-    sTL = sTLbuf;
+    sTB = sTBbuf;
     sG = sGbuf;
     const long long vsrow = (long long)U.slot * a.ncand_vs + U.cl;
     const int *vsorted = a.vs_vsorted + vsrow * a.nv_max;
@@ -116,7 +139,7 @@ __global__ void __launch_bounds__(NW * 64) attn_fwd_kernel(const AttnArgs a) {
     const int nwt = (last_tile >> 5) + 1;
     for (int w = tid; w < nwt; w += NT) sTB[w] = 0u;
     __syncthreads();
-    // slash lines: diagonal t covers keys [r_lo - t, r_hi - 1 - t] of this tile's rows
+    // diagonal t covers keys [r_lo - t, r_hi - 1 - t] of this tile's rows
     for (int x = tid; x < ndc; x += NT) {
       const int t = dsorted[x];
       if (t < 0 || t > r_hi - 1) continue;
@@ -124,32 +147,18 @@ __global__ void __launch_bounds__(NW * 64) attn_fwd_kernel(const AttnArgs a) {
       for (int kt = lo; kt <= hi; ++kt) atomicOr(&sTB[kt >> 5], 1u << (kt & 31));
     }
     __syncthreads();
-    if (tid == 0) {
-      int acc = 0;
-      for (int w = 0; w < nwt; ++w) {
-        sWordPre[w] = acc;
-        acc += __builtin_popcount(sTB[w]);
-      }
-      sWordPre[nwt] = acc;
+    {
+      int cnt = 0;
+      for (int w = 0; w < nwt; ++w) cnt += __builtin_popcount(sTB[w]);
+      n_contig = cnt;
     }
-    __syncthreads();
-    for (int w = tid; w < nwt; w += NT) {
-      uint32_t b = sTB[w];
-      int p = sWordPre[w];
-      while (b) {
-        const int bit = __builtin_ctz(b);
-        b &= b - 1;
-        sTL[p++] = w * 32 + bit;
-      }
-    }
-    n_contig = sWordPre[nwt];
-    // vertical columns outside the slash tiles are gathered (ascending order kept)
+    // vertical columns outside the diagonal tiles are gathered, ascending
     int total = 0;
     for (int x0 = 0; x0 < nvc; x0 += NT) {
       const int x = x0 + tid;
-      int j = (x < nvc) ? vsorted[x] : 0x7fffffff;
+      const int j = (x < nvc) ? vsorted[x] : 0x7fffffff;
       bool f = false;
-      if (x < nvc && j <= r_hi - 1) {
+      if (x < nvc && j >= 0 && j <= r_hi - 1) {
         const int kt = j >> 6;
         f = !((sTB[kt >> 5] >> (kt & 31)) & 1u);
       }
@@ -157,44 +166,80 @@ __global__ void __launch_bounds__(NW * 64) attn_fwd_kernel(const AttnArgs a) {
       const int before = __popcll(bal & ((1ull << lane) - 1ull));
       if (lane == 0) sScan[wave] = __popcll(bal);
       __syncthreads();
-      int woff = total;
-      for (int w = 0; w < wave; ++w) woff += sScan[w];
-      int blk = 0;
-      for (int w = 0; w < NW; ++w) blk += sScan[w];
+      int woff = total, blk = 0;
+      for (int w = 0; w < NW; ++w) {
+        if (w < wave) woff += sScan[w];
+        blk += sScan[w];
+      }
       if (f && woff + before < kMaxGather) sG[woff + before] = j;
       total += blk;
       __syncthreads();
-      if (x0 + NT <= nvc) {
-        const int jl = vsorted[min(x0 + NT - 1, nvc - 1)];
-        if (jl > r_hi - 1) break;  // sorted: later columns are all beyond the tile
-      }
+      if (x0 + NT <= nvc && vsorted[x0 + NT - 1] > r_hi - 1) break;  // sorted: rest is beyond
     }
     n_gather = min(total, kMaxGather);
     __syncthreads();
     ntiles = n_contig + (n_gather + 63) / 64;
+    st0 = 0;                         // bitmap word of the next contiguous tile
+    st1 = nwt > 0 ? (int)sTB[0] : 0; // remaining bits of that word
   } else if constexpr (PAT == P_DENSE) {
     ntiles = last_tile + 1;
   } else if constexpr (PAT == P_ASHAPE) {
-    ash_ns = min((a.sink + 63) >> 6, last_tile + 1);
+    const int ns = min((a.sink + 63) >> 6, last_tile + 1);
     const int wlo = max(0, r_lo - a.window + 1) >> 6;
-    ash_start2 = max(wlo, ash_ns);
-    ntiles = ash_ns + max(0, last_tile - ash_start2 + 1);
-  } else {  // P_BS: one 64-row query block per workgroup
+    st0 = ns;
+    st1 = max(wlo, ns);
+    ntiles = ns + max(0, last_tile - st1 + 1);
+  } else {  // P_BS: query blocks bq = base/64 (waves 0-1) and bq + 1 (waves 2-3)
     const int bq = base >> 6;
     const long long brow = ((long long)head * a.ncand_bs + U.cl) * a.nb + bq;
-    bs_list = a.bs_sorted + brow * a.k_max;
-    ntiles = a.bs_count[brow];
+    if (r_lo < base + 64) {
+      bs_a = a.bs_sorted + brow * a.k_max;
+      bs_na = a.bs_count[brow];
+    }
+    if (r_hi > base + 64 && bq + 1 < a.nb) {
+      bs_b = a.bs_sorted + (brow + 1) * a.k_max;
+      bs_nb = a.bs_count[brow + 1];
+    }
+    // size of the merged (union) list
+    int ia = 0, ib = 0, cnt = 0;
+    while (ia < bs_na || ib < bs_nb) {
+      const int va = ia < bs_na ? bs_a[ia] : 0x7fffffff;
+      const int vb = ib < bs_nb ? bs_b[ib] : 0x7fffffff;
+      ia += va <= vb;
+      ib += vb <= va;
+      ++cnt;
+    }
+    ntiles = cnt;
   }
 
-  // tile t -> first key (contiguous) or -(1 + gather offset) (gathered)
-  auto tile_key = [&](int t) -> int {
-    if constexpr (PAT == P_DENSE) return t * 64;
-    else if constexpr (PAT == P_ASHAPE) return (t < ash_ns ? t : ash_start2 + (t - ash_ns)) * 64;
-    else if constexpr (PAT == P_BS) return bs_list[t] * 64;
-    else return t < n_contig ? sTL[t] * 64 : -(1 + (t - n_contig) * 64);
+  // next tile in order (t increases by one per call)
+  int t_next = 0;
+  auto next_tile = [&]() -> TileRef {
+    const int t = t_next++;
+    if constexpr (PAT == P_DENSE) {
+      return TileRef{t * 64, 3};
+    } else if constexpr (PAT == P_ASHAPE) {
+      return TileRef{(t < st0 ? t : st1 + (t - st0)) * 64, 3};
+    } else if constexpr (PAT == P_BS) {
+      const int va = st0 < bs_na ? bs_a[st0] : 0x7fffffff;
+      const int vb = st1 < bs_nb ? bs_b[st1] : 0x7fffffff;
+      const int v = min(va, vb);
+      const int tag = (va == v ? 1 : 0) | (vb == v ? 2 : 0);
+      st0 += va == v;
+      st1 += vb == v;
+      return TileRef{v * 64, tag};
+    } else {
+      if (t < n_contig) {
+        while (st1 == 0) st1 = (int)sTB[++st0];
+        const int bit = __builtin_ctz((uint32_t)st1);
+        st1 &= st1 - 1;
+        return TileRef{(st0 * 32 + bit) * 64, 3};
+      }
+      return TileRef{-(1 + (t - n_contig) * 64), 3};
+    }
   };
 
-  // ---- Q fragment in registers (B operand of QK^T) ------------------------------------------
+  // ---- Q fragment in registers (B operand of QK^T) ---------------------------------------
   u32x4 qf[KS];
   {
     const bool ok = wave_active && my_row < a.n;
@@ -205,75 +250,50 @@ __global__ void __launch_bounds__(NW * 64) attn_fwd_kernel(const AttnArgs a) {
     }
   }
 
-  // ---- global -> register tile loader ----------------------------------------------------
-  u32x4 kr[KCH];
-  u32x4 vr[VBL][4];
-  auto key_of = [&](int key0, int kk) -> int {
+  // ---- tile loads: global -> LDS (direct for bf16, through registers for fp32) ----------
+  auto key_of_row = [&](int key0, int row) -> int {
     if constexpr (PAT == P_VS) {
       if (key0 < 0) {
-        const int g = -key0 - 1 + kk;
-        return g < n_gather ? sG[g] : -1;
+        const int g = -key0 - 1 + row;
+        return sG[g < n_gather ? g : -key0 - 1];
       }
     }
-    const int j = key0 + kk;
-    return j < a.n ? j : -1;
+    return min(key0 + row, a.n - 1);
   };
-  auto load_tile = [&](int key0) {
+  auto issue_tile = [&](bf16 *dstKV, int key0) {
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int cidx = tid + i * NT;
-      kr[i] = u32x4{0u, 0u, 0u, 0u};
-      if (cidx < KCH_TOT) {
-        const int row = cidx / (D / 8), cc = cidx % (D / 8);
-        const int j = key_of(key0, row);
-        if (j >= 0) kr[i] = load8<InT>(Kp + (long long)j * a.sk_t + 8 * cc);
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < VBL; ++i) {
-      const int b = tid + i * NT;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) vr[i][e] = u32x4{0u, 0u, 0u, 0u};
-      if (b < VBL_TOT) {
-        const int dg = b / 16, kg = b % 16;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int j = key_of(key0, 4 * kg + e);
-          if (j >= 0) vr[i][e] = load8<InT>(Vp + (long long)j * a.sv_t + 8 * dg);
-        }
-      }
-    }
-  };
-  auto store_tile = [&]() {
-#pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int cidx = tid + i * NT;
-      if (cidx < KCH_TOT) {
-        const int row = cidx / (D / 8), cc = cidx % (D / 8);
-        *(u32x4 *)&sK[row * KSTR + 8 * cc] = kr[i];
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < VBL; ++i) {
-      const int b = tid + i * NT;
-      if (b < VBL_TOT) {
-        const int dg = b / 16, kg = b % 16;
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          const uint32_t e0 = vr[i][0][w], e1 = vr[i][1][w], e2 = vr[i][2][w], e3 = vr[i][3][w];
-          u32x2 lo, hi;
-          lo[0] = (e0 & 0xffffu) | (e1 << 16);
-          lo[1] = (e2 & 0xffffu) | (e3 << 16);
-          hi[0] = (e0 >> 16) | (e1 & 0xffff0000u);
-          hi[1] = (e2 >> 16) | (e3 & 0xffff0000u);
-          *(u32x2 *)&sV[(8 * dg + 2 * w) * VSTR + 4 * kg] = lo;
-          *(u32x2 *)&sV[(8 * dg + 2 * w + 1) * VSTR + 4 * kg] = hi;
-        }
+    for (int i = 0; i < LPT; ++i) {
+      const int row_base = (i * NW + wave) * RPI;
+      const int row = row_base + lane / CPR;
+      const int c = (lane % CPR) ^ swz(row);
+      const int j = key_of_row(key0, row);
+      if constexpr (sizeof(InT) == 2) {
+        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)(Kp + (long long)j * a.sk_t + 8 * c),
+                                         (__attribute__((address_space(3))) void *)(dstKV + row_base * D), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)(Vp + (long long)j * a.sv_t + 8 * c),
+                                         (__attribute__((address_space(3))) void *)(dstKV + TE + row_base * D), 16, 0, 0);
+      } else {
+        const u32x4 kx = load8<InT>(Kp + (long long)j * a.sk_t + 8 * c);
+        const u32x4 vx = load8<InT>(Vp + (long long)j * a.sv_t + 8 * c);
+        *(u32x4 *)(dstKV + row_base * D + 8 * lane) = kx;
+        *(u32x4 *)(dstKV + TE + row_base * D + 8 * lane) = vx;
       }
     }
   };
 
-  // ---- main loop -------------------------------------------------------------------------
+  // ---- per-lane LDS fragment offsets -----------------------------------------------------
+  const int kswz = swz(l32);                 // K rows 32 mb + l32
+  const int g16 = lane >> 4, i16 = lane & 15;
+  const int esrc = i16 >> 2, qv = i16 & 3;   // transposed V read: source row / dd quad
+  const int vrow = 4 * hh + esrc;            // + 32 mb + 16 s + 8 half
+  const int vsw = 2 * esrc + hh;             // swz(vrow + ...) is lane-constant
+  int voff[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    const int dd0 = 32 * db + 16 * (g16 & 1) + 4 * qv;
+    voff[db] = vrow * D + (((dd0 >> 3) ^ vsw) << 3) + (dd0 & 7);
+  }
+
   f32x16 oacc[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db)
@@ -281,41 +301,31 @@ __global__ void __launch_bounds__(NW * 64) attn_fwd_kernel(const AttnArgs a) {
     for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
   const float c = a.c;
+  const int my_rows_tag = wave < 2 ? 1 : 2;
 
-  int key_next = ntiles > 0 ? tile_key(0) : 0;
-  if (ntiles > 0) load_tile(key_next);
-
-  for (int t = 0; t < ntiles; ++t) {
-    __syncthreads();
-    store_tile();
-    __syncthreads();
-    const int key0 = key_next;
-    if (t + 1 < ntiles) {
-      key_next = tile_key(t + 1);
-      load_tile(key_next);
-    }
-    if (!wave_active) continue;
-
-    // wave-uniform skip / mask decisions
+  auto compute_tile = [&](const bf16 *sKV, TileRef tr) {
+    const int key0 = tr.key0;
+    if (!wave_active || !(tr.tag & my_rows_tag)) return;
     bool need_mask = true;
-    int g_cnt = 0;
+    int g_cnt = 0, g0 = 0;
     if constexpr (PAT == P_VS) {
       if (key0 < 0) {
-        const int g0 = -key0 - 1;
+        g0 = -key0 - 1;
         g_cnt = min(64, n_gather - g0);
-        if (sG[g0] > w_hi) continue;
+        if (sG[g0] > w_hi) return;
       } else if (key0 > w_hi) {
-        continue;
+        return;
       }
     } else {
-      if (key0 > w_hi) continue;
+      if (key0 > w_hi) return;
       if constexpr (PAT == P_ASHAPE) {
-        if (key0 >= a.sink && key0 + 63 < w_lo - a.window + 1) continue;
+        if (key0 >= a.sink && key0 + 63 < w_lo - a.window + 1) return;
         need_mask = !(key0 + 63 <= w_lo && (key0 + 63 < a.sink || key0 > w_hi - a.window));
       } else {
         need_mask = key0 + 63 > w_lo;
       }
     }
+    const bf16 *sK = sKV, *sV = sKV + TE;
 
     f32x16 sacc[2];
 #pragma unroll
@@ -324,7 +334,7 @@ __global__ void __launch_bounds__(NW * 64) attn_fwd_kernel(const AttnArgs a) {
       for (int r = 0; r < 16; ++r) sacc[mb][r] = 0.f;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        const u32x4 kf = *(const u32x4 *)&sK[(32 * mb + l32) * KSTR + 16 * ks + 8 * hh];
+        const u32x4 kf = *(const u32x4 *)&sK[(32 * mb + l32) * D + (((2 * ks + hh) ^ kswz) << 3)];
         sacc[mb] = mfma32(kf, qf[ks], sacc[mb]);
       }
     }
@@ -334,7 +344,6 @@ __global__ void __launch_bounds__(NW * 64) attn_fwd_kernel(const AttnArgs a) {
       uint64_t M;
       if constexpr (PAT == P_VS) {
         if (key0 < 0) {
-          const int g0 = -key0 - 1;
           int lo = 0, hi = g_cnt;
           while (lo < hi) {
             const int mid = (lo + hi) >> 1;
@@ -343,8 +352,7 @@ __global__ void __launch_bounds__(NW * 64) attn_fwd_kernel(const AttnArgs a) {
           }
           M = prefix_mask(lo);
         } else {
-          const uint64_t w = bits64_at(dbits, a.nwords, i - key0 - 63);
-          const uint64_t md = __builtin_bitreverse64(w);
+          const uint64_t md = __builtin_bitreverse64(bits64_at(dbits, a.nwords, i - key0 - 63));
           const uint64_t mv = bits64_at(vbits, a.nwords, key0);
           M = (md | mv) & prefix_mask(i - key0 + 1);
         }
@@ -364,17 +372,27 @@ __global__ void __launch_bounds__(NW * 64) attn_fwd_kernel(const AttnArgs a) {
         }
     }
 
-    // online softmax (exp2 domain)
+    // online softmax, exp2 domain; the running max is only raised when a row's tile max
+    // exceeds it by more than 2^8 (probabilities stay <= 256 in between)
     float mx = -INFINITY;
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[mb][r]);
     mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
-    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    const float alpha = __builtin_amdgcn_exp2f((m_run - m_use) * c);
-    const float nmc = -m_use * c;
+    const bool raise = (mx - m_run) * c > 8.f;
+    if (__ballot(raise) != 0ull) {
+      const float m_new = fmaxf(m_run, mx);
+      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+      const float alpha = __builtin_amdgcn_exp2f((m_run - m_use) * c);
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+      m_run = m_new;
+    }
+    const float nmc = (m_run == -INFINITY) ? 0.f : -m_run * c;
     float psum = 0.f;
     u32x4 pb[2][2];
 #pragma unroll
@@ -388,28 +406,48 @@ __global__ void __launch_bounds__(NW * 64) attn_fwd_kernel(const AttnArgs a) {
           psum += p0 + p1;
           pb[mb][s][w] = pack_bf16x2(p0, p1);
         }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+    l_run += psum;
 
+    // O^T += V^T P^T; V read transposed from its row-major tile
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
-          const bf16 *vp = &sV[(32 * db + l32) * VSTR + 32 * mb + 16 * s + 4 * hh];
-          const u32x2 lo = *(const u32x2 *)vp;
-          const u32x2 hi = *(const u32x2 *)(vp + 8);
-          const u32x4 af = u32x4{lo[0], lo[1], hi[0], hi[1]};
+          const bf16 *vp = sV + voff[db] + (32 * mb + 16 * s) * D;
+          const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16 *)(vp));
+          const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16 *)(vp + 8 * D));
+          const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
+          const u32x4 af = u32x4{l2[0], l2[1], h2[0], h2[1]};
           oacc[db] = mfma32(af, pb[mb][s], oacc[db]);
         }
+  };
+
+  // ---- main loop: one barrier per tile, next tile in flight during compute --------------
+  TileRef cur{0, 0};
+  if (ntiles > 0) {
+    cur = next_tile();
+    issue_tile(sKV0, cur.key0);
+  }
+  for (int t = 0; t < ntiles; t += 2) {
+    lds_fence_barrier();  // tile t resident in sKV0; everyone done with sKV1
+    TileRef nxt{0, 0};
+    if (t + 1 < ntiles) {
+      nxt = next_tile();
+      issue_tile(sKV1, nxt.key0);
+    }
+    compute_tile(sKV0, cur);
+    if (t + 1 >= ntiles) break;
+    lds_fence_barrier();  // tile t+1 resident in sKV1; everyone done with sKV0
+    if (t + 2 < ntiles) {
+      cur = next_tile();
+      issue_tile(sKV0, cur.key0);
+    }
+    compute_tile(sKV1, nxt);
   }
 
-  // ---- epilogue ----------------------------------------------------------------------------
+  // ---- epilogue --------------------------------------------------------------------------
   if (!wave_active) return;
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   const int i = my_row;
@@ -431,13 +469,13 @@ __global__ void __launch_bounds__(NW * 64) attn_fwd_kernel(const AttnArgs a) {
 
 // ---- host side ---------------------------------------------------------------------------
 
-static int family_bm(int fam) { return (fam == RS_DENSE || fam == RS_ASHAPE) ? 128 : 64; }
+static int family_bm(int) { return 128; }
 
 static int tiles_of(const rs_unit &u, int bm) { return (u.s1 - 1) / bm - u.s0 / bm + 1; }
 
 size_t attn_ws_bytes(const rs_unit *units, int32_t nunits) {
   size_t items = 0;
-  for (int i = 0; i < nunits; ++i) items += (size_t)tiles_of(units[i], 64);
+  for (int i = 0; i < nunits; ++i) items += (size_t)tiles_of(units[i], 128);
   Arena ar(nullptr, 0);
   ar.take<DevUnit>((size_t)nunits);
   ar.take<int>(items);
@@ -467,22 +505,22 @@ static void build_order(const rs_unit *units, int nunits, int group, int bm,
       if (i < buckets[b].size()) order.push_back(buckets[b][i].second);
 }
 
-template <int D, int NW, int PAT>
+template <int D, int PAT>
 static hipError_t launch_pat(int dtype, const AttnArgs &a, int nitems, hipStream_t st) {
   if (dtype == RS_BF16)
-    hipLaunchKernelGGL((attn_fwd_kernel<D, NW, PAT, bf16>), dim3(nitems), dim3(NW * 64), 0, st, a);
+    hipLaunchKernelGGL((attn_fwd_kernel<D, PAT, bf16>), dim3(nitems), dim3(256), 0, st, a);
   else
-    hipLaunchKernelGGL((attn_fwd_kernel<D, NW, PAT, float>), dim3(nitems), dim3(NW * 64), 0, st, a);
+    hipLaunchKernelGGL((attn_fwd_kernel<D, PAT, float>), dim3(nitems), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
 template <int D>
 static hipError_t launch_d(int fam, int dtype, const AttnArgs &a, int nitems, hipStream_t st) {
   switch (fam) {
-    case RS_DENSE: return launch_pat<D, 4, P_DENSE>(dtype, a, nitems, st);
-    case RS_ASHAPE: return launch_pat<D, 4, P_ASHAPE>(dtype, a, nitems, st);
-    case RS_VSLASH: return launch_pat<D, 2, P_VS>(dtype, a, nitems, st);
-    default: return launch_pat<D, 2, P_BS>(dtype, a, nitems, st);
+    case RS_DENSE: return launch_pat<D, P_DENSE>(dtype, a, nitems, st);
+    case RS_ASHAPE: return launch_pat<D, P_ASHAPE>(dtype, a, nitems, st);
+    case RS_VSLASH: return launch_pat<D, P_VS>(dtype, a, nitems, st);
+    default: return launch_pat<D, P_BS>(dtype, a, nitems, st);
   }
 }
 
