@@ -8,7 +8,8 @@ sparse/dense attention launch per (pattern, budget) group.  Each head is split i
 segments of 16K rows (units).  The reported value is ms per layer (lower is better).
 
 Before timing (offline calibration, untimed): the kernel latency of every candidate is
-profiled per 16K key-length bucket on layer 0 (median of 3), the probe/route overhead is
+profiled per 16K key-length bucket on layer 0 (per-unit time of a launch over one key/value
+group's query heads, median over groups and over 3 reps), the probe/route overhead is
 measured, and the layer budget is T = (dense time of the layer) / 6.5.
 
     python bench.py [--steps K] [--warmup W] [--layers L] [--no-cpu-baseline]
@@ -196,19 +197,25 @@ def main():
     RL.probe_and_index(qkv0)
     torch.cuda.synchronize()
     edges = np.array([SEG * (b + 1) for b in range(N // SEG)], np.int32)
+    # t_ker(p, b, n): per candidate and key-length bucket, the median over key/value groups of
+    # the per-unit time of one launch holding that group's query heads (median of 3 reps)
     t_table = np.zeros((len(GRID), len(edges)))
     for c in range(len(GRID)):
         for b in range(len(edges)):
-            us = [i for i, u in enumerate(RL.unit_list) if u[2] == edges[b]]
-            ts = []
-            for _ in range(3):
-                a = ev()
-                RL.run_group(qkv0, c, us)
-                z = ev()
-                z.synchronize()
-                ts.append(a.elapsed_time(z))
-            t_table[c, b] = float(np.median(ts)) * 1e3 / len(us)
-    log("t_ker (us/unit) dense:", np.round(t_table[0], 1).tolist())
+            per_group = []
+            for g in range(HKV):
+                us = [i for i, u in enumerate(RL.unit_list) if u[2] == edges[b] and u[0] // (HQ // HKV) == g]
+                ts = []
+                for _ in range(3):
+                    a = ev()
+                    RL.run_group(qkv0, c, us)
+                    z = ev()
+                    z.synchronize()
+                    ts.append(a.elapsed_time(z))
+                per_group.append(float(np.median(ts)) / len(us))
+            t_table[c, b] = float(np.median(per_group)) * 1e3
+    for c in range(len(GRID)):
+        log(f"t_ker {GRID[c]} (us/unit):", np.round(t_table[c], 1).tolist())
     # probe + index + coverage time, and the host routing overhead
     tp = []
     for _ in range(3):

@@ -23,7 +23,7 @@
 namespace rs {
 
 constexpr int kProbeMaxRows = 256;  // sampled rows per unit
-constexpr int kChunk = 256;         // keys per workgroup in passes 2 and 3
+constexpr int kChunk = 128;         // keys per workgroup in the three passes
 constexpr int kMaxCand = 16;
 
 struct ProbeUnit {
@@ -43,6 +43,7 @@ struct ProbeArgs {
   float c, scale;
   int local_w;
   const ProbeUnit *units;
+  const int4 *groups;  // up to 4 units sharing a key/value head and a segment (-1 pads)
   const int *rows, *subset;
   float *row_max, *row_sum;
   // pass 2 partials / outputs
@@ -58,33 +59,6 @@ struct ProbeArgs {
   float *cov_part;
 };
 
-// K rows [k0 + 32 mb + l32] as MFMA A fragments, straight from global memory.
-template <int D, typename InT>
-__device__ __forceinline__ void load_k_frag(const InT *Kp, long long sk_t, int n, int k0, int l32,
-                                            int hh, u32x4 (&kf)[2][D / 16]) {
-#pragma unroll
-  for (int mb = 0; mb < 2; ++mb) {
-    const int j = k0 + 32 * mb + l32;
-#pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) {
-      kf[mb][ks] = u32x4{0u, 0u, 0u, 0u};
-      if (j < n) kf[mb][ks] = load8<InT>(Kp + (long long)j * sk_t + 16 * ks + 8 * hh);
-    }
-  }
-}
-
-template <int D>
-__device__ __forceinline__ void qk_tile(const u32x4 (&kf)[2][D / 16], const u32x4 (&qf)[D / 16],
-                                        f32x16 (&s)[2]) {
-#pragma unroll
-  for (int mb = 0; mb < 2; ++mb) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) s[mb][r] = 0.f;
-#pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) s[mb] = mfma32(kf[mb][ks], qf[ks], s[mb]);
-  }
-}
-
 // Orders this wave's LDS writes before its following LDS reads by other lanes.
 __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -97,113 +71,88 @@ __device__ __forceinline__ int acc_key(int mb, int r, int hh) {
   return 32 * mb + 8 * (r >> 2) + 4 * hh + (r & 3);
 }
 
-// ---- pass 1: row statistics -----------------------------------------------------------------
-// grid: (row block, unit); 4 waves split the key tiles of the unit round-robin.
-template <int D, typename InT>
-__global__ void __launch_bounds__(256) probe_stats_kernel(const ProbeArgs a) {
-  const int rb = blockIdx.x, u = blockIdx.y;
-  const ProbeUnit U = a.units[u];
-  if (32 * rb >= U.nrows) return;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, hh = lane >> 5;
-  const int ridx = 32 * rb + l32;
-  const int row = ridx < U.nrows ? a.rows[(long long)u * a.rmax + ridx] : -1;
-  int maxrow = 0;
-  for (int x = 32 * rb; x < min(U.nrows, 32 * rb + 32); ++x) maxrow = max(maxrow, a.rows[(long long)u * a.rmax + x]);
-  const InT *Qp = (const InT *)a.q + (long long)U.head * a.sq_h;
-  const InT *Kp = (const InT *)a.k + (long long)(U.head / a.group) * a.sk_h;
-  u32x4 qf[D / 16];
-#pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks) {
-    qf[ks] = u32x4{0u, 0u, 0u, 0u};
-    if (row >= 0) qf[ks] = load8<InT>(Qp + (long long)row * a.sq_t + 16 * ks + 8 * hh);
-  }
-  float m_run = -INFINITY, l_run = 0.f;
-  const int ntile = (maxrow >> 6) + 1;
-  for (int kt = wave; kt < ntile; kt += 4) {
-    u32x4 kf[2][D / 16];
-    load_k_frag<D, InT>(Kp, a.sk_t, a.n, 64 * kt, l32, hh, kf);
-    f32x16 s[2];
-    qk_tile<D>(kf, qf, s);
-    float mx = -INFINITY;
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int j = 64 * kt + acc_key(mb, r, hh);
-        if (j > row) s[mb][r] = -INFINITY;
-        mx = fmaxf(mx, s[mb][r]);
-      }
-    const float m_new = fmaxf(m_run, mx);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    float ps = 0.f;
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) ps += __builtin_amdgcn_exp2f((s[mb][r] - m_use) * a.c);
-    l_run = l_run * __builtin_amdgcn_exp2f((m_run - m_use) * a.c) + ps;
-    m_run = m_new;
-  }
-  // combine the two lane halves, then the four waves
-  __shared__ float sm[4][32], sl[4][32];
-  {
-    const float mo = __shfl_xor(m_run, 32), lo = __shfl_xor(l_run, 32);
-    const float mm = fmaxf(m_run, mo);
-    const float mu = mm == -INFINITY ? 0.f : mm;
-    const float ll = l_run * __builtin_amdgcn_exp2f((m_run - mu) * a.c) + lo * __builtin_amdgcn_exp2f((mo - mu) * a.c);
-    if (hh == 0) {
-      sm[wave][l32] = mm;
-      sl[wave][l32] = ll;
-    }
-  }
-  __syncthreads();
-  if (tid < 32 && ridx < U.nrows) {
-    float M = -INFINITY;
-    for (int w = 0; w < 4; ++w) M = fmaxf(M, sm[w][tid]);
-    float L = 0.f;
-    for (int w = 0; w < 4; ++w) L += sl[w][tid] * __builtin_amdgcn_exp2f((sm[w][tid] - M) * a.c);
-    a.row_max[(long long)u * a.rmax + ridx] = M * a.scale;
-    a.row_sum[(long long)u * a.rmax + ridx] = L;
-  }
+__device__ __forceinline__ int swz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
+
+// Barrier after which every wave's direct-to-LDS copies (global_load_lds, counted by
+// vmcnt) and LDS accesses are complete.  The explicit vmcnt wait is required: the
+// compiler's LDS release fence does not always wait for the LDS DMA.
+__device__ __forceinline__ void lds_fence_barrier() {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-// ---- passes 2 and 3: normalised probabilities over one 256-key chunk --------------------
-// grid: (chunk, unit); wave w handles row blocks w, w+4, ... against the chunk's 4 tiles.
-template <int D, typename InT, bool COVER>
+enum { M_STATS = 0, M_SCORES = 1, M_COVER = 2 };
+
+// ---- the three passes over one 128-key chunk --------------------------------------------
+// grid: (chunk, unit group).  A group holds the units of up to 4 query heads that share a
+// key/value head and a segment, hence the same sampled rows and keys: the chunk's keys are
+// copied to LDS once (row-major, XOR-swizzled 16-byte chunks) and wave w handles every
+// sampled-row block of the group's unit w against the chunk's 2 tiles.
+//   M_STATS   per (row, chunk): max and sum of exp over the chunk's visible keys
+//   M_SCORES  normalised a_ij -> col, diagonal partials, block entropy, local mass
+//   M_COVER   normalised a_ij -> per-candidate kept mass
+template <int D, typename InT, int MODE>
 __global__ void __launch_bounds__(256) probe_chunk_kernel(const ProbeArgs a) {
-  const int ch = blockIdx.x, u = blockIdx.y;
-  const ProbeUnit U = a.units[u];
+  constexpr int CPR = D / 8, RPI = 64 / CPR;
+  constexpr int NLOAD = kChunk / RPI / 4;  // 16-byte loads per thread for the chunk
+  constexpr int NT = kChunk / 64;          // tiles per chunk
+  const int ch = blockIdx.x;
+  const int4 grp = a.groups[blockIdx.y];
+  const ProbeUnit U0 = a.units[grp.x];     // shared head group, segment and sampled rows
   const int c0 = ch * kChunk;
-  if (c0 >= U.s1) return;
+  if (c0 >= U0.s1) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, hh = lane >> 5;
-  const InT *Qp = (const InT *)a.q + (long long)U.head * a.sq_h;
-  const InT *Kp = (const InT *)a.k + (long long)(U.head / a.group) * a.sk_h;
-  const int nrb = (U.nrows + 31) / 32;
+  const int u = wave == 0 ? grp.x : wave == 1 ? grp.y : wave == 2 ? grp.z : grp.w;
+  const InT *Kp = (const InT *)a.k + (long long)(U0.head / a.group) * a.sk_h;
 
-  __shared__ float sP[4][32][65];                // per-wave probability tile [row][key]
-  __shared__ int sRows[4][32];                   // sampled rows of each wave's block
-  __shared__ float sCol[4][kChunk];              // per-wave column sums
-  __shared__ float sDg[4][kChunk + kProbeMaxRows];  // per-wave diagonal partials
-  const int dw = kChunk + U.nR;                  // diagonals touched by R rows in this chunk
-  const int dbase = U.r0 - (c0 + kChunk - 1);    // smallest such diagonal
-  if constexpr (!COVER) {
-    for (int x = tid; x < 4 * kChunk; x += 256) (&sCol[0][0])[x] = 0.f;
-    for (int x = lane; x < dw; x += 64) sDg[wave][x] = 0.f;
+  __shared__ __align__(16) bf16 sK[kChunk * D];
+  __shared__ int sRows[4][32];
+#pragma unroll
+  for (int i = 0; i < NLOAD; ++i) {
+    const int row_base = (i * 4 + wave) * RPI;
+    const int row = row_base + lane / CPR;
+    const int cc = (lane % CPR) ^ swz(row);
+    const int j = min(c0 + row, a.n - 1);
+    if constexpr (sizeof(InT) == 2) {
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)(Kp + (long long)j * a.sk_t + 8 * cc),
+                                       (__attribute__((address_space(3))) void *)(sK + row_base * D), 16, 0, 0);
+    } else {
+      *(u32x4 *)(sK + row_base * D + 8 * lane) = load8<InT>(Kp + (long long)j * a.sk_t + 8 * cc);
+    }
   }
-  __syncthreads();
 
-  for (int rb = wave; rb < nrb; rb += 4) {
+  // pass-specific shared state (one slice per wave = per unit)
+  float (*sP)[65] = nullptr;
+  float *sCol = nullptr, *sDg = nullptr;
+  const int dw = kChunk + U0.nR;                  // diagonals touched by R rows in this chunk
+  const int dbase = U0.r0 - (c0 + kChunk - 1);    // smallest such diagonal
+  if constexpr (MODE == M_SCORES) {
+    __shared__ float sPbuf[4][32][65];            // per-wave probability tile [row][key]
+    __shared__ float sColbuf[4][kChunk];          // per-unit column sums
+    __shared__ float sDgbuf[4][kChunk + kProbeMaxRows];
+    sP = sPbuf[wave];
+    sCol = sColbuf[wave];
+    sDg = sDgbuf[wave];
+    for (int x = lane; x < kChunk; x += 64) sCol[x] = 0.f;
+    for (int x = lane; x < dw; x += 64) sDg[x] = 0.f;
+  }
+  lds_fence_barrier();  // K chunk resident
+  if (u < 0) return;    // no unit for this wave (no barrier follows)
+
+  const ProbeUnit U = a.units[u];
+  const InT *Qp = (const InT *)a.q + (long long)U.head * a.sq_h;
+  const int nrb = (U.nrows + 31) / 32;
+  const int kswz = swz(l32);
+  for (int rb = 0; rb < nrb; ++rb) {
     const int ridx = 32 * rb + l32;
     const bool rvalid = ridx < U.nrows;
     const long long rofs = (long long)u * a.rmax + ridx;
     const int row = rvalid ? a.rows[rofs] : -1;
-    const int sub = rvalid ? a.subset[rofs] : -1;
-    const float nmc = rvalid ? -a.row_max[rofs] * kLog2e : 0.f;
-    const float invl = rvalid ? 1.f / a.row_sum[rofs] : 0.f;
     if (hh == 0) sRows[wave][l32] = row;
     wave_sync();
     const int rbmax = sRows[wave][min(31, U.nrows - 1 - 32 * rb)];  // rows ascending
-    // position within the block of its first recent row (recent rows are the last nR)
-    const int rfirst = max(0, (U.nrows - U.nR) - 32 * rb);
     if (rbmax < c0) {  // no row of the block sees this chunk (wave-uniform)
       wave_sync();
       continue;
@@ -214,103 +163,154 @@ __global__ void __launch_bounds__(256) probe_chunk_kernel(const ProbeArgs a) {
       qf[ks] = u32x4{0u, 0u, 0u, 0u};
       if (rvalid) qf[ks] = load8<InT>(Qp + (long long)row * a.sq_t + 16 * ks + 8 * hh);
     }
+    float nmc = 0.f, invl = 0.f;
+    int sub = -1;
+    if constexpr (MODE != M_STATS) {
+      nmc = rvalid ? -a.row_max[rofs] * kLog2e : 0.f;
+      invl = rvalid ? 1.f / a.row_sum[rofs] : 0.f;
+      sub = rvalid ? a.subset[rofs] : -1;
+    }
+    const bool isR = sub == 0;
+    const bool blockR = (MODE == M_SCORES) && (__ballot(isR && hh == 0) != 0ull);
+    const int rfirst = max(0, (U.nrows - U.nR) - 32 * rb);  // first recent row in the block
+    float m_run = -INFINITY, l_run = 0.f;
     float ent = 0.f, loc = 0.f;
     float cov[kMaxCand];
 #pragma unroll
     for (int c = 0; c < kMaxCand; ++c) cov[c] = 0.f;
-    const bool isR = sub == 0;
-    // does the block hold recent rows? (wave-uniform)
-    const bool blockR = __ballot(isR && hh == 0) != 0ull;
 
-    for (int tt = 0; tt < kChunk / 64; ++tt) {
+    for (int tt = 0; tt < NT; ++tt) {
       const int k0 = c0 + 64 * tt;
       if (k0 > rbmax) break;
-      u32x4 kf[2][D / 16];
-      load_k_frag<D, InT>(Kp, a.sk_t, a.n, k0, l32, hh, kf);
       f32x16 s[2];
-      qk_tile<D>(kf, qf, s);
-      float p[2][16];
-      float bsum = 0.f, lsum = 0.f;
-      const int lo_local = row - a.local_w + 1;  // keys >= lo_local are in the local band
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
+      for (int mb = 0; mb < 2; ++mb) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int j = k0 + acc_key(mb, r, hh);
-          const float v = (rvalid && j <= row) ? __builtin_amdgcn_exp2f(fmaf(s[mb][r], a.c, nmc)) * invl : 0.f;
-          p[mb][r] = v;
-          bsum += v;
-          if (j >= lo_local) lsum += v;
+        for (int r = 0; r < 16; ++r) s[mb][r] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < D / 16; ++ks) {
+          const u32x4 kf = *(const u32x4 *)&sK[(64 * tt + 32 * mb + l32) * D + (((2 * ks + hh) ^ kswz) << 3)];
+          s[mb] = mfma32(kf, qf[ks], s[mb]);
         }
-      if constexpr (!COVER) {
-        bsum += __shfl_xor(bsum, 32);
-        if (bsum > 0.f) ent -= bsum * logf(bsum);
-        loc += lsum;
-        if (blockR) {
+      }
+      if constexpr (MODE == M_STATS) {
+        float mx = -INFINITY;
 #pragma unroll
-          for (int mb = 0; mb < 2; ++mb)
+        for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) sP[wave][l32][acc_key(mb, r, hh)] = isR ? p[mb][r] : 0.f;
-          wave_sync();
-          // column sums: lane = key
-          {
-            float cs = 0.f;
-            for (int rr = 0; rr < 32; ++rr) cs += sP[wave][rr][lane];
-            sCol[wave][64 * tt + lane] += cs;
+          for (int r = 0; r < 16; ++r) {
+            const int j = k0 + acc_key(mb, r, hh);
+            if (j > row) s[mb][r] = -INFINITY;
+            mx = fmaxf(mx, s[mb][r]);
           }
-          // diagonal sums over the block's recent rows (consecutive, starting at i_first):
-          // diagonal t = i - j is stored at x = t - dbase
-          {
-            const int i_first = max(U.r0, sRows[wave][0]);
-            const int i_last = sRows[wave][min(31, U.nrows - 1 - 32 * rb)];
-            const int xlo = i_first - k0 - 63 - dbase;
-            const int xn = i_last - i_first + 64;
-            for (int xx = lane; xx < xn; xx += 64) {
-              const int x = xlo + xx;
-              const int t = x + dbase;
-              float ds = 0.f;
-              for (int i2 = i_first; i2 <= i_last; ++i2) {
-                const int kk = i2 - t - k0;
-                if (kk >= 0 && kk < 64) ds += sP[wave][i2 - i_first + rfirst][kk];
-              }
-              if (x >= 0 && x < dw) sDg[wave][x] += ds;
+        const float m_new = fmaxf(m_run, mx);
+        const float m_use = m_new == -INFINITY ? 0.f : m_new;
+        float ps = 0.f;
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) ps += __builtin_amdgcn_exp2f((s[mb][r] - m_use) * a.c);
+        l_run = l_run * __builtin_amdgcn_exp2f((m_run - m_use) * a.c) + ps;
+        m_run = m_new;
+        continue;
+      } else {
+        float p[2][16];
+        float bsum = 0.f, lsum = 0.f;
+        const int lo_local = row - a.local_w + 1;  // keys >= lo_local are in the local band
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int j = k0 + acc_key(mb, r, hh);
+            const float v = (rvalid && j <= row) ? __builtin_amdgcn_exp2f(fmaf(s[mb][r], a.c, nmc)) * invl : 0.f;
+            p[mb][r] = v;
+            bsum += v;
+            if constexpr (MODE == M_SCORES) {
+              if (j >= lo_local) lsum += v;
             }
           }
-          wave_sync();
-        }
-      } else {
-        const int bq = row >> 6;
-        const int kt = k0 >> 6;
+        if constexpr (MODE == M_SCORES) {
+          bsum += __shfl_xor(bsum, 32);
+          if (bsum > 0.f) ent -= bsum * logf(bsum);
+          loc += lsum;
+          if (blockR) {
 #pragma unroll
-        for (int c = 0; c < kMaxCand; ++c) {
-          if (c >= a.ncand) break;
-          const CandDev cd = a.cand[c];
-          if (cd.fam == RS_DENSE) continue;
-          uint64_t M;
-          if (cd.fam == RS_ASHAPE) {
-            M = prefix_mask(cd.a - k0) | ~prefix_mask(row - cd.b + 1 - k0);
-          } else if (cd.fam == RS_VSLASH) {
-            const long long vrow = ((long long)u * a.ncand_vs + cd.cl) * a.nwords;
-            const uint64_t md = __builtin_bitreverse64(bits64_at(a.vs_dbits + vrow, a.nwords, row - k0 - 63));
-            const uint64_t mv = bits64_at(a.vs_vbits + vrow, a.nwords, k0);
-            M = md | mv;
-          } else {
-            const long long brow = (((long long)U.head * a.ncand_bs + cd.cl) * a.nb + (rvalid ? bq : 0)) * a.nbw;
-            const bool in = rvalid && ((a.bs_bits[brow + (kt >> 5)] >> (kt & 31)) & 1u);
-            M = in ? ~0ull : 0ull;
+            for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+              for (int r = 0; r < 16; ++r) sP[l32][acc_key(mb, r, hh)] = isR ? p[mb][r] : 0.f;
+            wave_sync();
+            {  // column sums: lane = key
+              float cs = 0.f;
+              for (int rr = 0; rr < 32; ++rr) cs += sP[rr][lane];
+              sCol[64 * tt + lane] += cs;
+            }
+            {  // diagonal t = i - j over the block's recent rows, stored at t - dbase
+              const int i_first = max(U.r0, sRows[wave][0]);
+              const int i_last = rbmax;
+              const int xlo = i_first - k0 - 63 - dbase;
+              const int xn = i_last - i_first + 64;
+              for (int xx = lane; xx < xn; xx += 64) {
+                const int x = xlo + xx;
+                const int t = x + dbase;
+                float ds = 0.f;
+                for (int i2 = i_first; i2 <= i_last; ++i2) {
+                  const int kk = i2 - t - k0;
+                  if (kk >= 0 && kk < 64) ds += sP[i2 - i_first + rfirst][kk];
+                }
+                if (x >= 0 && x < dw) sDg[x] += ds;
+              }
+            }
+            wave_sync();
           }
-          M >>= 4 * hh;
-          float cs = 0.f;
+        } else {  // M_COVER: kept mass of every candidate; whole-tile shortcuts first
+          const int bq = row >> 6;
+          const int kt = k0 >> 6;
+          const float tsum = bsum;
 #pragma unroll
-          for (int mb = 0; mb < 2; ++mb)
+          for (int c = 0; c < kMaxCand; ++c) {
+            if (c >= a.ncand) break;
+            const CandDev cd = a.cand[c];
+            if (cd.fam == RS_DENSE) continue;
+            uint64_t M;
+            if (cd.fam == RS_ASHAPE) {
+              M = prefix_mask(cd.a - k0) | ~prefix_mask(row - cd.b + 1 - k0);
+            } else if (cd.fam == RS_VSLASH) {
+              const long long vr = ((long long)u * a.ncand_vs + cd.cl) * a.nwords;
+              const uint64_t md = __builtin_bitreverse64(bits64_at(a.vs_dbits + vr, a.nwords, row - k0 - 63));
+              const uint64_t mv = bits64_at(a.vs_vbits + vr, a.nwords, k0);
+              M = md | mv;
+            } else {
+              const long long br = (((long long)U.head * a.ncand_bs + cd.cl) * a.nb + (rvalid ? bq : 0)) * a.nbw;
+              M = (rvalid && ((a.bs_bits[br + (kt >> 5)] >> (kt & 31)) & 1u)) ? ~0ull : 0ull;
+            }
+            M >>= 4 * hh;
+            const uint64_t sel = M & 0x0f0f0f0f0f0f0f0full;  // key slots held by this lane
+            if (sel == 0x0f0f0f0f0f0f0f0full) {
+              cov[c] += tsum;
+            } else if (sel != 0ull) {
+              float cs = 0.f;
 #pragma unroll
-            for (int r = 0; r < 16; ++r)
-              if ((M >> (32 * mb + 8 * (r >> 2) + (r & 3))) & 1ull) cs += p[mb][r];
-          cov[c] += cs;
+              for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                  if ((sel >> (32 * mb + 8 * (r >> 2) + (r & 3))) & 1ull) cs += p[mb][r];
+              cov[c] += cs;
+            }
+          }
         }
       }
     }
-    if constexpr (!COVER) {
+    if constexpr (MODE == M_STATS) {
+      const float mo = __shfl_xor(m_run, 32), lo = __shfl_xor(l_run, 32);
+      const float mm = fmaxf(m_run, mo);
+      const float mu = mm == -INFINITY ? 0.f : mm;
+      const float ll = l_run * __builtin_amdgcn_exp2f((m_run - mu) * a.c) + lo * __builtin_amdgcn_exp2f((mo - mu) * a.c);
+      if (rvalid && hh == 0) {
+        const long long o = ((long long)u * a.nchunks + ch) * a.rmax + ridx;
+        a.ent_part[o] = mm;  // chunk max (raw dot product) in the entropy partial slot
+        a.loc_part[o] = ll;  // chunk sum in the local-mass partial slot
+      }
+    } else if constexpr (MODE == M_SCORES) {
       loc += __shfl_xor(loc, 32);
       if (rvalid && hh == 0) {
         const long long o = ((long long)u * a.nchunks + ch) * a.rmax + ridx;
@@ -323,19 +323,35 @@ __global__ void __launch_bounds__(256) probe_chunk_kernel(const ProbeArgs a) {
         if (rvalid && hh == 0) a.cov_part[(((long long)u * a.nchunks + ch) * a.ncand + c) * a.rmax + ridx] = tot;
       }
     }
+    wave_sync();
   }
-  if constexpr (!COVER) {
-    __syncthreads();
-    for (int x = tid; x < kChunk; x += 256) {
+  if constexpr (MODE == M_SCORES) {
+    wave_sync();
+    for (int x = lane; x < kChunk; x += 64) {
       const int j = c0 + x;
-      if (j < a.n) {
-        const float v = (j < U.s1) ? sCol[0][x] + sCol[1][x] + sCol[2][x] + sCol[3][x] : 0.f;
-        a.col[(long long)u * a.n + j] = v;
-      }
+      if (j < a.n) a.col[(long long)u * a.n + j] = (j < U.s1) ? sCol[x] : 0.f;
     }
-    for (int x = tid; x < dw; x += 256)
-      a.diag_part[((long long)u * a.nchunks + ch) * a.diag_w + x] = sDg[0][x] + sDg[1][x] + sDg[2][x] + sDg[3][x];
+    for (int x = lane; x < dw; x += 64) a.diag_part[((long long)u * a.nchunks + ch) * a.diag_w + x] = sDg[x];
   }
+}
+
+// ---- combination of pass 1: per-row max and sum over the chunks ------------------------
+__global__ void probe_stats_combine_kernel(const ProbeArgs a) {
+  const int u = blockIdx.y;
+  const ProbeUnit U = a.units[u];
+  const int x = blockIdx.x * blockDim.x + threadIdx.x;
+  if (x >= U.nrows) return;
+  const int row = a.rows[(long long)u * a.rmax + x];
+  const int nch = (row / kChunk) + 1;
+  float M = -INFINITY;
+  for (int ch = 0; ch < nch; ++ch) M = fmaxf(M, a.ent_part[((long long)u * a.nchunks + ch) * a.rmax + x]);
+  float L = 0.f;
+  for (int ch = 0; ch < nch; ++ch) {
+    const long long o = ((long long)u * a.nchunks + ch) * a.rmax + x;
+    L += a.loc_part[o] * __builtin_amdgcn_exp2f((a.ent_part[o] - M) * a.c);
+  }
+  a.row_max[(long long)u * a.rmax + x] = M * a.scale;
+  a.row_sum[(long long)u * a.rmax + x] = L;
 }
 
 // ---- finalisation of pass 2: diagonals, descriptors, zero tails -------------------------
@@ -361,7 +377,7 @@ __global__ void probe_finish_kernel(const ProbeArgs a, float *diag, float *entro
   }
   if (x < U.nrows) {
     const int row = a.rows[(long long)u * a.rmax + x];
-    const int nch = (row >> 8) + 1;  // chunks holding keys <= row
+    const int nch = (row / kChunk) + 1;  // chunks holding keys <= row
     float e = 0.f, l = 0.f;
     for (int ch = 0; ch < nch; ++ch) {
       const long long o = ((long long)u * a.nchunks + ch) * a.rmax + x;
@@ -385,7 +401,7 @@ __global__ void cover_finish_kernel(const ProbeArgs a, float *cov_rows, float *c
     if (a.cand[c].fam == RS_DENSE) {
       m = 1.f;
     } else {
-      const int nch = (row >> 8) + 1;
+      const int nch = (row / kChunk) + 1;
       for (int ch = 0; ch < nch; ++ch) m += a.cov_part[(((long long)u * a.nchunks + ch) * a.ncand + c) * a.rmax + x];
     }
     cov_rows[((long long)u * a.ncand + c) * a.rmax + x] = m;
@@ -510,6 +526,7 @@ size_t probe_ws_bytes(const rs_qkv *qkv, int32_t nunits, const rs_probe_cfg *cfg
   const int nb = (qkv->n + 63) / 64;
   Arena ar(nullptr, 0);
   ar.take<ProbeUnit>(nunits);
+  ar.take<int4>(nunits);
   ar.take<float>((size_t)nunits * nchunks * (kChunk + rmax));     // diag partials
   ar.take<float>((size_t)nunits * nchunks * rmax * 2);            // entropy / local partials
   ar.take<float>((size_t)nunits * nchunks * rmax * kMaxCand);     // coverage partials
@@ -521,15 +538,16 @@ size_t probe_ws_bytes(const rs_qkv *qkv, int32_t nunits, const rs_probe_cfg *cfg
 }
 
 template <int D, typename InT>
-static hipError_t launch_rows(const ProbeArgs &pa, int nunits, int mode, float *diag, float *ent, float *loc,
+static hipError_t launch_rows(const ProbeArgs &pa, int nunits, int ngroups, int mode, float *diag, float *ent, float *loc,
                               float *cov_rows, float *cov, hipStream_t st) {
   if (mode == 0) {
-    hipLaunchKernelGGL((probe_stats_kernel<D, InT>), dim3((pa.rmax + 31) / 32, nunits), dim3(256), 0, st, pa);
-    hipLaunchKernelGGL((probe_chunk_kernel<D, InT, false>), dim3(pa.nchunks, nunits), dim3(256), 0, st, pa);
+    hipLaunchKernelGGL((probe_chunk_kernel<D, InT, M_STATS>), dim3(pa.nchunks, ngroups), dim3(256), 0, st, pa);
+    hipLaunchKernelGGL(probe_stats_combine_kernel, dim3((pa.rmax + 255) / 256, nunits), dim3(256), 0, st, pa);
+    hipLaunchKernelGGL((probe_chunk_kernel<D, InT, M_SCORES>), dim3(pa.nchunks, ngroups), dim3(256), 0, st, pa);
     hipLaunchKernelGGL(probe_finish_kernel, dim3((std::max(pa.n, pa.rmax) + 255) / 256, nunits), dim3(256), 0, st,
                        pa, diag, ent, loc);
   } else {
-    hipLaunchKernelGGL((probe_chunk_kernel<D, InT, true>), dim3(pa.nchunks, nunits), dim3(256), 0, st, pa);
+    hipLaunchKernelGGL((probe_chunk_kernel<D, InT, M_COVER>), dim3(pa.nchunks, ngroups), dim3(256), 0, st, pa);
     hipLaunchKernelGGL(cover_finish_kernel, dim3(pa.ncand, nunits), dim3(kProbeMaxRows), 0, st, pa, cov_rows, cov);
   }
   return hipGetLastError();
@@ -546,6 +564,7 @@ rs_status probe_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int
     return fail(RS_ERR_WORKSPACE, "probe workspace too small: need " + std::to_string(need));
   Arena ar(ws, ws_bytes);
   ProbeUnit *d_units = ar.take<ProbeUnit>(nunits);
+  int4 *d_groups = ar.take<int4>(nunits);
   float *diag_part = ar.take<float>((size_t)nunits * nchunks * (kChunk + rmax));
   float *ent_part = ar.take<float>((size_t)nunits * nchunks * rmax);
   float *loc_part = ar.take<float>((size_t)nunits * nchunks * rmax);
@@ -570,6 +589,38 @@ rs_status probe_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int
     }
   }
   RS_HIP(hipMemcpyAsync(d_units, hu.data(), hu.size() * sizeof(ProbeUnit), hipMemcpyHostToDevice, st));
+  // unit groups: the query heads of one key/value head over the same segment, up to 4
+  std::vector<int4> hg;
+  {
+    const int G = qkv->hq / qkv->hkv;
+    std::vector<std::vector<int>> open_lists;
+    std::vector<long long> keys;
+    for (int u = 0; u < nunits; ++u) {
+      const long long key = ((long long)(units[u].head / G) * (kMaxN + 1) + units[u].s0) * (kMaxN + 1) + units[u].s1;
+      int slot = -1;
+      for (size_t k = 0; k < keys.size(); ++k)
+        if (keys[k] == key && open_lists[k].size() < 4) {
+          slot = (int)k;
+          break;
+        }
+      if (slot < 0) {
+        keys.push_back(key);
+        open_lists.push_back({});
+        slot = (int)keys.size() - 1;
+      }
+      open_lists[slot].push_back(u);
+    }
+    for (auto &l : open_lists) {
+      int4 g{-1, -1, -1, -1};
+      g.x = l[0];
+      if (l.size() > 1) g.y = l[1];
+      if (l.size() > 2) g.z = l[2];
+      if (l.size() > 3) g.w = l[3];
+      hg.push_back(g);
+    }
+  }
+  const int ngroups = (int)hg.size();
+  RS_HIP(hipMemcpyAsync(d_groups, hg.data(), hg.size() * sizeof(int4), hipMemcpyHostToDevice, st));
   const bool cover = idx != nullptr;
   if (!cover) {
     RS_HIP(hipMemcpyAsync(out->rows, hrows.data(), hrows.size() * 4, hipMemcpyHostToDevice, st));
@@ -581,7 +632,7 @@ rs_status probe_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int
   pa.sq_h = qkv->sq_h; pa.sq_t = qkv->sq_t; pa.sk_h = qkv->sk_h; pa.sk_t = qkv->sk_t;
   pa.n = qkv->n; pa.group = qkv->hq / qkv->hkv; pa.rmax = rmax; pa.nchunks = nchunks;
   pa.c = scale * kLog2e; pa.scale = scale; pa.local_w = cfg->local_w;
-  pa.units = d_units; pa.rows = out->rows; pa.subset = out->subset;
+  pa.units = d_units; pa.groups = d_groups; pa.rows = out->rows; pa.subset = out->subset;
   pa.row_max = out->row_max; pa.row_sum = out->row_sum;
   pa.col = out->col; pa.diag_part = diag_part; pa.ent_part = ent_part; pa.loc_part = loc_part;
   pa.diag_w = kChunk + rmax;
@@ -602,11 +653,11 @@ rs_status probe_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int
     hipError_t e;
     const int mode = cover ? 1 : 0;
     if (qkv->d == 128)
-      e = qkv->dtype == RS_BF16 ? launch_rows<128, bf16>(pa, nunits, mode, out->diag, out->entropy, out->local, out->cov_rows, out->cov, st)
-                                : launch_rows<128, float>(pa, nunits, mode, out->diag, out->entropy, out->local, out->cov_rows, out->cov, st);
+      e = qkv->dtype == RS_BF16 ? launch_rows<128, bf16>(pa, nunits, ngroups, mode, out->diag, out->entropy, out->local, out->cov_rows, out->cov, st)
+                                : launch_rows<128, float>(pa, nunits, ngroups, mode, out->diag, out->entropy, out->local, out->cov_rows, out->cov, st);
     else
-      e = qkv->dtype == RS_BF16 ? launch_rows<64, bf16>(pa, nunits, mode, out->diag, out->entropy, out->local, out->cov_rows, out->cov, st)
-                                : launch_rows<64, float>(pa, nunits, mode, out->diag, out->entropy, out->local, out->cov_rows, out->cov, st);
+      e = qkv->dtype == RS_BF16 ? launch_rows<64, bf16>(pa, nunits, ngroups, mode, out->diag, out->entropy, out->local, out->cov_rows, out->cov, st)
+                                : launch_rows<64, float>(pa, nunits, ngroups, mode, out->diag, out->entropy, out->local, out->cov_rows, out->cov, st);
     if (e != hipSuccess) return hip_check(e, "probe kernels");
   }
   if (!cover && (cfg->flags & RS_PROBE_BLOCKMEAN)) {

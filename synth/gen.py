@@ -22,6 +22,12 @@ Recipe (all draws from numpy PCG64, ``seed = 1000 * config + layer``):
   structure stream ``[seed, 7]``), ``sqrt(k*sqrt(d)) * u`` added to the chosen keys and
   to the chosen queries, so the logit rises by k background standard deviations;
 * cast: round-to-nearest-even to bf16 (configs 2-5); config 1 stays float32.
+
+Config 5 draws a regime per key/value group (local 0.35, sink 0.30, vertical 0.28,
+diffuse 0.07) with context-scaled strengths so that the structured regimes hold about
+98% of the softmax mass at 128K: local band lam = 17; sinks (4 keys) and 64 vertical
+columns at k = ln(1.65 n / count) + 4; sink and vertical heads also carry the local band;
+diffuse heads get no plants.
 """
 from __future__ import annotations
 
@@ -122,14 +128,14 @@ def layer_spec(cfg: int, layer: int = 0, n: int | None = None) -> LayerSpec:
             cols = np.sort(rs.choice(np.arange(4, n), size=min(nv, max(n - 4, 0)), replace=False))
             lam = 0.0 if cfg == 1 else 4.0
             groups.append(GroupPlants(regime, sink_k=4.0, vert_k=3.0, vert_cols=cols, local_lam=lam))
-        elif regime == "sink":
+        elif regime == "sink":       # attention sinks plus a local band (A-shape-like head)
             k = math.log(1.65 * n / 4) + 4.0
-            groups.append(GroupPlants(regime, sink_k=k))
-        elif regime == "vertical":
+            groups.append(GroupPlants(regime, sink_k=k, local_lam=17.0))
+        elif regime == "vertical":   # vertical key columns plus a local band (vertical-slash head)
             nv = 64
             cols = np.sort(rs.choice(np.arange(4, n), size=min(nv, max(n - 4, 0)), replace=False))
             k = math.log(1.65 * n / nv) + 4.0
-            groups.append(GroupPlants(regime, vert_k=k, vert_cols=cols))
+            groups.append(GroupPlants(regime, vert_k=k, vert_cols=cols, local_lam=17.0))
         elif regime == "local":
             groups.append(GroupPlants(regime, local_lam=17.0))
         else:

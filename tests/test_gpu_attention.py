@@ -179,3 +179,29 @@ def test_deterministic_bitwise():
     a, _ = _run_dense(q, k, v, units)
     b, _ = _run_dense(q, k, v, units)
     assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("fam", ["dense", "ashape", "bs"])
+def test_repeated_runs_bitwise_identical(fam):
+    """Many key tiles per workgroup and several repetitions: every LDS tile must be fully
+    resident before it is read, so repeated runs agree bit for bit."""
+    import torch
+    n, hq, hkv, d = 6000, 8, 2, 128
+    q, k, v = _inputs(n, hq, hkv, d, seed=23)
+    units = [(h, 0, n, 1, h) for h in range(hq)]
+    if fam == "dense":
+        grid, ib = [(_rs.RS_DENSE, 0, 0)], None
+        runs = [_run_dense(q, k, v, [u[:3] for u in units])[0] for _ in range(4)]
+    else:
+        if fam == "ashape":
+            grid, ib = [(_rs.RS_DENSE, 0, 0), (_rs.RS_ASHAPE, 64, 2048)], None
+        else:
+            grid = [(_rs.RS_DENSE, 0, 0), (_rs.RS_BSPARSE, 30, 64)]
+            ib = _rs.IndexBuffers(hq, n, hq, grid)
+            nb = (n + 63) // 64
+            r = np.random.default_rng(1)
+            for h in range(hq):
+                fill_bs(ib, h, 0, [sorted(set(r.permutation(bq)[:29].tolist()) | {bq}) for bq in range(nb)])
+        runs = [_run_sparse(q, k, v, units, grid, ib)[0] for _ in range(4)]
+    for o in runs[1:]:
+        assert np.array_equal(o, runs[0])
