@@ -202,7 +202,9 @@ rs_status rs_probe(const rs_qkv *qkv, const rs_unit *units, int32_t nunits, cons
   if (out->nunits != nunits || out->rmax != rmax || out->n != qkv->n || out->nb != (qkv->n + 63) / 64 ||
       out->hq != qkv->hq)
     return fail(RS_ERR_INVALID_ARG, "probe output dimensions do not match");
-  if (!out->rows || !out->subset || !out->nsub || !out->row_max || !out->row_sum)
+  const bool need_rows = (cfg->flags & RS_PROBE_ROWS) || idx != nullptr;
+  if (need_rows && rmax == 0) return fail(RS_ERR_INVALID_ARG, "sampled-row probe needs at least one row");
+  if (need_rows && (!out->rows || !out->subset || !out->nsub || !out->row_max || !out->row_sum))
     return fail(RS_ERR_INVALID_ARG, "probe row arrays missing");
   if (idx == nullptr) {
     if ((cfg->flags & RS_PROBE_ROWS) && (!out->col || !out->diag || !out->entropy || !out->local))

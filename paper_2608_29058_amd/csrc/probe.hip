@@ -622,7 +622,7 @@ rs_status probe_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int
   const int ngroups = (int)hg.size();
   RS_HIP(hipMemcpyAsync(d_groups, hg.data(), hg.size() * sizeof(int4), hipMemcpyHostToDevice, st));
   const bool cover = idx != nullptr;
-  if (!cover) {
+  if (!cover && (cfg->flags & RS_PROBE_ROWS)) {
     RS_HIP(hipMemcpyAsync(out->rows, hrows.data(), hrows.size() * 4, hipMemcpyHostToDevice, st));
     RS_HIP(hipMemcpyAsync(out->subset, hsub.data(), hsub.size() * 4, hipMemcpyHostToDevice, st));
     RS_HIP(hipMemcpyAsync(out->nsub, hn.data(), hn.size() * 4, hipMemcpyHostToDevice, st));
