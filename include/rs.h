@@ -113,8 +113,8 @@ typedef struct rs_probe_out {
   float *row_sum;    /* [nunits][rmax] sum_j exp(l_ij - row_max)                  */
   float *col;        /* [nunits][n] col[j] = sum over R rows of a_ij (0 for j >= s1) */
   float *diag;       /* [nunits][n] diag[t] = sum over R rows of a_{i,i-t}           */
-  float *entropy;    /* [nunits][rmax] 64-block entropy / log(#visible blocks)    */
-  float *local;      /* [nunits][rmax] attention mass within (i - local_w, i]      */
+  float *entropy;    /* [nunits][rmax] 64-block entropy / log(#visible blocks) (coverage call) */
+  float *local;      /* [nunits][rmax] attention mass within (i - local_w, i]  (coverage call) */
   float *lbs;        /* [hq][nb*(nb+1)/2] pooled logits, row bq at bq*(bq+1)/2, or NULL */
   float *cov_rows;   /* [nunits][ncand][rmax] m_i(c): mass of row i kept by candidate c */
   float *cov;        /* [nunits][ncand][4] m_hat, m_R, m_U, m_B (subset means; 0 if empty) */
@@ -178,12 +178,13 @@ typedef struct rs_route_out {
 
 /* ---- probe (Sec. 3.2, Eq. 3; coverage of Sec. 3.2-3.3) -------------------------------
  * Scores mode (idx == NULL): for each unit, samples rows as in rs_probe_cfg, computes
- * exact softmax statistics of the sampled rows over keys [0, s1), the recent-row column
- * and diagonal scores and the per-row descriptors (flag RS_PROBE_ROWS), and the
- * block-mean pooled logits L_bs of every query head (flag RS_PROBE_BLOCKMEAN).
+ * exact softmax statistics of the sampled rows over keys [0, s1) and the recent-row
+ * column and diagonal scores (flag RS_PROBE_ROWS), and the block-mean pooled logits L_bs
+ * of every query head (flag RS_PROBE_BLOCKMEAN).
  * Coverage mode (idx != NULL, after a scores call on the same `out`): for each unit,
- * candidate and sampled row, m_i(c) = sum of a_ij over the candidate's key set, and the
- * subset means.  `grid`/`ncand` give the candidates (ignored in scores mode). */
+ * candidate and sampled row, m_i(c) = sum of a_ij over the candidate's key set, the subset
+ * means, and the per-row descriptors (entropy, local mass).  `grid`/`ncand` give the
+ * candidates (ignored in scores mode). */
 size_t rs_probe_workspace_size(const rs_qkv *qkv, const rs_unit *units, int32_t nunits,
                                const rs_probe_cfg *cfg);
 rs_status rs_probe(const rs_qkv *qkv, const rs_unit *units, int32_t nunits,
@@ -208,7 +209,8 @@ rs_status rs_build_indices(const rs_probe_out *scores, const rs_unit *units, int
  * non-empty subset means (dense: 0); greedy risk-per-microsecond substitutions from
  * all-dense until t_probe + sum t <= T_layer; then each sparse choice with
  * m_lower < tau takes the smallest larger budget of its family with m_lower >= tau, else
- * dense; units grouped by candidate.  Returns RS_ERR_BUDGET_INFEASIBLE (route still
+ * the cheapest sparse candidate of any family with m_lower >= tau, else dense; units
+ * grouped by candidate.  Returns RS_ERR_BUDGET_INFEASIBLE (route still
  * filled in) when the final total exceeds T_layer. */
 rs_status rs_route_layer(const rs_route_in *in, const rs_route_cfg *cfg, rs_route_out *out);
 

@@ -3,8 +3,8 @@
 Sec. 3.4: one candidate per unit, minimise the summed risk subject to
 t_probe + sum t_ker <= T_layer (Eqs. 6-8), solved greedily from the all-dense choice by
 risk-per-microsecond substitutions; then candidates whose lower mass is below tau get
-the next larger budget of their family that passes, else dense; finally units are
-grouped by (pattern, budget).  The greedy, expand/fallback and grouping follow the
+the next larger budget of their family that passes, else the cheapest other sparse
+candidate that passes, else dense; finally units are grouped by (pattern, budget).  The greedy, expand/fallback and grouping follow the
 inference-procedure table (steps 3-6).
 
 Reading of the greedy (the paper gives one sentence): start with every unit on the
@@ -76,9 +76,12 @@ def greedy(R, t, choice, t_probe, T_layer):
     return choice, over
 
 
-def expand_or_fallback(choice, fam, brank, ML, tau, dense_c):
-    """Candidates with m_lower < tau take the smallest larger budget of their family
-    whose m_lower >= tau, else the dense candidate (Sec. 3.4)."""
+def expand_or_fallback(choice, fam, brank, ML, tau, dense_c, t):
+    """A sparse choice whose lower mass is below tau first expands its budget: the smallest
+    larger budget of the same family with m_lower >= tau.  If none passes, the router
+    switches to dense only "if no sparse candidate satisfies the threshold" (Sec. 3.4): the
+    cheapest sparse candidate of any family with m_lower >= tau (lowest time, then lowest
+    candidate index), else the dense candidate."""
     out = list(choice)
     C = len(fam)
     nfb = 0
@@ -87,12 +90,21 @@ def expand_or_fallback(choice, fam, brank, ML, tau, dense_c):
             continue
         larger = sorted((brank[c2], c2) for c2 in range(C)
                         if fam[c2] == fam[c] and brank[c2] > brank[c])
-        pick = dense_c
+        pick = None
         for _, c2 in larger:
             if ML[u, c2] >= tau:
                 pick = c2
                 break
-        if pick == dense_c:
+        if pick is None:
+            best_t = None
+            for c2 in range(C):
+                if fam[c2] == DENSE or not ML[u, c2] >= tau:
+                    continue
+                if best_t is None or t[u, c2] < best_t:
+                    best_t = t[u, c2]
+                    pick = c2
+        if pick is None:
+            pick = dense_c
             nfb += 1
         out[u] = pick
     return out, nfb
@@ -124,7 +136,7 @@ def route_layer(mhat, msub, nsub, e, t, fam, brank, t_probe, T_layer, tau, alpha
                         np.asarray(e, dtype=np.float64), fam, alpha, beta, delta_q)
     t = np.asarray(t, dtype=np.float64)
     choice, over_solve = greedy(R, t, [dense_c] * U, t_probe, T_layer)
-    choice, nfb = expand_or_fallback(choice, fam, list(brank), ML, tau, dense_c)
+    choice, nfb = expand_or_fallback(choice, fam, list(brank), ML, tau, dense_c, t)
     tot = total_time(t, choice, t_probe)
     rsum = 0.0
     for u, c in enumerate(choice):

@@ -4,10 +4,10 @@
 // For each unit (query head h, rows [s0, s1)) the sampled rows I = R u U u Bd are scored
 // exactly against keys [0, s1):
 //   pass 1  row statistics: max_j l_ij and sum_j exp(l_ij - max) over j <= i;
-//   pass 2  normalised a_ij reduced into col[j] = sum_{i in R} a_ij,
-//           diag[t] = sum_{i in R} a_{i,i-t}, and per row the 64-key block entropy and
-//           the local-band mass;
-//   pass 3  (coverage) m_i(c) = sum_{j in S_i(c)} a_ij for every candidate c.
+//   pass 2  normalised a_ij of the recent rows reduced into col[j] = sum_{i in R} a_ij and
+//           diag[t] = sum_{i in R} a_{i,i-t};
+//   pass 3  (coverage) m_i(c) = sum_{j in S_i(c)} a_ij for every candidate c, and per row
+//           the 64-key block entropy and the local-band mass.
 // Logit tiles are bf16 MFMA products (S^T = K_tile x Q_rows^T, one lane per sampled row),
 // statistics fp32.  Every cross-workgroup reduction goes through per-chunk partials
 // summed in a fixed order, so results are deterministic.
@@ -91,8 +91,8 @@ enum { M_STATS = 0, M_SCORES = 1, M_COVER = 2 };
 // copied to LDS once (row-major, XOR-swizzled 16-byte chunks) and wave w handles every
 // sampled-row block of the group's unit w against the chunk's 2 tiles.
 //   M_STATS   per (row, chunk): max and sum of exp over the chunk's visible keys
-//   M_SCORES  normalised a_ij -> col, diagonal partials, block entropy, local mass
-//   M_COVER   normalised a_ij -> per-candidate kept mass
+//   M_SCORES  normalised a_ij of the recent rows -> col and diagonal partials
+//   M_COVER   normalised a_ij -> per-candidate kept mass, block entropy and local mass
 template <int D, typename InT, int MODE>
 __global__ void __launch_bounds__(256) probe_chunk_kernel(const ProbeArgs a) {
   constexpr int CPR = D / 8, RPI = 64 / CPR;
@@ -145,7 +145,9 @@ __global__ void __launch_bounds__(256) probe_chunk_kernel(const ProbeArgs a) {
   const InT *Qp = (const InT *)a.q + (long long)U.head * a.sq_h;
   const int nrb = (U.nrows + 31) / 32;
   const int kswz = swz(l32);
-  for (int rb = 0; rb < nrb; ++rb) {
+  // the scores pass only needs the recent rows (the last nR sampled rows)
+  const int rb_first = (MODE == M_SCORES) ? (U0.nrows - U0.nR) / 32 : 0;
+  for (int rb = rb_first; rb < nrb; ++rb) {
     const int ridx = 32 * rb + l32;
     const bool rvalid = ridx < U.nrows;
     const long long rofs = (long long)u * a.rmax + ridx;
@@ -225,14 +227,11 @@ __global__ void __launch_bounds__(256) probe_chunk_kernel(const ProbeArgs a) {
             const float v = (rvalid && j <= row) ? __builtin_amdgcn_exp2f(fmaf(s[mb][r], a.c, nmc)) * invl : 0.f;
             p[mb][r] = v;
             bsum += v;
-            if constexpr (MODE == M_SCORES) {
+            if constexpr (MODE == M_COVER) {
               if (j >= lo_local) lsum += v;
             }
           }
         if constexpr (MODE == M_SCORES) {
-          bsum += __shfl_xor(bsum, 32);
-          if (bsum > 0.f) ent -= bsum * logf(bsum);
-          loc += lsum;
           if (blockR) {
 #pragma unroll
             for (int mb = 0; mb < 2; ++mb)
@@ -262,10 +261,15 @@ __global__ void __launch_bounds__(256) probe_chunk_kernel(const ProbeArgs a) {
             }
             wave_sync();
           }
-        } else {  // M_COVER: kept mass of every candidate; whole-tile shortcuts first
+        } else {  // M_COVER: kept mass of every candidate (whole-tile shortcuts first), descriptors
           const int bq = row >> 6;
           const int kt = k0 >> 6;
           const float tsum = bsum;
+          {
+            const float bt = bsum + __shfl_xor(bsum, 32);  // mass of the row in this 64-key block
+            if (bt > 0.f) ent -= bt * logf(bt);
+            loc += lsum;
+          }
 #pragma unroll
           for (int c = 0; c < kMaxCand; ++c) {
             if (c >= a.ncand) break;
@@ -306,21 +310,20 @@ __global__ void __launch_bounds__(256) probe_chunk_kernel(const ProbeArgs a) {
       const float mu = mm == -INFINITY ? 0.f : mm;
       const float ll = l_run * __builtin_amdgcn_exp2f((m_run - mu) * a.c) + lo * __builtin_amdgcn_exp2f((mo - mu) * a.c);
       if (rvalid && hh == 0) {
-        const long long o = ((long long)u * a.nchunks + ch) * a.rmax + ridx;
+        const long long o = ((long long)u * a.rmax + ridx) * a.nchunks + ch;
         a.ent_part[o] = mm;  // chunk max (raw dot product) in the entropy partial slot
         a.loc_part[o] = ll;  // chunk sum in the local-mass partial slot
       }
-    } else if constexpr (MODE == M_SCORES) {
+    } else if constexpr (MODE == M_COVER) {
       loc += __shfl_xor(loc, 32);
       if (rvalid && hh == 0) {
-        const long long o = ((long long)u * a.nchunks + ch) * a.rmax + ridx;
-        a.ent_part[o] = ent;
+        const long long o = ((long long)u * a.rmax + ridx) * a.nchunks + ch;
+        a.ent_part[o] = ent;  // the stats partials were consumed before this pass
         a.loc_part[o] = loc;
       }
-    } else {
       for (int c = 0; c < a.ncand; ++c) {
         const float tot = cov[c] + __shfl_xor(cov[c], 32);
-        if (rvalid && hh == 0) a.cov_part[(((long long)u * a.nchunks + ch) * a.ncand + c) * a.rmax + ridx] = tot;
+        if (rvalid && hh == 0) a.cov_part[(((long long)u * a.ncand + c) * a.rmax + ridx) * a.nchunks + ch] = tot;
       }
     }
     wave_sync();
@@ -335,26 +338,44 @@ __global__ void __launch_bounds__(256) probe_chunk_kernel(const ProbeArgs a) {
   }
 }
 
-// ---- combination of pass 1: per-row max and sum over the chunks ------------------------
+// ---- combination of the per-chunk partials: one wave per sampled row --------------------
+// Partials of a row are contiguous over chunks; lanes stride over the chunks holding keys
+// <= row in a fixed order and the wave reduces with a fixed xor-butterfly, so the result is
+// deterministic.
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+// grid: (ceil(rmax / 4), nunits), 256 threads; wave = one sampled row
 __global__ void probe_stats_combine_kernel(const ProbeArgs a) {
   const int u = blockIdx.y;
   const ProbeUnit U = a.units[u];
-  const int x = blockIdx.x * blockDim.x + threadIdx.x;
+  const int x = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (x >= U.nrows) return;
   const int row = a.rows[(long long)u * a.rmax + x];
-  const int nch = (row / kChunk) + 1;
+  const int nch = row / kChunk + 1;
+  const float *pm = a.ent_part + ((long long)u * a.rmax + x) * a.nchunks;
+  const float *pl = a.loc_part + ((long long)u * a.rmax + x) * a.nchunks;
   float M = -INFINITY;
-  for (int ch = 0; ch < nch; ++ch) M = fmaxf(M, a.ent_part[((long long)u * a.nchunks + ch) * a.rmax + x]);
+  for (int ch = lane; ch < nch; ch += 64) M = fmaxf(M, pm[ch]);
+  M = wave_max(M);
   float L = 0.f;
-  for (int ch = 0; ch < nch; ++ch) {
-    const long long o = ((long long)u * a.nchunks + ch) * a.rmax + x;
-    L += a.loc_part[o] * __builtin_amdgcn_exp2f((a.ent_part[o] - M) * a.c);
+  for (int ch = lane; ch < nch; ch += 64) L += pl[ch] * __builtin_amdgcn_exp2f((pm[ch] - M) * a.c);
+  L = wave_sum(L);
+  if (lane == 0) {
+    a.row_max[(long long)u * a.rmax + x] = M * a.scale;
+    a.row_sum[(long long)u * a.rmax + x] = L;
   }
-  a.row_max[(long long)u * a.rmax + x] = M * a.scale;
-  a.row_sum[(long long)u * a.rmax + x] = L;
 }
 
-// ---- finalisation of pass 2: diagonals, descriptors, zero tails -------------------------
+// diagonals from their chunk partials, zero tails of col/diag: one thread per position
 __global__ void probe_finish_kernel(const ProbeArgs a, float *diag, float *entropy, float *local) {
   const int u = blockIdx.y;
   const ProbeUnit U = a.units[u];
@@ -362,7 +383,7 @@ __global__ void probe_finish_kernel(const ProbeArgs a, float *diag, float *entro
   if (x < a.n) {
     float v = 0.f;
     if (x < U.s1 && U.nR > 0) {
-      // chunks whose diagonal range [r0 - c0 - 255, r0 + nR - 1 - c0] holds t = x
+      // chunks whose diagonal range [r0 - c0 - (kChunk-1), r0 + nR - 1 - c0] holds t = x
       const int chi = min((U.r0 + U.nR - 1 - x) / kChunk, (U.s1 - 1) / kChunk);
       const int clo_num = U.r0 - (kChunk - 1) - x;
       const int clo = clo_num <= 0 ? 0 : (clo_num + kChunk - 1) / kChunk;
@@ -375,40 +396,57 @@ __global__ void probe_finish_kernel(const ProbeArgs a, float *diag, float *entro
     diag[(long long)u * a.n + x] = v;
     if (x >= U.s1) a.col[(long long)u * a.n + x] = 0.f;
   }
-  if (x < U.nrows) {
-    const int row = a.rows[(long long)u * a.rmax + x];
-    const int nch = (row / kChunk) + 1;  // chunks holding keys <= row
-    float e = 0.f, l = 0.f;
-    for (int ch = 0; ch < nch; ++ch) {
-      const long long o = ((long long)u * a.nchunks + ch) * a.rmax + x;
-      e += a.ent_part[o];
-      l += a.loc_part[o];
-    }
+}
+
+// descriptors: entropy and local mass of each sampled row, one wave per row
+__global__ void probe_desc_kernel(const ProbeArgs a, float *entropy, float *local) {
+  const int u = blockIdx.y;
+  const ProbeUnit U = a.units[u];
+  const int x = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (x >= U.nrows) return;
+  const int row = a.rows[(long long)u * a.rmax + x];
+  const int nch = row / kChunk + 1;
+  const float *pe = a.ent_part + ((long long)u * a.rmax + x) * a.nchunks;
+  const float *pl = a.loc_part + ((long long)u * a.rmax + x) * a.nchunks;
+  float e = 0.f, l = 0.f;
+  for (int ch = lane; ch < nch; ch += 64) {
+    e += pe[ch];
+    l += pl[ch];
+  }
+  e = wave_sum(e);
+  l = wave_sum(l);
+  if (lane == 0) {
     const int nvis = row / 64 + 1;
     entropy[(long long)u * a.rmax + x] = nvis > 1 ? e / logf((float)nvis) : 0.f;
     local[(long long)u * a.rmax + x] = l;
   }
 }
 
+// coverage per sampled row and candidate, then the subset means; grid (ncand, nunits)
 __global__ void cover_finish_kernel(const ProbeArgs a, float *cov_rows, float *cov) {
   const int u = blockIdx.y, c = blockIdx.x;
   const ProbeUnit U = a.units[u];
   __shared__ float sm[kProbeMaxRows];
-  const int x = threadIdx.x;  // blockDim = kProbeMaxRows
-  float m = 0.f;
-  if (x < U.nrows) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int x = wave; x < U.nrows; x += 4) {
     const int row = a.rows[(long long)u * a.rmax + x];
+    float m;
     if (a.cand[c].fam == RS_DENSE) {
       m = 1.f;
     } else {
-      const int nch = (row / kChunk) + 1;
-      for (int ch = 0; ch < nch; ++ch) m += a.cov_part[(((long long)u * a.nchunks + ch) * a.ncand + c) * a.rmax + x];
+      const int nch = row / kChunk + 1;
+      const float *pc = a.cov_part + (((long long)u * a.ncand + c) * a.rmax + x) * a.nchunks;
+      float acc = 0.f;
+      for (int ch = lane; ch < nch; ch += 64) acc += pc[ch];
+      m = wave_sum(acc);
     }
-    cov_rows[((long long)u * a.ncand + c) * a.rmax + x] = m;
+    if (lane == 0) {
+      sm[x] = m;
+      cov_rows[((long long)u * a.ncand + c) * a.rmax + x] = m;
+    }
   }
-  sm[x] = m;
   __syncthreads();
-  if (x == 0) {
+  if (threadIdx.x == 0) {
     float tot = 0.f, sub[3] = {0.f, 0.f, 0.f};
     int cnt[3] = {0, 0, 0};
     for (int r = 0; r < U.nrows; ++r) {
@@ -421,20 +459,40 @@ __global__ void cover_finish_kernel(const ProbeArgs a, float *cov_rows, float *c
     }
     float *o = cov + ((long long)u * a.ncand + c) * 4;
     o[0] = U.nrows ? tot / U.nrows : 0.f;
-    for (int s = 0; s < 3; ++s) o[1 + s] = cnt[s] ? sub[s] / cnt[s] : 0.f;
+    for (int s2 = 0; s2 < 3; ++s2) o[1 + s2] = cnt[s2] ? sub[s2] / cnt[s2] : 0.f;
   }
 }
 
 // ---- block-mean estimator ----------------------------------------------------------------
 template <typename InT>
-__global__ void block_pool_kernel(const InT *x, long long s_h, long long s_t, int n, int d, float *out) {
-  const int b = blockIdx.x, h = blockIdx.y;  // blockDim = d
+__global__ void __launch_bounds__(256) block_pool_kernel(const InT *x, long long s_h, long long s_t, int n, int d,
+                                                         float *out) {
+  // one 64-row block of one head: thread = (row group of 16, 8-dim chunk); 16-byte loads
+  const int b = blockIdx.x, h = blockIdx.y;
   const int t = threadIdx.x;
+  const int cpr = d / 8, rpp = 256 / cpr;  // chunks per row, rows per pass
+  const int rg = t / cpr, cc = t % cpr;
   const int r0 = b * 64, r1 = min(n, r0 + 64);
-  const InT *p = x + (long long)h * s_h + t;
-  float acc = 0.f;
-  for (int r = r0; r < r1; ++r) acc += (float)p[(long long)r * s_t];
-  out[((long long)h * gridDim.x + b) * d + t] = acc / (float)(r1 - r0);
+  const InT *p = x + (long long)h * s_h + 8 * cc;
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int r = r0 + rg; r < r1; r += rpp) {
+    const u32x4 v = load8<InT>(p + (long long)r * s_t);
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      acc[2 * w] += __builtin_bit_cast(float, v[w] << 16);
+      acc[2 * w + 1] += __builtin_bit_cast(float, v[w] & 0xffff0000u);
+    }
+  }
+  __shared__ float sacc[256][9];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) sacc[t][e] = acc[e];
+  __syncthreads();
+  if (t < d) {
+    const int c2 = t / 8, e = t % 8;
+    float s = 0.f;
+    for (int g = 0; g < rpp; ++g) s += sacc[g * cpr + c2][e];  // fixed order
+    out[((long long)h * gridDim.x + b) * d + t] = s / (float)(r1 - r0);
+  }
 }
 
 // L[h][bq][bk] = qbar . kbar * scale for bk <= bq; 64 x 64 output tiles, fp32 FMA.
@@ -542,13 +600,13 @@ static hipError_t launch_rows(const ProbeArgs &pa, int nunits, int ngroups, int 
                               float *cov_rows, float *cov, hipStream_t st) {
   if (mode == 0) {
     hipLaunchKernelGGL((probe_chunk_kernel<D, InT, M_STATS>), dim3(pa.nchunks, ngroups), dim3(256), 0, st, pa);
-    hipLaunchKernelGGL(probe_stats_combine_kernel, dim3((pa.rmax + 255) / 256, nunits), dim3(256), 0, st, pa);
+    hipLaunchKernelGGL(probe_stats_combine_kernel, dim3((pa.rmax + 3) / 4, nunits), dim3(256), 0, st, pa);
     hipLaunchKernelGGL((probe_chunk_kernel<D, InT, M_SCORES>), dim3(pa.nchunks, ngroups), dim3(256), 0, st, pa);
-    hipLaunchKernelGGL(probe_finish_kernel, dim3((std::max(pa.n, pa.rmax) + 255) / 256, nunits), dim3(256), 0, st,
-                       pa, diag, ent, loc);
+    hipLaunchKernelGGL(probe_finish_kernel, dim3((pa.n + 255) / 256, nunits), dim3(256), 0, st, pa, diag, ent, loc);
   } else {
     hipLaunchKernelGGL((probe_chunk_kernel<D, InT, M_COVER>), dim3(pa.nchunks, ngroups), dim3(256), 0, st, pa);
-    hipLaunchKernelGGL(cover_finish_kernel, dim3(pa.ncand, nunits), dim3(kProbeMaxRows), 0, st, pa, cov_rows, cov);
+    hipLaunchKernelGGL(cover_finish_kernel, dim3(pa.ncand, nunits), dim3(256), 0, st, pa, cov_rows, cov);
+    hipLaunchKernelGGL(probe_desc_kernel, dim3((pa.rmax + 3) / 4, nunits), dim3(256), 0, st, pa, ent, loc);
   }
   return hipGetLastError();
 }
@@ -662,14 +720,14 @@ rs_status probe_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int
   }
   if (!cover && (cfg->flags & RS_PROBE_BLOCKMEAN)) {
     if (qkv->dtype == RS_BF16) {
-      hipLaunchKernelGGL(block_pool_kernel<bf16>, dim3(nb, qkv->hq), dim3(qkv->d), 0, st, (const bf16 *)qkv->q,
+      hipLaunchKernelGGL(block_pool_kernel<bf16>, dim3(nb, qkv->hq), dim3(256), 0, st, (const bf16 *)qkv->q,
                          (long long)qkv->sq_h, (long long)qkv->sq_t, qkv->n, qkv->d, qbar);
-      hipLaunchKernelGGL(block_pool_kernel<bf16>, dim3(nb, qkv->hkv), dim3(qkv->d), 0, st, (const bf16 *)qkv->k,
+      hipLaunchKernelGGL(block_pool_kernel<bf16>, dim3(nb, qkv->hkv), dim3(256), 0, st, (const bf16 *)qkv->k,
                          (long long)qkv->sk_h, (long long)qkv->sk_t, qkv->n, qkv->d, kbar);
     } else {
-      hipLaunchKernelGGL(block_pool_kernel<float>, dim3(nb, qkv->hq), dim3(qkv->d), 0, st, (const float *)qkv->q,
+      hipLaunchKernelGGL(block_pool_kernel<float>, dim3(nb, qkv->hq), dim3(256), 0, st, (const float *)qkv->q,
                          (long long)qkv->sq_h, (long long)qkv->sq_t, qkv->n, qkv->d, qbar);
-      hipLaunchKernelGGL(block_pool_kernel<float>, dim3(nb, qkv->hkv), dim3(qkv->d), 0, st, (const float *)qkv->k,
+      hipLaunchKernelGGL(block_pool_kernel<float>, dim3(nb, qkv->hkv), dim3(256), 0, st, (const float *)qkv->k,
                          (long long)qkv->sk_h, (long long)qkv->sk_t, qkv->n, qkv->d, kbar);
     }
     const int nbt = (nb + 63) / 64;

@@ -10,7 +10,8 @@
 //             (unit, candidate) of minimum (R(c) - R(cur)) / (t(cur) - t(c)) among
 //             strictly cheaper candidates, first minimum in (unit, candidate) order
 //   expand    a sparse choice with m_lower < tau takes the smallest larger budget of its
-//             family with m_lower >= tau, else dense
+//             family with m_lower >= tau, else the cheapest sparse candidate of any family
+//             with m_lower >= tau (ties: lowest index), else dense
 //   group     units grouped by candidate, grid order, ascending units
 #include <algorithm>
 #include <string>
@@ -118,12 +119,13 @@ extern "C" rs_status rs_route_layer(const rs_route_in *in, const rs_route_cfg *c
     }
     choice[bu] = bc;
   }
-  // expand or fall back
+  // expand or fall back: larger budgets of the family first, then the cheapest passing
+  // sparse candidate of any family ("dense if no sparse candidate satisfies tau")
   int nfb = 0;
   for (int u = 0; u < U; ++u) {
     const int c = choice[u];
     if (fam[c] == RS_DENSE || ML[(size_t)u * C + c] >= cfg->tau) continue;
-    int pick = dense_c, pick_rank = 1 << 30;
+    int pick = -1, pick_rank = 1 << 30;
     for (int c2 = 0; c2 < C; ++c2) {
       if (fam[c2] != fam[c] || brank[c2] <= brank[c]) continue;
       if (ML[(size_t)u * C + c2] >= cfg->tau && brank[c2] < pick_rank) {
@@ -131,7 +133,21 @@ extern "C" rs_status rs_route_layer(const rs_route_in *in, const rs_route_cfg *c
         pick_rank = brank[c2];
       }
     }
-    if (pick == dense_c) ++nfb;
+    if (pick < 0) {
+      double best_t = 0.0;
+      for (int c2 = 0; c2 < C; ++c2) {
+        if (fam[c2] == RS_DENSE || !(ML[(size_t)u * C + c2] >= cfg->tau)) continue;
+        const double tt = t[(size_t)u * C + c2];
+        if (pick < 0 || tt < best_t) {
+          best_t = tt;
+          pick = c2;
+        }
+      }
+    }
+    if (pick < 0) {
+      pick = dense_c;
+      ++nfb;
+    }
     choice[u] = pick;
   }
   const double tot = total();

@@ -59,17 +59,36 @@ __device__ void radix_select(const float *vals, int len, int K, uint32_t *T_out,
       if ((key & maskhi) == prefix) atomicAdd(&sHist[(key >> (8 * byte)) & 255u], 1);
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
-      int cum = 0, sel = 0;
-      for (int b = 255; b >= 0; --b) {
-        if (cum + sHist[b] >= krem) {
-          sel = b;
-          break;
-        }
-        cum += sHist[b];
+    if (threadIdx.x < 64) {
+      // lane l owns bins 255-4l .. 252-4l (descending); wave-wide inclusive scan of counts
+      const int l = threadIdx.x;
+      int c4[4], own = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        c4[q] = sHist[255 - 4 * l - q];
+        own += c4[q];
       }
-      sBcast[0] = sel;
-      sBcast[1] = krem - cum;
+      int incl = own;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(incl, o);
+        if (l >= o) incl += y;
+      }
+      const int excl = incl - own;
+      // the selected bin lies in the first lane whose inclusive count reaches krem
+      if (excl < krem && incl >= krem) {
+        int cum = excl, sel = 255 - 4 * l;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (cum + c4[q] >= krem) {
+            sel = 255 - 4 * l - q;
+            break;
+          }
+          cum += c4[q];
+        }
+        sBcast[0] = sel;
+        sBcast[1] = krem - cum;
+      }
     }
     __syncthreads();
     prefix |= (uint32_t)sBcast[0] << (8 * byte);

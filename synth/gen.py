@@ -19,8 +19,9 @@ Recipe (all draws from numpy PCG64, ``seed = 1000 * config + layer``):
 * RoPE, rotate-half convention: pair f = dims (f, f + d/2), theta_f = 500000^(-2f/d),
   position = token index (no long-context frequency rescaling);
 * planted "+k sigma" boosts (after RoPE): direction u (orthonormal set drawn from the
-  structure stream ``[seed, 7]``), ``sqrt(k*sqrt(d)) * u`` added to the chosen keys and
-  to the chosen queries, so the logit rises by k background standard deviations;
+  structure stream ``[seed, 7]``, orthogonal to the rotary pairs of the local-band
+  vector), ``sqrt(k*sqrt(d)) * u`` added to the chosen keys and to the chosen queries, so
+  the logit rises by k background standard deviations;
 * cast: round-to-nearest-even to bf16 (configs 2-5); config 1 stays float32.
 
 Config 5 draws a regime per key/value group (local 0.35, sink 0.30, vertical 0.28,
@@ -115,6 +116,12 @@ def layer_spec(cfg: int, layer: int = 0, n: int | None = None) -> LayerSpec:
     seed = 1000 * cfg + layer
     rs = np.random.default_rng([seed, 7])
     g = rs.standard_normal((d, 16))
+    # planted directions live outside the rotary pairs that carry the local-band vector, so
+    # that u . R_j c = 0 for every position j (no position-dependent cross terms)
+    theta = ROPE_BASE ** (-2.0 * np.arange(d // 2, dtype=np.float64) / d)
+    band = np.nonzero((theta >= 1e-3) & (theta <= 1e-1))[0]
+    g[band] = 0.0
+    g[band + d // 2] = 0.0
     qmat, _ = np.linalg.qr(g)
     dirs = qmat.T.astype(np.float64)          # rows orthonormal
     groups = []

@@ -86,8 +86,24 @@ def test_tau_expands_then_falls_back():
     fam = [RT.DENSE, RT.VSLASH, RT.VSLASH, RT.VSLASH]
     brank = [0, 0, 1, 2]
     ML = np.array([[1, 0.5, 0.96, 0.99], [1, 0.5, 0.6, 0.7], [1, 0.97, 0.98, 0.99]])
-    out, nfb = RT.expand_or_fallback([1, 1, 1], fam, brank, ML, 0.95, 0)
+    t = np.ones((3, 4))
+    out, nfb = RT.expand_or_fallback([1, 1, 1], fam, brank, ML, 0.95, 0, t)
     assert out == [2, 0, 1] and nfb == 1
+
+
+def test_tau_switches_to_cheapest_passing_sparse_candidate():
+    # A-shape fails tau at both budgets; vertical-slash (two budgets) and block-sparse pass:
+    # the cheaper passing candidate is taken, dense only when no sparse candidate passes
+    fam = [RT.DENSE, RT.ASHAPE, RT.ASHAPE, RT.VSLASH, RT.VSLASH, RT.BSPARSE]
+    brank = [0, 0, 1, 0, 1, 0]
+    ML = np.array([[1, 0.5, 0.6, 0.96, 0.99, 0.97],
+                   [1, 0.5, 0.6, 0.90, 0.99, 0.97],
+                   [1, 0.5, 0.6, 0.90, 0.91, 0.92]])
+    t = np.array([[100, 2, 5, 30, 40, 20],
+                  [100, 2, 5, 30, 40, 50],
+                  [100, 2, 5, 30, 40, 50]], dtype=float)
+    out, nfb = RT.expand_or_fallback([1, 1, 1], fam, brank, ML, 0.95, 0, t)
+    assert out == [5, 4, 0] and nfb == 1
 
 
 def test_grouping():
