@@ -254,6 +254,9 @@ def main():
     ms_per_layer = total_ms / args.steps
 
     # ---- per-phase / per-family accounting (after the timed region) -------------------------
+    cand_units = [0] * len(GRID)
+    cand_pairs = [0] * len(GRID)
+    cand_time = [0.0] * len(GRID)
     fam_time = {f: 0.0 for f in FAM_NAME}
     fam_flops = {f: 0.0 for f in FAM_NAME}
     fam_launches = {f: 0 for f in FAM_NAME}
@@ -294,6 +297,9 @@ def main():
                     cv, cdn = ic["vs_count"][u, cl]
                     pairs += pairs_vs(s0, s1, ic["vs_v"][u, cl, :cv], ic["vs_d"][u, cl, :cdn])
             fl = 4.0 * D * pairs
+            cand_units[cand] += len(us)
+            cand_pairs[cand] += pairs
+            cand_time[cand] += dt
             fam_time[fam] += dt
             fam_flops[fam] += fl
             fam_launches[fam] += 1
@@ -338,6 +344,10 @@ def main():
         "family_ms_per_layer": {FAM_NAME[f]: round(fam_time[f] / args.steps, 4) for f in FAM_NAME},
         "family_tflops": {FAM_NAME[f]: (round(fam_flops[f] / (fam_time[f] * 1e-3) / 1e12, 1) if fam_time[f] else None)
                           for f in FAM_NAME},
+        "candidates": [{"cand": list(GRID[c]), "units_per_layer": round(cand_units[c] / args.steps, 2),
+                        "ms_per_layer": round(cand_time[c] / args.steps, 4),
+                        "tflops": (round(4.0 * D * cand_pairs[c] / (cand_time[c] * 1e-3) / 1e12, 1)
+                                   if cand_time[c] else None)} for c in range(len(GRID))],
         "fallback_units_per_layer": round(n_units_fb / args.steps, 2),
         "dense_units_per_layer": round(n_units_dense / args.steps, 2),
         "wall_ms_timed": round(wall_ms, 1),

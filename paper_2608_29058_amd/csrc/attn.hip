@@ -78,9 +78,33 @@ __device__ __forceinline__ void lds_fence_barrier() {
 
 // Per-tile description produced ahead of its use (the next tile is issued while the
 // current one is computed).
+// Three consecutive bitmap words around a bit position (loaded ahead of their use).
+struct Win3 {
+  uint32_t x0, x1, x2;
+};
+
+__device__ __forceinline__ Win3 load_win(const uint32_t *bits, int nwords, int pos) {
+  const int w = pos >> 5;
+  Win3 r;
+  r.x0 = (w >= 0 && w < nwords) ? bits[w] : 0u;
+  r.x1 = (w + 1 >= 0 && w + 1 < nwords) ? bits[w + 1] : 0u;
+  r.x2 = (w + 2 >= 0 && w + 2 < nwords) ? bits[w + 2] : 0u;
+  return r;
+}
+
+// the 64 bits starting at `pos` from a window loaded with load_win(.., pos)
+__device__ __forceinline__ uint64_t win_bits(const Win3 &r, int pos) {
+  const int sh = pos & 31;
+  uint64_t v = ((uint64_t)r.x0 | ((uint64_t)r.x1 << 32)) >> sh;
+  if (sh) v |= (uint64_t)r.x2 << (64 - sh);
+  return v;
+}
+
 struct TileRef {
   int key0;  // first key of a contiguous tile, or -(1 + gather offset)
   int tag;   // bit 0: rows of waves 0-1 use it, bit 1: rows of waves 2-3 (block-sparse)
+  Win3 wd;   // vertical-slash: diagonal-bitmap words of this lane's row (prefetched)
+  Win3 wv;   // vertical-slash: column-bitmap words of the tile (prefetched)
 };
 
 template <int D, int PAT, typename InT>
@@ -221,9 +245,9 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const AttnArgs a) {
   auto next_tile = [&]() -> TileRef {
     const int t = t_next++;
     if constexpr (PAT == P_DENSE) {
-      return TileRef{t * 64, 3};
+      return TileRef{t * 64, 3, {0u, 0u, 0u}, {0u, 0u, 0u}};
     } else if constexpr (PAT == P_ASHAPE) {
-      return TileRef{(t < st0 ? t : st1 + (t - st0)) * 64, 3};
+      return TileRef{(t < st0 ? t : st1 + (t - st0)) * 64, 3, {0u, 0u, 0u}, {0u, 0u, 0u}};
     } else if constexpr (PAT == P_BS) {
       const int va = st0 < bs_na ? bs_a[st0] : 0x7fffffff;
       const int vb = st1 < bs_nb ? bs_b[st1] : 0x7fffffff;
@@ -231,15 +255,21 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const AttnArgs a) {
       const int tag = (va == v ? 1 : 0) | (vb == v ? 2 : 0);
       st0 += va == v;
       st1 += vb == v;
-      return TileRef{v * 64, tag};
+      return TileRef{v * 64, tag, {0u, 0u, 0u}, {0u, 0u, 0u}};
     } else {
       if (t < n_contig) {
         while (st1 == 0) st1 = (int)sTB[++st0];
         const int bit = __builtin_ctz((uint32_t)st1);
         st1 &= st1 - 1;
-        return TileRef{(st0 * 32 + bit) * 64, 3};
+        const int key0 = (st0 * 32 + bit) * 64;
+        TileRef tr{key0, 3, {0u, 0u, 0u}, {0u, 0u, 0u}};
+        // bitmap words of the element mask, fetched with the tile so that their latency
+        // hides behind the previous tile's compute
+        tr.wd = load_win(dbits, a.nwords, my_row - key0 - 63);
+        tr.wv = load_win(vbits, a.nwords, key0);
+        return tr;
       }
-      return TileRef{-(1 + (t - n_contig) * 64), 3};
+      return TileRef{-(1 + (t - n_contig) * 64), 3, {0u, 0u, 0u}, {0u, 0u, 0u}};
     }
   };
 
@@ -356,8 +386,8 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const AttnArgs a) {
           }
           M = prefix_mask(lo);
         } else {
-          const uint64_t md = __builtin_bitreverse64(bits64_at(dbits, a.nwords, i - key0 - 63));
-          const uint64_t mv = bits64_at(vbits, a.nwords, key0);
+          const uint64_t md = __builtin_bitreverse64(win_bits(tr.wd, i - key0 - 63));
+          const uint64_t mv = win_bits(tr.wv, key0);
           M = (md | mv) & prefix_mask(i - key0 + 1);
         }
       } else if constexpr (PAT == P_ASHAPE) {
@@ -429,14 +459,14 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const AttnArgs a) {
   };
 
   // ---- main loop: one barrier per tile, next tile in flight during compute --------------
-  TileRef cur{0, 0};
+  TileRef cur{0, 0, {0u, 0u, 0u}, {0u, 0u, 0u}};
   if (ntiles > 0) {
     cur = next_tile();
     issue_tile(sKV0, cur.key0);
   }
   for (int t = 0; t < ntiles; t += 2) {
     lds_fence_barrier();  // tile t resident in sKV0; everyone done with sKV1
-    TileRef nxt{0, 0};
+    TileRef nxt{0, 0, {0u, 0u, 0u}, {0u, 0u, 0u}};
     if (t + 1 < ntiles) {
       nxt = next_tile();
       issue_tile(sKV1, nxt.key0);
