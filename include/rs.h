@@ -26,7 +26,9 @@
  *    h / (hq / hkv).  O is bf16 [hq][n][d] with strides (so_h, so_t).
  *  - A unit covers query rows [s0, s1) of one query head; its rows see keys [0, s1)
  *    causally (key j visible to row i iff j <= i), as in chunked prefill.
- *  - Supported: d in {64, 128}; hq a multiple of hkv; n <= 262144.
+ *  - Supported: d in {64, 128}; hq a multiple of hkv; n <= 262144; one head's K rows
+ *    ((n - 1) * sk_t + d elements) and V rows span less than 4 GiB (else
+ *    RS_ERR_UNSUPPORTED).
  */
 #ifndef RS_H
 #define RS_H

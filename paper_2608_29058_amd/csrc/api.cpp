@@ -43,7 +43,11 @@ rs_status check_qkv(const rs_qkv *qkv, float *scale) {
     return fail(RS_ERR_INVALID_ARG, "token stride smaller than head dim");
   if (!aligned(qkv->q, 16) || !aligned(qkv->k, 16) || !aligned(qkv->v, 16))
     return fail(RS_ERR_INVALID_ARG, "q, k and v must be 16-byte aligned");
-  (void)esz;
+  // the attention kernels address one head's K and V rows with 32-bit byte offsets
+  const uint64_t span_k = ((uint64_t)(qkv->n - 1) * (uint64_t)qkv->sk_t + (uint64_t)qkv->d) * esz;
+  const uint64_t span_v = ((uint64_t)(qkv->n - 1) * (uint64_t)qkv->sv_t + (uint64_t)qkv->d) * esz;
+  if (span_k > 0xffffffffull || span_v > 0xffffffffull)
+    return fail(RS_ERR_UNSUPPORTED, "one head's K or V rows must span less than 4 GiB");
   float sc = qkv->scale;
   if (sc == 0.f) sc = 1.f / std::sqrt((float)qkv->d);
   if (!(sc > 0.f) || !std::isfinite(sc)) return fail(RS_ERR_INVALID_ARG, "scale must be positive and finite");

@@ -294,19 +294,48 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const AttnArgs a) {
     }
     return min(key0 + row, a.n - 1);
   };
+  // bf16 tiles are copied with buffer loads whose per-lane byte offset is the same for every
+  // tile (row within the tile and swizzled chunk); the tile's first key enters as a scalar
+  // offset.  One head's K (V) rows span less than 4 GiB (checked by the host).
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const int lrow0 = wave_u * RPI + lane / CPR;        // tile row of load 0; load i adds i*NW*RPI
+  const int lchunk = (lane % CPR) ^ swz(lrow0);       // swz() sees only row & 7: same for all i
+  const uint32_t bK = (uint32_t)(a.sk_t * sizeof(InT)), bV = (uint32_t)(a.sv_t * sizeof(InT));
+  [[maybe_unused]] const __amdgpu_buffer_rsrc_t rK = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)Kp, (short)0, (int)((uint32_t)(a.n - 1) * bK + D * sizeof(InT)), 0x00020000);
+  [[maybe_unused]] const __amdgpu_buffer_rsrc_t rV = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)Vp, (short)0, (int)((uint32_t)(a.n - 1) * bV + D * sizeof(InT)), 0x00020000);
+  [[maybe_unused]] const uint32_t voK = (uint32_t)lrow0 * bK + 16u * (uint32_t)lchunk;
+  [[maybe_unused]] const uint32_t voV = (uint32_t)lrow0 * bV + 16u * (uint32_t)lchunk;
   auto issue_tile = [&](bf16 *dstKV, int key0) {
+    if constexpr (sizeof(InT) == 2) {
+      bf16 *dK = dstKV + wave_u * RPI * D, *dV = dK + TE;
+      if (key0 >= 0 && key0 + 64 <= a.n) {  // contiguous rows: offsets are scalar
 #pragma unroll
-    for (int i = 0; i < LPT; ++i) {
-      const int row_base = (i * NW + wave) * RPI;
-      const int row = row_base + lane / CPR;
-      const int c = (lane % CPR) ^ swz(row);
-      const int j = key_of_row(key0, row);
-      if constexpr (sizeof(InT) == 2) {
-        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)(Kp + (long long)j * a.sk_t + 8 * c),
-                                         (__attribute__((address_space(3))) void *)(dstKV + row_base * D), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)(Vp + (long long)j * a.sv_t + 8 * c),
-                                         (__attribute__((address_space(3))) void *)(dstKV + TE + row_base * D), 16, 0, 0);
-      } else {
+        for (int i = 0; i < LPT; ++i) {
+          const uint32_t r0 = (uint32_t)(key0 + i * NW * RPI);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rK, (__attribute__((address_space(3))) void *)(dK + i * NW * RPI * D),
+                                                   16, voK, r0 * bK, 0, 0);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rV, (__attribute__((address_space(3))) void *)(dV + i * NW * RPI * D),
+                                                   16, voV, r0 * bV, 0, 0);
+        }
+      } else {  // gathered rows, or the last tile (rows clamped to the sequence)
+#pragma unroll
+        for (int i = 0; i < LPT; ++i) {
+          const uint32_t j = (uint32_t)key_of_row(key0, lrow0 + i * NW * RPI);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rK, (__attribute__((address_space(3))) void *)(dK + i * NW * RPI * D),
+                                                   16, j * bK + 16u * (uint32_t)lchunk, 0, 0, 0);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rV, (__attribute__((address_space(3))) void *)(dV + i * NW * RPI * D),
+                                                   16, j * bV + 16u * (uint32_t)lchunk, 0, 0, 0);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < LPT; ++i) {
+        const int row_base = (i * NW + wave) * RPI;
+        const int row = row_base + lane / CPR;
+        const int c = (lane % CPR) ^ swz(row);
+        const int j = key_of_row(key0, row);
         const u32x4 kx = load8<InT>(Kp + (long long)j * a.sk_t + 8 * c);
         const u32x4 vx = load8<InT>(Vp + (long long)j * a.sv_t + 8 * c);
         *(u32x4 *)(dstKV + row_base * D + 8 * lane) = kx;
@@ -373,6 +402,7 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const AttnArgs a) {
       }
     }
 
+    bool has_key = true;
     if (need_mask) {
       const int i = my_row;
       uint64_t M;
@@ -397,49 +427,70 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const AttnArgs a) {
         M = prefix_mask(i - key0 + 1);
       }
       M >>= 4 * hh;
+      // this lane's keys are bits 0-3 of every byte of M; a kept key keeps its logit,
+      // a dropped one becomes -inf (bit-field extract to 0 / ~0, then bit-field insert)
+      has_key = (M & 0x0F0F0F0F0F0F0F0Full) != 0ull;
+      const uint32_t Mw[2] = {(uint32_t)M, (uint32_t)(M >> 32)};
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int kk = 32 * mb + 8 * (r >> 2) + (r & 3);
-          if (!((M >> kk) & 1ull)) sacc[mb][r] = -INFINITY;
+          const int kk = 8 * (r >> 2) + (r & 3);
+          const uint32_t keep = (uint32_t)__builtin_amdgcn_sbfe((int)Mw[mb], kk, 1);
+          // the element goes through a scalar: bit_cast of a vector element in place reads
+          // element 0 with this compiler
+          const float x = sacc[mb][r];
+          sacc[mb][r] = __builtin_bit_cast(float, (keep & __builtin_bit_cast(uint32_t, x)) | (~keep & 0xff800000u));
         }
     }
 
-    // online softmax, exp2 domain; the running max is only raised when a row's tile max
-    // exceeds it by more than 2^8 (probabilities stay <= 256 in between)
-    float mx = -INFINITY;
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[mb][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const bool raise = (mx - m_run) * c > 8.f;
-    if (__ballot(raise) != 0ull) {
-      const float m_new = fmaxf(m_run, mx);
-      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-      const float alpha = __builtin_amdgcn_exp2f((m_run - m_use) * c);
-      l_run *= alpha;
-#pragma unroll
-      for (int db = 0; db < DB; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
-      m_run = m_new;
-    }
-    const float nmc = (m_run == -INFINITY) ? 0.f : -m_run * c;
-    float psum = 0.f;
+    // Online softmax in the exp2 domain with a lazily raised running max m_run: the tile's
+    // probabilities are first formed against the current m_run; only if some lane's sum
+    // exceeds 2^8 (so every probability stays <= 2^8 otherwise), or a row sees its first
+    // kept key, is the exact tile max taken, m_run raised, O rescaled and P formed again.
+    // Row sums are taken over the bf16-rounded probabilities that also multiply V.
+    const bf16x2 ones = {(bf16)1.f, (bf16)1.f};
     u32x4 pb[2][2];
+    auto form_p = [&](float nmc) -> float {
+      float ps = 0.f;
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+      for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-      for (int s = 0; s < 2; ++s)
+        for (int s = 0; s < 2; ++s)
 #pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[mb][8 * s + 2 * w], c, nmc));
-          const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[mb][8 * s + 2 * w + 1], c, nmc));
-          psum += p0 + p1;
-          pb[mb][s][w] = pack_bf16x2(p0, p1);
+          for (int w = 0; w < 4; ++w) {
+            const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[mb][8 * s + 2 * w], c, nmc));
+            const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[mb][8 * s + 2 * w + 1], c, nmc));
+            const bf16x2 pk = cvt_bf16x2(p0, p1);
+            pb[mb][s][w] = __builtin_bit_cast(uint32_t, pk);
+            ps = __builtin_amdgcn_fdot2_f32_bf16(pk, ones, ps, false);
+          }
+      return ps;
+    };
+    float psum = form_p((m_run == -INFINITY) ? 0.f : -m_run * c);
+    const uint64_t want = __ballot(!(psum <= 256.f) || (m_run == -INFINITY && has_key));
+    if (want != 0ull) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[mb][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      // both lanes of a row take the same decision
+      if (((want >> l32) | (want >> (l32 + 32))) & 1ull) {
+        const float m_new = fmaxf(m_run, mx);
+        if (m_new > m_run) {
+          const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c);  // 0 for m_run = -inf
+          l_run *= alpha;
+#pragma unroll
+          for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+          m_run = m_new;
         }
+      }
+      psum = form_p((m_run == -INFINITY) ? 0.f : -m_run * c);
+    }
     l_run += psum;
 
     // O^T += V^T P^T; V read transposed from its row-major tile

@@ -54,9 +54,16 @@ struct Arena {
 // ---- device helpers ----------------------------------------------------------------------
 #if defined(__HIP_DEVICE_COMPILE__) || defined(__HIPCC__)
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// Two floats rounded to nearest-even bf16 and packed (one v_cvt_pk_bf16_f32).
+__device__ __forceinline__ bf16x2 cvt_bf16x2(float lo, float hi) {
+  return __builtin_convertvector(f32x2{lo, hi}, bf16x2);
+}
+
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  bf16 a = (bf16)lo, b = (bf16)hi;
-  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+  return __builtin_bit_cast(uint32_t, cvt_bf16x2(lo, hi));
 }
 
 // 8 consecutive elements as 8 bf16 packed in 4 dwords (fp32 input is rounded to bf16).
