@@ -59,10 +59,15 @@ struct AttnArgs {
 constexpr int kMaxTiles = kMaxN / 64;  // key tiles of the longest supported sequence
 constexpr int kMaxGather = 2048;       // vertical columns gathered per query tile
 
-// XOR swizzle of the 16-byte chunk index of LDS row r.  K fragment reads (8 consecutive
-// rows, one chunk) and transposed V reads (4 consecutive rows, 2 adjacent chunks) then hit
-// 8 distinct chunk positions, i.e. distinct banks.
-__device__ __forceinline__ int swz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
+// XOR swizzle of the 16-byte chunk index of LDS row r.  With d = 128 a 256-byte row spans all
+// 64 LDS banks; rows 0-15 then give K fragment reads (16 rows, one chunk column per 16
+// lanes) and transposed V reads (4 rows x 4 adjacent chunks per 32 lanes) distinct banks.
+// With d = 64 (128-byte rows) a 3-bit swizzle over 8 rows does the same.
+template <int D>
+__device__ __forceinline__ int swz(int r) {
+  if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
+  else return ((r & 3) << 1) | ((r >> 2) & 1);
+}
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 
@@ -78,28 +83,6 @@ __device__ __forceinline__ void lds_fence_barrier() {
 
 // Per-tile description produced ahead of its use (the next tile is issued while the
 // current one is computed).
-// Three consecutive bitmap words around a bit position (loaded ahead of their use).
-struct Win3 {
-  uint32_t x0, x1, x2;
-};
-
-__device__ __forceinline__ Win3 load_win(const uint32_t *bits, int nwords, int pos) {
-  const int w = pos >> 5;
-  Win3 r;
-  r.x0 = (w >= 0 && w < nwords) ? bits[w] : 0u;
-  r.x1 = (w + 1 >= 0 && w + 1 < nwords) ? bits[w + 1] : 0u;
-  r.x2 = (w + 2 >= 0 && w + 2 < nwords) ? bits[w + 2] : 0u;
-  return r;
-}
-
-// the 64 bits starting at `pos` from a window loaded with load_win(.., pos)
-__device__ __forceinline__ uint64_t win_bits(const Win3 &r, int pos) {
-  const int sh = pos & 31;
-  uint64_t v = ((uint64_t)r.x0 | ((uint64_t)r.x1 << 32)) >> sh;
-  if (sh) v |= (uint64_t)r.x2 << (64 - sh);
-  return v;
-}
-
 struct TileRef {
   int key0;  // first key of a contiguous tile, or -(1 + gather offset)
   int tag;   // bit 0: rows of waves 0-1 use it, bit 1: rows of waves 2-3 (block-sparse)
@@ -117,11 +100,17 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const AttnArgs a) {
   constexpr int LPT = 64 / RPI / NW;     // loads per thread per K (or V) tile
   constexpr int TE = 64 * D;             // elements of one K or V tile
 
-  __shared__ __align__(16) bf16 sKV0[2 * TE];  // [K tile | V tile], row-major, swizzled
-  __shared__ __align__(16) bf16 sKV1[2 * TE];
+  // K and V tiles are double-buffered separately (K runs one tile ahead of V), row-major and
+  // swizzled.  Four distinct arrays, addressed with a parity known at compile time, let the
+  // compiler see that a copy in flight never overlaps the tiles being read.
+  __shared__ __align__(16) bf16 sK0[TE];
+  __shared__ __align__(16) bf16 sK1[TE];
+  __shared__ __align__(16) bf16 sV0[TE];
+  __shared__ __align__(16) bf16 sV1[TE];
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
 
   const int item = a.order[blockIdx.x];
@@ -297,9 +286,8 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const AttnArgs a) {
   // bf16 tiles are copied with buffer loads whose per-lane byte offset is the same for every
   // tile (row within the tile and swizzled chunk); the tile's first key enters as a scalar
   // offset.  One head's K (V) rows span less than 4 GiB (checked by the host).
-  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-  const int lrow0 = wave_u * RPI + lane / CPR;        // tile row of load 0; load i adds i*NW*RPI
-  const int lchunk = (lane % CPR) ^ swz(lrow0);       // swz() sees only row & 7: same for all i
+  const int lrow0 = wave * RPI + lane / CPR;          // tile row of load 0; load i adds i*NW*RPI
+  const int lchunk = (lane % CPR) ^ swz<D>(lrow0);    // swz sees only row & 15: same for all i
   const uint32_t bK = (uint32_t)(a.sk_t * sizeof(InT)), bV = (uint32_t)(a.sv_t * sizeof(InT));
   [[maybe_unused]] const __amdgpu_buffer_rsrc_t rK = __builtin_amdgcn_make_buffer_rsrc(
       (void *)Kp, (short)0, (int)((uint32_t)(a.n - 1) * bK + D * sizeof(InT)), 0x00020000);
@@ -307,26 +295,25 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const AttnArgs a) {
       (void *)Vp, (short)0, (int)((uint32_t)(a.n - 1) * bV + D * sizeof(InT)), 0x00020000);
   [[maybe_unused]] const uint32_t voK = (uint32_t)lrow0 * bK + 16u * (uint32_t)lchunk;
   [[maybe_unused]] const uint32_t voV = (uint32_t)lrow0 * bV + 16u * (uint32_t)lchunk;
-  auto issue_tile = [&](bf16 *dstKV, int key0) {
+  // one K or V tile (64 key rows) into dst
+  auto issue = [&](bf16 *dst, int key0, bool isV) {
+    const InT *src = isV ? Vp : Kp;
+    const long long st = isV ? a.sv_t : a.sk_t;
     if constexpr (sizeof(InT) == 2) {
-      bf16 *dK = dstKV + wave_u * RPI * D, *dV = dK + TE;
+      const __amdgpu_buffer_rsrc_t rs = isV ? rV : rK;
+      const uint32_t b = isV ? bV : bK, vo = isV ? voV : voK;
+      bf16 *dw = dst + wave * RPI * D;
       if (key0 >= 0 && key0 + 64 <= a.n) {  // contiguous rows: offsets are scalar
 #pragma unroll
-        for (int i = 0; i < LPT; ++i) {
-          const uint32_t r0 = (uint32_t)(key0 + i * NW * RPI);
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(rK, (__attribute__((address_space(3))) void *)(dK + i * NW * RPI * D),
-                                                   16, voK, r0 * bK, 0, 0);
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(rV, (__attribute__((address_space(3))) void *)(dV + i * NW * RPI * D),
-                                                   16, voV, r0 * bV, 0, 0);
-        }
+        for (int i = 0; i < LPT; ++i)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void *)(dw + i * NW * RPI * D),
+                                                   16, vo, (uint32_t)(key0 + i * NW * RPI) * b, 0, 0);
       } else {  // gathered rows, or the last tile (rows clamped to the sequence)
 #pragma unroll
         for (int i = 0; i < LPT; ++i) {
           const uint32_t j = (uint32_t)key_of_row(key0, lrow0 + i * NW * RPI);
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(rK, (__attribute__((address_space(3))) void *)(dK + i * NW * RPI * D),
-                                                   16, j * bK + 16u * (uint32_t)lchunk, 0, 0, 0);
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(rV, (__attribute__((address_space(3))) void *)(dV + i * NW * RPI * D),
-                                                   16, j * bV + 16u * (uint32_t)lchunk, 0, 0, 0);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void *)(dw + i * NW * RPI * D),
+                                                   16, j * b + 16u * (uint32_t)lchunk, 0, 0, 0);
         }
       }
     } else {
@@ -334,27 +321,26 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const AttnArgs a) {
       for (int i = 0; i < LPT; ++i) {
         const int row_base = (i * NW + wave) * RPI;
         const int row = row_base + lane / CPR;
-        const int c = (lane % CPR) ^ swz(row);
+        const int cc = (lane % CPR) ^ swz<D>(row);
         const int j = key_of_row(key0, row);
-        const u32x4 kx = load8<InT>(Kp + (long long)j * a.sk_t + 8 * c);
-        const u32x4 vx = load8<InT>(Vp + (long long)j * a.sv_t + 8 * c);
-        *(u32x4 *)(dstKV + row_base * D + 8 * lane) = kx;
-        *(u32x4 *)(dstKV + TE + row_base * D + 8 * lane) = vx;
+        *(u32x4 *)(dst + row_base * D + 8 * lane) = load8<InT>(src + (long long)j * st + 8 * cc);
       }
     }
   };
 
   // ---- per-lane LDS fragment offsets -----------------------------------------------------
-  const int kswz = swz(l32);                 // K rows 32 mb + l32
+  const int kswz = swz<D>(l32);                 // K rows 32 mb + l32
   const int g16 = lane >> 4, i16 = lane & 15;
   const int esrc = i16 >> 2, qv = i16 & 3;   // transposed V read: source row / dd quad
   const int vrow = 4 * hh + esrc;            // + 32 mb + 16 s + 8 half
-  const int vsw = 2 * esrc + hh;             // swz(vrow + ...) is lane-constant
-  int voff[DB];
+  // swz<D>(vrow + 8 half + 16 s + 32 mb) depends on the half only
+  const int vsw0 = swz<D>(vrow), vsw1 = swz<D>(vrow + 8);
+  int voff[DB], voff1[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) {
     const int dd0 = 32 * db + 16 * (g16 & 1) + 4 * qv;
-    voff[db] = vrow * D + (((dd0 >> 3) ^ vsw) << 3) + (dd0 & 7);
+    voff[db] = vrow * D + (((dd0 >> 3) ^ vsw0) << 3) + (dd0 & 7);
+    voff1[db] = (vrow + 8) * D + (((dd0 >> 3) ^ vsw1) << 3) + (dd0 & 7);
   }
 
   f32x16 oacc[DB];
@@ -365,171 +351,232 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const AttnArgs a) {
   float m_run = -INFINITY, l_run = 0.f;
   const float c = a.c;
   const int my_rows_tag = wave < 2 ? 1 : 2;
+  const bf16x2 ones = {(bf16)1.f, (bf16)1.f};
 
-  auto compute_tile = [&](const bf16 *sKV, TileRef tr) {
+  // Dense and A-shape compute every tile of the list for every wave (a tile outside a
+  // wave's rows is fully masked), so that the softmax of one tile and the products of the
+  // next form one branch-free block the scheduler interleaves.
+  constexpr bool kOverlap = PAT == P_DENSE || PAT == P_ASHAPE;
+
+  // ---- per-tile plan of this wave: participation, mask need, active 32-key halves ---------
+  struct Plan {
+    bool on, need_mask, do0, do1;
+    uint64_t Mvs;  // vertical-slash contiguous tile: this lane's kept keys (after half shift)
+    int g0, g_cnt; // vertical-slash gathered tile: first column slot, column count
+  };
+  auto plan_of = [&](const TileRef &tr, bool valid) -> Plan {
+    Plan p{false, true, true, true, 0ull, 0, 0};
+    if (!valid) return p;
     const int key0 = tr.key0;
-    if (!wave_active || !(tr.tag & my_rows_tag)) return;
-    bool need_mask = true;
-    int g_cnt = 0, g0 = 0;
+    if constexpr (kOverlap) {
+      p.on = true;
+      if constexpr (PAT == P_ASHAPE)
+        p.need_mask = !(key0 + 63 <= w_lo && (key0 + 63 < a.sink || key0 > w_hi - a.window));
+      else
+        p.need_mask = key0 + 63 > w_lo;
+      return p;
+    }
+    if (!wave_active || !(tr.tag & my_rows_tag)) return p;
     if constexpr (PAT == P_VS) {
       if (key0 < 0) {
-        g0 = -key0 - 1;
-        g_cnt = min(64, n_gather - g0);
-        if (sG[g0] > w_hi) return;
-      } else if (key0 > w_hi) {
-        return;
+        p.g0 = -key0 - 1;
+        p.g_cnt = min(64, n_gather - p.g0);
+        p.on = sG[p.g0] <= w_hi;
+        p.do1 = p.g_cnt > 32;
+      } else if (key0 <= w_hi) {
+        // the lane's kept keys are known before any product: a 32-key half no row of the
+        // wave keeps skips both of its products
+        const int i = my_row;
+        const uint64_t md = __builtin_bitreverse64(win_bits(tr.wd, i - key0 - 63));
+        const uint64_t mv = win_bits(tr.wv, key0);
+        p.Mvs = ((md | mv) & prefix_mask(i - key0 + 1)) >> (4 * hh);
+        p.do0 = __ballot(((uint32_t)p.Mvs & 0x0f0f0f0fu) != 0u) != 0ull;
+        p.do1 = __ballot(((uint32_t)(p.Mvs >> 32) & 0x0f0f0f0fu) != 0u) != 0ull;
+        p.on = p.do0 || p.do1;
       }
-    } else {
-      if (key0 > w_hi) return;
-      if constexpr (PAT == P_ASHAPE) {
-        if (key0 >= a.sink && key0 + 63 < w_lo - a.window + 1) return;
-        need_mask = !(key0 + 63 <= w_lo && (key0 + 63 < a.sink || key0 > w_hi - a.window));
-      } else {
-        need_mask = key0 + 63 > w_lo;
-      }
+    } else {  // block-sparse
+      p.on = key0 <= w_hi;
+      p.need_mask = key0 + 63 > w_lo;
     }
-    const bf16 *sK = sKV, *sV = sKV + TE;
+    return p;
+  };
 
-    f32x16 sacc[2];
+  // ---- S^T[64 keys x 32 rows] = K_tile x Q^T ---------------------------------------------
+  auto qk = [&](f32x16 (&s)[2], const bf16 *sKt, const Plan &p) {
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb) {
+      const bool dm = mb ? p.do1 : p.do0;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[mb][r] = 0.f;
+      for (int r = 0; r < 16; ++r) s[mb][r] = 0.f;
+      if constexpr (PAT == P_VS)
+        if (!dm) continue;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        const u32x4 kf = *(const u32x4 *)&sK[(32 * mb + l32) * D + (((2 * ks + hh) ^ kswz) << 3)];
-        sacc[mb] = mfma32(kf, qf[ks], sacc[mb]);
+        const u32x4 kf = *(const u32x4 *)&sKt[(32 * mb + l32) * D + (((2 * ks + hh) ^ kswz) << 3)];
+        s[mb] = mfma32(kf, qf[ks], s[mb]);
       }
     }
+  };
 
-    bool has_key = true;
-    if (need_mask) {
-      const int i = my_row;
-      uint64_t M;
-      if constexpr (PAT == P_VS) {
-        if (key0 < 0) {
-          int lo = 0, hi = g_cnt;
-          while (lo < hi) {
-            const int mid = (lo + hi) >> 1;
-            if (sG[g0 + mid] <= i) lo = mid + 1;
-            else hi = mid;
-          }
-          M = prefix_mask(lo);
-        } else {
-          const uint64_t md = __builtin_bitreverse64(win_bits(tr.wd, i - key0 - 63));
-          const uint64_t mv = win_bits(tr.wv, key0);
-          M = (md | mv) & prefix_mask(i - key0 + 1);
+  // ---- masks: this lane's keys are bits 0-3 of every byte of M (after the half shift); a
+  // kept key keeps its logit, a dropped one (or a skipped half) becomes -inf ---------------
+  auto apply_mask = [&](f32x16 (&s)[2], const TileRef &tr, const Plan &p) -> bool {
+    const int key0 = tr.key0, i = my_row;
+    uint64_t M;
+    if constexpr (PAT == P_VS) {
+      if (key0 < 0) {
+        int lo = 0, hi = p.g_cnt;
+        while (lo < hi) {
+          const int mid = (lo + hi) >> 1;
+          if (sG[p.g0 + mid] <= i) lo = mid + 1;
+          else hi = mid;
         }
-      } else if constexpr (PAT == P_ASHAPE) {
-        const uint64_t keep = prefix_mask(a.sink - key0) | ~prefix_mask(i - a.window + 1 - key0);
-        M = keep & prefix_mask(i - key0 + 1);
+        M = prefix_mask(lo) >> (4 * hh);
       } else {
-        M = prefix_mask(i - key0 + 1);
+        M = p.Mvs;
       }
-      M >>= 4 * hh;
-      // this lane's keys are bits 0-3 of every byte of M; a kept key keeps its logit,
-      // a dropped one becomes -inf (bit-field extract to 0 / ~0, then bit-field insert)
-      has_key = (M & 0x0F0F0F0F0F0F0F0Full) != 0ull;
-      const uint32_t Mw[2] = {(uint32_t)M, (uint32_t)(M >> 32)};
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int kk = 8 * (r >> 2) + (r & 3);
-          const uint32_t keep = (uint32_t)__builtin_amdgcn_sbfe((int)Mw[mb], kk, 1);
-          // the element goes through a scalar: bit_cast of a vector element in place reads
-          // element 0 with this compiler
-          const float x = sacc[mb][r];
-          sacc[mb][r] = __builtin_bit_cast(float, (keep & __builtin_bit_cast(uint32_t, x)) | (~keep & 0xff800000u));
-        }
+      if (!p.do0) M &= ~0xffffffffull;
+      if (!p.do1) M &= 0xffffffffull;
+    } else if constexpr (PAT == P_ASHAPE) {
+      const uint64_t keep = prefix_mask(a.sink - key0) | ~prefix_mask(i - a.window + 1 - key0);
+      M = (keep & prefix_mask(i - key0 + 1)) >> (4 * hh);
+    } else {
+      M = prefix_mask(i - key0 + 1) >> (4 * hh);
     }
-
-    // Online softmax in the exp2 domain with a lazily raised running max m_run: the tile's
-    // probabilities are first formed against the current m_run; only if some lane's sum
-    // exceeds 2^8 (so every probability stays <= 2^8 otherwise), or a row sees its first
-    // kept key, is the exact tile max taken, m_run raised, O rescaled and P formed again.
-    // Row sums are taken over the bf16-rounded probabilities that also multiply V.
-    const bf16x2 ones = {(bf16)1.f, (bf16)1.f};
-    u32x4 pb[2][2];
-    auto form_p = [&](float nmc) -> float {
-      float ps = 0.f;
+    const uint32_t Mw[2] = {(uint32_t)M, (uint32_t)(M >> 32)};
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
+    for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-        for (int s = 0; s < 2; ++s)
-#pragma unroll
-          for (int w = 0; w < 4; ++w) {
-            const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[mb][8 * s + 2 * w], c, nmc));
-            const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[mb][8 * s + 2 * w + 1], c, nmc));
-            const bf16x2 pk = cvt_bf16x2(p0, p1);
-            pb[mb][s][w] = __builtin_bit_cast(uint32_t, pk);
-            ps = __builtin_amdgcn_fdot2_f32_bf16(pk, ones, ps, false);
-          }
-      return ps;
-    };
-    float psum = form_p((m_run == -INFINITY) ? 0.f : -m_run * c);
-    const uint64_t want = __ballot(!(psum <= 256.f) || (m_run == -INFINITY && has_key));
-    if (want != 0ull) {
-      float mx = -INFINITY;
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[mb][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      // both lanes of a row take the same decision
-      if (((want >> l32) | (want >> (l32 + 32))) & 1ull) {
-        const float m_new = fmaxf(m_run, mx);
-        if (m_new > m_run) {
-          const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c);  // 0 for m_run = -inf
-          l_run *= alpha;
-#pragma unroll
-          for (int db = 0; db < DB; ++db)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
-          m_run = m_new;
-        }
+      for (int r = 0; r < 16; ++r) {
+        const uint32_t keep = (uint32_t)__builtin_amdgcn_sbfe((int)Mw[mb], 8 * (r >> 2) + (r & 3), 1);
+        // the element goes through a scalar: bit_cast of a vector element in place reads
+        // element 0 with this compiler
+        const float x = s[mb][r];
+        s[mb][r] = __builtin_bit_cast(float, (keep & __builtin_bit_cast(uint32_t, x)) | (~keep & 0xff800000u));
       }
-      psum = form_p((m_run == -INFINITY) ? 0.f : -m_run * c);
-    }
-    l_run += psum;
+    return (M & 0x0F0F0F0F0F0F0F0Full) != 0ull;
+  };
 
-    // O^T += V^T P^T; V read transposed from its row-major tile
+  // ---- online softmax in the exp2 domain with a lazily raised running max ------------------
+  // P is formed against the current m_run; only if some lane's probability sum exceeds 2^8
+  // (so every probability stays <= 2^8 otherwise), or a row sees its first kept key, is the
+  // exact tile max taken, m_run raised, O rescaled and P formed again.  Row sums are taken
+  // over the bf16-rounded probabilities that also multiply V.
+  u32x4 pb[2][2];
+  auto form_p = [&](const f32x16 (&s)[2], float nmc) -> float {
+    float ps = 0.f;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(s[mb][8 * h + 2 * w], c, nmc));
+          const float p1 = __builtin_amdgcn_exp2f(fmaf(s[mb][8 * h + 2 * w + 1], c, nmc));
+          const bf16x2 pk = cvt_bf16x2(p0, p1);
+          pb[mb][h][w] = __builtin_bit_cast(uint32_t, pk);
+          ps = __builtin_amdgcn_fdot2_f32_bf16(pk, ones, ps, false);
+        }
+    return ps;
+  };
+
+  // ---- O^T[d x 32 rows] += V^T x P^T (V read transposed from its row-major tile) ----------
+  auto pv = [&](const bf16 *sVt, const Plan &p) {
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
+      for (int mb = 0; mb < 2; ++mb) {
+        if constexpr (PAT == P_VS)
+          if (!(mb ? p.do1 : p.do0)) continue;
 #pragma unroll
-        for (int s = 0; s < 2; ++s) {
-          const bf16 *vp = sV + voff[db] + (32 * mb + 16 * s) * D;
+        for (int h = 0; h < 2; ++h) {
+          const bf16 *vp = sVt + voff[db] + (32 * mb + 16 * h) * D;
+          const bf16 *vq = sVt + voff1[db] + (32 * mb + 16 * h) * D;
           const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16 *)(vp));
-          const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16 *)(vp + 8 * D));
+          const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16 *)(vq));
           const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
-          const u32x4 af = u32x4{l2[0], l2[1], h2[0], h2[1]};
-          oacc[db] = mfma32(af, pb[mb][s], oacc[db]);
+          oacc[db] = mfma32(u32x4{l2[0], l2[1], h2[0], h2[1]}, pb[mb][h], oacc[db]);
         }
+      }
   };
 
-  // ---- main loop: one barrier per tile, next tile in flight during compute --------------
-  TileRef cur{0, 0, {0u, 0u, 0u}, {0u, 0u, 0u}};
+  // ---- one pipeline step: tile t's softmax and P V, tile t+1's products -------------------
+  // On entry sc holds S^T of tile t; K of tile t+1 (in kn) and V of tile t (in vc) are resident
+  // after the barrier.  The step copies K of tile t+2 into kc (released by tile t's products)
+  // and V of tile t+1 into vn (released by tile t-1's P V).
+  TileRef Tc{0, 0, {0u, 0u, 0u}, {0u, 0u, 0u}}, Tn = Tc;
+  Plan Pc = plan_of(Tc, false), Pn = Pc;
+  auto step = [&](int t, f32x16 (&sc)[2], f32x16 (&sn)[2], bf16 *kc, bf16 *kn, bf16 *vc, bf16 *vn) {
+    TileRef T2{0, 0, {0u, 0u, 0u}, {0u, 0u, 0u}};
+    if (t + 2 < ntiles) T2 = next_tile();
+    lds_fence_barrier();
+    if (t + 2 < ntiles) issue(kc, T2.key0, false);
+    if (t + 1 < ntiles) issue(vn, Tn.key0, true);
+    Pn = plan_of(Tn, t + 1 < ntiles);
+    bool has_key = true;
+    if (kOverlap || Pc.on)
+      if (PAT == P_VS || Pc.need_mask) has_key = apply_mask(sc, Tc, Pc);
+    // tile t+1's products beside tile t's softmax
+    if (kOverlap || Pn.on) qk(sn, kn, Pn);
+    if (kOverlap || Pc.on) {
+      float psum = form_p(sc, (m_run == -INFINITY) ? 0.f : -m_run * c);
+      const uint64_t want = __ballot(!(psum <= 256.f) || (m_run == -INFINITY && has_key));
+      if constexpr (kOverlap) {
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // K fragment read
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // product
+          __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);  // softmax
+        }
+      }
+      if (want != 0ull) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[mb][r]);
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        // both lanes of a row take the same decision
+        if (((want >> l32) | (want >> (l32 + 32))) & 1ull) {
+          const float m_new = fmaxf(m_run, mx);
+          if (m_new > m_run) {
+            const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c);  // 0 for m_run = -inf
+            l_run *= alpha;
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+              for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+            m_run = m_new;
+          }
+        }
+        psum = form_p(sc, (m_run == -INFINITY) ? 0.f : -m_run * c);
+      }
+      l_run += psum;
+      pv(vc, Pc);
+    }
+    Tc = Tn;
+    Tn = T2;
+    Pc = Pn;
+  };
+
+  // ---- main loop ---------------------------------------------------------------------------
+  f32x16 sA[2], sB[2];
   if (ntiles > 0) {
-    cur = next_tile();
-    issue_tile(sKV0, cur.key0);
+    Tc = next_tile();
+    issue(sK0, Tc.key0, false);
+    issue(sV0, Tc.key0, true);
+    if (ntiles > 1) {
+      Tn = next_tile();
+      issue(sK1, Tn.key0, false);
+    }
+    lds_fence_barrier();
+    Pc = plan_of(Tc, true);
+    if (kOverlap || Pc.on) qk(sA, sK0, Pc);
   }
   for (int t = 0; t < ntiles; t += 2) {
-    lds_fence_barrier();  // tile t resident in sKV0; everyone done with sKV1
-    TileRef nxt{0, 0, {0u, 0u, 0u}, {0u, 0u, 0u}};
-    if (t + 1 < ntiles) {
-      nxt = next_tile();
-      issue_tile(sKV1, nxt.key0);
-    }
-    compute_tile(sKV0, cur);
+    step(t, sA, sB, sK0, sK1, sV0, sV1);
     if (t + 1 >= ntiles) break;
-    lds_fence_barrier();  // tile t+1 resident in sKV1; everyone done with sKV0
-    if (t + 2 < ntiles) {
-      cur = next_tile();
-      issue_tile(sKV0, cur.key0);
-    }
-    compute_tile(sKV1, nxt);
+    step(t + 1, sB, sA, sK1, sK0, sV1, sV0);
   }
 
   // ---- epilogue --------------------------------------------------------------------------

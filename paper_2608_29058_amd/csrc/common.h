@@ -109,6 +109,29 @@ __device__ __forceinline__ uint64_t bits64_at(const uint32_t *bits, int nwords, 
   return r;
 }
 
+// Three consecutive bitmap words around a bit position (loaded ahead of their use).
+struct Win3 {
+  uint32_t x0, x1, x2;
+};
+
+__device__ __forceinline__ Win3 load_win(const uint32_t *bits, int nwords, int pos) {
+  const int w = pos >> 5;
+  Win3 r;
+  r.x0 = (w >= 0 && w < nwords) ? bits[w] : 0u;
+  r.x1 = (w + 1 >= 0 && w + 1 < nwords) ? bits[w + 1] : 0u;
+  r.x2 = (w + 2 >= 0 && w + 2 < nwords) ? bits[w + 2] : 0u;
+  return r;
+}
+
+// the 64 bits starting at `pos` from a window loaded with load_win(.., pos)
+__device__ __forceinline__ uint64_t win_bits(const Win3 &r, int pos) {
+  const int sh = pos & 31;
+  uint64_t v = ((uint64_t)r.x0 | ((uint64_t)r.x1 << 32)) >> sh;
+  if (sh) v |= (uint64_t)r.x2 << (64 - sh);
+  return v;
+}
+
+
 // order-preserving map of a float to uint32 (larger value => larger key; -0.0 < +0.0)
 __device__ __forceinline__ uint32_t float_key(float f) {
   uint32_t u = __builtin_bit_cast(uint32_t, f);

@@ -23,8 +23,11 @@
 namespace rs {
 
 constexpr int kProbeMaxRows = 256;  // sampled rows per unit
-constexpr int kChunk = 128;         // keys per workgroup in the three passes
+constexpr int kRange = 1024;        // keys per workgroup range in the three passes
 constexpr int kMaxCand = 16;
+constexpr int kPrefVs = 3;   // vertical-slash candidates whose bitmap words are prefetched
+constexpr int kPrefBs = 3;   // block-sparse candidates whose selection words are prefetched
+constexpr int kSkew = 98;    // row stride of the skewed probability tile (96 columns + pad)
 
 struct ProbeUnit {
   int head, s0, s1, nrows;  // nrows = sampled rows actually present
@@ -48,10 +51,14 @@ struct ProbeArgs {
   float *row_max, *row_sum;
   // pass 2 partials / outputs
   float *col, *diag_part, *ent_part, *loc_part;
-  int diag_w;  // width of a diagonal partial row (kChunk + rmax)
+  int diag_w;  // width of a diagonal partial row (kRange + rmax)
   // pass 3
   int ncand;
   CandDev cand[kMaxCand];
+  int ncov;                  // candidates with a general kept-mass accumulator
+  int cov_cand[kMaxCand];    // accumulator slot -> candidate
+  int nvs_pref, vs_pref_c[kPrefVs], vs_pref_cl[kPrefVs];  // prefetched vertical-slash candidates
+  int nbs_pref, bs_pref_c[kPrefBs], bs_pref_cl[kPrefBs];  // prefetched block-sparse candidates
   const uint32_t *vs_vbits, *vs_dbits;
   int nwords, ncand_vs;
   const uint32_t *bs_bits;
@@ -71,7 +78,14 @@ __device__ __forceinline__ int acc_key(int mb, int r, int hh) {
   return 32 * mb + 8 * (r >> 2) + 4 * hh + (r & 3);
 }
 
-__device__ __forceinline__ int swz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
+// XOR swizzle of the 16-byte chunk index of LDS row r: with d = 128 (256-byte rows spanning
+// all 64 banks) the K fragment reads of 16 consecutive rows hit distinct banks; d = 64 uses
+// a 3-bit swizzle over 8 rows.
+template <int D>
+__device__ __forceinline__ int swz(int r) {
+  if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
+  else return ((r & 3) << 1) | ((r >> 2) & 1);
+}
 
 // Barrier after which every wave's direct-to-LDS copies (global_load_lds, counted by
 // vmcnt) and LDS accesses are complete.  The explicit vmcnt wait is required: the
@@ -85,114 +99,222 @@ __device__ __forceinline__ void lds_fence_barrier() {
 
 enum { M_STATS = 0, M_SCORES = 1, M_COVER = 2 };
 
-// ---- the three passes over one 128-key chunk --------------------------------------------
-// grid: (chunk, unit group).  A group holds the units of up to 4 query heads that share a
-// key/value head and a segment, hence the same sampled rows and keys: the chunk's keys are
-// copied to LDS once (row-major, XOR-swizzled 16-byte chunks) and wave w handles every
-// sampled-row block of the group's unit w against the chunk's 2 tiles.
-//   M_STATS   per (row, chunk): max and sum of exp over the chunk's visible keys
+// s_waitcnt immediate (gfx9 encoding) waiting until at most n vector-memory operations are
+// outstanding, with no wait on the other counters
+constexpr int vm_wait_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+
+// ---- the three passes over one key range ------------------------------------------------
+// grid: (key range, unit group, row-block pair).  A group holds the units of up to 4 query
+// heads that share a key/value head and a segment, hence the same sampled rows and keys; wave
+// w computes unit w.  Sampled rows are split into 32-row blocks aligned at the end of the
+// (ascending) row list, so the recent rows fill the last blocks, and blocks are paired from
+// the end.  A workgroup streams the 64-key tiles of its range through two LDS buffers (direct
+// buffer-to-LDS copies, one barrier per tile) and keeps the Q fragments of its block pair in
+// registers for the whole range.  The scores pass takes every pair holding recent rows in one
+// workgroup, so column sums and diagonal partials of a range have a single writer.
+//   M_STATS   per (row, range): max and sum of exp over the range's visible keys
 //   M_SCORES  normalised a_ij of the recent rows -> col and diagonal partials
 //   M_COVER   normalised a_ij -> per-candidate kept mass, block entropy and local mass
-template <int D, typename InT, int MODE>
-__global__ void __launch_bounds__(256) probe_chunk_kernel(const ProbeArgs a) {
-  constexpr int CPR = D / 8, RPI = 64 / CPR;
-  constexpr int NLOAD = kChunk / RPI / 4;  // 16-byte loads per thread for the chunk
-  constexpr int NT = kChunk / 64;          // tiles per chunk
-  const int ch = blockIdx.x;
+template <int D, typename InT, int MODE, int NCV>
+__global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) {
+  constexpr int KS = D / 16, CPR = D / 8, RPI = 64 / CPR, LPT = 64 / RPI / 4;
+  constexpr int TE = 64 * D;
+  // two K tile buffers: the next tile (and, for coverage, its bitmap words) is fetched while
+  // the current one is computed.  Deeper rings do not help here: the compiler waits for all
+  // LDS-bound copies before any LDS read.
+  constexpr int NBUF = 2;
+  __shared__ __align__(16) bf16 sKb[NBUF][TE];
+  __shared__ int sRows[2][32];
+
+  const int rg = blockIdx.x;
   const int4 grp = a.groups[blockIdx.y];
-  const ProbeUnit U0 = a.units[grp.x];     // shared head group, segment and sampled rows
-  const int c0 = ch * kChunk;
+  const ProbeUnit U0 = a.units[grp.x];
+  const int c0 = rg * kRange;
   if (c0 >= U0.s1) return;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, hh = lane >> 5;
+  const int kend = min(c0 + kRange, U0.s1);
+  const int nrows = U0.nrows, nrb = (nrows + 31) / 32;
+  int p_lo, p_hi;
+  if constexpr (MODE == M_SCORES) {
+    if (U0.nR <= 0) return;
+    p_lo = 0;
+    p_hi = (U0.nR - 1) / 64 + 1;
+  } else {
+    p_lo = blockIdx.z;
+    p_hi = p_lo + 1;
+    if (2 * p_lo >= nrb) return;
+  }
+  const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hh = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int u = wave == 0 ? grp.x : wave == 1 ? grp.y : wave == 2 ? grp.z : grp.w;
   const InT *Kp = (const InT *)a.k + (long long)(U0.head / a.group) * a.sk_h;
 
-  __shared__ __align__(16) bf16 sK[kChunk * D];
-  __shared__ int sRows[4][32];
+  // K tile copies: per-lane byte offset fixed, the tile's first key as a scalar offset
+  const int lrow0 = wave * RPI + lane / CPR;
+  const int lchunk = (lane % CPR) ^ swz<D>(lrow0);
+  const uint32_t bK = (uint32_t)(a.sk_t * sizeof(InT));
+  [[maybe_unused]] const __amdgpu_buffer_rsrc_t rK = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)Kp, (short)0, (int)((uint32_t)(a.n - 1) * bK + D * sizeof(InT)), 0x00020000);
+  const uint32_t voK = (uint32_t)lrow0 * bK + 16u * (uint32_t)lchunk;
+  auto issue_tile = [&](bf16 *dst, int k0) {
+    bf16 *dK = dst + wave * RPI * D;
 #pragma unroll
-  for (int i = 0; i < NLOAD; ++i) {
-    const int row_base = (i * 4 + wave) * RPI;
-    const int row = row_base + lane / CPR;
-    const int cc = (lane % CPR) ^ swz(row);
-    const int j = min(c0 + row, a.n - 1);
-    if constexpr (sizeof(InT) == 2) {
-      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)(Kp + (long long)j * a.sk_t + 8 * cc),
-                                       (__attribute__((address_space(3))) void *)(sK + row_base * D), 16, 0, 0);
-    } else {
-      *(u32x4 *)(sK + row_base * D + 8 * lane) = load8<InT>(Kp + (long long)j * a.sk_t + 8 * cc);
+    for (int i = 0; i < LPT; ++i) {
+      const int rr = lrow0 + i * 4 * RPI;
+      if constexpr (sizeof(InT) == 2) {
+        if (k0 + 64 <= a.n) {
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rK, (__attribute__((address_space(3))) void *)(dK + i * 4 * RPI * D),
+                                                   16, voK, (uint32_t)(k0 + i * 4 * RPI) * bK, 0, 0);
+        } else {
+          const uint32_t j = (uint32_t)min(k0 + rr, a.n - 1);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rK, (__attribute__((address_space(3))) void *)(dK + i * 4 * RPI * D),
+                                                   16, j * bK + 16u * (uint32_t)lchunk, 0, 0, 0);
+        }
+      } else {
+        const int j = min(k0 + rr, a.n - 1);
+        *(u32x4 *)(dK + i * 4 * RPI * D + 8 * lane) = load8<InT>(Kp + (long long)j * a.sk_t + 8 * lchunk);
+      }
     }
-  }
+  };
 
-  // pass-specific shared state (one slice per wave = per unit)
-  float (*sP)[65] = nullptr;
+  // scores pass: a skewed probability tile per wave, and per-unit column sums and diagonal
+  // partials of this range, all in LDS
+  float (*sD)[kSkew] = nullptr;
   float *sCol = nullptr, *sDg = nullptr;
-  const int dw = kChunk + U0.nR;                  // diagonals touched by R rows in this chunk
-  const int dbase = U0.r0 - (c0 + kChunk - 1);    // smallest such diagonal
+  const int dw = kRange + U0.nR;                // diagonals touched by recent rows in this range
+  const int dbase = U0.r0 - (c0 + kRange - 1);  // smallest such diagonal
   if constexpr (MODE == M_SCORES) {
-    __shared__ float sPbuf[4][32][65];            // per-wave probability tile [row][key]
-    __shared__ float sColbuf[4][kChunk];          // per-unit column sums
-    __shared__ float sDgbuf[4][kChunk + kProbeMaxRows];
-    sP = sPbuf[wave];
+    __shared__ float sDbuf[4][32][kSkew];
+    __shared__ float sColbuf[4][kRange];
+    __shared__ float sDgbuf[4][kRange + kProbeMaxRows];
+    sD = sDbuf[wave];
     sCol = sColbuf[wave];
     sDg = sDgbuf[wave];
-    for (int x = lane; x < kChunk; x += 64) sCol[x] = 0.f;
+    for (int x = lane; x < kRange; x += 64) sCol[x] = 0.f;
     for (int x = lane; x < dw; x += 64) sDg[x] = 0.f;
+    for (int x = lane; x < 32 * kSkew; x += 64) sD[x / kSkew][x % kSkew] = 0.f;
   }
-  lds_fence_barrier();  // K chunk resident
-  if (u < 0) return;    // no unit for this wave (no barrier follows)
 
-  const ProbeUnit U = a.units[u];
-  const InT *Qp = (const InT *)a.q + (long long)U.head * a.sq_h;
-  const int nrb = (U.nrows + 31) / 32;
-  const int kswz = swz(l32);
-  // the scores pass only needs the recent rows (the last nR sampled rows)
-  const int rb_first = (MODE == M_SCORES) ? (U0.nrows - U0.nR) / 32 : 0;
-  for (int rb = rb_first; rb < nrb; ++rb) {
-    const int ridx = 32 * rb + l32;
-    const bool rvalid = ridx < U.nrows;
-    const long long rofs = (long long)u * a.rmax + ridx;
-    const int row = rvalid ? a.rows[rofs] : -1;
-    if (hh == 0) sRows[wave][l32] = row;
-    wave_sync();
-    const int rbmax = sRows[wave][min(31, U.nrows - 1 - 32 * rb)];  // rows ascending
-    if (rbmax < c0) {  // no row of the block sees this chunk (wave-uniform)
-      wave_sync();
-      continue;
-    }
-    u32x4 qf[D / 16];
-#pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) {
-      qf[ks] = u32x4{0u, 0u, 0u, 0u};
-      if (rvalid) qf[ks] = load8<InT>(Qp + (long long)row * a.sq_t + 16 * ks + 8 * hh);
-    }
-    float nmc = 0.f, invl = 0.f;
-    int sub = -1;
-    if constexpr (MODE != M_STATS) {
-      nmc = rvalid ? -a.row_max[rofs] * kLog2e : 0.f;
-      invl = rvalid ? 1.f / a.row_sum[rofs] : 0.f;
-      sub = rvalid ? a.subset[rofs] : -1;
-    }
-    const bool isR = sub == 0;
-    const bool blockR = (MODE == M_SCORES) && (__ballot(isR && hh == 0) != 0ull);
-    const int rfirst = max(0, (U.nrows - U.nR) - 32 * rb);  // first recent row in the block
-    float m_run = -INFINITY, l_run = 0.f;
-    float ent = 0.f, loc = 0.f;
-    float cov[kMaxCand];
-#pragma unroll
-    for (int c = 0; c < kMaxCand; ++c) cov[c] = 0.f;
+  const int kswz = swz<D>(l32);
+  const InT *Qp = u >= 0 ? (const InT *)a.q + (long long)a.units[u].head * a.sq_h : nullptr;
+  const float c = a.c;
 
-    for (int tt = 0; tt < NT; ++tt) {
-      const int k0 = c0 + 64 * tt;
-      if (k0 > rbmax) break;
-      f32x16 s[2];
+  for (int pr = p_lo; pr < p_hi; ++pr) {
+    // ---- the pair's two blocks: rows, Q fragments, per-row constants ------------------------
+    const int b1 = nrb - 1 - 2 * pr, b0 = b1 - 1;
+    __syncthreads();  // previous pair done with sRows and the tile buffers
+    if (tid < 64) {
+      const int s = tid >> 5, b = s ? b1 : b0;
+      const int x = nrows - 32 * (nrb - b) + (tid & 31);
+      sRows[s][tid & 31] = (b >= 0 && x >= 0) ? a.rows[(long long)grp.x * a.rmax + x] : -1;
+    }
+    __syncthreads();
+    const int rmax0 = sRows[0][31], rmax1 = sRows[1][31];  // rows ascending; -1: no block
+    const int kstop = min(kend, rmax1 + 1);                 // keys beyond the last row are unseen
+    if (kstop <= c0) continue;                              // uniform over the workgroup
+    const int nt = (kstop - c0 + 63) >> 6;
+
+    int xr[2], row[2];
+    u32x4 qf[2][KS];
+    float nmc[2];
+    bool isR[2];
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int b = s ? b1 : b0;
+      xr[s] = nrows - 32 * (nrb - b) + l32;
+      row[s] = sRows[s][l32];
+      const bool ok = u >= 0 && row[s] >= 0;
+      const long long rofs = (long long)u * a.rmax + xr[s];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        qf[s][ks] = u32x4{0u, 0u, 0u, 0u};
+        if (ok) qf[s][ks] = load8<InT>(Qp + (long long)row[s] * a.sq_t + 16 * ks + 8 * hh);
+      }
+      nmc[s] = -INFINITY;
+      isR[s] = false;
+      if constexpr (MODE != M_STATS) {
+        // a_ij = exp2(l_ij * c - (row_max * log2 e + log2 row_sum))
+        if (ok) nmc[s] = -a.row_max[rofs] * kLog2e - __builtin_amdgcn_logf(a.row_sum[rofs]);
+        isR[s] = ok && xr[s] >= nrows - U0.nR;
+      }
+    }
+    float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
+    float ent[2] = {0.f, 0.f}, loc[2] = {0.f, 0.f};
+    float cov[2][NCV], covv[2][kPrefVs], covb[2][kPrefBs];
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+#pragma unroll
+      for (int q = 0; q < NCV; ++q) cov[s][q] = 0.f;
+#pragma unroll
+      for (int k = 0; k < kPrefVs; ++k) covv[s][k] = 0.f;
+#pragma unroll
+      for (int k = 0; k < kPrefBs; ++k) covb[s][k] = 0.f;
+    }
+
+    // coverage pass: diagonal-bitmap windows (vertical-slash) and block-selection words
+    // (block-sparse) of each row, fetched together with the K copy of the tile they serve
+    struct Pref {
+      Win3 wd[2][kPrefVs];
+      uint32_t bw[2][kPrefBs];
+    };
+    auto fetch = [&](int k0, Pref &f) {
+      if constexpr (MODE == M_COVER) {
+        const int kt = k0 >> 6;
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+          const bool ok = u >= 0 && row[s] >= 0;
+#pragma unroll
+          for (int k = 0; k < kPrefVs; ++k) {
+            f.wd[s][k] = Win3{0u, 0u, 0u};
+            if (k < a.nvs_pref && ok)
+              f.wd[s][k] = load_win(a.vs_dbits + ((long long)u * a.ncand_vs + a.vs_pref_cl[k]) * a.nwords, a.nwords,
+                                    row[s] - k0 - 63);
+          }
+#pragma unroll
+          for (int k = 0; k < kPrefBs; ++k) {
+            f.bw[s][k] = 0u;
+            if (k < a.nbs_pref && ok)
+              f.bw[s][k] = a.bs_bits[(((long long)a.units[u].head * a.ncand_bs + a.bs_pref_cl[k]) * a.nb + (row[s] >> 6)) *
+                                         a.nbw + (kt >> 5)];
+          }
+        }
+      }
+    };
+
+    // ---- one block against one tile -------------------------------------------------------
+    auto block_tile = [&](const bf16 *sK, int k0, int s, const Pref &f) {
+      const int rmx = s ? rmax1 : rmax0;
+      if (u < 0 || rmx < k0) return;  // block absent or entirely before the tile
+      const int i = row[s];
+      f32x16 sacc[2];
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) s[mb][r] = 0.f;
+        for (int r = 0; r < 16; ++r) sacc[mb][r] = 0.f;
 #pragma unroll
-        for (int ks = 0; ks < D / 16; ++ks) {
-          const u32x4 kf = *(const u32x4 *)&sK[(64 * tt + 32 * mb + l32) * D + (((2 * ks + hh) ^ kswz) << 3)];
-          s[mb] = mfma32(kf, qf[ks], s[mb]);
+        for (int ks = 0; ks < KS; ++ks) {
+          const u32x4 kf = *(const u32x4 *)&sK[(32 * mb + l32) * D + (((2 * ks + hh) ^ kswz) << 3)];
+          sacc[mb] = mfma32(kf, qf[s][ks], sacc[mb]);
+        }
+      }
+      // keys after the row: a row before the tile sees none of it; a row inside the tile
+      // (some lane of the wave) masks element-wise
+      const bool none = i < k0;
+      const bool part = __ballot(i >= k0 && i < k0 + 63) != 0ull;
+      float x[2][16];
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) x[mb][r] = sacc[mb][r];
+      if (part) {
+        const uint64_t M = prefix_mask(i - k0 + 1) >> (4 * hh);
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb) {
+          const uint32_t w = (uint32_t)(M >> (32 * mb));
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const uint32_t keep = (uint32_t)__builtin_amdgcn_sbfe((int)w, 8 * (r >> 2) + (r & 3), 1);
+            x[mb][r] = __builtin_bit_cast(float, (keep & __builtin_bit_cast(uint32_t, x[mb][r])) | (~keep & 0xff800000u));
+          }
         }
       }
       if constexpr (MODE == M_STATS) {
@@ -200,141 +322,184 @@ __global__ void __launch_bounds__(256) probe_chunk_kernel(const ProbeArgs a) {
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int j = k0 + acc_key(mb, r, hh);
-            if (j > row) s[mb][r] = -INFINITY;
-            mx = fmaxf(mx, s[mb][r]);
-          }
-        const float m_new = fmaxf(m_run, mx);
+          for (int r = 0; r < 16; ++r) mx = fmaxf(mx, x[mb][r]);
+        if (none) mx = -INFINITY;
+        const float m_new = fmaxf(m_run[s], mx);
         const float m_use = m_new == -INFINITY ? 0.f : m_new;
+        const float nm = none ? -INFINITY : -m_use * c;
         float ps = 0.f;
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) ps += __builtin_amdgcn_exp2f((s[mb][r] - m_use) * a.c);
-        l_run = l_run * __builtin_amdgcn_exp2f((m_run - m_use) * a.c) + ps;
-        m_run = m_new;
-        continue;
+          for (int r = 0; r < 16; ++r) ps += __builtin_amdgcn_exp2f(fmaf(x[mb][r], c, nm));
+        l_run[s] = l_run[s] * __builtin_amdgcn_exp2f((m_run[s] - m_use) * c) + ps;
+        m_run[s] = m_new;
       } else {
-        float p[2][16];
-        float bsum = 0.f, lsum = 0.f;
-        const int lo_local = row - a.local_w + 1;  // keys >= lo_local are in the local band
+        const float nm = none ? -INFINITY : nmc[s];
+        float tsum = 0.f;
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const int j = k0 + acc_key(mb, r, hh);
-            const float v = (rvalid && j <= row) ? __builtin_amdgcn_exp2f(fmaf(s[mb][r], a.c, nmc)) * invl : 0.f;
-            p[mb][r] = v;
-            bsum += v;
-            if constexpr (MODE == M_COVER) {
-              if (j >= lo_local) lsum += v;
-            }
+            x[mb][r] = __builtin_amdgcn_exp2f(fmaf(x[mb][r], c, nm));
+            tsum += x[mb][r];
           }
         if constexpr (MODE == M_SCORES) {
-          if (blockR) {
+          if (__ballot(isR[s]) == 0ull) return;
+          // skewed tile: row lane r, key kk -> sD[r][kk - r + 31].  Key columns and diagonals
+          // (kk - r constant) of the block are then both plain columns of sD; entries no key
+          // maps to stay zero.  Recent rows are consecutive and end at lane 31, so diagonal
+          // column e holds t = (last row - k0) - e.
 #pragma unroll
-            for (int mb = 0; mb < 2; ++mb)
+          for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-              for (int r = 0; r < 16; ++r) sP[l32][acc_key(mb, r, hh)] = isR ? p[mb][r] : 0.f;
-            wave_sync();
-            {  // column sums: lane = key
-              float cs = 0.f;
-              for (int rr = 0; rr < 32; ++rr) cs += sP[rr][lane];
-              sCol[64 * tt + lane] += cs;
-            }
-            {  // diagonal t = i - j over the block's recent rows, stored at t - dbase
-              const int i_first = max(U.r0, sRows[wave][0]);
-              const int i_last = rbmax;
-              const int xlo = i_first - k0 - 63 - dbase;
-              const int xn = i_last - i_first + 64;
-              for (int xx = lane; xx < xn; xx += 64) {
-                const int x = xlo + xx;
-                const int t = x + dbase;
-                float ds = 0.f;
-                for (int i2 = i_first; i2 <= i_last; ++i2) {
-                  const int kk = i2 - t - k0;
-                  if (kk >= 0 && kk < 64) ds += sP[i2 - i_first + rfirst][kk];
-                }
-                if (x >= 0 && x < dw) sDg[x] += ds;
+            for (int r = 0; r < 16; ++r) sD[l32][acc_key(mb, r, hh) - l32 + 31] = isR[s] ? x[mb][r] : 0.f;
+          wave_sync();
+          float cs = 0.f, d0 = 0.f, d1 = 0.f;
+          const int e1 = min(64 + lane, kSkew - 1);
+#pragma unroll
+          for (int rr = 0; rr < 32; ++rr) {
+            cs += sD[rr][lane - rr + 31];
+            d0 += sD[rr][lane];
+            d1 += sD[rr][e1];
+          }
+          sCol[k0 - c0 + lane] += cs;
+          const int tb = rmx - k0 - dbase;
+          if (tb - lane >= 0 && tb - lane < dw) sDg[tb - lane] += d0;
+          if (lane < 31 && tb - 64 - lane >= 0 && tb - 64 - lane < dw) sDg[tb - 64 - lane] += d1;
+          wave_sync();
+        } else {  // M_COVER
+          const float bt = tsum + __shfl_xor(tsum, 32);  // mass of the row in this 64-key block
+          if (bt > 0.f) ent[s] -= bt * logf(bt);
+          // kept mass of a 64-bit key mask (bits of this lane's keys after the half shift)
+          auto masked = [&](uint64_t M) -> float {
+            float cs = 0.f;
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb) {
+              const uint32_t w = (uint32_t)(M >> (32 * mb));
+#pragma unroll
+              for (int r = 0; r < 16; ++r) {
+                const uint32_t keep = (uint32_t)__builtin_amdgcn_sbfe((int)w, 8 * (r >> 2) + (r & 3), 1);
+                cs += __builtin_bit_cast(float, keep & __builtin_bit_cast(uint32_t, x[mb][r]));
               }
             }
-            wave_sync();
-          }
-        } else {  // M_COVER: kept mass of every candidate (whole-tile shortcuts first), descriptors
-          const int bq = row >> 6;
+            return cs;
+          };
+          // mass of the keys j >= lo: whole tile, none, or element-wise (wave-uniform choice)
+          auto from = [&](int lo) -> float {
+            const bool all = lo <= k0, nil = lo > k0 + 63;
+            if (__ballot(all) == ~0ull) return tsum;
+            if (__ballot(nil) == ~0ull) return 0.f;
+            const float m = masked(~prefix_mask(lo - k0) >> (4 * hh));
+            return all ? tsum : nil ? 0.f : m;
+          };
+          loc[s] += from(i - a.local_w + 1);
           const int kt = k0 >> 6;
-          const float tsum = bsum;
-          {
-            const float bt = bsum + __shfl_xor(bsum, 32);  // mass of the row in this 64-key block
-            if (bt > 0.f) ent -= bt * logf(bt);
-            loc += lsum;
+#pragma unroll
+          for (int k = 0; k < kPrefVs; ++k) {
+            if (k >= a.nvs_pref) break;
+            const uint64_t md = __builtin_bitreverse64(win_bits(f.wd[s][k], i - k0 - 63));
+            const uint64_t mv = bits64_at(a.vs_vbits + ((long long)u * a.ncand_vs + a.vs_pref_cl[k]) * a.nwords, a.nwords, k0);
+            covv[s][k] += masked((md | mv) >> (4 * hh));
           }
 #pragma unroll
-          for (int c = 0; c < kMaxCand; ++c) {
-            if (c >= a.ncand) break;
-            const CandDev cd = a.cand[c];
-            if (cd.fam == RS_DENSE) continue;
-            uint64_t M;
+          for (int k = 0; k < kPrefBs; ++k) {
+            if (k >= a.nbs_pref) break;
+            if ((f.bw[s][k] >> (kt & 31)) & 1u) covb[s][k] += tsum;
+          }
+#pragma unroll
+          for (int q = 0; q < NCV; ++q) {
+            if (q >= a.ncov) break;
+            const CandDev cd = a.cand[a.cov_cand[q]];
             if (cd.fam == RS_ASHAPE) {
-              M = prefix_mask(cd.a - k0) | ~prefix_mask(row - cd.b + 1 - k0);
+              const float sink = k0 + 63 < cd.a ? tsum : k0 >= cd.a ? 0.f : masked(prefix_mask(cd.a - k0) >> (4 * hh));
+              // window keys j >= i - b + 1 that are not sink keys
+              cov[s][q] += sink + from(max(i - cd.b + 1, cd.a));
             } else if (cd.fam == RS_VSLASH) {
               const long long vr = ((long long)u * a.ncand_vs + cd.cl) * a.nwords;
-              const uint64_t md = __builtin_bitreverse64(bits64_at(a.vs_dbits + vr, a.nwords, row - k0 - 63));
+              const uint64_t md = __builtin_bitreverse64(bits64_at(a.vs_dbits + vr, a.nwords, i - k0 - 63));
               const uint64_t mv = bits64_at(a.vs_vbits + vr, a.nwords, k0);
-              M = md | mv;
-            } else {
-              const long long br = (((long long)U.head * a.ncand_bs + cd.cl) * a.nb + (rvalid ? bq : 0)) * a.nbw;
-              M = (rvalid && ((a.bs_bits[br + (kt >> 5)] >> (kt & 31)) & 1u)) ? ~0ull : 0ull;
-            }
-            M >>= 4 * hh;
-            const uint64_t sel = M & 0x0f0f0f0f0f0f0f0full;  // key slots held by this lane
-            if (sel == 0x0f0f0f0f0f0f0f0full) {
-              cov[c] += tsum;
-            } else if (sel != 0ull) {
-              float cs = 0.f;
-#pragma unroll
-              for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-                for (int r = 0; r < 16; ++r)
-                  if ((sel >> (32 * mb + 8 * (r >> 2) + (r & 3))) & 1ull) cs += p[mb][r];
-              cov[c] += cs;
+              cov[s][q] += masked((md | mv) >> (4 * hh));
+            } else if (cd.fam == RS_BSPARSE) {
+              const long long br = (((long long)a.units[u].head * a.ncand_bs + cd.cl) * a.nb + (max(i, 0) >> 6)) * a.nbw;
+              if ((a.bs_bits[br + (kt >> 5)] >> (kt & 31)) & 1u) cov[s][q] += tsum;
             }
           }
         }
       }
+    };
+
+    // ---- stream the range's tiles ---------------------------------------------------------
+    // The Q fragments and row constants are waited for here, visibly to the compiler, so that
+    // no wait for them lands inside the tile loop (where it would drain the tile copies).
+    __builtin_amdgcn_s_waitcnt(vm_wait_imm(0));
+    Pref fcur, fnext;
+#pragma unroll
+    for (int t = 0; t < NBUF - 1; ++t)
+      if (t < nt) issue_tile(sKb[t], c0 + 64 * t);
+    fetch(c0, fcur);
+    for (int t = 0; t < nt; ++t) {
+      __builtin_amdgcn_s_waitcnt(vm_wait_imm(0));  // tile t (and its bitmap words) landed
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+      if (t + NBUF - 1 < nt) {
+        issue_tile(sKb[(t + NBUF - 1) % NBUF], c0 + 64 * (t + NBUF - 1));
+        fetch(c0 + 64 * (t + 1), fnext);
+      }
+      block_tile(sKb[t % NBUF], c0 + 64 * t, 0, fcur);
+      block_tile(sKb[t % NBUF], c0 + 64 * t, 1, fcur);
+      fcur = fnext;
     }
-    if constexpr (MODE == M_STATS) {
-      const float mo = __shfl_xor(m_run, 32), lo = __shfl_xor(l_run, 32);
-      const float mm = fmaxf(m_run, mo);
-      const float mu = mm == -INFINITY ? 0.f : mm;
-      const float ll = l_run * __builtin_amdgcn_exp2f((m_run - mu) * a.c) + lo * __builtin_amdgcn_exp2f((mo - mu) * a.c);
-      if (rvalid && hh == 0) {
-        const long long o = ((long long)u * a.rmax + ridx) * a.nchunks + ch;
-        a.ent_part[o] = mm;  // chunk max (raw dot product) in the entropy partial slot
-        a.loc_part[o] = ll;  // chunk sum in the local-mass partial slot
-      }
-    } else if constexpr (MODE == M_COVER) {
-      loc += __shfl_xor(loc, 32);
-      if (rvalid && hh == 0) {
-        const long long o = ((long long)u * a.rmax + ridx) * a.nchunks + ch;
-        a.ent_part[o] = ent;  // the stats partials were consumed before this pass
-        a.loc_part[o] = loc;
-      }
-      for (int c = 0; c < a.ncand; ++c) {
-        const float tot = cov[c] + __shfl_xor(cov[c], 32);
-        if (rvalid && hh == 0) a.cov_part[(((long long)u * a.ncand + c) * a.rmax + ridx) * a.nchunks + ch] = tot;
+
+    // ---- per-row partials of this range ------------------------------------------------------
+    if (u >= 0) {
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        const bool ok = row[s] >= 0 && hh == 0;
+        const long long o = ((long long)u * a.rmax + xr[s]) * a.nchunks + rg;
+        auto cov_out = [&](int cand, float v) {
+          const float tot = v + __shfl_xor(v, 32);
+          if (ok) a.cov_part[(((long long)u * a.ncand + cand) * a.rmax + xr[s]) * a.nchunks + rg] = tot;
+        };
+        if constexpr (MODE == M_STATS) {
+          const float mo = __shfl_xor(m_run[s], 32), lo = __shfl_xor(l_run[s], 32);
+          const float mm = fmaxf(m_run[s], mo);
+          const float mu = mm == -INFINITY ? 0.f : mm;
+          const float ll = l_run[s] * __builtin_amdgcn_exp2f((m_run[s] - mu) * c) +
+                           lo * __builtin_amdgcn_exp2f((mo - mu) * c);
+          if (ok) {
+            a.ent_part[o] = mm;  // range max (raw dot product) in the entropy partial slot
+            a.loc_part[o] = ll;  // range sum in the local-mass partial slot
+          }
+        } else if constexpr (MODE == M_COVER) {
+          const float lt = loc[s] + __shfl_xor(loc[s], 32);
+          if (ok) {
+            a.ent_part[o] = ent[s];  // the stats partials were consumed before this pass
+            a.loc_part[o] = lt;
+          }
+#pragma unroll
+          for (int q = 0; q < NCV; ++q)
+            if (q < a.ncov) cov_out(a.cov_cand[q], cov[s][q]);
+#pragma unroll
+          for (int k = 0; k < kPrefVs; ++k)
+            if (k < a.nvs_pref) cov_out(a.vs_pref_c[k], covv[s][k]);
+#pragma unroll
+          for (int k = 0; k < kPrefBs; ++k)
+            if (k < a.nbs_pref) cov_out(a.bs_pref_c[k], covb[s][k]);
+        }
       }
     }
-    wave_sync();
   }
   if constexpr (MODE == M_SCORES) {
-    wave_sync();
-    for (int x = lane; x < kChunk; x += 64) {
-      const int j = c0 + x;
-      if (j < a.n) a.col[(long long)u * a.n + j] = (j < U.s1) ? sCol[x] : 0.f;
+    __syncthreads();
+    if (u >= 0) {
+      for (int x = lane; x < kRange; x += 64) {
+        const int j = c0 + x;
+        if (j < a.n) a.col[(long long)u * a.n + j] = (j < U0.s1) ? sCol[x] : 0.f;
+      }
+      for (int x = lane; x < dw; x += 64) a.diag_part[((long long)u * a.nchunks + rg) * a.diag_w + x] = sDg[x];
     }
-    for (int x = lane; x < dw; x += 64) a.diag_part[((long long)u * a.nchunks + ch) * a.diag_w + x] = sDg[x];
   }
 }
 
@@ -360,7 +525,7 @@ __global__ void probe_stats_combine_kernel(const ProbeArgs a) {
   const int x = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (x >= U.nrows) return;
   const int row = a.rows[(long long)u * a.rmax + x];
-  const int nch = row / kChunk + 1;
+  const int nch = row / kRange + 1;
   const float *pm = a.ent_part + ((long long)u * a.rmax + x) * a.nchunks;
   const float *pl = a.loc_part + ((long long)u * a.rmax + x) * a.nchunks;
   float M = -INFINITY;
@@ -383,14 +548,14 @@ __global__ void probe_finish_kernel(const ProbeArgs a, float *diag, float *entro
   if (x < a.n) {
     float v = 0.f;
     if (x < U.s1 && U.nR > 0) {
-      // chunks whose diagonal range [r0 - c0 - (kChunk-1), r0 + nR - 1 - c0] holds t = x
-      const int chi = min((U.r0 + U.nR - 1 - x) / kChunk, (U.s1 - 1) / kChunk);
-      const int clo_num = U.r0 - (kChunk - 1) - x;
-      const int clo = clo_num <= 0 ? 0 : (clo_num + kChunk - 1) / kChunk;
+      // chunks whose diagonal range [r0 - c0 - (kRange-1), r0 + nR - 1 - c0] holds t = x
+      const int chi = min((U.r0 + U.nR - 1 - x) / kRange, (U.s1 - 1) / kRange);
+      const int clo_num = U.r0 - (kRange - 1) - x;
+      const int clo = clo_num <= 0 ? 0 : (clo_num + kRange - 1) / kRange;
       for (int ch = clo; ch <= chi; ++ch) {
-        const int dbase = U.r0 - (ch * kChunk + kChunk - 1);
+        const int dbase = U.r0 - (ch * kRange + kRange - 1);
         const int xi = x - dbase;
-        if (xi >= 0 && xi < kChunk + U.nR) v += a.diag_part[((long long)u * a.nchunks + ch) * a.diag_w + xi];
+        if (xi >= 0 && xi < kRange + U.nR) v += a.diag_part[((long long)u * a.nchunks + ch) * a.diag_w + xi];
       }
     }
     diag[(long long)u * a.n + x] = v;
@@ -405,7 +570,7 @@ __global__ void probe_desc_kernel(const ProbeArgs a, float *entropy, float *loca
   const int x = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (x >= U.nrows) return;
   const int row = a.rows[(long long)u * a.rmax + x];
-  const int nch = row / kChunk + 1;
+  const int nch = row / kRange + 1;
   const float *pe = a.ent_part + ((long long)u * a.rmax + x) * a.nchunks;
   const float *pl = a.loc_part + ((long long)u * a.rmax + x) * a.nchunks;
   float e = 0.f, l = 0.f;
@@ -434,7 +599,7 @@ __global__ void cover_finish_kernel(const ProbeArgs a, float *cov_rows, float *c
     if (a.cand[c].fam == RS_DENSE) {
       m = 1.f;
     } else {
-      const int nch = row / kChunk + 1;
+      const int nch = row / kRange + 1;
       const float *pc = a.cov_part + (((long long)u * a.ncand + c) * a.rmax + x) * a.nchunks;
       float acc = 0.f;
       for (int ch = lane; ch < nch; ch += 64) acc += pc[ch];
@@ -580,12 +745,12 @@ static int rmax_of(const rs_probe_cfg *cfg) { return cfg->r_rec + cfg->r_uni + c
 
 size_t probe_ws_bytes(const rs_qkv *qkv, int32_t nunits, const rs_probe_cfg *cfg) {
   const int rmax = rmax_of(cfg);
-  const long long nchunks = (qkv->n + kChunk - 1) / kChunk;
+  const long long nchunks = (qkv->n + kRange - 1) / kRange;
   const int nb = (qkv->n + 63) / 64;
   Arena ar(nullptr, 0);
   ar.take<ProbeUnit>(nunits);
   ar.take<int4>(nunits);
-  ar.take<float>((size_t)nunits * nchunks * (kChunk + rmax));     // diag partials
+  ar.take<float>((size_t)nunits * nchunks * (kRange + rmax));     // diag partials
   ar.take<float>((size_t)nunits * nchunks * rmax * 2);            // entropy / local partials
   ar.take<float>((size_t)nunits * nchunks * rmax * kMaxCand);     // coverage partials
   if (cfg->flags & RS_PROBE_BLOCKMEAN) {
@@ -598,13 +763,17 @@ size_t probe_ws_bytes(const rs_qkv *qkv, int32_t nunits, const rs_probe_cfg *cfg
 template <int D, typename InT>
 static hipError_t launch_rows(const ProbeArgs &pa, int nunits, int ngroups, int mode, float *diag, float *ent, float *loc,
                               float *cov_rows, float *cov, hipStream_t st) {
+  const int npairs = ((pa.rmax + 31) / 32 + 1) / 2;  // row-block pairs of the fullest unit
   if (mode == 0) {
-    hipLaunchKernelGGL((probe_chunk_kernel<D, InT, M_STATS>), dim3(pa.nchunks, ngroups), dim3(256), 0, st, pa);
+    hipLaunchKernelGGL((probe_range_kernel<D, InT, M_STATS, 1>), dim3(pa.nchunks, ngroups, npairs), dim3(256), 0, st, pa);
     hipLaunchKernelGGL(probe_stats_combine_kernel, dim3((pa.rmax + 3) / 4, nunits), dim3(256), 0, st, pa);
-    hipLaunchKernelGGL((probe_chunk_kernel<D, InT, M_SCORES>), dim3(pa.nchunks, ngroups), dim3(256), 0, st, pa);
+    hipLaunchKernelGGL((probe_range_kernel<D, InT, M_SCORES, 1>), dim3(pa.nchunks, ngroups), dim3(256), 0, st, pa);
     hipLaunchKernelGGL(probe_finish_kernel, dim3((pa.n + 255) / 256, nunits), dim3(256), 0, st, pa, diag, ent, loc);
   } else {
-    hipLaunchKernelGGL((probe_chunk_kernel<D, InT, M_COVER>), dim3(pa.nchunks, ngroups), dim3(256), 0, st, pa);
+    if (pa.ncov <= 4)
+      hipLaunchKernelGGL((probe_range_kernel<D, InT, M_COVER, 4>), dim3(pa.nchunks, ngroups, npairs), dim3(256), 0, st, pa);
+    else
+      hipLaunchKernelGGL((probe_range_kernel<D, InT, M_COVER, kMaxCand>), dim3(pa.nchunks, ngroups, npairs), dim3(256), 0, st, pa);
     hipLaunchKernelGGL(cover_finish_kernel, dim3(pa.ncand, nunits), dim3(256), 0, st, pa, cov_rows, cov);
     hipLaunchKernelGGL(probe_desc_kernel, dim3((pa.rmax + 3) / 4, nunits), dim3(256), 0, st, pa, ent, loc);
   }
@@ -615,7 +784,7 @@ rs_status probe_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int
                        const rs_probe_cfg *cfg, const rs_candidate *grid, int32_t ncand,
                        const rs_index_set *idx, void *ws, size_t ws_bytes, rs_probe_out *out, hipStream_t st) {
   const int rmax = rmax_of(cfg);
-  const int nchunks = (qkv->n + kChunk - 1) / kChunk;
+  const int nchunks = (qkv->n + kRange - 1) / kRange;
   const int nb = (qkv->n + 63) / 64;
   const size_t need = probe_ws_bytes(qkv, nunits, cfg);
   if (!ws || ws_bytes < need)
@@ -623,7 +792,7 @@ rs_status probe_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int
   Arena ar(ws, ws_bytes);
   ProbeUnit *d_units = ar.take<ProbeUnit>(nunits);
   int4 *d_groups = ar.take<int4>(nunits);
-  float *diag_part = ar.take<float>((size_t)nunits * nchunks * (kChunk + rmax));
+  float *diag_part = ar.take<float>((size_t)nunits * nchunks * (kRange + rmax));
   float *ent_part = ar.take<float>((size_t)nunits * nchunks * rmax);
   float *loc_part = ar.take<float>((size_t)nunits * nchunks * rmax);
   float *cov_part = ar.take<float>((size_t)nunits * nchunks * rmax * kMaxCand);
@@ -693,7 +862,7 @@ rs_status probe_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int
   pa.units = d_units; pa.groups = d_groups; pa.rows = out->rows; pa.subset = out->subset;
   pa.row_max = out->row_max; pa.row_sum = out->row_sum;
   pa.col = out->col; pa.diag_part = diag_part; pa.ent_part = ent_part; pa.loc_part = loc_part;
-  pa.diag_w = kChunk + rmax;
+  pa.diag_w = kRange + rmax;
   pa.cov_part = cov_part;
   if (cover) {
     pa.ncand = ncand;
@@ -703,6 +872,15 @@ rs_status probe_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int
       if (grid[c].fam == RS_VSLASH) cl = nvs++;
       if (grid[c].fam == RS_BSPARSE) cl = nbs++;
       pa.cand[c] = CandDev{grid[c].fam, grid[c].a, grid[c].b, cl};
+      if (grid[c].fam == RS_VSLASH && pa.nvs_pref < kPrefVs) {
+        pa.vs_pref_c[pa.nvs_pref] = c;
+        pa.vs_pref_cl[pa.nvs_pref++] = cl;
+      } else if (grid[c].fam == RS_BSPARSE && pa.nbs_pref < kPrefBs) {
+        pa.bs_pref_c[pa.nbs_pref] = c;
+        pa.bs_pref_cl[pa.nbs_pref++] = cl;
+      } else if (grid[c].fam != RS_DENSE) {
+        pa.cov_cand[pa.ncov++] = c;
+      }
     }
     pa.vs_vbits = idx->vs_vbits; pa.vs_dbits = idx->vs_dbits; pa.nwords = idx->nwords; pa.ncand_vs = idx->ncand_vs;
     pa.bs_bits = idx->bs_bits; pa.nb = idx->nb; pa.nbw = idx->nbw; pa.ncand_bs = idx->ncand_bs;
