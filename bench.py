@@ -73,6 +73,82 @@ def pairs_vs(s0, s1, V, D):
     return int(round((cv[rows] + cd[rows] - conv[rows]).sum()))
 
 
+# ---- issued work: the 64-key x 128-row tiles the attention kernel schedules ---------------
+
+def _qtiles(s0, s1):
+    base = (s0 // 128) * 128
+    while base < s1:
+        yield max(s0, base), min(s1, base + 128)
+        base += 128
+
+
+def tiles_dense(s0, s1):
+    return sum((r_hi - 1) // 64 + 1 for _, r_hi in _qtiles(s0, s1))
+
+
+def tiles_ashape(s0, s1, sink, w):
+    tot = 0
+    for r_lo, r_hi in _qtiles(s0, s1):
+        last = (r_hi - 1) // 64
+        ns = min((sink + 63) // 64, last + 1)
+        st1 = max(max(0, r_lo - w + 1) // 64, ns)
+        tot += ns + max(0, last - st1 + 1)
+    return tot
+
+
+def tiles_bs(s0, s1, lists, counts):
+    tot = 0
+    for r_lo, r_hi in _qtiles(s0, s1):
+        bq = ((r_lo // 128) * 128) // 64
+        sel = []
+        if r_lo < 64 * bq + 64:
+            sel.append(lists[bq, :counts[bq]])
+        if r_hi > 64 * bq + 64 and bq + 1 < len(counts):
+            sel.append(lists[bq + 1, :counts[bq + 1]])
+        tot += len(np.unique(np.concatenate(sel))) if sel else 0
+    return tot
+
+
+def tiles_vs(s0, s1, V, D):
+    """Diagonal tiles (64-key tiles any selected diagonal crosses for the query tile's rows)
+    plus gathered tiles of the vertical columns outside them."""
+    D = np.asarray(D, np.int64)
+    V = np.asarray(V, np.int64)
+    tot = 0
+    for r_lo, r_hi in _qtiles(s0, s1):
+        nt = (r_hi - 1) // 64 + 1
+        mark = np.zeros(nt + 1, np.int64)
+        d = D[(D >= 0) & (D <= r_hi - 1)]
+        lo = np.maximum(0, r_lo - d) // 64
+        hi = (r_hi - 1 - d) // 64
+        np.add.at(mark, lo, 1)
+        np.add.at(mark, hi + 1, -1)
+        on = np.cumsum(mark)[:nt] > 0
+        v = V[(V >= 0) & (V <= r_hi - 1)]
+        g = int((~on[v // 64]).sum()) if len(v) else 0
+        tot += int(on.sum()) + (g + 63) // 64
+    return tot
+
+
+# ---- HBM traffic of the dominant kernel ------------------------------------------------------
+
+def measured_traffic(kernel):
+    """Calibrated HBM bytes per launch from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE runs
+    (profiles/attn_traffic.json), or None when the attention source or the dominant kernel
+    differs from the one measured."""
+    import hashlib
+    try:
+        with open(os.path.join(ROOT, "profiles", "attn_traffic.json")) as f:
+            t = json.load(f)
+        with open(os.path.join(ROOT, "paper_2608_29058_amd", "csrc", "attn.hip"), "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()
+    except OSError:
+        return None
+    if t.get("attn_hip_sha256") != sha or t.get("kernel") != kernel:
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
 # ---- CPU baseline: the oracle on a bounded sample ------------------------------------------
 
 def cpu_baseline(q, k, v, route, t_table, edges, knobs, rows_per_unit=32):
@@ -259,6 +335,7 @@ def main():
     cand_time = [0.0] * len(GRID)
     fam_time = {f: 0.0 for f in FAM_NAME}
     fam_flops = {f: 0.0 for f in FAM_NAME}
+    fam_issued = {f: 0.0 for f in FAM_NAME}
     fam_launches = {f: 0 for f in FAM_NAME}
     ph = {"probe_index_coverage": 0.0, "d2h_route": 0.0, "attention": 0.0}
     n_units_fb = 0
@@ -277,25 +354,34 @@ def main():
             RL.probe_and_index(RL.qkv(q, k, v))
             torch.cuda.synchronize()
             cache[li] = dict(bs_count=RL.ib.bs_count.cpu().numpy(), vs_count=RL.ib.vs_count.cpu().numpy(),
-                             vs_v=RL.ib.vs_vsorted.cpu().numpy(), vs_d=RL.ib.vs_dsorted.cpu().numpy())
+                             vs_v=RL.ib.vs_vsorted.cpu().numpy(), vs_d=RL.ib.vs_dsorted.cpu().numpy(),
+                             bs_lists={})
         ic = cache[li]
         for gi, (cand, us) in enumerate(route["groups"]):
             fam, a_, b_ = GRID[cand]
             dt = evs[2 + gi].elapsed_time(evs[3 + gi])
             pairs = 0
             cl = sum(1 for g in GRID[:cand] if g[0] == fam)
+            tiles = 0
             for u in us:
                 h, s0, s1 = RL.unit_list[u]
                 if fam == 0:
                     pairs += pairs_dense(s0, s1)
+                    tiles += tiles_dense(s0, s1)
                     n_units_dense += 1
                 elif fam == 1:
                     pairs += pairs_ashape(s0, s1, a_, b_)
+                    tiles += tiles_ashape(s0, s1, a_, b_)
                 elif fam == 3:
                     pairs += pairs_bs(s0, s1, ic["bs_count"][h, cl])
+                    if (h, cl) not in ic["bs_lists"]:
+                        ic["bs_lists"][(h, cl)] = RL.ib.bs_sorted[h, cl].cpu().numpy()
+                    tiles += tiles_bs(s0, s1, ic["bs_lists"][(h, cl)], ic["bs_count"][h, cl])
                 else:
                     cv, cdn = ic["vs_count"][u, cl]
                     pairs += pairs_vs(s0, s1, ic["vs_v"][u, cl, :cv], ic["vs_d"][u, cl, :cdn])
+                    tiles += tiles_vs(s0, s1, ic["vs_v"][u, cl, :cv], ic["vs_d"][u, cl, :cdn])
+            fam_issued[fam] += 4.0 * D * 64 * 128 * tiles
             fl = 4.0 * D * pairs
             cand_units[cand] += len(us)
             cand_pairs[cand] += pairs
@@ -323,7 +409,8 @@ def main():
     dom_avg_ms = fam_time[dom] / max(1, fam_launches[dom])
     dom_tflops = fam_flops[dom] / (fam_time[dom] * 1e-3) / 1e12 if fam_time[dom] > 0 else 0.0
     roofline = {"bound": "mfma", "achieved": round(dom_tflops, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(dom_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "frac": round(dom_tflops / PEAK_BF16_TFLOPS, 4),
+                "traffic": measured_traffic(f"attn_fwd_kernel[{FAM_NAME[dom]}]"),
                 "kernel": f"attn_fwd_kernel[{FAM_NAME[dom]}]", "avg_launch_ms": round(dom_avg_ms, 4),
                 "launches": fam_launches[dom],
                 "flops_def": "4*d*(kept query-key pairs) per launch"}
@@ -344,6 +431,11 @@ def main():
         "family_ms_per_layer": {FAM_NAME[f]: round(fam_time[f] / args.steps, 4) for f in FAM_NAME},
         "family_tflops": {FAM_NAME[f]: (round(fam_flops[f] / (fam_time[f] * 1e-3) / 1e12, 1) if fam_time[f] else None)
                           for f in FAM_NAME},
+        # issued = 4 d x (64-key x 128-row tiles scheduled); tile efficiency = kept / issued pairs
+        "family_issued_tflops": {FAM_NAME[f]: (round(fam_issued[f] / (fam_time[f] * 1e-3) / 1e12, 1)
+                                               if fam_time[f] else None) for f in FAM_NAME},
+        "family_tile_efficiency": {FAM_NAME[f]: (round(fam_flops[f] / fam_issued[f], 4) if fam_issued[f] else None)
+                                   for f in FAM_NAME},
         "candidates": [{"cand": list(GRID[c]), "units_per_layer": round(cand_units[c] / args.steps, 2),
                         "ms_per_layer": round(cand_time[c] / args.steps, 4),
                         "tflops": (round(4.0 * D * cand_pairs[c] / (cand_time[c] * 1e-3) / 1e12, 1)
