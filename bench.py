@@ -236,6 +236,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--layers", type=int, default=32)
     ap.add_argument("--dense-reps", type=int, default=2)
+    ap.add_argument("--calib-layers", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--json-out", default=None)
     args = ap.parse_args()
@@ -275,38 +276,30 @@ def main():
     edges = np.array([SEG * (b + 1) for b in range(N // SEG)], np.int32)
     # t_ker(p, b, n): per candidate and key-length bucket, the median over key/value groups of
     # the per-unit time of one launch holding that group's query heads (median of 3 reps)
-    t_table = np.zeros((len(GRID), len(edges)))
-    for c in range(len(GRID)):
-        for b in range(len(edges)):
-            per_group = []
-            for g in range(HKV):
-                us = [i for i, u in enumerate(RL.unit_list) if u[2] == edges[b] and u[0] // (HQ // HKV) == g]
-                ts = []
-                for _ in range(3):
-                    a = ev()
-                    RL.run_group(qkv0, c, us)
-                    z = ev()
-                    z.synchronize()
-                    ts.append(a.elapsed_time(z))
-                per_group.append(float(np.median(ts)) / len(us))
-            t_table[c, b] = float(np.median(per_group)) * 1e3
+    t_table = RL.profile_latency(qkv0, edges, reps=3)
     for c in range(len(GRID)):
         log(f"t_ker {GRID[c]} (us/unit):", np.round(t_table[c], 1).tolist())
     # probe + index + coverage time, and the host routing overhead
-    tp = []
-    for _ in range(3):
-        a = ev()
-        RL.probe_and_index(qkv0)
-        z = ev()
-        z.synchronize()
-        tp.append(a.elapsed_time(z))
+    tp_us = RL.profile_probe(qkv0, reps=3)
     RL.t_table, RL.edges = t_table, edges
     t_dense_layer_us = float(sum(t_table[0, int(np.searchsorted(edges, u[2]))] for u in RL.unit_list))
-    RL.knobs = RouteKnobs(T_layer_us=t_dense_layer_us / 6.5, tau=0.95, alpha=1.0, beta=0.0, delta_q=0.0)
+    # delta_q: one-sided 0.95-quantile of m_hat - m_true over every (unit, sparse candidate) of
+    # held-out layers, with the true mass from the dense and sparse kernels' LSE outputs
+    from paper_2608_29058_amd.audit import DenseRef, calibrate
+    calib = []
+    for l in range(64, 64 + args.calib_layers):
+        t = G.make_layer_torch(5, l, device=dev)
+        calib.append((t["q"], t["k"], t["v"]))
+    ref = DenseRef(RL)
+    delta_q, resid, _ = calibrate(RL, ref, calib, 0.95, log)
+    del ref, calib
+    torch.cuda.empty_cache()
+    log(f"delta_q {delta_q:.4f} from {resid.size} residuals")
+    RL.knobs = RouteKnobs(T_layer_us=t_dense_layer_us / 6.5, tau=0.95, alpha=1.0, beta=0.0, delta_q=delta_q)
     t0 = time.perf_counter()
     RL.route()
     t_route_host_us = (time.perf_counter() - t0) * 1e6
-    RL.t_probe_us = float(np.median(tp)) * 1e3 + t_route_host_us
+    RL.t_probe_us = tp_us + t_route_host_us
     log(f"t_probe {RL.t_probe_us:.0f} us, T_layer {RL.knobs.T_layer_us:.0f} us")
 
     # ---- warmup + timed steps ----------------------------------------------------------------
@@ -420,7 +413,8 @@ def main():
         "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": "routed prefill, 32 layers x GQA 32/8 d128 bf16, n=131072, 8 segments of 16384 "
-                               "per head, 9-candidate grid, tau=0.95, T_layer=dense/6.5",
+                               "per head, 9-candidate grid, tau=0.95 on m_lower = m_hat - delta_q (delta_q calibrated "
+                               "on held-out layers 64+), T_layer=dense/6.5",
                    "layers": args.layers, "n": N, "heads": [HQ, HKV], "head_dim": D, "segment": SEG},
         "roofline": roofline,
         "dense_ms_per_layer": round(dense_ms, 3),
@@ -445,6 +439,7 @@ def main():
         "wall_ms_timed": round(wall_ms, 1),
         "t_layer_budget_ms": round(RL.knobs.T_layer_us / 1e3, 3),
         "t_probe_ms": round(RL.t_probe_us / 1e3, 3),
+        "delta_q": round(delta_q, 5),
     }
     if not args.no_cpu_baseline:
         try:

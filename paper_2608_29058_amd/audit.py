@@ -1,0 +1,311 @@
+"""Dense-audited quality study of the routed layer (Sec. 3.3 certificate, Sec. 3.5 calibration,
+Sec. 4.1 metrics and ablations).
+
+Everything here measures the hot path; it computes no part of it.  Per unit (query head,
+segment) and routed candidate, from the kernels' own outputs:
+
+* true retained mass of row i:  m_i = exp(lse_S(i) - lse_dense(i)) (natural-log LSE over the
+  kept set and over every visible key, both written by the attention kernels); a unit's true
+  mass m_true is the mean over its rows;
+* E_rel = ||O - O~||_F / (||O||_F + eps) over the unit's rows, O from the dense kernel;
+* certificate (Eq. bound): per row ||O_i - O~_i||_2 <= 2 (1 - m_i) V_max with
+  V_max = max_{j < s1} ||v_j||_2.  The bound is linear in m, so averaged over a unit's rows it
+  reads mean_i ||O_i - O~_i|| <= 2 (1 - m_true) V_max.  With the probe estimate,
+  m_lower = max(0, m_hat - delta_q), and a routed sparse unit is covered when its mean row
+  error is <= 2 (1 - m_lower) V_max + allowance;
+* allowance for bf16 arithmetic (both kernels round P to bf16 before P V and sum the rounded
+  values, so each row's weights carry a relative error <= 2^-8: <= 2^-8 V_max per output;
+  outputs are rounded to bf16: <= 2^-9 ||O_i||; the LSE difference inherits the same 2^-8
+  relative error in m, worth 2^-7 V_max in the bound):
+  allow_i = 2^-6 V_max + 2^-9 (||O_i|| + ||O~_i||);
+* delta_q: the q-quantile of m_hat - m_true over every (unit, sparse candidate) of held-out
+  calibration layers, clipped at 0 (one-sided).
+
+python -m paper_2608_29058_amd.audit [--calib-layers 4] [--eval-layers 4] [--q 0.95]
+    [--sweep] [--ablations] [--json-out FILE]
+Workload: the 128K routed layer (GQA 32/8, d = 128, 8 segments of 16384 per head,
+9-candidate grid) on synthetic layers; calibration layers (64, 65, ...) are disjoint from the
+evaluation layers (0, 1, ...).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+from . import _rs
+from .pipeline import RoutedLayer, RouteKnobs
+
+EPS = 1e-12
+N, HQ, HKV, D, SEG = 131072, 32, 8, 128, 16384
+GRID = [(0, 0, 0), (1, 128, 1024), (1, 128, 4096), (2, 500, 256), (2, 1000, 2048), (2, 2000, 6096),
+        (3, 50, 64), (3, 100, 64), (3, 200, 64)]
+ONE_BUDGET = [0, 2, 4, 7]          # one budget per family: dense, A-shape 4096, VS 1000/2048, BS 100
+
+
+def bf16_allowance(vmax, o_norm, or_norm):
+    return 2.0 ** -6 * vmax + 2.0 ** -9 * (o_norm + or_norm)
+
+
+def _seg_view(RL, x):
+    """[hq, n, ...] -> [hq, nseg, seg, ...]; units are ordered segment-major, head-minor."""
+    seg = RL.unit_list[0][2] - RL.unit_list[0][1]
+    nseg = RL.n // seg
+    assert nseg * seg == RL.n and RL.nunits == nseg * RL.hq
+    assert all(u == (i % RL.hq, (i // RL.hq) * seg, (i // RL.hq + 1) * seg) for i, u in enumerate(RL.unit_list))
+    return x.reshape(RL.hq, nseg, seg, *x.shape[2:])
+
+
+def _unit_order(x):
+    """[hq, nseg] -> [U] in unit order."""
+    return x.transpose(0, 1).reshape(-1)
+
+
+def true_mass(RL, lse_s, lse_d):
+    """Per-row kept mass [hq, n] and per-unit mean [U] from the two LSE outputs."""
+    import torch
+    m = torch.exp(lse_s - lse_d).clamp(max=1.0)
+    return m, _unit_order(_seg_view(RL, m).mean(-1))
+
+
+def vmax_units(RL, v):
+    """V_max of every unit [hq, nseg]: the largest value-row norm over keys [0, s1)."""
+    import torch
+    G = RL.hq // RL.hkv
+    pref = torch.cummax(v.float().norm(dim=-1), dim=1).values      # [hkv, n]
+    seg = RL.unit_list[0][2] - RL.unit_list[0][1]
+    at_end = pref[:, seg - 1::seg]                                  # [hkv, nseg]
+    return at_end.repeat_interleave(G, dim=0)
+
+
+def unit_metrics(RL, o_r, lse_r, o_d, lse_d, v):
+    """Per-unit E_rel, true mass, mean row error, mean allowance, V_max and the fraction of
+    rows meeting the row bound with the true mass.  Returns a dict of [U] numpy arrays."""
+    od = _seg_view(RL, o_d.float())
+    orr = _seg_view(RL, o_r.float())
+    diff = (od - orr).norm(dim=-1)                                  # [hq, nseg, seg]
+    odn = od.norm(dim=-1)
+    orn = orr.norm(dim=-1)
+    e_rel = diff.pow(2).sum(-1).sqrt() / (odn.pow(2).sum(-1).sqrt() + EPS)
+    m_row, m_unit = true_mass(RL, lse_r, lse_d)
+    m_row = _seg_view(RL, m_row)
+    vm = vmax_units(RL, v)
+    allow = bf16_allowance(vm[..., None], odn, orn)
+    row_ok = (diff <= 2.0 * (1.0 - m_row) * vm[..., None] + allow).float().mean(-1)
+    out = dict(e_rel=e_rel, mean_err=diff.mean(-1), mean_allow=allow.mean(-1), vmax=vm, row_bound_ok=row_ok)
+    out = {k: _unit_order(t).cpu().numpy().astype(np.float64) for k, t in out.items()}
+    out["m_true"] = m_unit.cpu().numpy().astype(np.float64)
+    return out
+
+
+class DenseRef:
+    """Whole-row dense attention of a layer through the dense kernel (O and LSE)."""
+
+    def __init__(self, RL):
+        import torch
+        self.units = _rs.make_units([(h, 0, RL.n, 0, 0) for h in range(RL.hq)])
+        self.hq = RL.hq
+        self.o = torch.empty_like(RL.o)
+        self.lse = torch.empty((RL.hq, RL.n), dtype=torch.float32, device=RL.o.device)
+        self.ws = None
+
+    def __call__(self, qkv):
+        if self.ws is None:
+            self.ws = _rs.workspace(_rs.rs_attn_workspace_size(qkv, self.units, self.hq))
+        _rs.rs_dense_attn_prefill(qkv, self.units, self.hq, self.o, self.lse, self.ws)
+        return self.o, self.lse
+
+
+def calibrate(RL, ref, layers, q_level, log):
+    """delta_q from held-out layers: the residual m_hat - m_true of every sparse candidate on
+    every unit (each candidate launched over all units with its LSE)."""
+    import torch
+    resid, fam = [], []
+    lse_c = torch.empty((RL.hq, RL.n), dtype=torch.float32, device=RL.o.device)
+    all_u = list(range(RL.nunits))
+    for li, (q, k, v) in enumerate(layers):
+        qkv = RL.qkv(q, k, v)
+        _, lse_d = ref(qkv)
+        RL.probe_and_index(qkv)
+        m_hat = RL.pb.cov[:, :, 0].float().cpu().numpy()            # [U, C]
+        for c, g in enumerate(RL.grid):
+            if g[0] == _rs.RS_DENSE:
+                continue
+            RL.run_group(qkv, c, all_u, lse_c)
+            _, m_unit = true_mass(RL, lse_c, lse_d)
+            resid.append(m_hat[:, c] - m_unit.cpu().numpy())
+            fam += [g[0]] * RL.nunits
+        log(f"calibration layer {li + 1}/{len(layers)}")
+    r = np.concatenate(resid)
+    fam = np.asarray(fam)
+    per_fam = {int(f): dict(mean=float(r[fam == f].mean()), q=float(np.quantile(r[fam == f], q_level)),
+                            max=float(r[fam == f].max())) for f in np.unique(fam)}
+    return max(0.0, float(np.quantile(r, q_level))), r, per_fam
+
+
+def evaluate(RL, ref, layers, knobs, log, per_unit=False, fixed_route=None, label=""):
+    """Routed layers against the dense kernel: E_rel, certificate coverage, fallback rate,
+    ms/layer (CUDA events around one routed layer, after one untimed run of the same layer)."""
+    import torch
+    stream = torch.cuda.current_stream()
+    lse_r = torch.empty((RL.hq, RL.n), dtype=torch.float32, device=RL.o.device)
+    RL.knobs = knobs
+    e_rel, covered, row_ok, fb, ms, fam_units = [], [], [], [], [], {}
+    for q, k, v in layers:
+        qkv = RL.qkv(q, k, v)
+        o_d, lse_d = ref(qkv)
+        RL.run(q, k, v, per_unit=per_unit, fixed_route=fixed_route)
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        route = RL.run(q, k, v, lse=lse_r, per_unit=per_unit, fixed_route=fixed_route)
+        e1.record(stream)
+        e1.synchronize()
+        ms.append(e0.elapsed_time(e1))
+        fb.append(route["n_fallback"])
+        met = unit_metrics(RL, RL.o, lse_r, o_d, lse_d, v)
+        e_rel.append(met["e_rel"])
+        row_ok.append(met["row_bound_ok"])
+        for u, c in enumerate(route["choice"]):
+            f = RL.grid[c][0]
+            fam_units[f] = fam_units.get(f, 0) + 1
+            if f != _rs.RS_DENSE:
+                m_low = max(0.0, float(route["ML"][u, c]))
+                covered.append(met["mean_err"][u] <= 2.0 * (1.0 - m_low) * met["vmax"][u] + met["mean_allow"][u])
+    e = np.concatenate(e_rel)
+    worst = np.sort(e)[-max(1, len(e) // 10):]
+    res = dict(ms_per_layer=round(float(np.mean(ms)), 3), e_rel_mean=float(e.mean()),
+               e_rel_worst_decile=float(worst.mean()), e_rel_max=float(e.max()),
+               certificate_coverage=(float(np.mean(covered)) if covered else None),
+               sparse_units=len(covered), row_bound_true_mass=float(np.concatenate(row_ok).mean()),
+               fallback_units_per_layer=float(np.mean(fb)),
+               units_per_family={str(f): round(n / len(layers), 2) for f, n in sorted(fam_units.items())})
+    log(f"{label}: " + json.dumps(res))
+    return res
+
+
+def flops_table(RL, edges, us_per_flop):
+    """The predicted-FLOPs latency table: every (candidate, bucket) priced at one rate per
+    nominal kept pair (no hardware profiling).  Nominal pairs per row: dense i + 1; A-shape
+    min(i + 1, sink + window); vertical-slash min(i + 1, |V| + |D|); block-sparse
+    min(i + 1, k * block)."""
+    seg = RL.unit_list[0][2] - RL.unit_list[0][1]
+    t = np.zeros((RL.ncand, len(edges)))
+    for c, (fam, a_, b_) in enumerate(RL.grid):
+        cap = {_rs.RS_DENSE: np.inf, _rs.RS_ASHAPE: a_ + b_, _rs.RS_VSLASH: a_ + b_,
+               _rs.RS_BSPARSE: a_ * b_}[fam]
+        for b, s1 in enumerate(edges):
+            rows1 = np.arange(s1 - seg, s1, dtype=np.float64) + 1.0
+            t[c, b] = 4.0 * RL.d * np.minimum(rows1, cap).sum() * us_per_flop
+    return t
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--calib-layers", type=int, default=4)
+    ap.add_argument("--eval-layers", type=int, default=4)
+    ap.add_argument("--q", type=float, default=0.95)
+    ap.add_argument("--sweep", action="store_true")
+    ap.add_argument("--ablations", action="store_true")
+    ap.add_argument("--json-out", default=None)
+    args = ap.parse_args()
+
+    import torch
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    if root not in sys.path:
+        sys.path.insert(0, root)
+    from synth import gen as G
+
+    def log(*a):
+        print(*a, file=sys.stderr, flush=True)
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    _rs.lib()
+    RL = RoutedLayer(N, HQ, HKV, D, SEG, GRID)
+    ref = DenseRef(RL)
+    edges = np.array([SEG * (b + 1) for b in range(N // SEG)], np.int32)
+
+    def gen(layer):
+        t = G.make_layer_torch(5, layer, device=dev)
+        return t["q"], t["k"], t["v"]
+
+    t0 = time.perf_counter()
+    calib = [gen(64 + i) for i in range(args.calib_layers)]
+    evl = [gen(i) for i in range(args.eval_layers)]
+    torch.cuda.synchronize()
+    log(f"generated {len(calib) + len(evl)} layers ({time.perf_counter() - t0:.1f}s)")
+
+    # hardware latency table, probe time and budget, measured on the first evaluation layer
+    q0, k0, v0 = evl[0]
+    qkv0 = RL.qkv(q0, k0, v0)
+    RL.probe_and_index(qkv0)
+    RL.t_table, RL.edges = RL.profile_latency(qkv0, edges, reps=3), edges
+    RL.t_probe_us = RL.profile_probe(qkv0, reps=3)
+    t_dense = float(sum(RL.t_table[0, int(np.searchsorted(edges, u[2]))] for u in RL.unit_list))
+    T = t_dense / 6.5
+    log(f"latency table done: dense layer {t_dense / 1e3:.2f} ms, probe {RL.t_probe_us / 1e3:.2f} ms")
+
+    dq, resid, per_fam = calibrate(RL, ref, calib, args.q, log)
+    res = {"workload": "routed prefill, GQA 32/8 d128 bf16, n=131072, 8 x 16384 segments, 9-candidate grid",
+           "calibration": {"layers": [64 + i for i in range(args.calib_layers)], "q": args.q, "delta_q": dq,
+                           "residuals": int(resid.size), "residual_mean": float(resid.mean()),
+                           "residual_max": float(resid.max()), "per_family": per_fam},
+           "eval_layers": list(range(args.eval_layers)), "T_layer_us": T, "t_probe_us": RL.t_probe_us,
+           "dense_layer_us": t_dense}
+    kn = RouteKnobs(T_layer_us=T, tau=0.95, alpha=1.0, beta=0.0, delta_q=dq)
+    res["routed"] = evaluate(RL, ref, evl, kn, log, label=f"routed delta_q={dq:.4f}")
+    res["routed_delta_q0"] = evaluate(RL, ref, evl, RouteKnobs(T_layer_us=T, tau=0.95, alpha=1.0, beta=0.0),
+                                      log, label="routed delta_q=0")
+    if args.sweep:
+        pts = []
+        for tdiv in (10.0, 8.0, 6.5, 5.0, 4.0):
+            for tau in (0.85, 0.9, 0.95):
+                r = evaluate(RL, ref, evl, RouteKnobs(T_layer_us=t_dense / tdiv, tau=tau, alpha=1.0, beta=0.0,
+                                                       delta_q=dq), log, label=f"T=dense/{tdiv} tau={tau}")
+                pts.append(dict(T_div=tdiv, tau=tau, **r))
+        res["pareto"] = pts
+    if args.ablations:
+        ab = {}
+        # no input routing: the route taken on a calibration layer, reused on every layer
+        RL.knobs = kn
+        RL.probe_and_index(RL.qkv(*calib[0]))
+        fixed = RL.route()
+        ab["no_input_routing"] = evaluate(RL, ref, evl, kn, log, fixed_route=fixed, label="no input routing")
+        ab["no_uncertainty"] = evaluate(RL, ref, evl, RouteKnobs(T_layer_us=T, tau=0.95, alpha=0.0, beta=0.0,
+                                                                 delta_q=dq), log, label="alpha=0")
+        ab["no_dense_fallback"] = evaluate(RL, ref, evl, RouteKnobs(T_layer_us=T, tau=0.0, alpha=1.0, beta=0.0,
+                                                                    delta_q=dq), log, label="tau=0")
+        ab["per_head_launches"] = evaluate(RL, ref, evl, kn, log, per_unit=True, label="per-head launches")
+        measured = RL.t_table
+        rows_last = np.arange(N - SEG, N, dtype=np.float64) + 1.0
+        rate = measured[0, -1] / (4.0 * D * rows_last.sum())
+        RL.t_table = flops_table(RL, edges, rate)
+        ab["predicted_flops"] = evaluate(RL, ref, evl, kn, log, label="predicted FLOPs")
+        RL.t_table = measured
+        sub = [GRID[c] for c in ONE_BUDGET]
+        R1 = RoutedLayer(N, HQ, HKV, D, SEG, sub)
+        R1.t_table, R1.edges, R1.t_probe_us = measured[ONE_BUDGET], edges, RL.t_probe_us
+        ab["one_fixed_budget"] = evaluate(R1, ref, evl, kn, log, label="one budget per family")
+        del R1
+        Rr = RoutedLayer(N, HQ, HKV, D, SEG, GRID, r_uni=0, r_bnd=0)
+        Rr.probe_and_index(qkv0)
+        Rr.t_table, Rr.edges = measured, edges
+        Rr.t_probe_us = Rr.profile_probe(qkv0, reps=3)
+        ab["recent_queries_only"] = evaluate(Rr, ref, evl, kn, log, label="recent queries only")
+        res["ablations"] = ab
+    res["wall_s"] = round(time.perf_counter() - t0, 1)
+    line = json.dumps(res)
+    if args.json_out:
+        with open(args.json_out, "w") as f:
+            f.write(line + "\n")
+    print(line, flush=True)
+
+
+if __name__ == "__main__":
+    main()

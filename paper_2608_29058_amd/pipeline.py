@@ -102,17 +102,69 @@ class RoutedLayer:
         else:
             _rs.rs_sparse_attn_prefill(qkv, us, len(unit_idx), self.g, self.ncand, self.ib, self.o, lse, ws)
 
-    def run(self, q, k, v, events=None):
+    def run(self, q, k, v, events=None, lse=None, per_unit=False, fixed_route=None):
         """One routed layer; returns the route.  ``events`` (optional) is a callable
-        ``mark(name)`` used to record stream events between phases."""
+        ``mark(name)`` used to record stream events between phases; ``lse`` (optional,
+        float32 [hq, n]) receives the log-sum-exp of every row; ``per_unit`` launches each
+        unit on its own instead of one launch per (pattern, budget) group; ``fixed_route``
+        (a route returned earlier) replaces the input-conditional routing decision while the
+        index sets are still built from this input."""
         qkv = self.qkv(q, k, v)
         mark = events or (lambda name: None)
         mark("start")
         self.probe_and_index(qkv)
         mark("probe")
-        route = self.route()
+        route = self.route() if fixed_route is None else fixed_route
         mark("route")
         for ci, (cand, us) in enumerate(route["groups"]):
-            self.run_group(qkv, cand, us)
+            if per_unit:
+                for u in us:
+                    self.run_group(qkv, cand, [u], lse)
+            else:
+                self.run_group(qkv, cand, us, lse)
             mark(f"group{ci}")
         return route
+
+    # -- offline calibration (untimed) ---------------------------------------------------
+    def profile_latency(self, qkv, edges, reps=3):
+        """Kernel latency table t_ker[candidate][bucket] in us per unit: for every candidate
+        and key-length bucket, the median over key/value groups of the per-unit time of one
+        launch holding that group's query heads (each the median of ``reps`` launches)."""
+        import torch
+        stream = torch.cuda.current_stream()
+        G = self.hq // self.hkv
+        t = np.zeros((self.ncand, len(edges)))
+        for c in range(self.ncand):
+            for b in range(len(edges)):
+                per_group = []
+                for g in range(self.hkv):
+                    us = [i for i, u in enumerate(self.unit_list) if u[2] == edges[b] and u[0] // G == g]
+                    if not us:
+                        continue
+                    ts = []
+                    for _ in range(reps):
+                        e0 = torch.cuda.Event(enable_timing=True)
+                        e1 = torch.cuda.Event(enable_timing=True)
+                        e0.record(stream)
+                        self.run_group(qkv, c, us)
+                        e1.record(stream)
+                        e1.synchronize()
+                        ts.append(e0.elapsed_time(e1))
+                    per_group.append(float(np.median(ts)) / len(us))
+                t[c, b] = float(np.median(per_group)) * 1e3 if per_group else 0.0
+        return t
+
+    def profile_probe(self, qkv, reps=3):
+        """Median time of probe + indices + coverage, in us."""
+        import torch
+        stream = torch.cuda.current_stream()
+        ts = []
+        for _ in range(reps):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            self.probe_and_index(qkv)
+            e1.record(stream)
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return float(np.median(ts)) * 1e3

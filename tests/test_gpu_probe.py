@@ -42,11 +42,11 @@ def _inputs(n, hq, hkv, d, seed):
     return q, k, v
 
 
-def test_probe_scores_match_oracle():
+@pytest.mark.parametrize("rc", [(64, 16, 8), (64, 0, 0)])
+def test_probe_scores_match_oracle(rc):
     n, hq, hkv, d = 3000, 2, 1, 128
     q, k, v = _inputs(n, hq, hkv, d, 1)
     units = [(0, 0, 3000), (1, 1024, 2900), (0, 100, 164)]
-    rc = (64, 16, 8)
     res = _probe(q, k, v, units, rc, _rs.RS_PROBE_ROWS | _rs.RS_PROBE_BLOCKMEAN)
     pb = res["pb"]
     rows_g, sub_g = pb.rows.cpu().numpy(), pb.subset.cpu().numpy()
@@ -131,12 +131,12 @@ def test_indices_bit_exact_on_gpu_scores(tie):
             assert np.array_equal(rank_g[bq, :m], ranks[bq][:m])
 
 
-def test_coverage_matches_oracle():
+@pytest.mark.parametrize("rc", [(64, 16, 8), (64, 0, 0)])
+def test_coverage_matches_oracle(rc):
     import torch
     n, hq, hkv, d = 2200, 2, 1, 128
     q, k, v = _inputs(n, hq, hkv, d, 3)
     units = [(0, 0, n), (1, 512, 2100)]
-    rc = (64, 16, 8)
     res = _probe(q, k, v, units, rc, _rs.RS_PROBE_ROWS | _rs.RS_PROBE_BLOCKMEAN)
     pb = res["pb"]
     grid = [(_rs.RS_DENSE, 0, 0), (_rs.RS_ASHAPE, 64, 256), (_rs.RS_ASHAPE, 128, 1024),
