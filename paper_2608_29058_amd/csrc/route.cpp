@@ -95,29 +95,61 @@ extern "C" rs_status rs_route_layer(const rs_route_in *in, const rs_route_cfg *c
     for (int u = 0; u < U; ++u) tot = tot + t[(size_t)u * C + choice[u]];
     return tot;
   };
-  bool infeasible = false;
-  while (total() > cfg->T_layer_us) {
-    int bu = -1, bc = -1;
-    double best = 0.0;
-    for (int u = 0; u < U; ++u) {
-      const int cur = choice[u];
-      const double tc = t[(size_t)u * C + cur], rc = R[(size_t)u * C + cur];
-      for (int c = 0; c < C; ++c) {
-        const double tn = t[(size_t)u * C + c];
-        if (!(tn < tc)) continue;
-        const double rho = (R[(size_t)u * C + c] - rc) / (tc - tn);
-        if (bu < 0 || rho < best) {
-          best = rho;
-          bu = u;
-          bc = c;
-        }
-      }
+  // Greedy solve.  Each unit keeps its best substitution (minimum ratio, first candidate on
+  // ties); a tournament tree over the units yields the global minimum with the lowest unit
+  // winning ties, i.e. the first minimum of a scan in (unit, candidate) order.
+  struct Move {
+    double rho;
+    int c;  // -1: no strictly cheaper candidate
+  };
+  std::vector<Move> best(U);
+  auto unit_best = [&](int u) {
+    Move m{0.0, -1};
+    const int cur = choice[u];
+    const double tc = t[(size_t)u * C + cur], rc = R[(size_t)u * C + cur];
+    for (int c = 0; c < C; ++c) {
+      const double tn = t[(size_t)u * C + c];
+      if (!(tn < tc)) continue;
+      const double rho = (R[(size_t)u * C + c] - rc) / (tc - tn);
+      if (m.c < 0 || rho < m.rho) m = Move{rho, c};
     }
+    return m;
+  };
+  int P = 1;
+  while (P < U) P <<= 1;
+  std::vector<int> tree(2 * (size_t)P, -1);
+  auto win = [&](int l, int r) {  // l covers lower unit indices than r
+    if (l < 0) return r;
+    if (r < 0) return l;
+    return best[r].rho < best[l].rho ? r : l;
+  };
+  for (int u = 0; u < U; ++u) {
+    best[u] = unit_best(u);
+    tree[(size_t)P + u] = best[u].c >= 0 ? u : -1;
+  }
+  for (int i = P - 1; i >= 1; --i) tree[i] = win(tree[2 * i], tree[2 * i + 1]);
+  // The loop test is "fresh unit-order total > T_layer".  A running total is used while it
+  // is farther from T_layer than its possible drift from the fresh sum (each update and each
+  // term of a sum is off by at most one rounding: far below 1e-9 of the all-dense total); near
+  // the budget the fresh sum decides.
+  double est = total();
+  const double margin = 1e-9 * (est > 0.0 ? est : -est);
+  bool infeasible = false;
+  for (;;) {
+    if (!(est - cfg->T_layer_us > margin || cfg->T_layer_us - est > margin)) est = total();
+    if (!(est > cfg->T_layer_us)) break;
+    const int bu = tree[1];
     if (bu < 0) {
       infeasible = true;
       break;
     }
+    const int bc = best[bu].c;
+    est = (est - t[(size_t)bu * C + choice[bu]]) + t[(size_t)bu * C + bc];
     choice[bu] = bc;
+    best[bu] = unit_best(bu);
+    size_t i = (size_t)P + bu;
+    tree[i] = best[bu].c >= 0 ? bu : -1;
+    for (i >>= 1; i >= 1; i >>= 1) tree[i] = win(tree[2 * i], tree[2 * i + 1]);
   }
   // expand or fall back: larger budgets of the family first, then the cheapest passing
   // sparse candidate of any family ("dense if no sparse candidate satisfies tau")

@@ -152,3 +152,40 @@ def test_router_rejects_grid_without_dense():
     cov, nsub, s1, edges, tt = _random_instance(0, U=4)
     with pytest.raises(_rs.RsError):
         _rs.rs_route_layer(GRID[1:], cov[:, 1:], nsub, s1, tt[1:], edges, 1.0, 10.0, 0.9, 1.0, 0.0, 0.0)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_router_ties_and_exact_budget_match_oracle(seed):
+    """Coverage and latencies on coarse grids make many substitution ratios equal (ties go to
+    the lowest unit, then the lowest candidate); budgets set exactly to totals the greedy
+    passes through exercise the stopping test at equality."""
+    r = np.random.default_rng(1000 + seed)
+    U, C_ = 48, len(GRID)
+    cov = np.zeros((U, C_, 4), np.float32)
+    base = r.choice([0.875, 0.9375, 0.96875, 1.0], (U, C_)).astype(np.float32)
+    cov[:, :, 0] = base
+    for s in range(3):
+        cov[:, :, 1 + s] = base
+    cov[:, 0, :] = 1.0
+    nsub = np.tile(np.array([64, 64, 32], np.int32), (U, 1))
+    s1 = r.choice([16384, 32768], U).astype(np.int32)
+    edges = np.array([16384, 32768], np.int32)
+    tt = np.array([[64.0, 128.0]] + [[float(r.choice([4, 8, 16])), float(r.choice([8, 16, 32]))]
+                                     for _ in range(C_ - 1)])
+    t = _t_of(s1, edges, tt)
+    fam = [g[0] for g in GRID]
+    e0 = np.zeros((U, C_), np.float32)
+    # totals at which the greedy stops for some budgets (tau = 0 keeps them), then each of
+    # them, and its floating-point neighbours, as the budget
+    budgets = []
+    for frac in (0.2, 0.35, 0.5, 0.7):
+        r0 = RT.route_layer(cov[:, :, 0], cov[:, :, 1:], nsub, e0, t, fam, _brank(GRID), 2.0,
+                            2.0 + t[:, 0].sum() * frac, 0.0, 1.0, 0.0, 0.0)
+        budgets += [r0["total"], np.nextafter(r0["total"], 0.0), np.nextafter(r0["total"], np.inf)]
+    for T in budgets:
+        for tau in (0.0, 0.95):
+            st, got = _rs.rs_route_layer(GRID, cov, nsub, s1, tt, edges, 2.0, T, tau, 1.0, 0.0, 0.0)
+            ref = RT.route_layer(cov[:, :, 0], cov[:, :, 1:], nsub, e0, t, fam, _brank(GRID), 2.0, T, tau, 1.0,
+                                 0.0, 0.0)
+            assert got["choice"] == ref["choice"], (T, tau)
+            assert got["total"] == ref["total"] and got["over_budget"] == ref["over_budget"]
