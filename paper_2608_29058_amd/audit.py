@@ -171,11 +171,13 @@ def evaluate(RL, ref, layers, knobs, log, per_unit=False, fixed_route=None, labe
         met = unit_metrics(RL, RL.o, lse_r, o_d, lse_d, v)
         e_rel.append(met["e_rel"])
         row_ok.append(met["row_bound_ok"])
+        # lower mass of this layer's probe (a fixed route was chosen on another layer)
+        m_hat = RL.pb.cov[:, :, 0].double().cpu().numpy()
         for u, c in enumerate(route["choice"]):
             f = RL.grid[c][0]
             fam_units[f] = fam_units.get(f, 0) + 1
             if f != _rs.RS_DENSE:
-                m_low = max(0.0, float(route["ML"][u, c]))
+                m_low = max(0.0, float(m_hat[u, c]) - knobs.delta_q)
                 covered.append(met["mean_err"][u] <= 2.0 * (1.0 - m_low) * met["vmax"][u] + met["mean_allow"][u])
     e = np.concatenate(e_rel)
     worst = np.sort(e)[-max(1, len(e) // 10):]
