@@ -237,6 +237,8 @@ def main():
     ap.add_argument("--layers", type=int, default=32)
     ap.add_argument("--dense-reps", type=int, default=2)
     ap.add_argument("--calib-layers", type=int, default=4)
+    ap.add_argument("--route", choices=("device", "host"), default="device",
+                    help="routing on the device (no host synchronisation in a layer) or on the host")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--json-out", default=None)
     args = ap.parse_args()
@@ -296,16 +298,29 @@ def main():
     torch.cuda.empty_cache()
     log(f"delta_q {delta_q:.4f} from {resid.size} residuals")
     RL.knobs = RouteKnobs(T_layer_us=t_dense_layer_us / 6.5, tau=0.95, alpha=1.0, beta=0.0, delta_q=delta_q)
-    t0 = time.perf_counter()
-    RL.route()
-    t_route_host_us = (time.perf_counter() - t0) * 1e6
-    RL.t_probe_us = tp_us + t_route_host_us
+    device = args.route == "device"
+    if device:
+        RL.route_device()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(5):
+            e0 = ev()
+            RL.route_device()
+            e1 = ev()
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        t_route_us = float(np.median(ts)) * 1e3
+    else:
+        t0 = time.perf_counter()
+        RL.route()
+        t_route_us = (time.perf_counter() - t0) * 1e6
+    RL.t_probe_us = tp_us + t_route_us
     log(f"t_probe {RL.t_probe_us:.0f} us, T_layer {RL.knobs.T_layer_us:.0f} us")
 
     # ---- warmup + timed steps ----------------------------------------------------------------
     for s in range(args.warmup):
         q, k, v, _ = layers[s % args.layers]
-        RL.run(q, k, v)
+        RL.run(q, k, v, device_route=device)
     torch.cuda.synchronize()
     records = []
     t_wall0 = time.perf_counter()
@@ -314,8 +329,8 @@ def main():
         li = s % args.layers
         q, k, v, _ = layers[li]
         marks = []
-        route = RL.run(q, k, v, events=lambda name: marks.append((name, ev())))
-        records.append((li, route, marks))
+        RL.run(q, k, v, events=lambda name: marks.append((name, ev())), device_route=device)
+        records.append((li, marks))
     e_end = ev()
     torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - t_wall0) * 1e3
@@ -330,29 +345,43 @@ def main():
     fam_flops = {f: 0.0 for f in FAM_NAME}
     fam_issued = {f: 0.0 for f in FAM_NAME}
     fam_launches = {f: 0 for f in FAM_NAME}
-    ph = {"probe_index_coverage": 0.0, "d2h_route": 0.0, "attention": 0.0}
+    ph = {"probe_index_coverage": 0.0, "route": 0.0, "attention": 0.0}
+    for li, marks in records:
+        evs = [m[1] for m in marks]
+        ph["probe_index_coverage"] += evs[0].elapsed_time(evs[1])
+        ph["route"] += evs[1].elapsed_time(evs[2])
+        ph["attention"] += evs[2].elapsed_time(evs[-1])
+    # Per-family and per-candidate accounting: every layer of the timed steps again, routed on
+    # the host (the device route is checked to be identical), one launch per (pattern, budget)
+    # group with events around each, weighted by the layer's number of timed steps.
     n_units_fb = 0
     n_units_dense = 0
     routed_flops = 0.0
-    cache = {}
-    for li, route, marks in records:
-        names = [m[0] for m in marks]
-        evs = [m[1] for m in marks]
-        ph["probe_index_coverage"] += evs[0].elapsed_time(evs[1])
-        ph["d2h_route"] += evs[1].elapsed_time(evs[2])
-        ph["attention"] += evs[2].elapsed_time(evs[-1])
-        n_units_fb += route["n_fallback"]
-        if li not in cache:
-            q, k, v, _ = layers[li]
-            RL.probe_and_index(RL.qkv(q, k, v))
-            torch.cuda.synchronize()
-            cache[li] = dict(bs_count=RL.ib.bs_count.cpu().numpy(), vs_count=RL.ib.vs_count.cpu().numpy(),
-                             vs_v=RL.ib.vs_vsorted.cpu().numpy(), vs_d=RL.ib.vs_dsorted.cpu().numpy(),
-                             bs_lists={})
-        ic = cache[li]
+    route_mismatch = 0
+    routes = {}
+    uses = {}
+    for li, _ in records:
+        uses[li] = uses.get(li, 0) + 1
+    for li, w_l in sorted(uses.items()):
+        q, k, v, _ = layers[li]
+        qkv_l = RL.qkv(q, k, v)
+        RL.probe_and_index(qkv_l)
+        route = RL.route()
+        routes[li] = route
+        if device:
+            RL.route_device()
+            route_mismatch += int(RL.rb.choice[:RL.nunits].cpu().tolist() != route["choice"])
+        n_units_fb += w_l * route["n_fallback"]
+        ic = dict(bs_count=RL.ib.bs_count.cpu().numpy(), vs_count=RL.ib.vs_count.cpu().numpy(),
+                  vs_v=RL.ib.vs_vsorted.cpu().numpy(), vs_d=RL.ib.vs_dsorted.cpu().numpy(), bs_lists={})
+        gev = [ev()]
+        for cand, us in route["groups"]:
+            RL.run_group(qkv_l, cand, us)
+            gev.append(ev())
+        torch.cuda.synchronize()
         for gi, (cand, us) in enumerate(route["groups"]):
             fam, a_, b_ = GRID[cand]
-            dt = evs[2 + gi].elapsed_time(evs[3 + gi])
+            dt = w_l * gev[gi].elapsed_time(gev[gi + 1])
             pairs = 0
             cl = sum(1 for g in GRID[:cand] if g[0] == fam)
             tiles = 0
@@ -361,7 +390,7 @@ def main():
                 if fam == 0:
                     pairs += pairs_dense(s0, s1)
                     tiles += tiles_dense(s0, s1)
-                    n_units_dense += 1
+                    n_units_dense += w_l
                 elif fam == 1:
                     pairs += pairs_ashape(s0, s1, a_, b_)
                     tiles += tiles_ashape(s0, s1, a_, b_)
@@ -374,14 +403,14 @@ def main():
                     cv, cdn = ic["vs_count"][u, cl]
                     pairs += pairs_vs(s0, s1, ic["vs_v"][u, cl, :cv], ic["vs_d"][u, cl, :cdn])
                     tiles += tiles_vs(s0, s1, ic["vs_v"][u, cl, :cv], ic["vs_d"][u, cl, :cdn])
-            fam_issued[fam] += 4.0 * D * 64 * 128 * tiles
-            fl = 4.0 * D * pairs
-            cand_units[cand] += len(us)
-            cand_pairs[cand] += pairs
+            fam_issued[fam] += w_l * 4.0 * D * 64 * 128 * tiles
+            fl = w_l * 4.0 * D * pairs
+            cand_units[cand] += w_l * len(us)
+            cand_pairs[cand] += w_l * pairs
             cand_time[cand] += dt
             fam_time[fam] += dt
             fam_flops[fam] += fl
-            fam_launches[fam] += 1
+            fam_launches[fam] += w_l
             routed_flops += fl
     # dense reference: the whole layer through the dense kernel, same run
     qkv_d = RL.qkv(q0, k0, v0)
@@ -439,11 +468,13 @@ def main():
         "wall_ms_timed": round(wall_ms, 1),
         "t_layer_budget_ms": round(RL.knobs.T_layer_us / 1e3, 3),
         "t_probe_ms": round(RL.t_probe_us / 1e3, 3),
+        "routing": args.route,
+        "device_route_mismatches": route_mismatch if device else None,
         "delta_q": round(delta_q, 5),
     }
     if not args.no_cpu_baseline:
         try:
-            res["cpu_baseline"] = cpu_baseline(q0, k0, v0, records[0][1], t_table, edges, RL.knobs)
+            res["cpu_baseline"] = cpu_baseline(q0, k0, v0, routes[records[0][0]], t_table, edges, RL.knobs)
         except Exception as exc:  # reported, never fatal to the GPU measurement
             res["cpu_baseline"] = {"error": repr(exc)}
     line = json.dumps(res)

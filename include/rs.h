@@ -216,6 +216,64 @@ rs_status rs_build_indices(const rs_probe_out *scores, const rs_unit *units, int
  * filled in) when the final total exceeds T_layer. */
 rs_status rs_route_layer(const rs_route_in *in, const rs_route_cfg *cfg, rs_route_out *out);
 
+/* ---- calibrated error predictor (Sec. 3.3, the e term of Eq. 4) -------------------------
+ * e(u, c) = sum_k w[fam(c)][k] x_k(u, c), a monotone regressor: the weights are
+ * non-negative, so e never decreases when a feature grows.  They are fitted offline on
+ * dense calibration runs.  The features use only the probe's coverage call and the
+ * candidate's family:
+ *   x0 = 1 - m_hat(c)            x1 = u(c), max - min of the non-empty subset means
+ *   x2 = (1 - m_hat(c)) * H      x3 = (1 - m_hat(c)) * (1 - L)
+ * H and L are the means, over the unit's sampled rows, of the normalised block entropy and
+ * of the local-band mass.  Dense candidates get e = 0.  Sums are taken in fp64 and the
+ * result is rounded to fp32.
+ * e: device [nunits][ncand], written on `stream`.  Reads probe->cov, nsub, entropy and
+ * local, which the coverage call of rs_probe writes. */
+typedef struct rs_error_model {
+  float w[4][4]; /* [family][feature], each >= 0; the RS_DENSE row is ignored */
+} rs_error_model;
+rs_status rs_error_predict(const rs_probe_out *probe, const rs_candidate *grid, int32_t ncand,
+                           const rs_error_model *model, float *e, rs_stream stream);
+
+/* ---- device-side routing (Sec. 3.4: routing as a fused GPU reduction) -------------------
+ * Same decisions and outputs as rs_route_layer, bit for bit, computed by one workgroup on
+ * `stream`.  The attention launches of the layer then follow with no host synchronisation.
+ * `in` is read as by rs_route_layer, with two differences:
+ *  - cov, nsub, e, s1, t_table and bucket_edge are DEVICE pointers;
+ *  - grid is a host array and t_probe_us a value.
+ * Outputs go to the device arrays of `out`, with the dimensions of rs_route_out.  Over
+ * budget is reported in out->status; the call itself returns RS_OK.
+ * Limits: nunits <= 2048 and nunits * (ncand - 1) <= 4096 (else RS_ERR_UNSUPPORTED). */
+typedef struct rs_route_dev_out {
+  int32_t *choice, *group_cand, *group_start, *group_units; /* as in rs_route_out */
+  double *risk, *m_lower;                                   /* [nunits][ncand] */
+  int32_t *status; /* [4] ngroups, n_fallback, over_budget, infeasible */
+  double *totals;  /* [2] total_us, total_risk */
+} rs_route_dev_out;
+size_t rs_route_layer_device_workspace_size(int32_t nunits, int32_t ncand);
+rs_status rs_route_layer_device(const rs_route_in *in, const rs_route_cfg *cfg,
+                                const rs_route_dev_out *out, void *ws, size_t ws_bytes,
+                                rs_stream stream);
+
+/* ---- routed attention from a device route (Sec. 3.4 grouping, inference step 6) ---------
+ * Runs every unit u with candidate choice[u] (device int32 [nunits], e.g.
+ * rs_route_dev_out.choice): one launch per family present in the grid, each over all the
+ * units routed to any budget of that family.
+ *  - Work lists are built on the device by a planning kernel: query tiles bucketed by
+ *    key/value head, longest first.
+ *  - O and lse equal those of one rs_sparse_attn_prefill / rs_dense_attn_prefill call per
+ *    (pattern, budget) group.
+ *  - `units` is the layer's host unit list; `slot` is the unit's row in `idx`, and the
+ *    unit's `cand` field is ignored.
+ *  - Grids are sized for every unit picking the family; surplus workgroups exit at once.
+ *  - A unit whose choice lies outside [0, ncand) is not computed.
+ * Limit: nunits <= 2048 (else RS_ERR_UNSUPPORTED). */
+size_t rs_routed_attn_workspace_size(const rs_qkv *qkv, const rs_unit *units, int32_t nunits);
+rs_status rs_routed_attn_prefill(const rs_qkv *qkv, const rs_unit *units, int32_t nunits,
+                                 const rs_candidate *grid, int32_t ncand,
+                                 const rs_index_set *idx, const int32_t *choice, void *o,
+                                 int64_t so_h, int64_t so_t, float *lse, void *ws,
+                                 size_t ws_bytes, rs_stream stream);
+
 /* ---- attention (Sec. 2.1; kernels of Sec. 3.1) ------------------------------------------
  * Every unit of one call must use the same candidate (one (pattern, budget) group).
  * Writes rows [s0, s1) of O for each unit and, if lse != NULL, lse[head * n + i] =

@@ -11,8 +11,15 @@ subsets; Sec. 3.3 defines the risk (Eq. 4) and the lower confidence mass.  Readi
 * u(c) = max - min of the subset means over the non-empty subsets (0 with one subset);
 * m_lower = max(0, m_hat - delta_q);
 * risk R(c) = (1 - m_hat) + alpha * u + beta * e (Eq. 4), e the optional calibrated
-  error predictor (0 here); the dense candidate has m_hat = 1, u = 0 and risk 0 by
-  definition.
+  error predictor; the dense candidate has m_hat = 1, u = 0 and risk 0 by definition.
+
+Reading of e (Sec. 3.3 asks only for a small monotone regressor fitted offline on dense
+calibration runs, fed with probe descriptors and candidate metadata): with omega = 1 - m_hat,
+H and L the means over the unit's sampled rows of the normalised block entropy and of the
+local-band mass, the features are (omega, u, omega * H, omega * (1 - L)) and
+e = sum_k w[family][k] x_k with non-negative weights, hence monotone non-decreasing in every
+feature; dense candidates get 0.  Sums in fp64, e rounded to fp32.  The features and the model
+form are this reading, not the paper's: parity unpinned beyond the invariants its tests check.
 """
 from __future__ import annotations
 
@@ -55,3 +62,22 @@ def lower_mass(m_hat, delta_q):
 def risk(m_hat, u, e, alpha, beta):
     """Risk score of Eq. (4): (1 - m_hat) + alpha * u + beta * e."""
     return (1.0 - m_hat) + alpha * u + beta * e
+
+
+def error_features(m_hat, sub_means, sub_counts, entropy_rows, local_rows):
+    """(omega, u, omega * H, omega * (1 - L)) of one (unit, candidate)."""
+    om = 1.0 - float(m_hat)
+    uu = disagreement(sub_means, sub_counts)
+    ent = [float(x) for x in entropy_rows]
+    loc = [float(x) for x in local_rows]
+    H = sum(ent) / len(ent) if ent else 0.0
+    L = sum(loc) / len(loc) if loc else 0.0
+    return [om, uu, om * H, om * (1.0 - L)]
+
+
+def predict_error(features, weights):
+    """e = sum_k w_k x_k (fp64, in feature order), rounded to fp32."""
+    acc = 0.0
+    for w, x in zip(weights, features):
+        acc = acc + float(np.float32(w)) * float(x)
+    return float(np.float32(acc))

@@ -20,7 +20,9 @@ RS_PROBE_ROWS, RS_PROBE_BLOCKMEAN = 1, 2
 
 EXPORTS = ["rs_probe_workspace_size", "rs_probe", "rs_build_indices_workspace_size",
            "rs_build_indices", "rs_route_layer", "rs_attn_workspace_size",
-           "rs_sparse_attn_prefill", "rs_dense_attn_prefill", "rs_last_error", "rs_version"]
+           "rs_sparse_attn_prefill", "rs_dense_attn_prefill", "rs_error_predict",
+           "rs_route_layer_device_workspace_size", "rs_route_layer_device",
+           "rs_routed_attn_workspace_size", "rs_routed_attn_prefill", "rs_last_error", "rs_version"]
 
 P = C.c_void_p
 I32 = C.c_int32
@@ -82,6 +84,15 @@ class RsRouteOut(C.Structure):
                 ("total_risk", C.c_double)]
 
 
+class RsErrorModel(C.Structure):
+    _fields_ = [("w", (C.c_float * 4) * 4)]
+
+
+class RsRouteDevOut(C.Structure):
+    _fields_ = [("choice", P), ("group_cand", P), ("group_start", P), ("group_units", P),
+                ("risk", P), ("m_lower", P), ("status", P), ("totals", P)]
+
+
 _lib = None
 
 
@@ -95,7 +106,8 @@ def lib():
         L.rs_last_error.restype = C.c_char_p
         L.rs_version.restype = C.c_char_p
         for name in ("rs_probe_workspace_size", "rs_build_indices_workspace_size",
-                     "rs_attn_workspace_size"):
+                     "rs_attn_workspace_size", "rs_route_layer_device_workspace_size",
+                     "rs_routed_attn_workspace_size"):
             getattr(L, name).restype = C.c_size_t
         L.rs_probe_workspace_size.argtypes = [C.POINTER(RsQkv), C.POINTER(RsUnit), I32, C.POINTER(RsProbeCfg)]
         L.rs_probe.argtypes = [C.POINTER(RsQkv), C.POINTER(RsUnit), I32, C.POINTER(RsProbeCfg),
@@ -110,8 +122,17 @@ def lib():
                                              I32, C.POINTER(RsIndexSet), P, I64, I64, P, P, C.c_size_t, P]
         L.rs_dense_attn_prefill.argtypes = [C.POINTER(RsQkv), C.POINTER(RsUnit), I32, P, I64, I64, P, P,
                                             C.c_size_t, P]
+        L.rs_error_predict.argtypes = [C.POINTER(RsProbeOut), C.POINTER(RsCandidate), I32,
+                                       C.POINTER(RsErrorModel), P, P]
+        L.rs_route_layer_device_workspace_size.argtypes = [I32, I32]
+        L.rs_route_layer_device.argtypes = [C.POINTER(RsRouteIn), C.POINTER(RsRouteCfg), C.POINTER(RsRouteDevOut),
+                                            P, C.c_size_t, P]
+        L.rs_routed_attn_workspace_size.argtypes = [C.POINTER(RsQkv), C.POINTER(RsUnit), I32]
+        L.rs_routed_attn_prefill.argtypes = [C.POINTER(RsQkv), C.POINTER(RsUnit), I32, C.POINTER(RsCandidate),
+                                             I32, C.POINTER(RsIndexSet), P, P, I64, I64, P, P, C.c_size_t, P]
         for name in ("rs_probe", "rs_build_indices", "rs_route_layer", "rs_sparse_attn_prefill",
-                     "rs_dense_attn_prefill"):
+                     "rs_dense_attn_prefill", "rs_error_predict", "rs_route_layer_device",
+                     "rs_routed_attn_prefill"):
             getattr(L, name).restype = C.c_int
         _lib = L
     return _lib
@@ -310,3 +331,88 @@ def rs_route_layer(grid, cov, nsub, s1, t_table, bucket_edge, t_probe_us, T_laye
     return st, dict(choice=[int(x) for x in choice[:U]], groups=groups, total=out.total_us,
                     risk=out.total_risk, n_fallback=out.n_fallback, over_budget=bool(out.over_budget),
                     infeasible=bool(out.infeasible), R=risk[:U], ML=ml[:U])
+
+
+def make_error_model(w) -> RsErrorModel:
+    """w: [4][4] non-negative weights, [family][feature]."""
+    m = RsErrorModel()
+    for f in range(4):
+        for k in range(4):
+            m.w[f][k] = float(w[f][k])
+    return m
+
+
+def rs_error_predict(probe, grid, ncand, model, e, stream=None):
+    """e: float32 device tensor [nunits, ncand]."""
+    return _check(lib().rs_error_predict(C.byref(probe.c), grid, ncand, C.byref(model), _ptr(e),
+                                         _stream(stream)))
+
+
+class RouteDevBuffers:
+    """Device inputs and outputs of rs_route_layer_device for a fixed layer shape: the unit key
+    lengths, the latency table and its bucket edges (uploaded once), the route outputs and the
+    workspace."""
+
+    def __init__(self, grid, s1, t_table, bucket_edge, device="cuda"):
+        import numpy as np
+        import torch
+        grid = list(grid)
+        U, Cn = len(s1), len(grid)
+        self.U, self.C = U, Cn
+        self.grid = make_grid(grid)
+        i, d = torch.int32, torch.float64
+        self.s1 = torch.as_tensor(np.asarray(s1, np.int32), device=device)
+        self.t_table = torch.as_tensor(np.ascontiguousarray(t_table, np.float64), device=device)
+        self.bucket_edge = torch.as_tensor(np.asarray(bucket_edge, np.int32), device=device)
+        self.nbucket = len(bucket_edge)
+        self.choice = torch.zeros(max(U, 1), dtype=i, device=device)
+        self.group_cand = torch.zeros(Cn, dtype=i, device=device)
+        self.group_start = torch.zeros(Cn + 1, dtype=i, device=device)
+        self.group_units = torch.zeros(max(U, 1), dtype=i, device=device)
+        self.risk = torch.zeros((max(U, 1), Cn), dtype=d, device=device)
+        self.m_lower = torch.zeros((max(U, 1), Cn), dtype=d, device=device)
+        self.status = torch.zeros(4, dtype=i, device=device)
+        self.totals = torch.zeros(2, dtype=d, device=device)
+        self.ws = workspace(lib().rs_route_layer_device_workspace_size(U, Cn), device=device)
+        self.out = RsRouteDevOut(choice=self.choice.data_ptr(), group_cand=self.group_cand.data_ptr(),
+                                 group_start=self.group_start.data_ptr(), group_units=self.group_units.data_ptr(),
+                                 risk=self.risk.data_ptr(), m_lower=self.m_lower.data_ptr(),
+                                 status=self.status.data_ptr(), totals=self.totals.data_ptr())
+
+    def result(self):
+        """The route as rs_route_layer returns it (copies to the host; synchronises)."""
+        st = self.status.cpu().tolist()
+        tot = self.totals.cpu().tolist()
+        gc = self.group_cand.cpu().tolist()
+        gs = self.group_start.cpu().tolist()
+        gu = self.group_units.cpu().tolist()
+        ng = st[0]
+        return dict(choice=self.choice[:self.U].cpu().tolist(),
+                    groups=[(gc[k], gu[gs[k]:gs[k + 1]]) for k in range(ng)],
+                    total=tot[0], risk=tot[1], n_fallback=st[1], over_budget=bool(st[2]),
+                    infeasible=bool(st[3]), R=self.risk[:self.U].cpu().numpy(),
+                    ML=self.m_lower[:self.U].cpu().numpy())
+
+
+def rs_route_layer_device(rb, cov, nsub, t_probe_us, T_layer_us, tau, alpha, beta, delta_q, e=None,
+                          stream=None):
+    """cov: float32 device [U, C, 4], nsub: int32 device [U, 3], e: float32 device [U, C] or None."""
+    rin = RsRouteIn(nunits=rb.U, ncand=rb.C, grid=C.cast(rb.grid, P), cov=cov.data_ptr(), nsub=nsub.data_ptr(),
+                    e=e.data_ptr() if e is not None else None, s1=rb.s1.data_ptr(),
+                    t_table=rb.t_table.data_ptr(), bucket_edge=rb.bucket_edge.data_ptr(), nbucket=rb.nbucket,
+                    t_probe_us=t_probe_us)
+    cfg = RsRouteCfg(T_layer_us=T_layer_us, tau=tau, alpha=alpha, beta=beta, delta_q=delta_q)
+    return _check(lib().rs_route_layer_device(C.byref(rin), C.byref(cfg), C.byref(rb.out), _ptr(rb.ws),
+                                              rb.ws.numel(), _stream(stream)))
+
+
+def rs_routed_attn_workspace_size(qkv, units, nunits):
+    return lib().rs_routed_attn_workspace_size(C.byref(qkv), units, nunits)
+
+
+def rs_routed_attn_prefill(qkv, units, nunits, grid, ncand, idx, choice, o, lse, ws, stream=None):
+    """choice: int32 device tensor [nunits]."""
+    return _check(lib().rs_routed_attn_prefill(
+        C.byref(qkv), units, nunits, grid, ncand, C.byref(idx.c) if idx is not None else None, _ptr(choice),
+        _ptr(o), o.stride(0), o.stride(1), _ptr(lse), _ptr(ws), ws.numel() if ws is not None else 0,
+        _stream(stream)))

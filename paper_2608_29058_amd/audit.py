@@ -22,7 +22,11 @@ segment) and routed candidate, from the kernels' own outputs:
   calibration layers, clipped at 0 (one-sided).
 
 python -m paper_2608_29058_amd.audit [--calib-layers 4] [--eval-layers 4] [--q 0.95]
-    [--sweep] [--ablations] [--json-out FILE]
+    [--sweep] [--ablations] [--error-model] [--json-out FILE]
+
+With --error-model the error predictor e (rs_error_predict) is fitted on the calibration
+layers by non-negative least squares per family (E_rel on its four features) and the routed
+layers are evaluated with beta > 0.
 Workload: the 128K routed layer (GQA 32/8, d = 128, 8 segments of 16384 per head,
 9-candidate grid) on synthetic layers; calibration layers (64, 65, ...) are disjoint from the
 evaluation layers (0, 1, ...).
@@ -147,7 +151,7 @@ def calibrate(RL, ref, layers, q_level, log):
     return max(0.0, float(np.quantile(r, q_level))), r, per_fam
 
 
-def evaluate(RL, ref, layers, knobs, log, per_unit=False, fixed_route=None, label=""):
+def evaluate(RL, ref, layers, knobs, log, per_unit=False, fixed_route=None, label="", device_route=False):
     """Routed layers against the dense kernel: E_rel, certificate coverage, fallback rate,
     ms/layer (CUDA events around one routed layer, after one untimed run of the same layer)."""
     import torch
@@ -158,14 +162,16 @@ def evaluate(RL, ref, layers, knobs, log, per_unit=False, fixed_route=None, labe
     for q, k, v in layers:
         qkv = RL.qkv(q, k, v)
         o_d, lse_d = ref(qkv)
-        RL.run(q, k, v, per_unit=per_unit, fixed_route=fixed_route)
+        RL.run(q, k, v, per_unit=per_unit, fixed_route=fixed_route, device_route=device_route)
         torch.cuda.synchronize()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         e0.record(stream)
-        route = RL.run(q, k, v, lse=lse_r, per_unit=per_unit, fixed_route=fixed_route)
+        route = RL.run(q, k, v, lse=lse_r, per_unit=per_unit, fixed_route=fixed_route, device_route=device_route)
         e1.record(stream)
         e1.synchronize()
+        if device_route:
+            route = RL.rb.result()
         ms.append(e0.elapsed_time(e1))
         fb.append(route["n_fallback"])
         met = unit_metrics(RL, RL.o, lse_r, o_d, lse_d, v)
@@ -191,6 +197,54 @@ def evaluate(RL, ref, layers, knobs, log, per_unit=False, fixed_route=None, labe
     return res
 
 
+def error_features(RL):
+    """The four predictor features [4][U][C] of the layer in RL's probe buffers, computed by
+    rs_error_predict with one-hot weights (so the library's feature code is what is fitted)."""
+    import torch
+    out = []
+    for k in range(4):
+        w = np.zeros((4, 4), np.float32)
+        w[1:, k] = 1.0
+        e = torch.empty((RL.nunits, RL.ncand), dtype=torch.float32, device=RL.o.device)
+        _rs.rs_error_predict(RL.pb, RL.g, RL.ncand, _rs.make_error_model(w), e)
+        out.append(e.double().cpu().numpy())
+    return np.stack(out)
+
+
+def fit_error_model(RL, ref, layers, log):
+    """Non-negative least squares, per family, of E_rel(u, c) on the four features over every
+    (unit, sparse candidate) of the calibration layers (Sec. 3.3: a monotone regressor fitted
+    offline on dense calibration runs).  Returns the [4][4] weights and the fit R^2 per family."""
+    import torch
+    from scipy.optimize import nnls
+    X = {f: [] for f in (1, 2, 3)}
+    Y = {f: [] for f in (1, 2, 3)}
+    lse_c = torch.empty((RL.hq, RL.n), dtype=torch.float32, device=RL.o.device)
+    all_u = list(range(RL.nunits))
+    for li, (q, k, v) in enumerate(layers):
+        qkv = RL.qkv(q, k, v)
+        o_d, lse_d = ref(qkv)
+        RL.probe_and_index(qkv)
+        F = error_features(RL)
+        for c, g in enumerate(RL.grid):
+            if g[0] == _rs.RS_DENSE:
+                continue
+            RL.run_group(qkv, c, all_u, lse_c)
+            met = unit_metrics(RL, RL.o, lse_c, o_d, lse_d, v)
+            X[g[0]].append(F[:, :, c].T)
+            Y[g[0]].append(met["e_rel"])
+        log(f"error-model layer {li + 1}/{len(layers)}")
+    w = np.zeros((4, 4))
+    r2 = {}
+    for f in (1, 2, 3):
+        x = np.concatenate(X[f])
+        y = np.concatenate(Y[f])
+        w[f], _ = nnls(x, y)
+        pred = x @ w[f]
+        r2[f] = float(1.0 - ((y - pred) ** 2).sum() / max(((y - y.mean()) ** 2).sum(), 1e-30))
+    return w.astype(np.float32), r2
+
+
 def flops_table(RL, edges, us_per_flop):
     """The predicted-FLOPs latency table: every (candidate, bucket) priced at one rate per
     nominal kept pair (no hardware profiling).  Nominal pairs per row: dense i + 1; A-shape
@@ -214,6 +268,7 @@ def main():
     ap.add_argument("--q", type=float, default=0.95)
     ap.add_argument("--sweep", action="store_true")
     ap.add_argument("--ablations", action="store_true")
+    ap.add_argument("--error-model", action="store_true", help="fit e on the calibration layers, route with beta > 0")
     ap.add_argument("--json-out", default=None)
     args = ap.parse_args()
 
@@ -264,6 +319,13 @@ def main():
     res["routed"] = evaluate(RL, ref, evl, kn, log, label=f"routed delta_q={dq:.4f}")
     res["routed_delta_q0"] = evaluate(RL, ref, evl, RouteKnobs(T_layer_us=T, tau=0.95, alpha=1.0, beta=0.0),
                                       log, label="routed delta_q=0")
+    res["routed_device"] = evaluate(RL, ref, evl, kn, log, label="routed, device routing", device_route=True)
+    if args.error_model:
+        w, r2 = fit_error_model(RL, ref, calib, log)
+        res["error_model"] = {"weights": w.tolist(), "fit_r2": {str(f): v for f, v in r2.items()}}
+        for beta in (0.5, 1.0):
+            kb = RouteKnobs(T_layer_us=T, tau=0.95, alpha=1.0, beta=beta, delta_q=dq, error_model=w)
+            res[f"routed_beta{beta}"] = evaluate(RL, ref, evl, kb, log, label=f"routed beta={beta}")
     if args.sweep:
         pts = []
         for tdiv in (10.0, 8.0, 6.5, 5.0, 4.0):

@@ -2,9 +2,9 @@
 
     python -m paper_2608_29058_amd.build [-j N]
 
-Each HIP translation unit is compiled with hipcc for gfx950 only; the router is plain
-C++ compiled with floating-point contraction disabled (its fp64 operation order is part
-of its definition).
+Each HIP translation unit is compiled with hipcc for gfx950 only; the host router is plain
+C++ and, like the device router, is compiled with floating-point contraction disabled (its
+fp64 operation order is part of its definition).
 """
 from __future__ import annotations
 
@@ -22,7 +22,9 @@ LIB = os.path.join(HERE, "librs.so")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")
 
-HIP_SOURCES = ["attn.hip", "probe.hip", "topk.hip"]
+HIP_SOURCES = ["attn.hip", "probe.hip", "topk.hip", "route_dev.hip"]
+# sources whose fp64 operation order is part of their definition
+NO_CONTRACT = {"route_dev.hip"}
 HOST_HIP_SOURCES = ["api.cpp"]
 PLAIN_SOURCES = ["route.cpp"]
 
@@ -45,7 +47,8 @@ def build(jobs: int | None = None, verbose: bool = False) -> str:
     objs = []
     for s in HIP_SOURCES:
         o = os.path.join(BUILD, s + ".o")
-        cmds.append([HIPCC, *HIP_FLAGS, "-c", os.path.join(CSRC, s), "-o", o])
+        extra = ["-ffp-contract=off"] if s in NO_CONTRACT else []
+        cmds.append([HIPCC, *HIP_FLAGS, *extra, "-c", os.path.join(CSRC, s), "-o", o])
         objs.append(o)
     for s in HOST_HIP_SOURCES:
         o = os.path.join(BUILD, s + ".o")

@@ -103,6 +103,18 @@ static rs_status check_grid(const rs_candidate *grid, int32_t ncand) {
   return RS_OK;
 }
 
+size_t route_dev_ws_bytes(int32_t nunits, int32_t ncand);
+rs_status route_dev_launch(const rs_route_in *in, const rs_route_cfg *cfg, const rs_route_dev_out *out,
+                           const int *fam, const int *brank, int dense_c, void *ws, size_t ws_bytes,
+                           hipStream_t st);
+rs_status error_predict_launch(const rs_probe_out *p, const rs_candidate *grid, int32_t ncand,
+                               const rs_error_model *m, float *e, hipStream_t st);
+size_t routed_attn_ws_bytes(const rs_unit *units, int32_t nunits);
+rs_status routed_attn_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int32_t nunits,
+                             const rs_candidate *grid, int32_t ncand, const rs_index_set *idx, const int32_t *choice,
+                             void *o, int64_t so_h, int64_t so_t, float *lse, void *ws, size_t ws_bytes,
+                             hipStream_t st);
+
 static int cand_local_index(const rs_candidate *grid, int c) {
   int k = 0;
   for (int i = 0; i < c; ++i)
@@ -280,6 +292,99 @@ rs_status rs_build_indices(const rs_probe_out *scores, const rs_unit *units, int
   }
   if (nunits == 0 && nbs == 0) return RS_OK;
   return build_indices_launch(scores, units, nunits, grid, ncand, out, (hipStream_t)stream, ws, ws_bytes);
+}
+
+size_t rs_route_layer_device_workspace_size(int32_t nunits, int32_t ncand) {
+  if (nunits < 0 || ncand < 1) return 0;
+  return route_dev_ws_bytes(nunits, ncand);
+}
+
+rs_status rs_route_layer_device(const rs_route_in *in, const rs_route_cfg *cfg, const rs_route_dev_out *out,
+                                void *ws, size_t ws_bytes, rs_stream stream) {
+  g_err.clear();
+  if (!in || !cfg || !out) return fail(RS_ERR_INVALID_ARG, "route: NULL argument");
+  const int U = in->nunits, C = in->ncand;
+  if (U < 0 || C < 1 || C > 16 || !in->grid) return fail(RS_ERR_INVALID_ARG, "route: bad sizes (1 <= ncand <= 16)");
+  if (U > 0 && (!in->cov || !in->nsub || !in->s1)) return fail(RS_ERR_INVALID_ARG, "route: missing inputs");
+  if (in->nbucket < 1 || !in->t_table || !in->bucket_edge) return fail(RS_ERR_INVALID_ARG, "route: missing latency table");
+  if (!out->choice || !out->group_cand || !out->group_start || !out->group_units || !out->risk || !out->m_lower ||
+      !out->status || !out->totals)
+    return fail(RS_ERR_INVALID_ARG, "route: missing outputs");
+  int fam[16], brank[16], dense_c = -1;
+  for (int c = 0; c < C; ++c) {
+    fam[c] = in->grid[c].fam;
+    if (fam[c] < RS_DENSE || fam[c] > RS_BSPARSE) return fail(RS_ERR_INVALID_ARG, "route: unknown family");
+    brank[c] = cand_local_index(in->grid, c);
+    if (fam[c] == RS_DENSE && dense_c < 0) dense_c = c;
+  }
+  if (dense_c < 0) return fail(RS_ERR_INVALID_ARG, "route: the grid must contain a dense candidate");
+  return route_dev_launch(in, cfg, out, fam, brank, dense_c, ws, ws_bytes, (hipStream_t)stream);
+}
+
+rs_status rs_error_predict(const rs_probe_out *probe, const rs_candidate *grid, int32_t ncand,
+                           const rs_error_model *model, float *e, rs_stream stream) {
+  g_err.clear();
+  rs_status st;
+  if (!probe || !model || !e) return fail(RS_ERR_INVALID_ARG, "probe, model or e is NULL");
+  if ((st = check_grid(grid, ncand)) != RS_OK) return st;
+  if (probe->ncand != ncand) return fail(RS_ERR_INVALID_ARG, "probe coverage built for another grid");
+  if (probe->nunits > 0 && (!probe->cov || !probe->nsub || !probe->entropy || !probe->local))
+    return fail(RS_ERR_INVALID_ARG, "probe coverage or descriptor arrays missing");
+  for (int f = 0; f < 4; ++f)
+    for (int k = 0; k < 4; ++k)
+      if (!(model->w[f][k] >= 0.f) || !std::isfinite(model->w[f][k]))
+        return fail(RS_ERR_INVALID_ARG, "error-model weights must be finite and non-negative");
+  return error_predict_launch(probe, grid, ncand, model, e, (hipStream_t)stream);
+}
+
+size_t rs_routed_attn_workspace_size(const rs_qkv *qkv, const rs_unit *units, int32_t nunits) {
+  (void)qkv;
+  if (nunits <= 0 || !units) return 256;
+  return routed_attn_ws_bytes(units, nunits);
+}
+
+rs_status rs_routed_attn_prefill(const rs_qkv *qkv, const rs_unit *units, int32_t nunits, const rs_candidate *grid,
+                                 int32_t ncand, const rs_index_set *idx, const int32_t *choice, void *o, int64_t so_h,
+                                 int64_t so_t, float *lse, void *ws, size_t ws_bytes, rs_stream stream) {
+  g_err.clear();
+  float scale;
+  rs_status st;
+  if ((st = check_qkv(qkv, &scale)) != RS_OK) return st;
+  if ((st = check_units(qkv, units, nunits)) != RS_OK) return st;
+  if ((st = check_grid(grid, ncand)) != RS_OK) return st;
+  if ((st = check_out(o, so_h, so_t, qkv->d)) != RS_OK) return st;
+  if (nunits == 0) return RS_OK;
+  if (!choice) return fail(RS_ERR_INVALID_ARG, "choice is NULL");
+  bool vs = false, bs = false;
+  for (int c = 0; c < ncand; ++c) {
+    vs = vs || grid[c].fam == RS_VSLASH;
+    bs = bs || grid[c].fam == RS_BSPARSE;
+  }
+  if (vs || bs) {
+    if (!idx) return fail(RS_ERR_INVALID_ARG, "index set required");
+    if (idx->n != qkv->n) return fail(RS_ERR_INVALID_ARG, "index set built for another sequence length");
+  }
+  int nvs = 0, nbs = 0;
+  for (int c = 0; c < ncand; ++c) {
+    nvs += grid[c].fam == RS_VSLASH;
+    nbs += grid[c].fam == RS_BSPARSE;
+  }
+  if (vs) {
+    if (!idx->vs_vsorted || !idx->vs_dsorted || !idx->vs_count || !idx->vs_vbits || !idx->vs_dbits)
+      return fail(RS_ERR_INVALID_ARG, "vertical-slash arrays missing");
+    if (nvs > idx->ncand_vs || idx->nwords != (qkv->n + 31) / 32 || idx->nv_max > 2048)
+      return fail(RS_ERR_INVALID_ARG, "index set does not match the grid");
+    for (int i = 0; i < nunits; ++i)
+      if (units[i].slot < 0 || units[i].slot >= idx->nunits)
+        return fail(RS_ERR_INVALID_ARG, "unit slot outside the index set");
+  }
+  if (bs) {
+    if (!idx->bs_sorted || !idx->bs_count) return fail(RS_ERR_INVALID_ARG, "block-sparse arrays missing");
+    if (nbs > idx->ncand_bs || idx->nb != (qkv->n + 63) / 64 || idx->hq != qkv->hq)
+      return fail(RS_ERR_INVALID_ARG, "index set does not match the grid");
+  }
+  return routed_attn_launch(qkv, scale, units, nunits, grid, ncand, idx, choice, o, so_h, so_t, lse, ws, ws_bytes,
+                            (hipStream_t)stream);
 }
 
 }  // extern "C"

@@ -34,10 +34,6 @@ namespace rs {
 
 enum { P_DENSE = 0, P_ASHAPE = 1, P_VS = 2, P_BS = 3 };
 
-struct DevUnit {
-  int head, s0, s1, cl, slot, pad0, pad1, pad2;
-};
-
 struct AttnArgs {
   const void *q, *k, *v;
   long long sq_h, sq_t, sk_h, sk_t, sv_h, sv_t;
@@ -47,8 +43,10 @@ struct AttnArgs {
   int n, group;
   float c, scale;
   const DevUnit *units;
-  const int *order;
-  int sink, window;  // A-shape
+  const int *order;   // items; with queues, bucket b's at order[qoff[b] .. qoff[b] + qsize[b])
+  const int *qsize;   // [8] items per key/value bucket (device), or NULL: one item per workgroup
+  const int *qoff;    // [8]
+  int *qcount;        // [8] items taken per bucket (device counters, start at 0)
   const int *vs_vsorted, *vs_dsorted, *vs_count;
   const uint32_t *vs_vbits, *vs_dbits;
   int nv_max, ns_max, nwords, ncand_vs;
@@ -90,8 +88,9 @@ struct TileRef {
   Win3 wv;   // vertical-slash: column-bitmap words of the tile (prefetched)
 };
 
+// One work item: query tile `item & 0xffff` of unit `item >> 16` of the launch's unit list.
 template <int D, int PAT, typename InT>
-__global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const AttnArgs a) {
+__device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
   constexpr int NW = 4, NT = 256, BM = 128;
   constexpr int KS = D / 16;             // k-steps of the QK^T contraction
   constexpr int DB = D / 32;             // 32-row blocks of O^T
@@ -113,7 +112,6 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const AttnArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
 
-  const int item = a.order[blockIdx.x];
   const DevUnit U = a.units[item >> 16];
   const int qt = item & 0xffff;
   const int head = U.head, s0 = U.s0, s1 = U.s1;
@@ -201,8 +199,8 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const AttnArgs a) {
   } else if constexpr (PAT == P_DENSE) {
     ntiles = last_tile + 1;
   } else if constexpr (PAT == P_ASHAPE) {
-    const int ns = min((a.sink + 63) >> 6, last_tile + 1);
-    const int wlo = max(0, r_lo - a.window + 1) >> 6;
+    const int ns = min((U.sink + 63) >> 6, last_tile + 1);
+    const int wlo = max(0, r_lo - U.window + 1) >> 6;
     st0 = ns;
     st1 = max(wlo, ns);
     ntiles = ns + max(0, last_tile - st1 + 1);
@@ -371,7 +369,7 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const AttnArgs a) {
     if constexpr (kOverlap) {
       p.on = true;
       if constexpr (PAT == P_ASHAPE)
-        p.need_mask = !(key0 + 63 <= w_lo && (key0 + 63 < a.sink || key0 > w_hi - a.window));
+        p.need_mask = !(key0 + 63 <= w_lo && (key0 + 63 < U.sink || key0 > w_hi - U.window));
       else
         p.need_mask = key0 + 63 > w_lo;
       return p;
@@ -438,7 +436,7 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const AttnArgs a) {
       if (!p.do0) M &= ~0xffffffffull;
       if (!p.do1) M &= 0xffffffffull;
     } else if constexpr (PAT == P_ASHAPE) {
-      const uint64_t keep = prefix_mask(a.sink - key0) | ~prefix_mask(i - a.window + 1 - key0);
+      const uint64_t keep = prefix_mask(U.sink - key0) | ~prefix_mask(i - U.window + 1 - key0);
       M = (keep & prefix_mask(i - key0 + 1)) >> (4 * hh);
     } else {
       M = prefix_mask(i - key0 + 1) >> (4 * hh);
@@ -599,6 +597,39 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const AttnArgs a) {
     a.lse[(long long)head * a.n + i] = l_tot > 0.f ? m_run * a.scale + logf(l_tot) : -INFINITY;
 }
 
+// attn_fwd_kernel: workgroup b runs item order[b].  attn_fwd_queue_kernel: the grid is
+// persistent; workgroup b (on XCD b % 8 under round-robin dispatch) takes the next item of the
+// queue of key/value bucket b % 8 (items there are longest first), then of the other buckets
+// once its own is empty, until every queue is drained.  Each queue counter starts at 0 (the
+// planner writes it) and is only ever incremented, so every workgroup reaches the exit.
+template <int D, int PAT, typename InT>
+__global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const AttnArgs a) {
+  attn_item<D, PAT, InT>(a, a.order[blockIdx.x]);
+}
+
+template <int D, int PAT, typename InT>
+__global__ void __launch_bounds__(256, 2) attn_fwd_queue_kernel(const AttnArgs a) {
+  __shared__ int sItem;
+  const int x = (int)(blockIdx.x & 7u);
+  for (;;) {
+    __syncthreads();  // the previous item is done with the tile buffers and sItem
+    if (threadIdx.x == 0) {
+      int got = -1;
+      for (int k = 0; k < 8 && got < 0; ++k) {
+        const int b = (x + k) & 7;
+        if (__hip_atomic_load(&a.qcount[b], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= a.qsize[b]) continue;
+        const int r = atomicAdd(&a.qcount[b], 1);
+        if (r < a.qsize[b]) got = a.order[a.qoff[b] + r];
+      }
+      sItem = got;
+    }
+    __syncthreads();
+    const int it = sItem;
+    if (it < 0) break;
+    attn_item<D, PAT, InT>(a, it);
+  }
+}
+
 // ---- host side ---------------------------------------------------------------------------
 
 static int family_bm(int) { return 128; }
@@ -639,10 +670,17 @@ static void build_order(const rs_unit *units, int nunits, int group, int bm,
 
 template <int D, int PAT>
 static hipError_t launch_pat(int dtype, const AttnArgs &a, int nitems, hipStream_t st) {
-  if (dtype == RS_BF16)
-    hipLaunchKernelGGL((attn_fwd_kernel<D, PAT, bf16>), dim3(nitems), dim3(256), 0, st, a);
-  else
-    hipLaunchKernelGGL((attn_fwd_kernel<D, PAT, float>), dim3(nitems), dim3(256), 0, st, a);
+  if (a.qsize) {
+    if (dtype == RS_BF16)
+      hipLaunchKernelGGL((attn_fwd_queue_kernel<D, PAT, bf16>), dim3(nitems), dim3(256), 0, st, a);
+    else
+      hipLaunchKernelGGL((attn_fwd_queue_kernel<D, PAT, float>), dim3(nitems), dim3(256), 0, st, a);
+  } else {
+    if (dtype == RS_BF16)
+      hipLaunchKernelGGL((attn_fwd_kernel<D, PAT, bf16>), dim3(nitems), dim3(256), 0, st, a);
+    else
+      hipLaunchKernelGGL((attn_fwd_kernel<D, PAT, float>), dim3(nitems), dim3(256), 0, st, a);
+  }
   return hipGetLastError();
 }
 
@@ -654,6 +692,36 @@ static hipError_t launch_d(int fam, int dtype, const AttnArgs &a, int nitems, hi
     case RS_VSLASH: return launch_pat<D, P_VS>(dtype, a, nitems, st);
     default: return launch_pat<D, P_BS>(dtype, a, nitems, st);
   }
+}
+
+// One launch of a family's kernel over a device work list: `d_units` and `d_order` as built
+// by attn_launch (host; one workgroup per item, `nblocks` items) or by the device planner
+// (device routing; `queues` set, `nblocks` persistent workgroups drain the bucket queues).
+rs_status attn_launch_list(const rs_qkv *qkv, float scale, int fam, const rs_index_set *idx,
+                           const DevUnit *d_units, const int *d_order, const AttnQueues *queues, int nblocks,
+                           void *o, int64_t so_h, int64_t so_t, float *lse, hipStream_t st) {
+  if (nblocks <= 0) return RS_OK;
+  AttnArgs a{};
+  a.q = qkv->q; a.k = qkv->k; a.v = qkv->v;
+  a.sq_h = qkv->sq_h; a.sq_t = qkv->sq_t; a.sk_h = qkv->sk_h; a.sk_t = qkv->sk_t;
+  a.sv_h = qkv->sv_h; a.sv_t = qkv->sv_t;
+  a.o = (bf16 *)o; a.so_h = so_h; a.so_t = so_t; a.lse = lse;
+  a.n = qkv->n; a.group = qkv->hq / qkv->hkv; a.scale = scale; a.c = scale * kLog2e;
+  a.units = d_units; a.order = d_order;
+  if (queues) { a.qsize = queues->size; a.qoff = queues->off; a.qcount = queues->count; }
+  if (fam == RS_VSLASH) {
+    a.vs_vsorted = idx->vs_vsorted; a.vs_dsorted = idx->vs_dsorted; a.vs_count = idx->vs_count;
+    a.vs_vbits = idx->vs_vbits; a.vs_dbits = idx->vs_dbits;
+    a.nv_max = idx->nv_max; a.ns_max = idx->ns_max; a.nwords = idx->nwords; a.ncand_vs = idx->ncand_vs;
+  }
+  if (fam == RS_BSPARSE) {
+    a.bs_sorted = idx->bs_sorted; a.bs_count = idx->bs_count;
+    a.k_max = idx->k_max; a.nb = idx->nb; a.ncand_bs = idx->ncand_bs;
+  }
+  hipError_t e = qkv->d == 128 ? launch_d<128>(fam, qkv->dtype, a, nblocks, st)
+                               : launch_d<64>(fam, qkv->dtype, a, nblocks, st);
+  if (e != hipSuccess) return hip_check(e, "attention kernel launch");
+  return RS_OK;
 }
 
 // Shared entry of the dense and sparse calls (arguments validated by the caller).
@@ -678,32 +746,14 @@ rs_status attn_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int3
   std::vector<char> stage(off_order + order.size() * sizeof(int));
   DevUnit *h_units = (DevUnit *)stage.data();
   for (int u = 0; u < nunits; ++u) {
-    h_units[u] = DevUnit{units[u].head, units[u].s0, units[u].s1, cand_local, units[u].slot, 0, 0, 0};
+    h_units[u] = DevUnit{units[u].head, units[u].s0, units[u].s1, cand_local, units[u].slot,
+                         fam == RS_ASHAPE ? cand->a : 0, fam == RS_ASHAPE ? cand->b : 0, 0};
   }
   memcpy(stage.data() + off_order, order.data(), order.size() * sizeof(int));
   RS_HIP(hipMemcpyAsync(ws, stage.data(), stage.size(), hipMemcpyHostToDevice, st));
 
-  AttnArgs a{};
-  a.q = qkv->q; a.k = qkv->k; a.v = qkv->v;
-  a.sq_h = qkv->sq_h; a.sq_t = qkv->sq_t; a.sk_h = qkv->sk_h; a.sk_t = qkv->sk_t;
-  a.sv_h = qkv->sv_h; a.sv_t = qkv->sv_t;
-  a.o = (bf16 *)o; a.so_h = so_h; a.so_t = so_t; a.lse = lse;
-  a.n = qkv->n; a.group = group; a.scale = scale; a.c = scale * kLog2e;
-  a.units = d_units; a.order = d_order;
-  if (fam == RS_ASHAPE) { a.sink = cand->a; a.window = cand->b; }
-  if (fam == RS_VSLASH) {
-    a.vs_vsorted = idx->vs_vsorted; a.vs_dsorted = idx->vs_dsorted; a.vs_count = idx->vs_count;
-    a.vs_vbits = idx->vs_vbits; a.vs_dbits = idx->vs_dbits;
-    a.nv_max = idx->nv_max; a.ns_max = idx->ns_max; a.nwords = idx->nwords; a.ncand_vs = idx->ncand_vs;
-  }
-  if (fam == RS_BSPARSE) {
-    a.bs_sorted = idx->bs_sorted; a.bs_count = idx->bs_count;
-    a.k_max = idx->k_max; a.nb = idx->nb; a.ncand_bs = idx->ncand_bs;
-  }
-  hipError_t e = qkv->d == 128 ? launch_d<128>(fam, qkv->dtype, a, (int)order.size(), st)
-                               : launch_d<64>(fam, qkv->dtype, a, (int)order.size(), st);
-  if (e != hipSuccess) return hip_check(e, "attention kernel launch");
-  return RS_OK;
+  return attn_launch_list(qkv, scale, fam, idx, d_units, d_order, nullptr, (int)order.size(), o, so_h, so_t, lse,
+                          st);
 }
 
 }  // namespace rs

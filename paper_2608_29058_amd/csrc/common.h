@@ -36,6 +36,25 @@ rs_status hip_check(hipError_t e, const char *what);
 rs_status check_qkv(const rs_qkv *qkv, float *scale);
 rs_status check_units(const rs_qkv *qkv, const rs_unit *units, int32_t nunits);
 
+// Unit descriptor read by the attention kernels (work lists built on the host or on the device).
+struct DevUnit {
+  int head, s0, s1, cl, slot;  // cl: index of the unit's candidate among its family's
+  int sink, window;            // A-shape candidate of the unit
+  int pad;
+};
+
+// Device work queues of a persistent attention launch: per key/value bucket b (8), the items
+// order[off[b] .. off[b] + size[b]) and a counter of items taken (starts at 0).
+struct AttnQueues {
+  const int *size, *off;
+  int *count;
+};
+
+// One launch of a family's attention kernel over a device work list (attn.hip).
+rs_status attn_launch_list(const rs_qkv *qkv, float scale, int fam, const rs_index_set *idx,
+                           const DevUnit *d_units, const int *d_order, const AttnQueues *queues, int nblocks,
+                           void *o, int64_t so_h, int64_t so_t, float *lse, hipStream_t st);
+
 // bump allocator over a caller workspace
 struct Arena {
   char *base;

@@ -4,9 +4,12 @@ No arithmetic happens here: this module allocates caller-owned buffers once and 
 library in the order of the per-layer procedure (Sec. 3.4 and its table):
   1. rs_probe (scores: sampled rows, col/diag, descriptors, block-mean logits)
   2. rs_build_indices, then rs_probe (coverage of every candidate)
-  3-5. coverage copied to the host, rs_route_layer (latency lookup, greedy solve,
-       expand/fallback, grouping)
-  6. one rs_sparse_attn_prefill / rs_dense_attn_prefill launch per (pattern, budget) group.
+  3-5. rs_route_layer on the host after copying the coverage back (latency lookup, greedy
+       solve, expand/fallback, grouping), or rs_route_layer_device on the stream
+  6. one rs_sparse_attn_prefill / rs_dense_attn_prefill launch per (pattern, budget) group, or
+     after device routing one rs_routed_attn_prefill call (one launch per family, work lists
+     built on the device: no host synchronisation in the layer).
+With beta > 0 the calibrated error predictor (rs_error_predict) runs after the coverage.
 """
 from __future__ import annotations
 
@@ -24,6 +27,7 @@ class RouteKnobs:
     alpha: float = 1.0
     beta: float = 0.0
     delta_q: float = 0.0
+    error_model: object = None   # [4][4] non-negative weights of the error predictor (beta > 0)
 
 
 @dataclass
@@ -55,7 +59,12 @@ class RoutedLayer:
         self.s1 = np.array([u[2] for u in self.unit_list], np.int32)
         self.cov_host = torch.empty((self.nunits, self.ncand, 4), dtype=torch.float32, pin_memory=True)
         self.nsub_host = torch.empty((self.nunits, 3), dtype=torch.int32, pin_memory=True)
+        self.e = torch.zeros((self.nunits, self.ncand), dtype=torch.float32, device=device)
+        self.e_host = torch.empty((self.nunits, self.ncand), dtype=torch.float32, pin_memory=True)
+        self.rb = None
+        self._rb_table = None
         self._ws = None
+        self._ws_routed = None
         self.t_table = None
         self.edges = None
         self.t_probe_us = 0.0
@@ -79,16 +88,45 @@ class RoutedLayer:
         _rs.rs_build_indices(self.pb, self.units, self.nunits, self.g, self.ncand, ws, self.ib)
         _rs.rs_probe(qkv, self.units, self.nunits, self.cfg, self.g, self.ncand, self.ib, ws, self.pb)
 
+    def _use_e(self):
+        return self.knobs.beta > 0 and self.knobs.error_model is not None
+
+    def predict_error(self):
+        """e of the risk score from this layer's probe (rs_error_predict), on the stream."""
+        _rs.rs_error_predict(self.pb, self.g, self.ncand, _rs.make_error_model(self.knobs.error_model),
+                             self.e)
+
     def route(self):
         import torch
+        if self._use_e():
+            self.predict_error()
+            self.e_host.copy_(self.e, non_blocking=True)
         self.cov_host.copy_(self.pb.cov, non_blocking=True)
         self.nsub_host.copy_(self.pb.nsub, non_blocking=True)
         torch.cuda.current_stream().synchronize()
         k = self.knobs
         st, out = _rs.rs_route_layer(self.grid, self.cov_host.numpy(), self.nsub_host.numpy(), self.s1,
                                      self.t_table, self.edges, self.t_probe_us, k.T_layer_us, k.tau,
-                                     k.alpha, k.beta, k.delta_q)
+                                     k.alpha, k.beta, k.delta_q, e=self.e_host.numpy() if self._use_e() else None)
         return out
+
+    def route_device(self):
+        """rs_route_layer_device on the stream; the route stays in self.rb (device)."""
+        if self.rb is None or self._rb_table is not self.t_table:   # latency table uploaded once
+            self.rb = _rs.RouteDevBuffers(self.grid, self.s1, self.t_table, self.edges)
+            self._rb_table = self.t_table
+        k = self.knobs
+        if self._use_e():
+            self.predict_error()
+        _rs.rs_route_layer_device(self.rb, self.pb.cov, self.pb.nsub, self.t_probe_us, k.T_layer_us, k.tau, k.alpha,
+                                  k.beta, k.delta_q, e=self.e if self._use_e() else None)
+
+    def run_routed(self, qkv, lse=None):
+        """All units with the device route's choices: one rs_routed_attn_prefill call."""
+        if self._ws_routed is None:
+            self._ws_routed = _rs.workspace(_rs.rs_routed_attn_workspace_size(qkv, self.units, self.nunits))
+        _rs.rs_routed_attn_prefill(qkv, self.units, self.nunits, self.g, self.ncand, self.ib, self.rb.choice,
+                                   self.o, lse, self._ws_routed)
 
     def group_units(self, cand, unit_idx):
         return _rs.make_units([(self.unit_list[u][0], self.unit_list[u][1], self.unit_list[u][2], cand, u)
@@ -102,18 +140,26 @@ class RoutedLayer:
         else:
             _rs.rs_sparse_attn_prefill(qkv, us, len(unit_idx), self.g, self.ncand, self.ib, self.o, lse, ws)
 
-    def run(self, q, k, v, events=None, lse=None, per_unit=False, fixed_route=None):
-        """One routed layer; returns the route.  ``events`` (optional) is a callable
-        ``mark(name)`` used to record stream events between phases; ``lse`` (optional,
-        float32 [hq, n]) receives the log-sum-exp of every row; ``per_unit`` launches each
-        unit on its own instead of one launch per (pattern, budget) group; ``fixed_route``
-        (a route returned earlier) replaces the input-conditional routing decision while the
-        index sets are still built from this input."""
+    def run(self, q, k, v, events=None, lse=None, per_unit=False, fixed_route=None, device_route=False):
+        """One routed layer; returns the route (None with ``device_route``: it stays on the
+        device, in self.rb).  ``events`` (optional) is a callable ``mark(name)`` used to record
+        stream events between phases; ``lse`` (optional, float32 [hq, n]) receives the
+        log-sum-exp of every row; ``per_unit`` launches each unit on its own instead of one
+        launch per (pattern, budget) group; ``fixed_route`` (a route returned earlier) replaces
+        the input-conditional routing decision while the index sets are still built from this
+        input; ``device_route`` routes on the device and launches the attention from that route
+        with no host synchronisation."""
         qkv = self.qkv(q, k, v)
         mark = events or (lambda name: None)
         mark("start")
         self.probe_and_index(qkv)
         mark("probe")
+        if device_route:
+            self.route_device()
+            mark("route")
+            self.run_routed(qkv, lse)
+            mark("attention")
+            return None
         route = self.route() if fixed_route is None else fixed_route
         mark("route")
         for ci, (cand, us) in enumerate(route["groups"]):

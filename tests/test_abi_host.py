@@ -39,7 +39,8 @@ def test_struct_layouts_match_the_c_compiler(tmp_path):
     structs = {"rs_qkv": _rs.RsQkv, "rs_unit": _rs.RsUnit, "rs_candidate": _rs.RsCandidate,
                "rs_probe_cfg": _rs.RsProbeCfg, "rs_probe_out": _rs.RsProbeOut,
                "rs_index_set": _rs.RsIndexSet, "rs_route_in": _rs.RsRouteIn,
-               "rs_route_cfg": _rs.RsRouteCfg, "rs_route_out": _rs.RsRouteOut}
+               "rs_route_cfg": _rs.RsRouteCfg, "rs_route_out": _rs.RsRouteOut,
+               "rs_error_model": _rs.RsErrorModel, "rs_route_dev_out": _rs.RsRouteDevOut}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "rs.h"', 'int main(void) {']
     for cname, py in structs.items():
         lines.append(f'printf("{cname} size %zu\\n", sizeof({cname}));')
@@ -189,3 +190,50 @@ def test_router_ties_and_exact_budget_match_oracle(seed):
                                  0.0, 0.0)
             assert got["choice"] == ref["choice"], (T, tau)
             assert got["total"] == ref["total"] and got["over_budget"] == ref["over_budget"]
+
+
+def test_device_routing_entries_reject_bad_arguments_without_launch():
+    """Validation of the error predictor, the device router and the routed attention call
+    happens on the host, before anything is launched."""
+    L = _rs.lib()
+    grid = _rs.make_grid(GRID)
+    # error predictor: negative or non-finite weights
+    pb = _rs.RsProbeOut(nunits=1, rmax=4, n=64, nb=1, ncand=len(GRID), hq=1, cov=16, nsub=16, entropy=16, local=16)
+    w = [[0.0] * 4 for _ in range(4)]
+    w[2][1] = -1.0
+    st = L.rs_error_predict(C.byref(pb), grid, len(GRID), C.byref(_rs.make_error_model(w)), C.c_void_p(16), None)
+    assert st == _rs.RS_ERR_INVALID_ARG and b"non-negative" in L.rs_last_error()
+    w[2][1] = float("nan")
+    st = L.rs_error_predict(C.byref(pb), grid, len(GRID), C.byref(_rs.make_error_model(w)), C.c_void_p(16), None)
+    assert st == _rs.RS_ERR_INVALID_ARG
+    pb.ncand = 3
+    w[2][1] = 0.0
+    st = L.rs_error_predict(C.byref(pb), grid, len(GRID), C.byref(_rs.make_error_model(w)), C.c_void_p(16), None)
+    assert st == _rs.RS_ERR_INVALID_ARG and b"another grid" in L.rs_last_error()
+    # device router: grid without dense, too many units, workspace too small
+    out = _rs.RsRouteDevOut(choice=16, group_cand=16, group_start=16, group_units=16, risk=16, m_lower=16,
+                            status=16, totals=16)
+    cfg = _rs.RsRouteCfg(T_layer_us=1.0, tau=0.9, alpha=1.0, beta=0.0, delta_q=0.0)
+    g1 = _rs.make_grid(GRID[1:])
+    rin = _rs.RsRouteIn(nunits=4, ncand=len(GRID) - 1, grid=C.cast(g1, C.c_void_p), cov=16, nsub=16, s1=16,
+                        t_table=16, bucket_edge=16, nbucket=1)
+    st = L.rs_route_layer_device(C.byref(rin), C.byref(cfg), C.byref(out), C.c_void_p(16), 1 << 20, None)
+    assert st == _rs.RS_ERR_INVALID_ARG and b"dense" in L.rs_last_error()
+    rin = _rs.RsRouteIn(nunits=4096, ncand=len(GRID), grid=C.cast(grid, C.c_void_p), cov=16, nsub=16, s1=16,
+                        t_table=16, bucket_edge=16, nbucket=1)
+    st = L.rs_route_layer_device(C.byref(rin), C.byref(cfg), C.byref(out), C.c_void_p(16), 1 << 30, None)
+    assert st == _rs.RS_ERR_UNSUPPORTED
+    rin.nunits = 64
+    need = L.rs_route_layer_device_workspace_size(64, len(GRID))
+    st = L.rs_route_layer_device(C.byref(rin), C.byref(cfg), C.byref(out), C.c_void_p(16), need - 1, None)
+    assert st == _rs.RS_ERR_WORKSPACE
+    # routed attention: missing choice, missing index set for a sparse grid
+    q = _rs.RsQkv(q=16, k=16, v=16, dtype=_rs.RS_BF16, n=256, hq=2, hkv=1, d=128, sq_h=256 * 128, sq_t=128,
+                  sk_h=256 * 128, sk_t=128, sv_h=256 * 128, sv_t=128)
+    units = _rs.make_units([(0, 0, 256), (1, 0, 256)])
+    st = L.rs_routed_attn_prefill(C.byref(q), units, 2, grid, len(GRID), None, None, C.c_void_p(16), 256 * 128, 128,
+                                  None, C.c_void_p(16), 1 << 20, None)
+    assert st == _rs.RS_ERR_INVALID_ARG
+    st = L.rs_routed_attn_prefill(C.byref(q), units, 2, grid, len(GRID), None, C.c_void_p(16), C.c_void_p(16),
+                                  256 * 128, 128, None, C.c_void_p(16), 1 << 20, None)
+    assert st == _rs.RS_ERR_INVALID_ARG and b"index set" in L.rs_last_error()

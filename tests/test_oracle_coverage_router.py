@@ -108,3 +108,31 @@ def test_tau_switches_to_cheapest_passing_sparse_candidate():
 
 def test_grouping():
     assert RT.group([2, 0, 2, 1, 0], 4) == [(0, [1, 4]), (1, [3]), (2, [0, 2])]
+
+
+def test_error_predictor_by_hand_and_invariants():
+    """The calibrated error predictor e of Eq. 4 (features and model are a reading; see the
+    module docstring): a hand-worked case, and the invariants that pin the reading: zero
+    omitted mass and no disagreement give 0, and e never decreases when the omitted mass,
+    the disagreement, the entropy grow or the local mass shrinks."""
+    # m_hat 0.9, subset means (0.95, 0.85, 0.9) -> u = 0.1; mean entropy 0.5, mean local 0.8
+    x = CV.error_features(0.9, [0.95, 0.85, 0.9], [64, 64, 32], [0.25, 0.75], [0.7, 0.9])
+    assert np.allclose(x, [0.1, 0.1, 0.05, 0.02], atol=1e-15)
+    assert abs(CV.predict_error(x, [1.0, 2.0, 4.0, 8.0]) - 0.66) < 1e-7
+    # an empty subset does not enter u; no sampled rows give H = L = 0
+    x = CV.error_features(0.8, [0.7, 0.0, 0.9], [10, 0, 5], [], [])
+    assert np.allclose(x, [0.2, 0.2, 0.0, 0.2], atol=1e-15)
+    assert CV.predict_error(CV.error_features(1.0, [1.0, 1.0, 1.0], [1, 1, 1], [0.9], [0.1]), [3, 3, 3, 3]) == 0.0
+    r = np.random.default_rng(7)
+    for _ in range(200):
+        w = r.random(4)
+        mh, mh2 = sorted(r.random(2))[::-1]  # mh >= mh2: more omitted mass in the second
+        subs = list(r.random(3))
+        ent, loc = list(r.random(5)), list(r.random(5))
+        e1 = CV.predict_error(CV.error_features(mh, subs, [3, 3, 3], ent, loc), w)
+        e2 = CV.predict_error(CV.error_features(mh2, subs, [3, 3, 3], ent, loc), w)
+        assert e2 >= e1
+        e3 = CV.predict_error(CV.error_features(mh, subs, [3, 3, 3], [x + 0.1 for x in ent],
+                                                [x - 0.1 for x in loc]), w)
+        assert e3 >= e1
+        assert CV.predict_error(CV.error_features(mh, subs, [3, 3, 3], ent, loc), [0, 0, 0, 0]) == 0.0
