@@ -266,13 +266,17 @@ rs_status rs_route_layer_device(const rs_route_in *in, const rs_route_cfg *cfg,
  *    unit's `cand` field is ignored.
  *  - Grids are sized for every unit picking the family; surplus workgroups exit at once.
  *  - A unit whose choice lies outside [0, ncand) is not computed.
+ *  - `events` (optional, for measurement): five hipEvent_t.  events[0] is recorded on
+ *    `stream` after the planning kernel, then events[1..4] after the launches of the
+ *    dense, vertical-slash, block-sparse and A-shape families, in that order.  A family
+ *    absent from the grid records its event with no launch.
  * Limit: nunits <= 2048 (else RS_ERR_UNSUPPORTED). */
 size_t rs_routed_attn_workspace_size(const rs_qkv *qkv, const rs_unit *units, int32_t nunits);
 rs_status rs_routed_attn_prefill(const rs_qkv *qkv, const rs_unit *units, int32_t nunits,
                                  const rs_candidate *grid, int32_t ncand,
                                  const rs_index_set *idx, const int32_t *choice, void *o,
                                  int64_t so_h, int64_t so_t, float *lse, void *ws,
-                                 size_t ws_bytes, rs_stream stream);
+                                 size_t ws_bytes, void *const *events, rs_stream stream);
 
 /* ---- attention (Sec. 2.1; kernels of Sec. 3.1) ------------------------------------------
  * Every unit of one call must use the same candidate (one (pattern, budget) group).

@@ -129,7 +129,8 @@ def lib():
                                             P, C.c_size_t, P]
         L.rs_routed_attn_workspace_size.argtypes = [C.POINTER(RsQkv), C.POINTER(RsUnit), I32]
         L.rs_routed_attn_prefill.argtypes = [C.POINTER(RsQkv), C.POINTER(RsUnit), I32, C.POINTER(RsCandidate),
-                                             I32, C.POINTER(RsIndexSet), P, P, I64, I64, P, P, C.c_size_t, P]
+                                             I32, C.POINTER(RsIndexSet), P, P, I64, I64, P, P, C.c_size_t,
+                                             C.POINTER(P), P]
         for name in ("rs_probe", "rs_build_indices", "rs_route_layer", "rs_sparse_attn_prefill",
                      "rs_dense_attn_prefill", "rs_error_predict", "rs_route_layer_device",
                      "rs_routed_attn_prefill"):
@@ -410,9 +411,16 @@ def rs_routed_attn_workspace_size(qkv, units, nunits):
     return lib().rs_routed_attn_workspace_size(C.byref(qkv), units, nunits)
 
 
-def rs_routed_attn_prefill(qkv, units, nunits, grid, ncand, idx, choice, o, lse, ws, stream=None):
-    """choice: int32 device tensor [nunits]."""
+def rs_routed_attn_prefill(qkv, units, nunits, grid, ncand, idx, choice, o, lse, ws, events=None, stream=None):
+    """choice: int32 device tensor [nunits]; events: five torch.cuda.Event (timing enabled) or
+    None.  Each event is recorded once here first so that it exists."""
+    ev = None
+    if events is not None:
+        assert len(events) == 5
+        for e in events:
+            e.record()
+        ev = (P * 5)(*[C.c_void_p(e.cuda_event) for e in events])
     return _check(lib().rs_routed_attn_prefill(
         C.byref(qkv), units, nunits, grid, ncand, C.byref(idx.c) if idx is not None else None, _ptr(choice),
-        _ptr(o), o.stride(0), o.stride(1), _ptr(lse), _ptr(ws), ws.numel() if ws is not None else 0,
+        _ptr(o), o.stride(0), o.stride(1), _ptr(lse), _ptr(ws), ws.numel() if ws is not None else 0, ev,
         _stream(stream)))

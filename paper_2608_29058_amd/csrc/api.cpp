@@ -113,7 +113,7 @@ size_t routed_attn_ws_bytes(const rs_unit *units, int32_t nunits);
 rs_status routed_attn_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int32_t nunits,
                              const rs_candidate *grid, int32_t ncand, const rs_index_set *idx, const int32_t *choice,
                              void *o, int64_t so_h, int64_t so_t, float *lse, void *ws, size_t ws_bytes,
-                             hipStream_t st);
+                             void *const *events, hipStream_t st);
 
 static int cand_local_index(const rs_candidate *grid, int c) {
   int k = 0;
@@ -345,7 +345,8 @@ size_t rs_routed_attn_workspace_size(const rs_qkv *qkv, const rs_unit *units, in
 
 rs_status rs_routed_attn_prefill(const rs_qkv *qkv, const rs_unit *units, int32_t nunits, const rs_candidate *grid,
                                  int32_t ncand, const rs_index_set *idx, const int32_t *choice, void *o, int64_t so_h,
-                                 int64_t so_t, float *lse, void *ws, size_t ws_bytes, rs_stream stream) {
+                                 int64_t so_t, float *lse, void *ws, size_t ws_bytes, void *const *events,
+                                 rs_stream stream) {
   g_err.clear();
   float scale;
   rs_status st;
@@ -355,6 +356,9 @@ rs_status rs_routed_attn_prefill(const rs_qkv *qkv, const rs_unit *units, int32_
   if ((st = check_out(o, so_h, so_t, qkv->d)) != RS_OK) return st;
   if (nunits == 0) return RS_OK;
   if (!choice) return fail(RS_ERR_INVALID_ARG, "choice is NULL");
+  if (events)
+    for (int k = 0; k < 5; ++k)
+      if (!events[k]) return fail(RS_ERR_INVALID_ARG, "events must hold five events");
   bool vs = false, bs = false;
   for (int c = 0; c < ncand; ++c) {
     vs = vs || grid[c].fam == RS_VSLASH;
@@ -384,7 +388,7 @@ rs_status rs_routed_attn_prefill(const rs_qkv *qkv, const rs_unit *units, int32_
       return fail(RS_ERR_INVALID_ARG, "index set does not match the grid");
   }
   return routed_attn_launch(qkv, scale, units, nunits, grid, ncand, idx, choice, o, so_h, so_t, lse, ws, ws_bytes,
-                            (hipStream_t)stream);
+                            events, (hipStream_t)stream);
 }
 
 }  // extern "C"

@@ -254,11 +254,18 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
     // (block-sparse) of each row, fetched together with the K copy of the tile they serve
     struct Pref {
       Win3 wd[2][kPrefVs];
+      uint64_t mv[kPrefVs];  // column bits of the tile's keys
       uint32_t bw[2][kPrefBs];
     };
     auto fetch = [&](int k0, Pref &f) {
       if constexpr (MODE == M_COVER) {
         const int kt = k0 >> 6;
+#pragma unroll
+        for (int k = 0; k < kPrefVs; ++k) {
+          f.mv[k] = 0ull;
+          if (k < a.nvs_pref && u >= 0)
+            f.mv[k] = bits64_at(a.vs_vbits + ((long long)u * a.ncand_vs + a.vs_pref_cl[k]) * a.nwords, a.nwords, k0);
+        }
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
           const bool ok = u >= 0 && row[s] >= 0;
@@ -399,8 +406,8 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
           for (int k = 0; k < kPrefVs; ++k) {
             if (k >= a.nvs_pref) break;
             const uint64_t md = __builtin_bitreverse64(win_bits(f.wd[s][k], i - k0 - 63));
-            const uint64_t mv = bits64_at(a.vs_vbits + ((long long)u * a.ncand_vs + a.vs_pref_cl[k]) * a.nwords, a.nwords, k0);
-            covv[s][k] += masked((md | mv) >> (4 * hh));
+            const uint64_t m = (md | f.mv[k]) >> (4 * hh);
+            if (__ballot(m != 0ull) != 0ull) covv[s][k] += masked(m);  // wave-uniform skip
           }
 #pragma unroll
           for (int k = 0; k < kPrefBs; ++k) {
@@ -660,9 +667,11 @@ __global__ void __launch_bounds__(256) block_pool_kernel(const InT *x, long long
   }
 }
 
-// L[h][bq][bk] = qbar . kbar * scale for bk <= bq; 64 x 64 output tiles, fp32 FMA.
+// L[h][bq][bk] = qbar . kbar * scale for bk <= bq; 128 x 128 output tiles, each thread an
+// 8 x 8 block, fp32 FMA over the head dimension in order (d a multiple of 32).
 __global__ void __launch_bounds__(256) block_logits_kernel(const float *qbar, const float *kbar, int nb, int d,
                                                            int group, float scale, float *lbs) {
+  constexpr int TB = 128, KC = 32, LD = TB + 4;
   const int h = blockIdx.y;
   // decode lower-triangular tile index
   int tq = 0;
@@ -672,39 +681,43 @@ __global__ void __launch_bounds__(256) block_logits_kernel(const float *qbar, co
     ++tq;
   }
   const int tk = t;
-  const int nbt = (nb + 63) / 64;
-  if (tq >= nbt) return;
-  __shared__ float sq[32][65], sk[32][65];
+  __shared__ __align__(16) float sq[KC][LD], sk[KC][LD];
   const int tid = threadIdx.x;
-  const int tx = tid % 16, ty = tid / 16;  // each thread: rows ty*4.., cols tx*4..
-  float acc[4][4] = {};
+  const int tx = tid % 16, ty = tid / 16;  // each thread: rows ty*8.., cols tx*8..
+  float acc[8][8] = {};
   const float *qb = qbar + (long long)h * nb * d;
   const float *kb = kbar + (long long)(h / group) * nb * d;
-  for (int d0 = 0; d0 < d; d0 += 32) {
-    for (int x = tid; x < 64 * 32; x += 256) {
-      const int r = x / 32, cc = x % 32;
-      const int bq = tq * 64 + r, bk = tk * 64 + r;
+  for (int d0 = 0; d0 < d; d0 += KC) {
+    for (int x = tid; x < TB * KC; x += 256) {
+      const int r = x / KC, cc = x % KC;
+      const int bq = tq * TB + r, bk = tk * TB + r;
       sq[cc][r] = bq < nb ? qb[(long long)bq * d + d0 + cc] : 0.f;
       sk[cc][r] = bk < nb ? kb[(long long)bk * d + d0 + cc] : 0.f;
     }
     __syncthreads();
-    for (int cc = 0; cc < 32; ++cc) {
-      float qa[4], ka[4];
-      for (int i = 0; i < 4; ++i) qa[i] = sq[cc][ty * 4 + i];
-      for (int j = 0; j < 4; ++j) ka[j] = sk[cc][tx * 4 + j];
-      for (int i = 0; i < 4; ++i)
-        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(qa[i], ka[j], acc[i][j]);
+#pragma unroll 4
+    for (int cc = 0; cc < KC; ++cc) {
+      const f32x4 q0 = *(const f32x4 *)&sq[cc][ty * 8], q1 = *(const f32x4 *)&sq[cc][ty * 8 + 4];
+      const f32x4 k0 = *(const f32x4 *)&sk[cc][tx * 8], k1 = *(const f32x4 *)&sk[cc][tx * 8 + 4];
+      const float qa[8] = {q0[0], q0[1], q0[2], q0[3], q1[0], q1[1], q1[2], q1[3]};
+      const float ka[8] = {k0[0], k0[1], k0[2], k0[3], k1[0], k1[1], k1[2], k1[3]};
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[i][j] = fmaf(qa[i], ka[j], acc[i][j]);
     }
     __syncthreads();
   }
   float *lh = lbs + (long long)h * ((long long)nb * (nb + 1) / 2);
-  for (int i = 0; i < 4; ++i) {
-    const int bq = tq * 64 + ty * 4 + i;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int bq = tq * TB + ty * 8 + i;
     if (bq >= nb) continue;
-    for (int j = 0; j < 4; ++j) {
-      const int bk = tk * 64 + tx * 4 + j;
-      if (bk > bq) continue;
-      lh[(long long)bq * (bq + 1) / 2 + bk] = acc[i][j] * scale;
+    float *row = lh + (long long)bq * (bq + 1) / 2;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int bk = tk * TB + tx * 8 + j;
+      if (bk <= bq) row[bk] = acc[i][j] * scale;
     }
   }
 }
@@ -908,7 +921,7 @@ rs_status probe_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int
       hipLaunchKernelGGL(block_pool_kernel<float>, dim3(nb, qkv->hkv), dim3(256), 0, st, (const float *)qkv->k,
                          (long long)qkv->sk_h, (long long)qkv->sk_t, qkv->n, qkv->d, kbar);
     }
-    const int nbt = (nb + 63) / 64;
+    const int nbt = (nb + 127) / 128;
     hipLaunchKernelGGL(block_logits_kernel, dim3(nbt * (nbt + 1) / 2, qkv->hq), dim3(256), 0, st, qbar, kbar, nb,
                        qkv->d, qkv->hq / qkv->hkv, scale, out->lbs);
     RS_HIP(hipGetLastError());

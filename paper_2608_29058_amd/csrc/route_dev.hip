@@ -111,7 +111,8 @@ __global__ void __launch_bounds__(1024) route_kernel(const RouteArgs a) {
   __shared__ double sKey[kRouteMaxMoves];  // sort keys; later the per-unit times of a total
   __shared__ int sId[kRouteMaxMoves];
   __shared__ double sTot;
-  __shared__ int sFb, sCnt[kMaxCandR], sStart[kMaxCandR + 1];
+  __shared__ int sPlen[kRouteMaxUnits];
+  __shared__ int sFb, sNvalid, sCnt[kMaxCandR], sStart[kMaxCandR + 1];
 
   // latency, risk and lower mass per (unit, candidate)
   for (int i = tid; i < U * C; i += NT) {
@@ -181,6 +182,7 @@ __global__ void __launch_bounds__(1024) route_kernel(const RouteArgs a) {
       cur = bc;
     }
     a.plen[u] = len;
+    sPlen[u] = len;
     for (int j = len; j < W; ++j) {
       sKey[u * W + j] = INFINITY;
       sId[u * W + j] = 0x7fffffff;
@@ -211,13 +213,17 @@ __global__ void __launch_bounds__(1024) route_kernel(const RouteArgs a) {
       }
       __syncthreads();
     }
-  int nvalid = 0;
   for (int i = tid; i < Mp; i += NT) {
     const int id = sId[i];
     if (id != 0x7fffffff) a.rank[id] = i;
   }
-  for (int u = 0; u < U; ++u) nvalid += a.plen[u];  // same value in every thread
+  if (tid == 0) {
+    int nv = 0;
+    for (int u = 0; u < U; ++u) nv += sPlen[u];
+    sNvalid = nv;
+  }
   __syncthreads();
+  const int nvalid = sNvalid;
 
   // unit-order total after the first k moves of the merged order
   double *sTu = sKey;
@@ -225,7 +231,7 @@ __global__ void __launch_bounds__(1024) route_kernel(const RouteArgs a) {
     __syncthreads();
     for (int u = tid; u < U; u += NT) {
       int cnt = 0;
-      for (int j = 0; j < a.plen[u]; ++j) cnt += a.rank[u * W + j] < k;
+      for (int j = 0; j < sPlen[u]; ++j) cnt += a.rank[u * W + j] < k;
       const int ch = cnt == 0 ? a.dense_c : a.path[u * W + cnt - 1];
       sTu[u] = a.t[(long long)u * C + ch];
     }
@@ -259,7 +265,7 @@ __global__ void __launch_bounds__(1024) route_kernel(const RouteArgs a) {
   // the solve's choice, then expand or fall back
   for (int u = tid; u < U; u += NT) {
     int cnt = 0;
-    for (int j = 0; j < a.plen[u]; ++j) cnt += a.rank[u * W + j] < kstar;
+    for (int j = 0; j < sPlen[u]; ++j) cnt += a.rank[u * W + j] < kstar;
     int ch = cnt == 0 ? a.dense_c : a.path[u * W + cnt - 1];
     const double *ml = a.m_lower + (long long)u * C;
     if (a.fam[ch] != RS_DENSE && !(ml[ch] >= a.tau)) {
@@ -289,17 +295,19 @@ __global__ void __launch_bounds__(1024) route_kernel(const RouteArgs a) {
       ch = pick;
     }
     a.choice[u] = ch;
+    sId[u] = ch;                                   // the choice, for the serial loops below
+    sKey[u] = a.t[(long long)u * C + ch];          // its time
+    sKey[kRouteMaxUnits + u] = a.risk[(long long)u * C + ch];  // its risk
   }
   for (int c = tid; c < C; c += NT) sCnt[c] = 0;
   __syncthreads();
-  for (int u = tid; u < U; u += NT) atomicAdd(&sCnt[a.choice[u]], 1);
+  for (int u = tid; u < U; u += NT) atomicAdd(&sCnt[sId[u]], 1);
   __syncthreads();
   if (tid == 0) {
     double tot = a.t_probe, rsum = 0.0;
     for (int u = 0; u < U; ++u) {
-      const int ch = a.choice[u];
-      tot = tot + a.t[(long long)u * C + ch];
-      rsum = rsum + a.risk[(long long)u * C + ch];
+      tot = tot + sKey[u];
+      rsum = rsum + sKey[kRouteMaxUnits + u];
     }
     int ng = 0, pos = 0;
     for (int c = 0; c < C; ++c) {
@@ -324,7 +332,7 @@ __global__ void __launch_bounds__(1024) route_kernel(const RouteArgs a) {
   for (int c = tid; c < C; c += NT) {
     int pos = sStart[c];
     for (int u = 0; u < U; ++u)
-      if (a.choice[u] == c) a.group_units[pos++] = u;
+      if (sId[u] == c) a.group_units[pos++] = u;
   }
 }
 
@@ -345,18 +353,27 @@ __global__ void __launch_bounds__(1024) plan_kernel(const PlanArgs a) {
   __shared__ int sLu2u[kRouteMaxUnits];   // local unit -> unit
   __shared__ int sOff[kRouteMaxUnits + 1];  // local unit -> first flat item
   __shared__ int sBl[kRouteMaxUnits];     // units of each bucket, ascending
+  __shared__ int sK0[kRouteMaxUnits], sK1[kRouteMaxUnits];  // first and last query tile of a unit
+  __shared__ int sBk[kRouteMaxUnits];     // bucket of a unit, -1 when routed to another family
   __shared__ int sBs[9], sSize[8], sNl;
   const int U = a.U, bm = a.bm;
+  // per unit, in parallel: tiles, bucket and whether the unit is routed to this family
+  for (int u = tid; u < U; u += NT) {
+    const rs_unit un = a.units[u];
+    const int c = a.choice[u];
+    sK0[u] = un.s0 / bm;
+    sK1[u] = (un.s1 - 1) / bm;
+    sBk[u] = (c >= 0 && c < a.C && a.fam[c] == f) ? (un.head / a.group) & 7 : -1;
+  }
+  __syncthreads();
   if (tid == 0) {
     int nl = 0, cntb[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     for (int b = 0; b < 8; ++b) sSize[b] = 0;
     sOff[0] = 0;
     for (int u = 0; u < U; ++u) {
-      const int c = a.choice[u];
-      if (c < 0 || c >= a.C || a.fam[c] != f) continue;
-      const rs_unit &un = a.units[u];
-      const int nt = (un.s1 - 1) / bm - un.s0 / bm + 1;
-      const int b = (un.head / a.group) & 7;
+      const int b = sBk[u];
+      if (b < 0) continue;
+      const int nt = sK1[u] - sK0[u] + 1;
       sLu2u[nl] = u;
       sOff[nl + 1] = sOff[nl] + nt;
       sSize[b] += nt;
@@ -369,8 +386,7 @@ __global__ void __launch_bounds__(1024) plan_kernel(const PlanArgs a) {
     for (int b = 0; b < 8; ++b) fill[b] = sBs[b];
     for (int l = 0; l < nl; ++l) {
       const int u = sLu2u[l];
-      const int b = (a.units[u].head / a.group) & 7;
-      sBl[fill[b]++] = u;
+      sBl[fill[sBk[u]]++] = u;
     }
     sNl = nl;
     int off = 0;
@@ -400,15 +416,13 @@ __global__ void __launch_bounds__(1024) plan_kernel(const PlanArgs a) {
       else hi = mid - 1;
     }
     const int u = sLu2u[lo], t = i - sOff[lo];
-    const rs_unit &un = a.units[u];
-    const int key = un.s0 / bm + t;
-    const int b = (un.head / a.group) & 7;
+    const int key = sK0[u] + t;
+    const int b = sBk[u];
     // rank in the bucket: longer query tiles (larger key) first, then units ascending
     int r = 0;
     for (int x = sBs[b]; x < sBs[b + 1]; ++x) {
       const int v = sBl[x];
-      const rs_unit &w = a.units[v];
-      const int k0 = w.s0 / bm, k1 = (w.s1 - 1) / bm;
+      const int k0 = sK0[v], k1 = sK1[v];
       r += max(0, k1 - max(key + 1, k0) + 1);
       r += (v < u && k0 <= key && key <= k1) ? 1 : 0;
     }
@@ -512,7 +526,7 @@ size_t routed_attn_ws_bytes(const rs_unit *units, int32_t nunits) {
 rs_status routed_attn_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int32_t nunits,
                              const rs_candidate *grid, int32_t ncand, const rs_index_set *idx, const int32_t *choice,
                              void *o, int64_t so_h, int64_t so_t, float *lse, void *ws, size_t ws_bytes,
-                             hipStream_t st) {
+                             void *const *events, hipStream_t st) {
   if (nunits == 0) return RS_OK;
   if (nunits > kRouteMaxUnits) return fail(RS_ERR_UNSUPPORTED, "routed attention supports nunits <= 2048");
   const size_t need = routed_attn_ws_bytes(units, nunits);
@@ -555,13 +569,16 @@ rs_status routed_attn_launch(const rs_qkv *qkv, float scale, const rs_unit *unit
   const int nblocks = std::min(((2 * ncu + 7) / 8) * 8, ((items + 7) / 8) * 8);
   // dense first: its tiles are the longest
   const int fam_order[4] = {RS_DENSE, RS_VSLASH, RS_BSPARSE, RS_ASHAPE};
+  if (events) RS_HIP(hipEventRecord((hipEvent_t)events[0], st));
   for (int k = 0; k < 4; ++k) {
     const int f = fam_order[k];
-    if (!present[f]) continue;
-    const AttnQueues qs{p.qsize + 8 * f, p.qoff + 8 * f, p.qcount + 8 * f};
-    rs_status s = attn_launch_list(qkv, scale, f, idx, p.dunits + (size_t)f * nunits, p.order + (size_t)f * items,
-                                   &qs, nblocks, o, so_h, so_t, lse, st);
-    if (s != RS_OK) return s;
+    if (present[f]) {
+      const AttnQueues qs{p.qsize + 8 * f, p.qoff + 8 * f, p.qcount + 8 * f};
+      rs_status s = attn_launch_list(qkv, scale, f, idx, p.dunits + (size_t)f * nunits,
+                                     p.order + (size_t)f * items, &qs, nblocks, o, so_h, so_t, lse, st);
+      if (s != RS_OK) return s;
+    }
+    if (events) RS_HIP(hipEventRecord((hipEvent_t)events[1 + k], st));
   }
   return RS_OK;
 }

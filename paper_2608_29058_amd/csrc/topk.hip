@@ -160,36 +160,67 @@ struct VsArgs {
   uint32_t *vbits, *dbits;
 };
 
-// grid: (2 * ncand_vs, nunits); blockIdx.x = array * ncand_vs + candidate (array 0: V, 1: D)
+// grid: (2, nunits); blockIdx.x = array (0: V from col, 1: D from diag).  Budgets of the family
+// are nested prefixes of one ranking, so the largest budget is selected from the whole array
+// and every smaller one from the largest set (gathered, in ascending position, into LDS).
+constexpr int kVsGather = 8192;  // elements of the largest set kept in LDS
 __global__ void __launch_bounds__(1024) vs_select_kernel(const VsArgs a) {
   constexpr int NT = 1024;
   extern __shared__ uint32_t sBits[];  // nwords
   __shared__ int sHist[256], sBcast[2], sWave[NT / 64];
-  const int arr = blockIdx.x / a.ncand_vs, cl = blockIdx.x % a.ncand_vs;
+  __shared__ float sVal[kVsGather];
+  __shared__ int sPos[kVsGather];
+  const int arr = blockIdx.x;
   const int u = blockIdx.y;
   const int s1 = a.s1[u];
-  for (int w = threadIdx.x; w < a.nwords; w += NT) sBits[w] = 0u;
-  __syncthreads();
-  const long long row = (long long)u * a.ncand_vs + cl;
-  if (arr == 0) {
-    const float *vals = a.col + (long long)u * a.n;
-    select_top<NT>(vals, s1, a.nv[cl], sHist, sBcast, sWave,
-                   [&](int i) { atomicOr(&sBits[i >> 5], 1u << (i & 31)); });
-  } else {
-    const float *vals = a.diag + (long long)u * a.n + 1;  // diagonal 0 is forced
-    const int ns = a.ns[cl];
-    if (ns >= 1 && threadIdx.x == 0) atomicOr(&sBits[0], 1u);
-    select_top<NT>(vals, s1 - 1, ns - 1, sHist, sBcast, sWave, [&](int i) {
-      const int t = i + 1;
-      atomicOr(&sBits[t >> 5], 1u << (t & 31));
-    });
+  // the array and its offset: D selects diagonals [1, s1) and forces diagonal 0
+  const float *vals = arr == 0 ? a.col + (long long)u * a.n : a.diag + (long long)u * a.n + 1;
+  const int len = arr == 0 ? s1 : s1 - 1, off = arr == 0 ? 0 : 1;
+  auto budget = [&](int c) { return arr == 0 ? a.nv[c] : a.ns[c] - 1; };  // selected from vals
+  int cmax = 0;
+  for (int c = 1; c < a.ncand_vs; ++c)
+    if (budget(c) > budget(cmax)) cmax = c;
+  const int kmax = budget(cmax);
+  // largest set: bitmap, then its members in ascending position with their values (when it
+  // fits in LDS; otherwise every budget is selected from the whole array)
+  const bool gather = kmax <= kVsGather;
+  int nmax = 0;
+  if (gather) {
+    for (int w = threadIdx.x; w < a.nwords; w += NT) sBits[w] = 0u;
+    __syncthreads();
+    select_top<NT>(vals, len, kmax, sHist, sBcast, sWave,
+                   [&](int i) { atomicOr(&sBits[(i + off) >> 5], 1u << ((i + off) & 31)); });
+    __syncthreads();
+    nmax = bits_to_list<NT>(sBits, a.nwords, sPos, kVsGather, sWave);
+    __syncthreads();
+    for (int x = threadIdx.x; x < nmax; x += NT) sVal[x] = vals[sPos[x] - off];
+    __syncthreads();
   }
-  __syncthreads();
-  uint32_t *gb = (arr == 0 ? a.vbits : a.dbits) + row * a.nwords;
-  for (int w = threadIdx.x; w < a.nwords; w += NT) gb[w] = sBits[w];
-  int *list = arr == 0 ? a.vsorted + row * a.nv_max : a.dsorted + row * a.ns_max;
-  const int cnt = bits_to_list<NT>(sBits, a.nwords, list, arr == 0 ? a.nv_max : a.ns_max, sWave);
-  if (threadIdx.x == 0) a.count[row * 2 + arr] = cnt;
+  for (int c = 0; c < a.ncand_vs; ++c) {
+    const long long row = (long long)u * a.ncand_vs + c;
+    for (int w = threadIdx.x; w < a.nwords; w += NT) sBits[w] = 0u;
+    __syncthreads();
+    if (!gather) {
+      select_top<NT>(vals, len, budget(c), sHist, sBcast, sWave,
+                     [&](int i) { atomicOr(&sBits[(i + off) >> 5], 1u << ((i + off) & 31)); });
+    } else if (c == cmax) {
+      for (int x = threadIdx.x; x < nmax; x += NT) atomicOr(&sBits[sPos[x] >> 5], 1u << (sPos[x] & 31));
+    } else {
+      select_top<NT>(sVal, nmax, budget(c), sHist, sBcast, sWave, [&](int x) {
+        const int t = sPos[x];
+        atomicOr(&sBits[t >> 5], 1u << (t & 31));
+      });
+    }
+    __syncthreads();
+    if (arr == 1 && a.ns[c] >= 1 && threadIdx.x == 0) atomicOr(&sBits[0], 1u);  // diagonal 0
+    __syncthreads();
+    uint32_t *gb = (arr == 0 ? a.vbits : a.dbits) + row * a.nwords;
+    for (int w = threadIdx.x; w < a.nwords; w += NT) gb[w] = sBits[w];
+    int *list = arr == 0 ? a.vsorted + row * a.nv_max : a.dsorted + row * a.ns_max;
+    const int cnt = bits_to_list<NT>(sBits, a.nwords, list, arr == 0 ? a.nv_max : a.ns_max, sWave);
+    if (threadIdx.x == 0) a.count[row * 2 + arr] = cnt;
+    __syncthreads();
+  }
 }
 
 struct BsArgs {
@@ -287,7 +318,7 @@ rs_status build_indices_launch(const rs_probe_out *sc, const rs_unit *units, int
     va.vsorted = out->vs_vsorted; va.dsorted = out->vs_dsorted; va.count = out->vs_count;
     va.vbits = out->vs_vbits; va.dbits = out->vs_dbits;
     const size_t lds = (size_t)out->nwords * sizeof(uint32_t);
-    hipLaunchKernelGGL(vs_select_kernel, dim3(2 * nvs, nunits), dim3(1024), lds, st, va);
+    hipLaunchKernelGGL(vs_select_kernel, dim3(2, nunits), dim3(1024), lds, st, va);
     RS_HIP(hipGetLastError());
   }
   if (nbs > 0) {

@@ -121,12 +121,13 @@ class RoutedLayer:
         _rs.rs_route_layer_device(self.rb, self.pb.cov, self.pb.nsub, self.t_probe_us, k.T_layer_us, k.tau, k.alpha,
                                   k.beta, k.delta_q, e=self.e if self._use_e() else None)
 
-    def run_routed(self, qkv, lse=None):
-        """All units with the device route's choices: one rs_routed_attn_prefill call."""
+    def run_routed(self, qkv, lse=None, family_events=None):
+        """All units with the device route's choices: one rs_routed_attn_prefill call
+        (``family_events``: five timing events around its per-family launches)."""
         if self._ws_routed is None:
             self._ws_routed = _rs.workspace(_rs.rs_routed_attn_workspace_size(qkv, self.units, self.nunits))
         _rs.rs_routed_attn_prefill(qkv, self.units, self.nunits, self.g, self.ncand, self.ib, self.rb.choice,
-                                   self.o, lse, self._ws_routed)
+                                   self.o, lse, self._ws_routed, events=family_events)
 
     def group_units(self, cand, unit_idx):
         return _rs.make_units([(self.unit_list[u][0], self.unit_list[u][1], self.unit_list[u][2], cand, u)
@@ -140,7 +141,8 @@ class RoutedLayer:
         else:
             _rs.rs_sparse_attn_prefill(qkv, us, len(unit_idx), self.g, self.ncand, self.ib, self.o, lse, ws)
 
-    def run(self, q, k, v, events=None, lse=None, per_unit=False, fixed_route=None, device_route=False):
+    def run(self, q, k, v, events=None, lse=None, per_unit=False, fixed_route=None, device_route=False,
+            family_events=None):
         """One routed layer; returns the route (None with ``device_route``: it stays on the
         device, in self.rb).  ``events`` (optional) is a callable ``mark(name)`` used to record
         stream events between phases; ``lse`` (optional, float32 [hq, n]) receives the
@@ -148,7 +150,7 @@ class RoutedLayer:
         launch per (pattern, budget) group; ``fixed_route`` (a route returned earlier) replaces
         the input-conditional routing decision while the index sets are still built from this
         input; ``device_route`` routes on the device and launches the attention from that route
-        with no host synchronisation."""
+        with no host synchronisation (``family_events``: see run_routed)."""
         qkv = self.qkv(q, k, v)
         mark = events or (lambda name: None)
         mark("start")
@@ -157,7 +159,7 @@ class RoutedLayer:
         if device_route:
             self.route_device()
             mark("route")
-            self.run_routed(qkv, lse)
+            self.run_routed(qkv, lse, family_events)
             mark("attention")
             return None
         route = self.route() if fixed_route is None else fixed_route

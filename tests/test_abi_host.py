@@ -232,8 +232,8 @@ def test_device_routing_entries_reject_bad_arguments_without_launch():
                   sk_h=256 * 128, sk_t=128, sv_h=256 * 128, sv_t=128)
     units = _rs.make_units([(0, 0, 256), (1, 0, 256)])
     st = L.rs_routed_attn_prefill(C.byref(q), units, 2, grid, len(GRID), None, None, C.c_void_p(16), 256 * 128, 128,
-                                  None, C.c_void_p(16), 1 << 20, None)
+                                  None, C.c_void_p(16), 1 << 20, None, None)
     assert st == _rs.RS_ERR_INVALID_ARG
     st = L.rs_routed_attn_prefill(C.byref(q), units, 2, grid, len(GRID), None, C.c_void_p(16), C.c_void_p(16),
-                                  256 * 128, 128, None, C.c_void_p(16), 1 << 20, None)
+                                  256 * 128, 128, None, C.c_void_p(16), 1 << 20, None, None)
     assert st == _rs.RS_ERR_INVALID_ARG and b"index set" in L.rs_last_error()

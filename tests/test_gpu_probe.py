@@ -91,7 +91,8 @@ def test_indices_bit_exact_on_gpu_scores(tie):
     units = [(0, 0, n), (1, 0, n), (1, 700, 2000)]
     res = _probe(q, k, v, units, (64, 8, 8), _rs.RS_PROBE_ROWS | _rs.RS_PROBE_BLOCKMEAN)
     pb = res["pb"]
-    grid = [(_rs.RS_DENSE, 0, 0), (_rs.RS_VSLASH, 30, 100), (_rs.RS_VSLASH, 64, 256),
+    # three nested vertical-slash budgets: the smaller two are selected from the largest set
+    grid = [(_rs.RS_DENSE, 0, 0), (_rs.RS_VSLASH, 30, 100), (_rs.RS_VSLASH, 64, 256), (_rs.RS_VSLASH, 400, 1500),
             (_rs.RS_BSPARSE, 3, 64), (_rs.RS_BSPARSE, 9, 64)]
     g = _rs.make_grid(grid)
     ib = _rs.IndexBuffers(len(units), n, hq, grid)
@@ -102,7 +103,7 @@ def test_indices_bit_exact_on_gpu_scores(tie):
     nw = (n + 31) // 32
     from gpu_helpers import words_of
     for ui, (h, s0, s1) in enumerate(units):
-        for cl, (_, nv, ns) in enumerate(grid[1:3]):
+        for cl, (_, nv, ns) in enumerate(grid[1:4]):
             Vr, Dr, _, _ = IX.vs_indices(col[ui], diag[ui], s1, nv, ns)
             V, D, Vpad, Dpad = _gpu_vs_sets(ib, ui, cl)
             assert np.array_equal(V, Vr) and np.array_equal(D, Dr), (ui, cl)
@@ -118,7 +119,7 @@ def test_indices_bit_exact_on_gpu_scores(tie):
             L[bq, :bq + 1] = lbs[h, off:off + bq + 1]
             off += bq + 1
         rank_g = ib.bs_rank[h].cpu().numpy()
-        for cl, (_, kk, _) in enumerate(grid[3:]):
+        for cl, (_, kk, _) in enumerate(grid[4:]):
             sel, ranks = IX.bs_indices(L, kk)
             srt = ib.bs_sorted[h, cl].cpu().numpy()
             cnt = ib.bs_count[h, cl].cpu().numpy()
