@@ -29,7 +29,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "prefill attn ms/layer at 128K, GQA 32/8 d128 bf16; x vs dense; MFMA util"
 N, HQ, HKV, D, SEG = 131072, 32, 8, 128, 16384
-GRID = [(0, 0, 0), (1, 128, 1024), (1, 128, 4096), (2, 500, 256), (2, 1000, 2048), (2, 2000, 6096),
+GRID = [(0, 0, 0), (1, 128, 1024), (1, 128, 4096), (2, 500, 256), (2, 1000, 512), (2, 2000, 2048),
         (3, 50, 64), (3, 100, 64), (3, 200, 64)]
 FAM_NAME = {0: "dense", 1: "ashape", 2: "vslash", 3: "bsparse"}
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA

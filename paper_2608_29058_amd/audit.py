@@ -46,9 +46,9 @@ from .pipeline import RoutedLayer, RouteKnobs
 
 EPS = 1e-12
 N, HQ, HKV, D, SEG = 131072, 32, 8, 128, 16384
-GRID = [(0, 0, 0), (1, 128, 1024), (1, 128, 4096), (2, 500, 256), (2, 1000, 2048), (2, 2000, 6096),
+GRID = [(0, 0, 0), (1, 128, 1024), (1, 128, 4096), (2, 500, 256), (2, 1000, 512), (2, 2000, 2048),
         (3, 50, 64), (3, 100, 64), (3, 200, 64)]
-ONE_BUDGET = [0, 2, 4, 7]          # one budget per family: dense, A-shape 4096, VS 1000/2048, BS 100
+ONE_BUDGET = [0, 2, 4, 7]          # one budget per family: dense, A-shape 4096, VS 1000/512, BS 100
 
 
 def bf16_allowance(vmax, o_norm, or_norm):
