@@ -346,14 +346,17 @@ def main():
     fam_flops = {f: 0.0 for f in FAM_NAME}
     fam_issued = {f: 0.0 for f in FAM_NAME}
     fam_launches = {f: 0 for f in FAM_NAME}
-    ph = {"probe_index_coverage": 0.0, "route": 0.0, "attention": 0.0}
+    ph = {"transpose_v": 0.0, "probe_index_coverage": 0.0, "route": 0.0, "attention": 0.0}
     # timed per-family launch time (device routing: one persistent launch per family and layer)
     fam_time_timed = {f: 0.0 for f in FAM_NAME}
     for li, marks, fev in records:
         evs = [m[1] for m in marks]
-        ph["probe_index_coverage"] += evs[0].elapsed_time(evs[1])
-        ph["route"] += evs[1].elapsed_time(evs[2])
-        ph["attention"] += evs[2].elapsed_time(evs[-1])
+        at = {m[0]: m[1] for m in marks}
+        t0_probe = at.get("transpose_v", at["start"])
+        ph["transpose_v"] += at["start"].elapsed_time(t0_probe) if "transpose_v" in at else 0.0
+        ph["probe_index_coverage"] += t0_probe.elapsed_time(at["probe"])
+        ph["route"] += at["probe"].elapsed_time(at["route"])
+        ph["attention"] += at["route"].elapsed_time(evs[-1])
         if fev is not None:
             for k, f in enumerate((0, 2, 3, 1)):
                 fam_time_timed[f] += fev[k].elapsed_time(fev[k + 1])

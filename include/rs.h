@@ -67,6 +67,9 @@ typedef struct rs_qkv {
   int64_t sv_h, sv_t;
   float scale;               /* logit scale; 0 => 1/sqrt(d) */
   int32_t _pad1;
+  const void *vt;            /* optional (device): V in the transposed layout written by
+                                rs_transpose_v, or NULL.  When set, the dense, A-shape and
+                                block-sparse kernels read it in place of v. */
 } rs_qkv;
 
 /* One unit: rows [s0, s1) of query head `head`; `cand` indexes the candidate grid.
@@ -277,6 +280,16 @@ rs_status rs_routed_attn_prefill(const rs_qkv *qkv, const rs_unit *units, int32_
                                  const rs_index_set *idx, const int32_t *choice, void *o,
                                  int64_t so_h, int64_t so_t, float *lse, void *ws,
                                  size_t ws_bytes, void *const *events, rs_stream stream);
+
+/* ---- transposed V (an operand layout for the attention kernels) -------------------------
+ * Writes V of the layer into `vt` (device, bf16, rs_vt_bytes(qkv) bytes) as
+ * [hkv][d][npad] with npad = n rounded up to 64.  Within each group of 16 consecutive keys
+ * 16g + j, position j of a row holds key 16g + perm[j], perm = {0,1,2,3, 8,9,10,11,
+ * 4,5,6,7, 12,13,14,15}; keys >= n are zero.  fp32 V is rounded to bf16 (as on load).
+ * Point qkv->vt at the result: the P V products then read V^T fragments with plain 16-byte
+ * LDS reads instead of transposing loads.  Must be redone when V changes. */
+size_t rs_vt_bytes(const rs_qkv *qkv);
+rs_status rs_transpose_v(const rs_qkv *qkv, void *vt, rs_stream stream);
 
 /* ---- attention (Sec. 2.1; kernels of Sec. 3.1) ------------------------------------------
  * Every unit of one call must use the same candidate (one (pattern, budget) group).

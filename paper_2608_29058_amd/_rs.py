@@ -22,7 +22,8 @@ EXPORTS = ["rs_probe_workspace_size", "rs_probe", "rs_build_indices_workspace_si
            "rs_build_indices", "rs_route_layer", "rs_attn_workspace_size",
            "rs_sparse_attn_prefill", "rs_dense_attn_prefill", "rs_error_predict",
            "rs_route_layer_device_workspace_size", "rs_route_layer_device",
-           "rs_routed_attn_workspace_size", "rs_routed_attn_prefill", "rs_last_error", "rs_version"]
+           "rs_routed_attn_workspace_size", "rs_routed_attn_prefill", "rs_vt_bytes", "rs_transpose_v",
+           "rs_last_error", "rs_version"]
 
 P = C.c_void_p
 I32 = C.c_int32
@@ -33,7 +34,7 @@ class RsQkv(C.Structure):
     _fields_ = [("q", P), ("k", P), ("v", P), ("dtype", I32), ("n", I32), ("hq", I32),
                 ("hkv", I32), ("d", I32), ("_pad0", I32), ("sq_h", I64), ("sq_t", I64),
                 ("sk_h", I64), ("sk_t", I64), ("sv_h", I64), ("sv_t", I64),
-                ("scale", C.c_float), ("_pad1", I32)]
+                ("scale", C.c_float), ("_pad1", I32), ("vt", P)]
 
 
 class RsUnit(C.Structure):
@@ -107,8 +108,10 @@ def lib():
         L.rs_version.restype = C.c_char_p
         for name in ("rs_probe_workspace_size", "rs_build_indices_workspace_size",
                      "rs_attn_workspace_size", "rs_route_layer_device_workspace_size",
-                     "rs_routed_attn_workspace_size"):
+                     "rs_routed_attn_workspace_size", "rs_vt_bytes"):
             getattr(L, name).restype = C.c_size_t
+        L.rs_vt_bytes.argtypes = [C.POINTER(RsQkv)]
+        L.rs_transpose_v.argtypes = [C.POINTER(RsQkv), P, P]
         L.rs_probe_workspace_size.argtypes = [C.POINTER(RsQkv), C.POINTER(RsUnit), I32, C.POINTER(RsProbeCfg)]
         L.rs_probe.argtypes = [C.POINTER(RsQkv), C.POINTER(RsUnit), I32, C.POINTER(RsProbeCfg),
                                C.POINTER(RsCandidate), I32, C.POINTER(RsIndexSet), P, C.c_size_t,
@@ -133,7 +136,7 @@ def lib():
                                              C.POINTER(P), P]
         for name in ("rs_probe", "rs_build_indices", "rs_route_layer", "rs_sparse_attn_prefill",
                      "rs_dense_attn_prefill", "rs_error_predict", "rs_route_layer_device",
-                     "rs_routed_attn_prefill"):
+                     "rs_routed_attn_prefill", "rs_transpose_v"):
             getattr(L, name).restype = C.c_int
         _lib = L
     return _lib
@@ -164,14 +167,25 @@ def _stream(stream):
 
 # ---- argument builders ------------------------------------------------------------------
 
-def make_qkv(q, k, v, scale: float = 0.0) -> RsQkv:
-    """q: [hq, n, d], k/v: [hkv, n, d] device tensors (bf16 or float32, last dim contiguous)."""
+def make_qkv(q, k, v, scale: float = 0.0, vt=None) -> RsQkv:
+    """q: [hq, n, d], k/v: [hkv, n, d] device tensors (bf16 or float32, last dim contiguous);
+    vt: optional uint8 device tensor holding V in the rs_transpose_v layout."""
     import torch
     dt = {torch.bfloat16: RS_BF16, torch.float32: RS_F32}[q.dtype]
     assert k.dtype == q.dtype and v.dtype == q.dtype
     return RsQkv(q=q.data_ptr(), k=k.data_ptr(), v=v.data_ptr(), dtype=dt, n=q.shape[1], hq=q.shape[0],
                  hkv=k.shape[0], d=q.shape[2], sq_h=q.stride(0), sq_t=q.stride(1), sk_h=k.stride(0),
-                 sk_t=k.stride(1), sv_h=v.stride(0), sv_t=v.stride(1), scale=scale)
+                 sk_t=k.stride(1), sv_h=v.stride(0), sv_t=v.stride(1), scale=scale,
+                 vt=vt.data_ptr() if vt is not None else None)
+
+
+def rs_vt_bytes(qkv) -> int:
+    return lib().rs_vt_bytes(C.byref(qkv))
+
+
+def rs_transpose_v(qkv, vt, stream=None):
+    """vt: uint8 device tensor of rs_vt_bytes(qkv) bytes (or more)."""
+    return _check(lib().rs_transpose_v(C.byref(qkv), _ptr(vt), _stream(stream)))
 
 
 def make_units(units) -> C.Array:

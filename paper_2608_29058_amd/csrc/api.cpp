@@ -41,13 +41,15 @@ rs_status check_qkv(const rs_qkv *qkv, float *scale) {
       return fail(RS_ERR_INVALID_ARG, "strides must be non-negative multiples of 16 bytes");
   if (qkv->sq_t < qkv->d || qkv->sk_t < qkv->d || qkv->sv_t < qkv->d)
     return fail(RS_ERR_INVALID_ARG, "token stride smaller than head dim");
-  if (!aligned(qkv->q, 16) || !aligned(qkv->k, 16) || !aligned(qkv->v, 16))
-    return fail(RS_ERR_INVALID_ARG, "q, k and v must be 16-byte aligned");
+  if (!aligned(qkv->q, 16) || !aligned(qkv->k, 16) || !aligned(qkv->v, 16) || !aligned(qkv->vt, 16))
+    return fail(RS_ERR_INVALID_ARG, "q, k, v and vt must be 16-byte aligned");
   // the attention kernels address one head's K and V rows with 32-bit byte offsets
   const uint64_t span_k = ((uint64_t)(qkv->n - 1) * (uint64_t)qkv->sk_t + (uint64_t)qkv->d) * esz;
   const uint64_t span_v = ((uint64_t)(qkv->n - 1) * (uint64_t)qkv->sv_t + (uint64_t)qkv->d) * esz;
   if (span_k > 0xffffffffull || span_v > 0xffffffffull)
     return fail(RS_ERR_UNSUPPORTED, "one head's K or V rows must span less than 4 GiB");
+  if (qkv->vt && (uint64_t)qkv->d * (((uint64_t)qkv->n + 63) / 64 * 64) * 2ull > 0xffffffffull)
+    return fail(RS_ERR_UNSUPPORTED, "one head's V^T rows must span less than 4 GiB");
   float sc = qkv->scale;
   if (sc == 0.f) sc = 1.f / std::sqrt((float)qkv->d);
   if (!(sc > 0.f) || !std::isfinite(sc)) return fail(RS_ERR_INVALID_ARG, "scale must be positive and finite");
@@ -103,6 +105,8 @@ static rs_status check_grid(const rs_candidate *grid, int32_t ncand) {
   return RS_OK;
 }
 
+size_t vt_bytes(const rs_qkv *qkv);
+rs_status transpose_v_launch(const rs_qkv *qkv, void *vt, hipStream_t st);
 size_t route_dev_ws_bytes(int32_t nunits, int32_t ncand);
 rs_status route_dev_launch(const rs_route_in *in, const rs_route_cfg *cfg, const rs_route_dev_out *out,
                            const int *fam, const int *brank, int dense_c, void *ws, size_t ws_bytes,
@@ -389,6 +393,21 @@ rs_status rs_routed_attn_prefill(const rs_qkv *qkv, const rs_unit *units, int32_
   }
   return routed_attn_launch(qkv, scale, units, nunits, grid, ncand, idx, choice, o, so_h, so_t, lse, ws, ws_bytes,
                             events, (hipStream_t)stream);
+}
+
+size_t rs_vt_bytes(const rs_qkv *qkv) {
+  float scale;
+  if (check_qkv(qkv, &scale) != RS_OK) return 0;
+  return vt_bytes(qkv);
+}
+
+rs_status rs_transpose_v(const rs_qkv *qkv, void *vt, rs_stream stream) {
+  g_err.clear();
+  float scale;
+  rs_status st;
+  if ((st = check_qkv(qkv, &scale)) != RS_OK) return st;
+  if (!vt || !aligned(vt, 16)) return fail(RS_ERR_INVALID_ARG, "vt must be a 16-byte aligned device pointer");
+  return transpose_v_launch(qkv, vt, (hipStream_t)stream);
 }
 
 }  // extern "C"

@@ -47,6 +47,8 @@ struct AttnArgs {
   const int *qsize;   // [8] items per key/value bucket (device), or NULL: one item per workgroup
   const int *qoff;    // [8]
   int *qcount;        // [8] items taken per bucket (device counters, start at 0)
+  const bf16 *vt;  // V^T layout of rs_transpose_v (used by the VT instantiations)
+  int npad;
   const int *vs_vsorted, *vs_dsorted, *vs_count;
   const uint32_t *vs_vbits, *vs_dbits;
   int nv_max, ns_max, nwords, ncand_vs;
@@ -89,7 +91,8 @@ struct TileRef {
 };
 
 // One work item: query tile `item & 0xffff` of unit `item >> 16` of the launch's unit list.
-template <int D, int PAT, typename InT>
+// VT: V is read from the transposed copy (tiles of D rows x 64 keys), else from V itself.
+template <int D, int PAT, typename InT, bool VT>
 __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
   constexpr int NW = 4, NT = 256, BM = 128;
   constexpr int KS = D / 16;             // k-steps of the QK^T contraction
@@ -293,8 +296,29 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
       (void *)Vp, (short)0, (int)((uint32_t)(a.n - 1) * bV + D * sizeof(InT)), 0x00020000);
   [[maybe_unused]] const uint32_t voK = (uint32_t)lrow0 * bK + 16u * (uint32_t)lchunk;
   [[maybe_unused]] const uint32_t voV = (uint32_t)lrow0 * bV + 16u * (uint32_t)lchunk;
+  // V^T tile: D rows (dims) of 64 keys (128 bytes); a wave instruction copies 8 rows, lane l
+  // landing at row l / 8, chunk l % 8, which holds global chunk (l % 8) ^ ((row / 2) % 8) (the
+  // read-side swizzle).  Rows of load i are 8 (i NW + wave) + l / 8, so the swizzle is the same
+  // for every i.
+  const uint32_t bVT = (uint32_t)a.npad * 2u;
+  [[maybe_unused]] const __amdgpu_buffer_rsrc_t rVT = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)(a.vt + (long long)kvh * D * a.npad), (short)0, (int)((uint32_t)D * bVT), 0x00020000);
+  [[maybe_unused]] const uint32_t voVT =
+      (uint32_t)(8 * wave + lane / 8) * bVT + 16u * (uint32_t)((lane % 8) ^ ((4 * (wave & 1) + (lane >> 4)) & 7));
   // one K or V tile (64 key rows) into dst
   auto issue = [&](bf16 *dst, int key0, bool isV) {
+    if constexpr (VT) {
+      if (isV) {
+        constexpr int LPV = D / 8 / NW;  // 8-row groups per wave
+        static_assert(LPV == LPT && NW % 2 == 0, "V^T tile: same load count as a row tile");
+        bf16 *dw = dst + wave * 8 * 64;
+#pragma unroll
+        for (int i = 0; i < LPV; ++i)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rVT, (__attribute__((address_space(3))) void *)(dw + i * NW * 8 * 64),
+                                                   16, voVT, (uint32_t)key0 * 2u + (uint32_t)(i * NW * 8) * bVT, 0, 0);
+        return;
+      }
+    }
     const InT *src = isV ? Vp : Kp;
     const long long st = isV ? a.sv_t : a.sk_t;
     if constexpr (sizeof(InT) == 2) {
@@ -478,8 +502,23 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
     return ps;
   };
 
-  // ---- O^T[d x 32 rows] += V^T x P^T (V read transposed from its row-major tile) ----------
+  // ---- O^T[d x 32 rows] += V^T x P^T (V read transposed from its row-major tile, or, with
+  // VT, 8 consecutive keys of a V^T row per lane: the tile's keys are stored in the order in
+  // which the S^T accumulator hands them to P) ----------------------------------------------
+  [[maybe_unused]] const int vts = (l32 >> 1) & 7;
   auto pv = [&](const bf16 *sVt, const Plan &p) {
+    if constexpr (VT) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const u32x4 vv = *(const u32x4 *)(sVt + (32 * db + l32) * 64 + (((4 * mb + 2 * h + hh) ^ vts) << 3));
+            oacc[db] = mfma32(vv, pb[mb][h], oacc[db]);
+          }
+      return;
+    }
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -602,12 +641,12 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
 // queue of key/value bucket b % 8 (items there are longest first), then of the other buckets
 // once its own is empty, until every queue is drained.  Each queue counter starts at 0 (the
 // planner writes it) and is only ever incremented, so every workgroup reaches the exit.
-template <int D, int PAT, typename InT>
+template <int D, int PAT, typename InT, bool VT>
 __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const AttnArgs a) {
-  attn_item<D, PAT, InT>(a, a.order[blockIdx.x]);
+  attn_item<D, PAT, InT, VT>(a, a.order[blockIdx.x]);
 }
 
-template <int D, int PAT, typename InT>
+template <int D, int PAT, typename InT, bool VT>
 __global__ void __launch_bounds__(256, 2) attn_fwd_queue_kernel(const AttnArgs a) {
   __shared__ int sItem;
   const int x = (int)(blockIdx.x & 7u);
@@ -626,8 +665,70 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_queue_kernel(const AttnArgs a
     __syncthreads();
     const int it = sItem;
     if (it < 0) break;
-    attn_item<D, PAT, InT>(a, it);
+    attn_item<D, PAT, InT, VT>(a, it);
   }
+}
+
+// ---- V^T: [hkv][d][npad] bf16, keys permuted within groups of 16 ---------------------------
+// Position j of a 16-key group holds key perm[j]: in the P V product a lane of half hh supplies
+// the keys {4 hh .. 4 hh + 3, 8 + 4 hh .. 8 + 4 hh + 3} of each group of 16 (the order in which
+// the S^T accumulator hands them to P), which are then 8 consecutive positions.
+__device__ __forceinline__ int vt_perm(int j) { return (j & 3) | ((j & 4) << 1) | ((j & 8) >> 1); }
+
+// grid (npad / 64, hkv), 256 threads: 64 keys of one key/value head through LDS
+template <int D, typename InT>
+__global__ void __launch_bounds__(256) transpose_v_kernel(const InT *v, long long sv_h, long long sv_t, int n,
+                                                          int npad, bf16 *vt) {
+  constexpr int LD = D + 8;
+  __shared__ __align__(16) bf16 sT[64][LD];
+  const int k0 = blockIdx.x * 64, g = blockIdx.y, tid = threadIdx.x;
+  const InT *vp = v + (long long)g * sv_h;
+  // 64 rows x D, 8 elements per 16-byte chunk of the bf16 tile
+  for (int x = tid; x < 64 * (D / 8); x += 256) {
+    const int r = x / (D / 8), c = x % (D / 8), key = k0 + r;
+    u32x4 w = {0u, 0u, 0u, 0u};
+    if (key < n) w = load8<InT>(vp + (long long)key * sv_t + 8 * c);
+    *(u32x4 *)&sT[r][8 * c] = w;
+  }
+  __syncthreads();
+  bf16 *out = vt + (long long)g * D * npad + k0;
+  for (int x = tid; x < D * 8; x += 256) {
+    const int dd = x / 8, c = x % 8;  // row dd of V^T, positions 8c .. 8c + 7 of the 64 keys
+    bf16 e[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int p = 8 * c + j;
+      e[j] = sT[(p & ~15) + vt_perm(p & 15)][dd];
+    }
+    *(u32x4 *)(out + (long long)dd * npad + 8 * c) = __builtin_bit_cast(u32x4, e);
+  }
+}
+
+size_t vt_bytes(const rs_qkv *qkv) {
+  const long long npad = ((long long)qkv->n + 63) / 64 * 64;
+  return (size_t)qkv->hkv * qkv->d * npad * sizeof(bf16);
+}
+
+rs_status transpose_v_launch(const rs_qkv *qkv, void *vt, hipStream_t st) {
+  const int npad = (qkv->n + 63) / 64 * 64;
+  const dim3 grid(npad / 64, qkv->hkv);
+  if (qkv->d == 128) {
+    if (qkv->dtype == RS_BF16)
+      hipLaunchKernelGGL((transpose_v_kernel<128, bf16>), grid, dim3(256), 0, st, (const bf16 *)qkv->v,
+                         (long long)qkv->sv_h, (long long)qkv->sv_t, qkv->n, npad, (bf16 *)vt);
+    else
+      hipLaunchKernelGGL((transpose_v_kernel<128, float>), grid, dim3(256), 0, st, (const float *)qkv->v,
+                         (long long)qkv->sv_h, (long long)qkv->sv_t, qkv->n, npad, (bf16 *)vt);
+  } else {
+    if (qkv->dtype == RS_BF16)
+      hipLaunchKernelGGL((transpose_v_kernel<64, bf16>), grid, dim3(256), 0, st, (const bf16 *)qkv->v,
+                         (long long)qkv->sv_h, (long long)qkv->sv_t, qkv->n, npad, (bf16 *)vt);
+    else
+      hipLaunchKernelGGL((transpose_v_kernel<64, float>), grid, dim3(256), 0, st, (const float *)qkv->v,
+                         (long long)qkv->sv_h, (long long)qkv->sv_t, qkv->n, npad, (bf16 *)vt);
+  }
+  RS_HIP(hipGetLastError());
+  return RS_OK;
 }
 
 // ---- host side ---------------------------------------------------------------------------
@@ -670,16 +771,32 @@ static void build_order(const rs_unit *units, int nunits, int group, int bm,
 
 template <int D, int PAT>
 static hipError_t launch_pat(int dtype, const AttnArgs &a, int nitems, hipStream_t st) {
+  if (a.vt) {
+    if constexpr (PAT != P_VS) {  // vertical-slash gathers V rows: it keeps the row-major V
+      if (a.qsize) {
+        if (dtype == RS_BF16)
+          hipLaunchKernelGGL((attn_fwd_queue_kernel<D, PAT, bf16, true>), dim3(nitems), dim3(256), 0, st, a);
+        else
+          hipLaunchKernelGGL((attn_fwd_queue_kernel<D, PAT, float, true>), dim3(nitems), dim3(256), 0, st, a);
+      } else {
+        if (dtype == RS_BF16)
+          hipLaunchKernelGGL((attn_fwd_kernel<D, PAT, bf16, true>), dim3(nitems), dim3(256), 0, st, a);
+        else
+          hipLaunchKernelGGL((attn_fwd_kernel<D, PAT, float, true>), dim3(nitems), dim3(256), 0, st, a);
+      }
+      return hipGetLastError();
+    }
+  }
   if (a.qsize) {
     if (dtype == RS_BF16)
-      hipLaunchKernelGGL((attn_fwd_queue_kernel<D, PAT, bf16>), dim3(nitems), dim3(256), 0, st, a);
+      hipLaunchKernelGGL((attn_fwd_queue_kernel<D, PAT, bf16, false>), dim3(nitems), dim3(256), 0, st, a);
     else
-      hipLaunchKernelGGL((attn_fwd_queue_kernel<D, PAT, float>), dim3(nitems), dim3(256), 0, st, a);
+      hipLaunchKernelGGL((attn_fwd_queue_kernel<D, PAT, float, false>), dim3(nitems), dim3(256), 0, st, a);
   } else {
     if (dtype == RS_BF16)
-      hipLaunchKernelGGL((attn_fwd_kernel<D, PAT, bf16>), dim3(nitems), dim3(256), 0, st, a);
+      hipLaunchKernelGGL((attn_fwd_kernel<D, PAT, bf16, false>), dim3(nitems), dim3(256), 0, st, a);
     else
-      hipLaunchKernelGGL((attn_fwd_kernel<D, PAT, float>), dim3(nitems), dim3(256), 0, st, a);
+      hipLaunchKernelGGL((attn_fwd_kernel<D, PAT, float, false>), dim3(nitems), dim3(256), 0, st, a);
   }
   return hipGetLastError();
 }
@@ -708,6 +825,7 @@ rs_status attn_launch_list(const rs_qkv *qkv, float scale, int fam, const rs_ind
   a.o = (bf16 *)o; a.so_h = so_h; a.so_t = so_t; a.lse = lse;
   a.n = qkv->n; a.group = qkv->hq / qkv->hkv; a.scale = scale; a.c = scale * kLog2e;
   a.units = d_units; a.order = d_order;
+  a.vt = (const bf16 *)qkv->vt; a.npad = (qkv->n + 63) / 64 * 64;
   if (queues) { a.qsize = queues->size; a.qoff = queues->off; a.qcount = queues->count; }
   if (fam == RS_VSLASH) {
     a.vs_vsorted = idx->vs_vsorted; a.vs_dsorted = idx->vs_dsorted; a.vs_count = idx->vs_count;

@@ -667,11 +667,14 @@ __global__ void __launch_bounds__(256) block_pool_kernel(const InT *x, long long
   }
 }
 
-// L[h][bq][bk] = qbar . kbar * scale for bk <= bq; 128 x 128 output tiles, each thread an
-// 8 x 8 block, fp32 FMA over the head dimension in order (d a multiple of 32).
+// L[h][bq][bk] = qbar . kbar * scale for bk <= bq; 128 x 128 output tiles, each wave a 64 x 64
+// quarter as 2 x 2 fp32 MFMA blocks (v_mfma_f32_32x32x2_f32: fp32 products, fp32 sums).  The
+// head dimension goes through LDS in chunks of 32; within a group of 8 dims, lanes 0-31 take
+// dims 0-3 and lanes 32-63 dims 4-7 over four k-steps (any assignment of dims to k-steps is
+// the same sum, as long as A and B use the same one).
 __global__ void __launch_bounds__(256) block_logits_kernel(const float *qbar, const float *kbar, int nb, int d,
                                                            int group, float scale, float *lbs) {
-  constexpr int TB = 128, KC = 32, LD = TB + 4;
+  constexpr int TB = 128, KC = 32, LD = KC + 4;
   const int h = blockIdx.y;
   // decode lower-triangular tile index
   int tq = 0;
@@ -681,45 +684,60 @@ __global__ void __launch_bounds__(256) block_logits_kernel(const float *qbar, co
     ++tq;
   }
   const int tk = t;
-  __shared__ __align__(16) float sq[KC][LD], sk[KC][LD];
-  const int tid = threadIdx.x;
-  const int tx = tid % 16, ty = tid / 16;  // each thread: rows ty*8.., cols tx*8..
-  float acc[8][8] = {};
+  __shared__ __align__(16) float sq[TB][LD], sk[TB][LD];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wr = (wave >> 1) * 64, wc = (wave & 1) * 64;  // this wave's quarter
+  const int l32 = lane & 31, hh = lane >> 5;
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
   const float *qb = qbar + (long long)h * nb * d;
   const float *kb = kbar + (long long)(h / group) * nb * d;
   for (int d0 = 0; d0 < d; d0 += KC) {
-    for (int x = tid; x < TB * KC; x += 256) {
-      const int r = x / KC, cc = x % KC;
+    // 128 rows x 32 dims of each operand: 1024 float4, 4 per thread
+#pragma unroll
+    for (int x0 = 0; x0 < TB * KC / 4; x0 += 256) {
+      const int x = x0 + tid, r = x / (KC / 4), c4 = x % (KC / 4);
       const int bq = tq * TB + r, bk = tk * TB + r;
-      sq[cc][r] = bq < nb ? qb[(long long)bq * d + d0 + cc] : 0.f;
-      sk[cc][r] = bk < nb ? kb[(long long)bk * d + d0 + cc] : 0.f;
+      const f32x4 zq = {0.f, 0.f, 0.f, 0.f};
+      *(f32x4 *)&sq[r][4 * c4] = bq < nb ? *(const f32x4 *)&qb[(long long)bq * d + d0 + 4 * c4] : zq;
+      *(f32x4 *)&sk[r][4 * c4] = bk < nb ? *(const f32x4 *)&kb[(long long)bk * d + d0 + 4 * c4] : zq;
     }
     __syncthreads();
-#pragma unroll 4
-    for (int cc = 0; cc < KC; ++cc) {
-      const f32x4 q0 = *(const f32x4 *)&sq[cc][ty * 8], q1 = *(const f32x4 *)&sq[cc][ty * 8 + 4];
-      const f32x4 k0 = *(const f32x4 *)&sk[cc][tx * 8], k1 = *(const f32x4 *)&sk[cc][tx * 8 + 4];
-      const float qa[8] = {q0[0], q0[1], q0[2], q0[3], q1[0], q1[1], q1[2], q1[3]};
-      const float ka[8] = {k0[0], k0[1], k0[2], k0[3], k1[0], k1[1], k1[2], k1[3]};
 #pragma unroll
-      for (int i = 0; i < 8; ++i)
+    for (int g = 0; g < KC / 8; ++g) {
+      f32x4 a4[2], b4[2];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) acc[i][j] = fmaf(qa[i], ka[j], acc[i][j]);
+      for (int i = 0; i < 2; ++i) a4[i] = *(const f32x4 *)&sq[wr + 32 * i + l32][8 * g + 4 * hh];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) b4[j] = *(const f32x4 *)&sk[wc + 32 * j + l32][8 * g + 4 * hh];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4[i][e], b4[j][e], acc[i][j], 0, 0, 0);
     }
     __syncthreads();
   }
+  // D[row][col]: col = lane % 32, row = 8 (r / 4) + 4 (lane / 32) + r % 4
   float *lh = lbs + (long long)h * ((long long)nb * (nb + 1) / 2);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int bq = tq * TB + ty * 8 + i;
-    if (bq >= nb) continue;
-    float *row = lh + (long long)bq * (bq + 1) / 2;
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int bk = tk * TB + tx * 8 + j;
-      if (bk <= bq) row[bk] = acc[i][j] * scale;
+    for (int j = 0; j < 2; ++j) {
+      const int bk = tk * TB + wc + 32 * j + l32;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int bq = tq * TB + wr + 32 * i + 8 * (r >> 2) + 4 * hh + (r & 3);
+        if (bq < nb && bk <= bq) lh[(long long)bq * (bq + 1) / 2 + bk] = acc[i][j][r] * scale;
+      }
     }
-  }
 }
 
 // ---- host side ---------------------------------------------------------------------------

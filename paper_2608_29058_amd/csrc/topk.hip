@@ -20,26 +20,47 @@ namespace rs {
 
 constexpr int kMaxCandFam = 8;
 
-// inclusive prefix sum of v over the workgroup; returns it, total in *tot
+// The helpers below run over a group of NT threads: the whole workgroup, or with NT = 64 one
+// wave of it (each wave then works on its own data and LDS, synchronising only itself).
+template <int NT>
+__device__ __forceinline__ void gsync() {
+  if constexpr (NT == 64) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  } else {
+    __syncthreads();
+  }
+}
+template <int NT>
+__device__ __forceinline__ int gtid() {
+  return NT == 64 ? (int)(threadIdx.x & 63u) : (int)threadIdx.x;
+}
+
+// inclusive prefix sum of v over the group; returns it, total in *tot
 template <int NT>
 __device__ int block_incl_scan(int v, int *sWave, int *tot) {
   constexpr int NWV = NT / 64;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = gtid<NT>() >> 6;
   int x = v;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
     const int y = __shfl_up(x, o);
     if (lane >= o) x += y;
   }
+  if constexpr (NWV == 1) {
+    *tot = __shfl(x, 63);
+    return x;
+  }
   if (lane == 63) sWave[wave] = x;
-  __syncthreads();
+  gsync<NT>();
   int off = 0, all = 0;
   for (int w = 0; w < NWV; ++w) {
     const int t = sWave[w];
     if (w < wave) off += t;
     all += t;
   }
-  __syncthreads();
+  gsync<NT>();
   *tot = all;
   return x + off;
 }
@@ -52,16 +73,16 @@ __device__ void radix_select(const float *vals, int len, int K, uint32_t *T_out,
   uint32_t prefix = 0, maskhi = 0;
   int krem = K;
   for (int byte = 3; byte >= 0; --byte) {
-    for (int b = threadIdx.x; b < 256; b += NT) sHist[b] = 0;
-    __syncthreads();
-    for (int i = threadIdx.x; i < len; i += NT) {
+    for (int b = gtid<NT>(); b < 256; b += NT) sHist[b] = 0;
+    gsync<NT>();
+    for (int i = gtid<NT>(); i < len; i += NT) {
       const uint32_t key = float_key(vals[i]);
       if ((key & maskhi) == prefix) atomicAdd(&sHist[(key >> (8 * byte)) & 255u], 1);
     }
-    __syncthreads();
-    if (threadIdx.x < 64) {
+    gsync<NT>();
+    if (gtid<NT>() < 64) {
       // lane l owns bins 255-4l .. 252-4l (descending); wave-wide inclusive scan of counts
-      const int l = threadIdx.x;
+      const int l = gtid<NT>();
       int c4[4], own = 0;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -90,11 +111,11 @@ __device__ void radix_select(const float *vals, int len, int K, uint32_t *T_out,
         sBcast[1] = krem - cum;
       }
     }
-    __syncthreads();
+    gsync<NT>();
     prefix |= (uint32_t)sBcast[0] << (8 * byte);
     maskhi |= 0xffu << (8 * byte);
     krem = sBcast[1];
-    __syncthreads();
+    gsync<NT>();
   }
   *T_out = prefix;
   *take_out = krem;
@@ -105,18 +126,18 @@ template <int NT, typename F>
 __device__ void select_top(const float *vals, int len, int K, int *sHist, int *sBcast, int *sWave, F emit) {
   if (K <= 0) return;
   if (len <= K) {
-    for (int i = threadIdx.x; i < len; i += NT) emit(i);
+    for (int i = gtid<NT>(); i < len; i += NT) emit(i);
     return;
   }
   uint32_t T;
   int take;
   radix_select<NT>(vals, len, K, &T, &take, sHist, sBcast);
-  for (int i = threadIdx.x; i < len; i += NT)
+  for (int i = gtid<NT>(); i < len; i += NT)
     if (float_key(vals[i]) > T) emit(i);
   // equal keys: lowest positions first
   int seen = 0;
   for (int i0 = 0; i0 < len && seen < take; i0 += NT) {
-    const int i = i0 + threadIdx.x;
+    const int i = i0 + gtid<NT>();
     const int f = (i < len && float_key(vals[i]) == T) ? 1 : 0;
     int tot;
     const int incl = block_incl_scan<NT>(f, sWave, &tot);
@@ -130,7 +151,7 @@ template <int NT>
 __device__ int bits_to_list(const uint32_t *bits, int nwords, int *out, int cap, int *sWave) {
   constexpr int WPT_MAX = 16;
   const int wpt = (nwords + NT - 1) / NT;  // contiguous words per thread
-  const int w0 = threadIdx.x * wpt;
+  const int w0 = gtid<NT>() * wpt;
   int cnt = 0;
   for (int w = w0; w < min(nwords, w0 + wpt); ++w) cnt += __builtin_popcount(bits[w]);
   int tot;
@@ -146,7 +167,7 @@ __device__ int bits_to_list(const uint32_t *bits, int nwords, int *out, int cap,
     }
   }
   (void)WPT_MAX;
-  for (int x = tot + threadIdx.x; x < cap; x += NT) out[x] = -1;
+  for (int x = tot + gtid<NT>(); x < cap; x += NT) out[x] = -1;
   return tot;
 }
 
@@ -231,28 +252,35 @@ struct BsArgs {
   uint32_t *bits;
 };
 
-// grid: (nb, hq); one query block per workgroup
+// grid: (ceil(nb / 4), hq), 256 threads; one query block per wave (waves synchronise only
+// themselves: each has its own LDS)
 __global__ void __launch_bounds__(256) bs_select_kernel(const BsArgs a) {
-  constexpr int NT = 256;
+  constexpr int NT = 64;
   constexpr int SP = 256;  // sort capacity (k_max <= 256)
-  __shared__ int sHist[256], sBcast[2], sWave[NT / 64], sCnt;
-  __shared__ unsigned long long sKey[SP];
-  __shared__ uint32_t sB[kMaxN / 64 / 32];
-  const int bq = blockIdx.x, h = blockIdx.y;
+  constexpr int NBW = kMaxN / 64 / 32;
+  __shared__ int sHistA[4][256], sBcastA[4][2], sCntA[4];
+  __shared__ unsigned long long sKeyA[4][SP];
+  __shared__ uint32_t sBA[4][NBW];
+  const int w = (int)(threadIdx.x >> 6), l = (int)(threadIdx.x & 63u);
+  const int bq = (int)blockIdx.x * 4 + w, h = blockIdx.y;
+  if (bq >= a.nb) return;  // this wave has no query block; the others never wait for it
+  int *sHist = sHistA[w], *sBcast = sBcastA[w];
+  unsigned long long *sKey = sKeyA[w];
+  uint32_t *sB = sBA[w];
   const float *vals = a.lbs + (long long)h * ((long long)a.nb * (a.nb + 1) / 2) + (long long)bq * (bq + 1) / 2;
-  for (int x = threadIdx.x; x < SP; x += NT) sKey[x] = 0ull;
-  if (threadIdx.x == 0) sCnt = 0;
-  __syncthreads();
+  for (int x = l; x < SP; x += NT) sKey[x] = 0ull;
+  if (l == 0) sCntA[w] = 0;
+  gsync<NT>();
   const int K = a.k_max - 1;
-  select_top<NT>(vals, bq, K, sHist, sBcast, sWave, [&](int i) {
-    const int p = atomicAdd(&sCnt, 1);
+  select_top<NT>(vals, bq, K, sHist, sBcast, nullptr, [&](int i) {
+    const int p = atomicAdd(&sCntA[w], 1);
     sKey[p] = ((unsigned long long)float_key(vals[i]) << 32) | (unsigned long long)(0xffffffffu - (uint32_t)i);
   });
-  __syncthreads();
+  gsync<NT>();
   // bitonic sort, descending
   for (int size = 2; size <= SP; size <<= 1)
     for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int x = threadIdx.x; x < SP / 2; x += NT) {
+      for (int x = l; x < SP / 2; x += NT) {
         const int lo = 2 * x - (x & (stride - 1));
         const int hi = lo + stride;
         const bool desc = ((lo & size) == 0);
@@ -262,31 +290,30 @@ __global__ void __launch_bounds__(256) bs_select_kernel(const BsArgs a) {
           sKey[hi] = A;
         }
       }
-      __syncthreads();
+      gsync<NT>();
     }
   const int nsel = min(K, bq);
   int *rk = a.rank + ((long long)h * a.nb + bq) * a.k_max;
-  for (int x = threadIdx.x; x < a.k_max; x += NT) {
+  for (int x = l; x < a.k_max; x += NT) {
     int v = -1;
     if (x == 0) v = bq;
     else if (x - 1 < nsel) v = (int)(0xffffffffu - (uint32_t)(sKey[x - 1] & 0xffffffffull));
     rk[x] = v;
   }
-  __syncthreads();
   for (int c = 0; c < a.ncand_bs; ++c) {
-    for (int w = threadIdx.x; w < a.nbw; w += NT) sB[w] = 0u;
-    __syncthreads();
+    for (int x = l; x < a.nbw; x += NT) sB[x] = 0u;
+    gsync<NT>();
     const int take = min(a.k[c], bq + 1);
-    for (int x = threadIdx.x; x < take; x += NT) {
+    for (int x = l; x < take; x += NT) {
       const int blk = x == 0 ? bq : (int)(0xffffffffu - (uint32_t)(sKey[x - 1] & 0xffffffffull));
       atomicOr(&sB[blk >> 5], 1u << (blk & 31));
     }
-    __syncthreads();
+    gsync<NT>();
     const long long crow = ((long long)h * a.ncand_bs + c) * a.nb + bq;
-    for (int w = threadIdx.x; w < a.nbw; w += NT) a.bits[crow * a.nbw + w] = sB[w];
-    const int cnt = bits_to_list<NT>(sB, a.nbw, a.sorted + crow * a.k_max, a.k_max, sWave);
-    if (threadIdx.x == 0) a.count[crow] = cnt;
-    __syncthreads();
+    for (int x = l; x < a.nbw; x += NT) a.bits[crow * a.nbw + x] = sB[x];
+    const int cnt = bits_to_list<NT>(sB, a.nbw, a.sorted + crow * a.k_max, a.k_max, nullptr);
+    if (l == 0) a.count[crow] = cnt;
+    gsync<NT>();
   }
 }
 
@@ -324,7 +351,7 @@ rs_status build_indices_launch(const rs_probe_out *sc, const rs_unit *units, int
   if (nbs > 0) {
     ba.lbs = sc->lbs; ba.nb = out->nb; ba.hq = out->hq; ba.ncand_bs = nbs; ba.k_max = out->k_max; ba.nbw = out->nbw;
     ba.rank = out->bs_rank; ba.sorted = out->bs_sorted; ba.count = out->bs_count; ba.bits = out->bs_bits;
-    hipLaunchKernelGGL(bs_select_kernel, dim3(out->nb, out->hq), dim3(256), 0, st, ba);
+    hipLaunchKernelGGL(bs_select_kernel, dim3((out->nb + 3) / 4, out->hq), dim3(256), 0, st, ba);
     RS_HIP(hipGetLastError());
   }
   return RS_OK;

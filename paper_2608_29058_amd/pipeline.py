@@ -2,6 +2,7 @@
 
 No arithmetic happens here: this module allocates caller-owned buffers once and calls the
 library in the order of the per-layer procedure (Sec. 3.4 and its table):
+  0. rs_transpose_v (V in the operand layout of the dense, A-shape and block-sparse kernels)
   1. rs_probe (scores: sampled rows, col/diag, descriptors, block-mean logits)
   2. rs_build_indices, then rs_probe (coverage of every candidate)
   3-5. rs_route_layer on the host after copying the coverage back (latency lookup, greedy
@@ -40,7 +41,7 @@ class RoutedLayer:
     """Buffers and call order of one routed layer for fixed shapes."""
 
     def __init__(self, n, hq, hkv, d, seg_len, grid, r_rec=64, r_uni=64, r_bnd=32, local_w=1024,
-                 device="cuda"):
+                 device="cuda", use_vt=True):
         import torch
         self.n, self.hq, self.hkv, self.d = n, hq, hkv, d
         self.grid = list(grid)
@@ -56,6 +57,9 @@ class RoutedLayer:
         self.pb = _rs.ProbeBuffers(self.nunits, self.rmax, n, hq, self.ncand, blockmean=True, device=device)
         self.ib = _rs.IndexBuffers(self.nunits, n, hq, self.grid, device=device)
         self.o = torch.empty((hq, n, d), dtype=torch.bfloat16, device=device)
+        # V in the transposed operand layout of rs_transpose_v (rewritten by every qkv() call)
+        self.vt = (torch.empty(hkv * d * ((n + 63) // 64 * 64) * 2, dtype=torch.uint8, device=device)
+                   if use_vt else None)
         self.s1 = np.array([u[2] for u in self.unit_list], np.int32)
         self.cov_host = torch.empty((self.nunits, self.ncand, 4), dtype=torch.float32, pin_memory=True)
         self.nsub_host = torch.empty((self.nunits, 3), dtype=torch.int32, pin_memory=True)
@@ -71,7 +75,15 @@ class RoutedLayer:
         self.knobs = RouteKnobs()
 
     def qkv(self, q, k, v):
-        return _rs.make_qkv(q, k, v)
+        """The layer's rs_qkv.  With the transposed-V layout on, this also (re)writes V^T of this
+        layer into self.vt on the stream (rs_transpose_v): the returned descriptor is valid until
+        the next qkv() call."""
+        if self.vt is None:
+            return _rs.make_qkv(q, k, v)
+        qkv = _rs.make_qkv(q, k, v, vt=self.vt)
+        assert _rs.rs_vt_bytes(qkv) == self.vt.numel()
+        _rs.rs_transpose_v(qkv, self.vt)
+        return qkv
 
     def workspace(self, qkv):
         if self._ws is None:
@@ -151,9 +163,11 @@ class RoutedLayer:
         the input-conditional routing decision while the index sets are still built from this
         input; ``device_route`` routes on the device and launches the attention from that route
         with no host synchronisation (``family_events``: see run_routed)."""
-        qkv = self.qkv(q, k, v)
         mark = events or (lambda name: None)
         mark("start")
+        qkv = self.qkv(q, k, v)
+        if self.vt is not None:
+            mark("transpose_v")
         self.probe_and_index(qkv)
         mark("probe")
         if device_route:
@@ -203,7 +217,7 @@ class RoutedLayer:
         return t
 
     def profile_probe(self, qkv, reps=3):
-        """Median time of probe + indices + coverage, in us."""
+        """Median time of the V transpose (when on) + probe + indices + coverage, in us."""
         import torch
         stream = torch.cuda.current_stream()
         ts = []
@@ -211,6 +225,8 @@ class RoutedLayer:
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
             e0.record(stream)
+            if self.vt is not None:
+                _rs.rs_transpose_v(qkv, self.vt)
             self.probe_and_index(qkv)
             e1.record(stream)
             e1.synchronize()

@@ -67,3 +67,13 @@ def check_close(got, ref, tag, max_abs=2e-2, rel_f=1e-2):
     rf = np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-30)
     assert err <= max_abs and rf <= rel_f, f"{tag}: max-abs {err:.3e} rel-F {rf:.3e}"
     return err, rf
+
+
+def with_vt(qkv):
+    """Return ``(qkv, buffer)`` with V also written in the transposed operand layout
+    (rs_transpose_v) and qkv.vt pointing at it; keep the buffer alive while qkv is used."""
+    import torch
+    buf = torch.empty(_rs.rs_vt_bytes(qkv), dtype=torch.uint8, device="cuda")
+    _rs.rs_transpose_v(qkv, buf)
+    qkv.vt = buf.data_ptr()
+    return qkv, buf

@@ -12,7 +12,7 @@ from oracle import patterns as P
 from paper_2608_29058_amd import _rs
 from synth import gen as G
 
-from gpu_helpers import check_close, dev, fill_bs, fill_vs, out_tensor
+from gpu_helpers import check_close, dev, fill_bs, fill_vs, out_tensor, with_vt
 
 pytestmark = pytest.mark.gpu
 
@@ -28,11 +28,13 @@ def _inputs(n, hq, hkv, d, seed, dtype="bf16"):
     return q, k, v
 
 
-def _run_dense(q, k, v, units, dtype="bf16", lse=False):
+def _run_dense(q, k, v, units, dtype="bf16", lse=False, vt=False):
     import torch
     hq, n, d = q.shape
     qd, kd, vd = dev(q, dtype), dev(k, dtype), dev(v, dtype)
     qkv = _rs.make_qkv(qd, kd, vd)
+    if vt:
+        qkv, _vt = with_vt(qkv)
     u = _rs.make_units(units)
     ws = _rs.workspace(_rs.rs_attn_workspace_size(qkv, u, len(units)))
     o = out_tensor(hq, n, d)
@@ -45,10 +47,11 @@ def _run_dense(q, k, v, units, dtype="bf16", lse=False):
 @pytest.mark.parametrize("n,hq,hkv,d,dtype", [(1000, 4, 2, 128, "bf16"), (4097, 2, 1, 128, "bf16"),
                                               (700, 2, 2, 64, "bf16"), (2048, 1, 1, 64, "f32"),
                                               (64, 1, 1, 128, "bf16"), (1, 1, 1, 128, "bf16")])
-def test_dense_matches_oracle(n, hq, hkv, d, dtype):
+@pytest.mark.parametrize("vt", [False, True])
+def test_dense_matches_oracle(n, hq, hkv, d, dtype, vt):
     q, k, v = _inputs(n, hq, hkv, d, seed=n + d)
     units = [(h, 0, n) for h in range(hq)]
-    o, lse = _run_dense(q, k, v, units, dtype, lse=True)
+    o, lse = _run_dense(q, k, v, units, dtype, lse=True, vt=vt)
     g = hq // hkv
     for h in range(hq):
         ref = A.dense_attention(q[h], k[h // g], v[h // g])
@@ -59,11 +62,12 @@ def test_dense_matches_oracle(n, hq, hkv, d, dtype):
         np.testing.assert_allclose(lse[h], logsumexp(lg, axis=1), atol=2e-3, rtol=1e-4)
 
 
-def test_dense_segments_write_only_their_rows():
+@pytest.mark.parametrize("vt", [False, True])
+def test_dense_segments_write_only_their_rows(vt):
     n, hq, hkv, d = 1500, 2, 1, 128
     q, k, v = _inputs(n, hq, hkv, d, seed=7)
     units = [(0, 100, 700), (1, 640, 1500), (0, 1200, 1201)]
-    o, _ = _run_dense(q, k, v, units)
+    o, _ = _run_dense(q, k, v, units, vt=vt)
     written = np.zeros((hq, n), bool)
     for h, s0, s1 in units:
         written[h, s0:s1] = True
@@ -72,11 +76,13 @@ def test_dense_segments_write_only_their_rows():
     assert np.isnan(o[~written]).all()
 
 
-def _run_sparse(q, k, v, units, grid, ib, dtype="bf16"):
+def _run_sparse(q, k, v, units, grid, ib, dtype="bf16", vt=False):
     import torch
     hq, n, d = q.shape
     qd, kd, vd = dev(q, dtype), dev(k, dtype), dev(v, dtype)
     qkv = _rs.make_qkv(qd, kd, vd)
+    if vt:
+        qkv, _vt = with_vt(qkv)
     u = _rs.make_units(units)
     g = _rs.make_grid(grid)
     ws = _rs.workspace(_rs.rs_attn_workspace_size(qkv, u, len(units)))
@@ -89,12 +95,13 @@ def _run_sparse(q, k, v, units, grid, ib, dtype="bf16"):
 
 @pytest.mark.parametrize("n,sink,window", [(3000, 128, 1024), (2500, 0, 1), (1800, 100, 300),
                                            (700, 4, 64), (5000, 130, 1000)])
-def test_ashape_matches_oracle(n, sink, window):
+@pytest.mark.parametrize("vt", [False, True])
+def test_ashape_matches_oracle(n, sink, window, vt):
     hq, hkv, d = 2, 1, 128
     q, k, v = _inputs(n, hq, hkv, d, seed=sink + window)
     grid = [(_rs.RS_DENSE, 0, 0), (_rs.RS_ASHAPE, sink, window)]
     units = [(0, 0, n, 1), (1, 640, n, 1)]
-    o, lse = _run_sparse(q, k, v, units, grid, None)
+    o, lse = _run_sparse(q, k, v, units, grid, None, vt=vt)
     for h, s0, s1, _ in units:
         rows = np.arange(s0, s1)
         ref, rl = A.masked_attention(q[h], k[0], v[0], rows, P.ashape_mask(rows, s1, sink, window))
@@ -103,7 +110,8 @@ def test_ashape_matches_oracle(n, sink, window):
 
 
 @pytest.mark.parametrize("n,k_blocks", [(2000, 5), (4096, 12), (1100, 40)])
-def test_block_sparse_matches_oracle(n, k_blocks):
+@pytest.mark.parametrize("vt", [False, True])
+def test_block_sparse_matches_oracle(n, k_blocks, vt):
     hq, hkv, d = 4, 2, 128
     q, k, v = _inputs(n, hq, hkv, d, seed=n)
     nb = (n + 63) // 64
@@ -119,7 +127,7 @@ def test_block_sparse_matches_oracle(n, k_blocks):
         sels[h] = sel
         fill_bs(ib, h, 0, sel)
     units = [(h, 0 if h % 2 == 0 else 320, n, 1) for h in range(hq)]
-    o, _ = _run_sparse(q, k, v, units, grid, ib)
+    o, _ = _run_sparse(q, k, v, units, grid, ib, vt=vt)
     g = hq // hkv
     for h, s0, s1, _ in units:
         rows = np.arange(s0, s1)
@@ -130,7 +138,8 @@ def test_block_sparse_matches_oracle(n, k_blocks):
 
 @pytest.mark.parametrize("n,nv,ns,spread", [(3000, 40, 300, "local"), (2048, 64, 256, "scatter"),
                                             (4100, 200, 1500, "mixed"), (900, 0, 1, "diag_only")])
-def test_vertical_slash_matches_oracle(n, nv, ns, spread):
+@pytest.mark.parametrize("vt", [False, True])   # the vertical-slash kernel ignores vt
+def test_vertical_slash_matches_oracle(n, nv, ns, spread, vt):
     hq, hkv, d = 2, 1, 128
     q, k, v = _inputs(n, hq, hkv, d, seed=nv + ns)
     grid = [(_rs.RS_DENSE, 0, 0), (_rs.RS_VSLASH, nv, ns)]
@@ -150,7 +159,7 @@ def test_vertical_slash_matches_oracle(n, nv, ns, spread):
             D = np.array([0])
         fill_vs(ib, slot, 0, V, D)
         sets.append((V, D))
-    o, _ = _run_sparse(q, k, v, units, grid, ib)
+    o, _ = _run_sparse(q, k, v, units, grid, ib, vt=vt)
     for slot, (h, s0, s1, _, _) in enumerate(units):
         rows = np.arange(s0, s1)
         V, D = sets[slot]
@@ -205,3 +214,27 @@ def test_repeated_runs_bitwise_identical(fam):
         runs = [_run_sparse(q, k, v, units, grid, ib)[0] for _ in range(4)]
     for o in runs[1:]:
         assert np.array_equal(o, runs[0])
+
+
+@pytest.mark.parametrize("n,hkv,d,dtype", [(1000, 2, 128, "bf16"), (64, 1, 64, "bf16"), (130, 3, 128, "f32"),
+                                           (1, 1, 64, "bf16")])
+def test_transpose_v_layout(n, hkv, d, dtype):
+    """rs_transpose_v: [hkv][d][npad] bf16, keys permuted within groups of 16, zero past n."""
+    import torch
+    r = np.random.default_rng(n + d)
+    v = r.standard_normal((hkv, n, d)).astype(np.float32)
+    vd = dev(v, dtype)
+    qkv = _rs.make_qkv(vd, vd, vd)
+    npad = (n + 63) // 64 * 64
+    assert _rs.rs_vt_bytes(qkv) == hkv * d * npad * 2
+    buf = torch.full((hkv * d * npad * 2,), 0xAB, dtype=torch.uint8, device="cuda")
+    _rs.rs_transpose_v(qkv, buf)
+    torch.cuda.synchronize()
+    got = buf.cpu().numpy().view(np.uint16).reshape(hkv, d, npad)
+    perm = np.array([0, 1, 2, 3, 8, 9, 10, 11, 4, 5, 6, 7, 12, 13, 14, 15])
+    keys = (np.arange(npad) // 16) * 16 + perm[np.arange(npad) % 16]
+    want = np.zeros((hkv, d, npad), np.uint16)
+    vb = G.bf16_bits(v)                                 # round to nearest even, as on load
+    ok = keys < n
+    want[:, :, ok] = np.transpose(vb[:, keys[ok], :], (0, 2, 1))
+    np.testing.assert_array_equal(got, want)
