@@ -114,7 +114,8 @@ typedef struct rs_probe_out {
   int32_t *rows;     /* [nunits][rmax] sampled rows ascending, -1 padded        (written) */
   int32_t *subset;   /* [nunits][rmax] 0 = R, 1 = U, 2 = Bd, -1 padded           (written) */
   int32_t *nsub;     /* [nunits][3] subset sizes                                 (written) */
-  float *row_max;    /* [nunits][rmax] max scaled logit of the row over keys <= i */
+  float *row_max;    /* [nunits][rmax] max scaled logit of the row over keys <= i (rows
+                        as described under rs_probe) */
   float *row_sum;    /* [nunits][rmax] sum_j exp(l_ij - row_max)                  */
   float *col;        /* [nunits][n] col[j] = sum over R rows of a_ij (0 for j >= s1) */
   float *diag;       /* [nunits][n] diag[t] = sum over R rows of a_{i,i-t}           */
@@ -183,13 +184,16 @@ typedef struct rs_route_out {
 
 /* ---- probe (Sec. 3.2, Eq. 3; coverage of Sec. 3.2-3.3) -------------------------------
  * Scores mode (idx == NULL): for each unit, samples rows as in rs_probe_cfg, computes
- * exact softmax statistics of the sampled rows over keys [0, s1) and the recent-row
- * column and diagonal scores (flag RS_PROBE_ROWS), and the block-mean pooled logits L_bs
- * of every query head (flag RS_PROBE_BLOCKMEAN).
- * Coverage mode (idx != NULL, after a scores call on the same `out`): for each unit,
- * candidate and sampled row, m_i(c) = sum of a_ij over the candidate's key set, the subset
- * means, and the per-row descriptors (entropy, local mass).  `grid`/`ncand` give the
- * candidates (ignored in scores mode). */
+ * exact softmax statistics over keys [0, s1) of the last ceil(r_rec / 64) * 64 sampled rows
+ * (the recent rows among them), the recent-row column and diagonal scores (flag
+ * RS_PROBE_ROWS), and the block-mean pooled logits L_bs of every query head (flag
+ * RS_PROBE_BLOCKMEAN).
+ * Coverage mode (idx != NULL, after a scores call on the same `out`; reads its sampled
+ * rows): for each unit, candidate and sampled row, m_i(c) = sum of a_ij over the
+ * candidate's key set, the subset means, the per-row descriptors (entropy, local mass) and
+ * the softmax statistics (row_max, row_sum) of every sampled row, each row normalised by
+ * its own running max while the keys stream past.  `grid`/`ncand` give the candidates
+ * (ignored in scores mode). */
 size_t rs_probe_workspace_size(const rs_qkv *qkv, const rs_unit *units, int32_t nunits,
                                const rs_probe_cfg *cfg);
 rs_status rs_probe(const rs_qkv *qkv, const rs_unit *units, int32_t nunits,

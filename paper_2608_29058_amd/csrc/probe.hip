@@ -3,11 +3,12 @@
 //
 // For each unit (query head h, rows [s0, s1)) the sampled rows I = R u U u Bd are scored
 // exactly against keys [0, s1):
-//   pass 1  row statistics: max_j l_ij and sum_j exp(l_ij - max) over j <= i;
+//   pass 1  row statistics of the recent rows: max_j l_ij and sum_j exp(l_ij - max), j <= i;
 //   pass 2  normalised a_ij of the recent rows reduced into col[j] = sum_{i in R} a_ij and
 //           diag[t] = sum_{i in R} a_{i,i-t};
-//   pass 3  (coverage) m_i(c) = sum_{j in S_i(c)} a_ij for every candidate c, and per row
-//           the 64-key block entropy and the local-band mass.
+//   pass 3  (coverage) for every sampled row, with its own running max (online
+//           normalisation): the row statistics, m_i(c) = sum_{j in S_i(c)} a_ij for every
+//           candidate c, the 64-key block entropy and the local-band mass.
 // Logit tiles are bf16 MFMA products (S^T = K_tile x Q_rows^T, one lane per sampled row),
 // statistics fp32.  Every cross-workgroup reduction goes through per-chunk partials
 // summed in a fixed order, so results are deterministic.
@@ -51,6 +52,8 @@ struct ProbeArgs {
   float *row_max, *row_sum;
   // pass 2 partials / outputs
   float *col, *diag_part, *ent_part, *loc_part;
+  float *max_part, *sum_part;  // coverage pass: per (row, range) running max and sum
+  int stats_rows;              // rows (from the end of the row list) the statistics pass covers
   int diag_w;  // width of a diagonal partial row (kRange + rmax)
   // pass 3
   int ncand;
@@ -71,6 +74,35 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// cs += x[r] for every r = 0..15 (in that order) whose bit 8 (r / 4) + r % 4 of w is set:
+// sign-extended bit, and, add per element, in one instruction group.  Left to the optimiser,
+// bit-extract + and becomes a compare into a lane mask and a select (with a hazard wait per
+// element), or all bits are extracted ahead of the sums (16 more live registers); separate
+// groups per element each get a wait of their own.
+__device__ __forceinline__ void masked_add16(float &cs, uint32_t w, const float (&x)[16]) {
+  float t;
+  asm(
+      "v_bfe_i32 %1, %2, 0, 1\n\tv_and_b32 %1, %1, %3\n\tv_add_f32 %0, %0, %1\n\t"
+      "v_bfe_i32 %1, %2, 1, 1\n\tv_and_b32 %1, %1, %4\n\tv_add_f32 %0, %0, %1\n\t"
+      "v_bfe_i32 %1, %2, 2, 1\n\tv_and_b32 %1, %1, %5\n\tv_add_f32 %0, %0, %1\n\t"
+      "v_bfe_i32 %1, %2, 3, 1\n\tv_and_b32 %1, %1, %6\n\tv_add_f32 %0, %0, %1\n\t"
+      "v_bfe_i32 %1, %2, 8, 1\n\tv_and_b32 %1, %1, %7\n\tv_add_f32 %0, %0, %1\n\t"
+      "v_bfe_i32 %1, %2, 9, 1\n\tv_and_b32 %1, %1, %8\n\tv_add_f32 %0, %0, %1\n\t"
+      "v_bfe_i32 %1, %2, 10, 1\n\tv_and_b32 %1, %1, %9\n\tv_add_f32 %0, %0, %1\n\t"
+      "v_bfe_i32 %1, %2, 11, 1\n\tv_and_b32 %1, %1, %10\n\tv_add_f32 %0, %0, %1\n\t"
+      "v_bfe_i32 %1, %2, 16, 1\n\tv_and_b32 %1, %1, %11\n\tv_add_f32 %0, %0, %1\n\t"
+      "v_bfe_i32 %1, %2, 17, 1\n\tv_and_b32 %1, %1, %12\n\tv_add_f32 %0, %0, %1\n\t"
+      "v_bfe_i32 %1, %2, 18, 1\n\tv_and_b32 %1, %1, %13\n\tv_add_f32 %0, %0, %1\n\t"
+      "v_bfe_i32 %1, %2, 19, 1\n\tv_and_b32 %1, %1, %14\n\tv_add_f32 %0, %0, %1\n\t"
+      "v_bfe_i32 %1, %2, 24, 1\n\tv_and_b32 %1, %1, %15\n\tv_add_f32 %0, %0, %1\n\t"
+      "v_bfe_i32 %1, %2, 25, 1\n\tv_and_b32 %1, %1, %16\n\tv_add_f32 %0, %0, %1\n\t"
+      "v_bfe_i32 %1, %2, 26, 1\n\tv_and_b32 %1, %1, %17\n\tv_add_f32 %0, %0, %1\n\t"
+      "v_bfe_i32 %1, %2, 27, 1\n\tv_and_b32 %1, %1, %18\n\tv_add_f32 %0, %0, %1"
+      : "+v"(cs), "=&v"(t)
+      : "v"(w), "v"(x[0]), "v"(x[1]), "v"(x[2]), "v"(x[3]), "v"(x[4]), "v"(x[5]), "v"(x[6]), "v"(x[7]),
+        "v"(x[8]), "v"(x[9]), "v"(x[10]), "v"(x[11]), "v"(x[12]), "v"(x[13]), "v"(x[14]), "v"(x[15]));
 }
 
 // key offset within a 64-key tile of accumulator element (mb, r) for lane half hh
@@ -114,7 +146,9 @@ constexpr int vm_wait_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4)
 // workgroup, so column sums and diagonal partials of a range have a single writer.
 //   M_STATS   per (row, range): max and sum of exp over the range's visible keys
 //   M_SCORES  normalised a_ij of the recent rows -> col and diagonal partials
-//   M_COVER   normalised a_ij -> per-candidate kept mass, block entropy and local mass
+//   M_COVER   exp(l_ij - running max of the range) -> per (row, range): max, sum, kept mass
+//             per candidate, sum of B log B over the range's 64-key blocks (B the block's
+//             mass) and local mass, all relative to that max
 template <int D, typename InT, int MODE, int NCV>
 __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) {
   constexpr int KS = D / 16, CPR = D / 8, RPI = 64 / CPR, LPT = 64 / RPI / 4;
@@ -231,7 +265,7 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
       }
       nmc[s] = -INFINITY;
       isR[s] = false;
-      if constexpr (MODE != M_STATS) {
+      if constexpr (MODE == M_SCORES) {
         // a_ij = exp2(l_ij * c - (row_max * log2 e + log2 row_sum))
         if (ok) nmc[s] = -a.row_max[rofs] * kLog2e - __builtin_amdgcn_logf(a.row_sum[rofs]);
         isR[s] = ok && xr[s] >= nrows - U0.nR;
@@ -342,7 +376,39 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
         l_run[s] = l_run[s] * __builtin_amdgcn_exp2f((m_run[s] - m_use) * c) + ps;
         m_run[s] = m_new;
       } else {
-        const float nm = none ? -INFINITY : nmc[s];
+        float nm = none ? -INFINITY : nmc[s];
+        if constexpr (MODE == M_COVER) {
+          // online normalisation: the row's running max over this range (both halves of the
+          // row see the same max); raising it rescales every accumulator of the row, and
+          // S = sum B log B becomes alpha (S + log(alpha) Z) for alpha = exp(m_old - m_new)
+          float mx = -INFINITY;
+#pragma unroll
+          for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, x[mb][r]);
+          if (none) mx = -INFINITY;
+          mx = fmaxf(mx, __shfl_xor(mx, 32));
+          if (__ballot(mx > m_run[s]) != 0ull) {
+            const float zt = l_run[s] + __shfl_xor(l_run[s], 32);
+            if (mx > m_run[s]) {
+              if (m_run[s] != -INFINITY) {  // else every accumulator is still zero
+                const float la = (m_run[s] - mx) * c;  // log2 alpha
+                const float al = __builtin_amdgcn_exp2f(la);
+                ent[s] = al * (ent[s] + la * kLn2 * zt);
+                l_run[s] *= al;
+                loc[s] *= al;
+#pragma unroll
+                for (int q = 0; q < NCV; ++q) cov[s][q] *= al;
+#pragma unroll
+                for (int k = 0; k < kPrefVs; ++k) covv[s][k] *= al;
+#pragma unroll
+                for (int k = 0; k < kPrefBs; ++k) covb[s][k] *= al;
+              }
+              m_run[s] = mx;
+            }
+          }
+          nm = none ? -INFINITY : -m_run[s] * c;
+        }
         float tsum = 0.f;
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb)
@@ -377,19 +443,13 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
           wave_sync();
         } else {  // M_COVER
           const float bt = tsum + __shfl_xor(tsum, 32);  // mass of the row in this 64-key block
-          if (bt > 0.f) ent[s] -= bt * logf(bt);
+          if (bt > 0.f) ent[s] += bt * logf(bt);
+          l_run[s] += tsum;
           // kept mass of a 64-bit key mask (bits of this lane's keys after the half shift)
           auto masked = [&](uint64_t M) -> float {
             float cs = 0.f;
-#pragma unroll
-            for (int mb = 0; mb < 2; ++mb) {
-              const uint32_t w = (uint32_t)(M >> (32 * mb));
-#pragma unroll
-              for (int r = 0; r < 16; ++r) {
-                const uint32_t keep = (uint32_t)__builtin_amdgcn_sbfe((int)w, 8 * (r >> 2) + (r & 3), 1);
-                cs += __builtin_bit_cast(float, keep & __builtin_bit_cast(uint32_t, x[mb][r]));
-              }
-            }
+            masked_add16(cs, (uint32_t)M, x[0]);
+            masked_add16(cs, (uint32_t)(M >> 32), x[1]);
             return cs;
           };
           // mass of the keys j >= lo: whole tile, none, or element-wise (wave-uniform choice)
@@ -481,8 +541,11 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
           }
         } else if constexpr (MODE == M_COVER) {
           const float lt = loc[s] + __shfl_xor(loc[s], 32);
+          const float zt = l_run[s] + __shfl_xor(l_run[s], 32);
           if (ok) {
-            a.ent_part[o] = ent[s];  // the stats partials were consumed before this pass
+            a.max_part[o] = m_run[s];  // raw dot product, as in the statistics pass
+            a.sum_part[o] = zt;
+            a.ent_part[o] = ent[s];
             a.loc_part[o] = lt;
           }
 #pragma unroll
@@ -530,7 +593,7 @@ __global__ void probe_stats_combine_kernel(const ProbeArgs a) {
   const int u = blockIdx.y;
   const ProbeUnit U = a.units[u];
   const int x = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (x >= U.nrows) return;
+  if (x >= U.nrows || x < U.nrows - a.stats_rows) return;
   const int row = a.rows[(long long)u * a.rmax + x];
   const int nch = row / kRange + 1;
   const float *pm = a.ent_part + ((long long)u * a.rmax + x) * a.nchunks;
@@ -570,69 +633,82 @@ __global__ void probe_finish_kernel(const ProbeArgs a, float *diag, float *entro
   }
 }
 
-// descriptors: entropy and local mass of each sampled row, one wave per row
-__global__ void probe_desc_kernel(const ProbeArgs a, float *entropy, float *local) {
+// coverage pass partials of each sampled row combined over its ranges (one wave per row):
+// with M the row's max, a range's partials (relative to its own max m) are weighted by
+// w = exp(m - M); Z = sum w z, m_i(c) = sum w cov(c) / Z, local mass likewise, and with
+// S = sum over 64-key blocks of B log B (B relative to M) = sum w (s + log(w) z), the block
+// entropy is log Z - S / Z.  Writes row_max / row_sum, the descriptors and m_i(c).
+// grid (ceil(rmax / 4), nunits), 256 threads
+__global__ void cover_combine_kernel(const ProbeArgs a, float *entropy, float *local, float *cov_rows) {
   const int u = blockIdx.y;
   const ProbeUnit U = a.units[u];
   const int x = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (x >= U.nrows) return;
   const int row = a.rows[(long long)u * a.rmax + x];
   const int nch = row / kRange + 1;
-  const float *pe = a.ent_part + ((long long)u * a.rmax + x) * a.nchunks;
-  const float *pl = a.loc_part + ((long long)u * a.rmax + x) * a.nchunks;
-  float e = 0.f, l = 0.f;
+  const long long base = ((long long)u * a.rmax + x) * a.nchunks;
+  const float *pm = a.max_part + base, *pz = a.sum_part + base;
+  const float *pe = a.ent_part + base, *pl = a.loc_part + base;
+  float M = -INFINITY;
+  for (int ch = lane; ch < nch; ch += 64) M = fmaxf(M, pm[ch]);
+  M = wave_max(M);
+  // a range with no visible key has z = 0 (and m = -inf): it contributes nothing
+  auto lw = [&](int ch) { return pz[ch] > 0.f ? (pm[ch] - M) * a.c : -INFINITY; };  // log2 w
+  float Z = 0.f, S = 0.f, L = 0.f;
   for (int ch = lane; ch < nch; ch += 64) {
-    e += pe[ch];
-    l += pl[ch];
+    const float l2 = lw(ch);
+    if (l2 == -INFINITY) continue;
+    const float w = __builtin_amdgcn_exp2f(l2);
+    Z += w * pz[ch];
+    S += w * (pe[ch] + l2 * kLn2 * pz[ch]);
+    L += w * pl[ch];
   }
-  e = wave_sum(e);
-  l = wave_sum(l);
+  Z = wave_sum(Z);
+  S = wave_sum(S);
+  L = wave_sum(L);
+  const float inv = Z > 0.f ? 1.f / Z : 0.f;
+  for (int c = 0; c < a.ncand; ++c) {
+    float m = 1.f;
+    if (a.cand[c].fam != RS_DENSE) {
+      const float *pc = a.cov_part + (((long long)u * a.ncand + c) * a.rmax + x) * a.nchunks;
+      float acc = 0.f;
+      for (int ch = lane; ch < nch; ch += 64) {
+        const float l2 = lw(ch);
+        if (l2 != -INFINITY) acc += __builtin_amdgcn_exp2f(l2) * pc[ch];
+      }
+      m = wave_sum(acc) * inv;
+    }
+    if (lane == 0) cov_rows[((long long)u * a.ncand + c) * a.rmax + x] = m;
+  }
   if (lane == 0) {
+    const long long o = (long long)u * a.rmax + x;
+    a.row_max[o] = M * a.scale;
+    a.row_sum[o] = Z;
     const int nvis = row / 64 + 1;
-    entropy[(long long)u * a.rmax + x] = nvis > 1 ? e / logf((float)nvis) : 0.f;
-    local[(long long)u * a.rmax + x] = l;
+    entropy[o] = (nvis > 1 && Z > 0.f) ? (logf(Z) - S * inv) / logf((float)nvis) : 0.f;
+    local[o] = L * inv;
   }
 }
 
-// coverage per sampled row and candidate, then the subset means; grid (ncand, nunits)
-__global__ void cover_finish_kernel(const ProbeArgs a, float *cov_rows, float *cov) {
+// subset means of the per-row coverage; grid (ncand, nunits)
+__global__ void cover_means_kernel(const ProbeArgs a, const float *cov_rows, float *cov) {
   const int u = blockIdx.y, c = blockIdx.x;
   const ProbeUnit U = a.units[u];
-  __shared__ float sm[kProbeMaxRows];
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  for (int x = wave; x < U.nrows; x += 4) {
-    const int row = a.rows[(long long)u * a.rmax + x];
-    float m;
-    if (a.cand[c].fam == RS_DENSE) {
-      m = 1.f;
-    } else {
-      const int nch = row / kRange + 1;
-      const float *pc = a.cov_part + (((long long)u * a.ncand + c) * a.rmax + x) * a.nchunks;
-      float acc = 0.f;
-      for (int ch = lane; ch < nch; ch += 64) acc += pc[ch];
-      m = wave_sum(acc);
-    }
-    if (lane == 0) {
-      sm[x] = m;
-      cov_rows[((long long)u * a.ncand + c) * a.rmax + x] = m;
+  if (threadIdx.x != 0) return;
+  float tot = 0.f, sub[3] = {0.f, 0.f, 0.f};
+  int cnt[3] = {0, 0, 0};
+  const float *m = cov_rows + ((long long)u * a.ncand + c) * a.rmax;
+  for (int r = 0; r < U.nrows; ++r) {
+    const int s = a.subset[(long long)u * a.rmax + r];
+    tot += m[r];
+    if (s >= 0 && s < 3) {
+      sub[s] += m[r];
+      cnt[s]++;
     }
   }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    float tot = 0.f, sub[3] = {0.f, 0.f, 0.f};
-    int cnt[3] = {0, 0, 0};
-    for (int r = 0; r < U.nrows; ++r) {
-      const int s = a.subset[(long long)u * a.rmax + r];
-      tot += sm[r];
-      if (s >= 0 && s < 3) {
-        sub[s] += sm[r];
-        cnt[s]++;
-      }
-    }
-    float *o = cov + ((long long)u * a.ncand + c) * 4;
-    o[0] = U.nrows ? tot / U.nrows : 0.f;
-    for (int s2 = 0; s2 < 3; ++s2) o[1 + s2] = cnt[s2] ? sub[s2] / cnt[s2] : 0.f;
-  }
+  float *o = cov + ((long long)u * a.ncand + c) * 4;
+  o[0] = U.nrows ? tot / U.nrows : 0.f;
+  for (int s2 = 0; s2 < 3; ++s2) o[1 + s2] = cnt[s2] ? sub[s2] / cnt[s2] : 0.f;
 }
 
 // ---- block-mean estimator ----------------------------------------------------------------
@@ -782,7 +858,7 @@ size_t probe_ws_bytes(const rs_qkv *qkv, int32_t nunits, const rs_probe_cfg *cfg
   ar.take<ProbeUnit>(nunits);
   ar.take<int4>(nunits);
   ar.take<float>((size_t)nunits * nchunks * (kRange + rmax));     // diag partials
-  ar.take<float>((size_t)nunits * nchunks * rmax * 2);            // entropy / local partials
+  ar.take<float>((size_t)nunits * nchunks * rmax * 4);            // max / sum / entropy / local partials
   ar.take<float>((size_t)nunits * nchunks * rmax * kMaxCand);     // coverage partials
   if (cfg->flags & RS_PROBE_BLOCKMEAN) {
     ar.take<float>((size_t)qkv->hq * nb * qkv->d);
@@ -796,8 +872,13 @@ static hipError_t launch_rows(const ProbeArgs &pa, int nunits, int ngroups, int 
                               float *cov_rows, float *cov, hipStream_t st) {
   const int npairs = ((pa.rmax + 31) / 32 + 1) / 2;  // row-block pairs of the fullest unit
   if (mode == 0) {
-    hipLaunchKernelGGL((probe_range_kernel<D, InT, M_STATS, 1>), dim3(pa.nchunks, ngroups, npairs), dim3(256), 0, st, pa);
-    hipLaunchKernelGGL(probe_stats_combine_kernel, dim3((pa.rmax + 3) / 4, nunits), dim3(256), 0, st, pa);
+    // statistics of the row pairs holding recent rows (pairs are taken from the end of the
+    // ascending row list, where the recent rows are); the coverage pass normalises online
+    const int spairs = std::min(npairs, pa.stats_rows / 64);
+    if (spairs > 0) {
+      hipLaunchKernelGGL((probe_range_kernel<D, InT, M_STATS, 1>), dim3(pa.nchunks, ngroups, spairs), dim3(256), 0, st, pa);
+      hipLaunchKernelGGL(probe_stats_combine_kernel, dim3((pa.rmax + 3) / 4, nunits), dim3(256), 0, st, pa);
+    }
     hipLaunchKernelGGL((probe_range_kernel<D, InT, M_SCORES, 1>), dim3(pa.nchunks, ngroups), dim3(256), 0, st, pa);
     hipLaunchKernelGGL(probe_finish_kernel, dim3((pa.n + 255) / 256, nunits), dim3(256), 0, st, pa, diag, ent, loc);
   } else {
@@ -805,8 +886,8 @@ static hipError_t launch_rows(const ProbeArgs &pa, int nunits, int ngroups, int 
       hipLaunchKernelGGL((probe_range_kernel<D, InT, M_COVER, 4>), dim3(pa.nchunks, ngroups, npairs), dim3(256), 0, st, pa);
     else
       hipLaunchKernelGGL((probe_range_kernel<D, InT, M_COVER, kMaxCand>), dim3(pa.nchunks, ngroups, npairs), dim3(256), 0, st, pa);
-    hipLaunchKernelGGL(cover_finish_kernel, dim3(pa.ncand, nunits), dim3(256), 0, st, pa, cov_rows, cov);
-    hipLaunchKernelGGL(probe_desc_kernel, dim3((pa.rmax + 3) / 4, nunits), dim3(256), 0, st, pa, ent, loc);
+    hipLaunchKernelGGL(cover_combine_kernel, dim3((pa.rmax + 3) / 4, nunits), dim3(256), 0, st, pa, ent, loc, cov_rows);
+    hipLaunchKernelGGL(cover_means_kernel, dim3(pa.ncand, nunits), dim3(64), 0, st, pa, cov_rows, cov);
   }
   return hipGetLastError();
 }
@@ -826,6 +907,8 @@ rs_status probe_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int
   float *diag_part = ar.take<float>((size_t)nunits * nchunks * (kRange + rmax));
   float *ent_part = ar.take<float>((size_t)nunits * nchunks * rmax);
   float *loc_part = ar.take<float>((size_t)nunits * nchunks * rmax);
+  float *max_part = ar.take<float>((size_t)nunits * nchunks * rmax);
+  float *sum_part = ar.take<float>((size_t)nunits * nchunks * rmax);
   float *cov_part = ar.take<float>((size_t)nunits * nchunks * rmax * kMaxCand);
   float *qbar = nullptr, *kbar = nullptr;
   if (cfg->flags & RS_PROBE_BLOCKMEAN) {
@@ -890,9 +973,11 @@ rs_status probe_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int
   pa.sq_h = qkv->sq_h; pa.sq_t = qkv->sq_t; pa.sk_h = qkv->sk_h; pa.sk_t = qkv->sk_t;
   pa.n = qkv->n; pa.group = qkv->hq / qkv->hkv; pa.rmax = rmax; pa.nchunks = nchunks;
   pa.c = scale * kLog2e; pa.scale = scale; pa.local_w = cfg->local_w;
+  pa.stats_rows = (cfg->r_rec + 63) / 64 * 64;
   pa.units = d_units; pa.groups = d_groups; pa.rows = out->rows; pa.subset = out->subset;
   pa.row_max = out->row_max; pa.row_sum = out->row_sum;
   pa.col = out->col; pa.diag_part = diag_part; pa.ent_part = ent_part; pa.loc_part = loc_part;
+  pa.max_part = max_part; pa.sum_part = sum_part;
   pa.diag_w = kRange + rmax;
   pa.cov_part = cov_part;
   if (cover) {
