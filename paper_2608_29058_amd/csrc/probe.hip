@@ -69,11 +69,13 @@ struct ProbeArgs {
   float *cov_part;
 };
 
-// Orders this wave's LDS writes before its following LDS reads by other lanes.
+// Orders this wave's LDS writes before its following LDS reads by other lanes.  The LDS
+// executes one wave's accesses in issue order, so only the compiler has to be kept from
+// moving them; a memory fence here would also make it wait for the K tile copy in flight.
 __device__ __forceinline__ void wave_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  asm volatile("" ::: "memory");
   __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  asm volatile("" ::: "memory");
 }
 
 // cs += x[r] for every r = 0..15 (in that order) whose bit 8 (r / 4) + r % 4 of w is set:
@@ -149,15 +151,19 @@ constexpr int vm_wait_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4)
 //   M_COVER   exp(l_ij - running max of the range) -> per (row, range): max, sum, kept mass
 //             per candidate, sum of B log B over the range's 64-key blocks (B the block's
 //             mass) and local mass, all relative to that max
-template <int D, typename InT, int MODE, int NCV>
+// GEN: the candidates without prefetched bitmap words (cov_cand) may include vertical-slash
+// and block-sparse ones, whose words are then read inside the tile loop; without GEN they
+// are all A-shape (no memory reads).
+template <int D, typename InT, int MODE, int NCV, bool GEN = true>
 __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) {
   constexpr int KS = D / 16, CPR = D / 8, RPI = 64 / CPR, LPT = 64 / RPI / 4;
   constexpr int TE = 64 * D;
   // two K tile buffers: the next tile (and, for coverage, its bitmap words) is fetched while
-  // the current one is computed.  Deeper rings do not help here: the compiler waits for all
-  // LDS-bound copies before any LDS read.
-  constexpr int NBUF = 2;
-  __shared__ __align__(16) bf16 sKb[NBUF][TE];
+  // the current one is computed.  The copy is issued once both blocks have read the current
+  // tile (after the second block's products): the compiler makes every LDS read wait for the
+  // LDS-bound copies in flight, so the copy overlaps the second block's softmax and coverage
+  // work.
+  __shared__ __align__(16) bf16 sKb[2][TE];
   __shared__ int sRows[2][32];
 
   const int rg = blockIdx.x;
@@ -189,7 +195,7 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
   [[maybe_unused]] const __amdgpu_buffer_rsrc_t rK = __builtin_amdgcn_make_buffer_rsrc(
       (void *)Kp, (short)0, (int)((uint32_t)(a.n - 1) * bK + D * sizeof(InT)), 0x00020000);
   const uint32_t voK = (uint32_t)lrow0 * bK + 16u * (uint32_t)lchunk;
-  auto issue_tile = [&](bf16 *dst, int k0) {
+  auto issue_tile = [&](bf16 *dst, int k0) __attribute__((always_inline)) {
     bf16 *dK = dst + wave * RPI * D;
 #pragma unroll
     for (int i = 0; i < LPT; ++i) {
@@ -291,7 +297,7 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
       uint64_t mv[kPrefVs];  // column bits of the tile's keys
       uint32_t bw[2][kPrefBs];
     };
-    auto fetch = [&](int k0, Pref &f) {
+    auto fetch = [&](int k0, Pref &f) __attribute__((always_inline)) {
       if constexpr (MODE == M_COVER) {
         const int kt = k0 >> 6;
 #pragma unroll
@@ -321,12 +327,10 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
       }
     };
 
-    // ---- one block against one tile -------------------------------------------------------
-    auto block_tile = [&](const bf16 *sK, int k0, int s, const Pref &f) {
+    // ---- one block against one tile: products, then the rest -----------------------------
+    auto qk_block = [&](const bf16 *sK, int k0, int s, f32x16 (&sacc)[2]) __attribute__((always_inline)) {
       const int rmx = s ? rmax1 : rmax0;
       if (u < 0 || rmx < k0) return;  // block absent or entirely before the tile
-      const int i = row[s];
-      f32x16 sacc[2];
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb) {
 #pragma unroll
@@ -337,6 +341,11 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
           sacc[mb] = mfma32(kf, qf[s][ks], sacc[mb]);
         }
       }
+    };
+    auto block_tile = [&](const f32x16 (&sacc)[2], int k0, int s, const Pref &f) __attribute__((always_inline)) {
+      const int rmx = s ? rmax1 : rmax0;
+      if (u < 0 || rmx < k0) return;  // block absent or entirely before the tile
+      const int i = row[s];
       // keys after the row: a row before the tile sees none of it; a row inside the tile
       // (some lane of the wave) masks element-wise
       const bool none = i < k0;
@@ -446,14 +455,14 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
           if (bt > 0.f) ent[s] += bt * logf(bt);
           l_run[s] += tsum;
           // kept mass of a 64-bit key mask (bits of this lane's keys after the half shift)
-          auto masked = [&](uint64_t M) -> float {
+          auto masked = [&](uint64_t M) __attribute__((always_inline)) -> float {
             float cs = 0.f;
             masked_add16(cs, (uint32_t)M, x[0]);
             masked_add16(cs, (uint32_t)(M >> 32), x[1]);
             return cs;
           };
           // mass of the keys j >= lo: whole tile, none, or element-wise (wave-uniform choice)
-          auto from = [&](int lo) -> float {
+          auto from = [&](int lo) __attribute__((always_inline)) -> float {
             const bool all = lo <= k0, nil = lo > k0 + 63;
             if (__ballot(all) == ~0ull) return tsum;
             if (__ballot(nil) == ~0ull) return 0.f;
@@ -482,6 +491,7 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
               const float sink = k0 + 63 < cd.a ? tsum : k0 >= cd.a ? 0.f : masked(prefix_mask(cd.a - k0) >> (4 * hh));
               // window keys j >= i - b + 1 that are not sink keys
               cov[s][q] += sink + from(max(i - cd.b + 1, cd.a));
+            } else if (!GEN) {
             } else if (cd.fam == RS_VSLASH) {
               const long long vr = ((long long)u * a.ncand_vs + cd.cl) * a.nwords;
               const uint64_t md = __builtin_bitreverse64(bits64_at(a.vs_dbits + vr, a.nwords, i - k0 - 63));
@@ -501,21 +511,23 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
     // no wait for them lands inside the tile loop (where it would drain the tile copies).
     __builtin_amdgcn_s_waitcnt(vm_wait_imm(0));
     Pref fcur, fnext;
-#pragma unroll
-    for (int t = 0; t < NBUF - 1; ++t)
-      if (t < nt) issue_tile(sKb[t], c0 + 64 * t);
+    issue_tile(sKb[0], c0);
     fetch(c0, fcur);
     for (int t = 0; t < nt; ++t) {
       __builtin_amdgcn_s_waitcnt(vm_wait_imm(0));  // tile t (and its bitmap words) landed
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
       __builtin_amdgcn_s_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-      if (t + NBUF - 1 < nt) {
-        issue_tile(sKb[(t + NBUF - 1) % NBUF], c0 + 64 * (t + NBUF - 1));
-        fetch(c0 + 64 * (t + 1), fnext);
+      const int k0 = c0 + 64 * t;
+      f32x16 S[2];
+      qk_block(sKb[t & 1], k0, 0, S);
+      block_tile(S, k0, 0, fcur);
+      qk_block(sKb[t & 1], k0, 1, S);
+      if (t + 1 < nt) {
+        issue_tile(sKb[(t + 1) & 1], k0 + 64);
+        fetch(k0 + 64, fnext);
       }
-      block_tile(sKb[t % NBUF], c0 + 64 * t, 0, fcur);
-      block_tile(sKb[t % NBUF], c0 + 64 * t, 1, fcur);
+      block_tile(S, k0, 1, fcur);
       fcur = fnext;
     }
 
@@ -882,7 +894,11 @@ static hipError_t launch_rows(const ProbeArgs &pa, int nunits, int ngroups, int 
     hipLaunchKernelGGL((probe_range_kernel<D, InT, M_SCORES, 1>), dim3(pa.nchunks, ngroups), dim3(256), 0, st, pa);
     hipLaunchKernelGGL(probe_finish_kernel, dim3((pa.n + 255) / 256, nunits), dim3(256), 0, st, pa, diag, ent, loc);
   } else {
-    if (pa.ncov <= 4)
+    bool ashape_only = true;
+    for (int q = 0; q < pa.ncov; ++q) ashape_only = ashape_only && pa.cand[pa.cov_cand[q]].fam == RS_ASHAPE;
+    if (ashape_only && pa.ncov <= 2)
+      hipLaunchKernelGGL((probe_range_kernel<D, InT, M_COVER, 2, false>), dim3(pa.nchunks, ngroups, npairs), dim3(256), 0, st, pa);
+    else if (pa.ncov <= 4)
       hipLaunchKernelGGL((probe_range_kernel<D, InT, M_COVER, 4>), dim3(pa.nchunks, ngroups, npairs), dim3(256), 0, st, pa);
     else
       hipLaunchKernelGGL((probe_range_kernel<D, InT, M_COVER, kMaxCand>), dim3(pa.nchunks, ngroups, npairs), dim3(256), 0, st, pa);
