@@ -65,19 +65,23 @@ __device__ int block_incl_scan(int v, int *sWave, int *tot) {
   return x + off;
 }
 
-// Radix select over keys of vals[0, len): finds the key T of rank K (1-based, descending)
-// and how many elements equal to T are taken.  Requires len > K >= 1.
+// Radix select over keys of vals[0, len): finds the key T of rank K (1-based, descending),
+// how many elements equal to T are taken and how many there are.  Requires len > K >= 1.
+// sHist holds one 256-bin histogram per wave of the group (values of similar magnitude share
+// their leading digits: one histogram for all waves would serialise their atomics).
 template <int NT>
-__device__ void radix_select(const float *vals, int len, int K, uint32_t *T_out, int *take_out, int *sHist,
-                             int *sBcast) {
+__device__ void radix_select(const float *vals, int len, int K, uint32_t *T_out, int *take_out, int *eq_out,
+                             int *sHist, int *sBcast) {
+  constexpr int NWV = NT / 64;
   uint32_t prefix = 0, maskhi = 0;
   int krem = K;
+  int *myHist = sHist + 256 * (gtid<NT>() >> 6);
   for (int byte = 3; byte >= 0; --byte) {
-    for (int b = gtid<NT>(); b < 256; b += NT) sHist[b] = 0;
+    for (int b = gtid<NT>(); b < 256 * NWV; b += NT) sHist[b] = 0;
     gsync<NT>();
     for (int i = gtid<NT>(); i < len; i += NT) {
       const uint32_t key = float_key(vals[i]);
-      if ((key & maskhi) == prefix) atomicAdd(&sHist[(key >> (8 * byte)) & 255u], 1);
+      if ((key & maskhi) == prefix) atomicAdd(&myHist[(key >> (8 * byte)) & 255u], 1);
     }
     gsync<NT>();
     if (gtid<NT>() < 64) {
@@ -86,7 +90,8 @@ __device__ void radix_select(const float *vals, int len, int K, uint32_t *T_out,
       int c4[4], own = 0;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        c4[q] = sHist[255 - 4 * l - q];
+        c4[q] = 0;
+        for (int w = 0; w < NWV; ++w) c4[q] += sHist[256 * w + 255 - 4 * l - q];
         own += c4[q];
       }
       int incl = own;
@@ -98,23 +103,26 @@ __device__ void radix_select(const float *vals, int len, int K, uint32_t *T_out,
       const int excl = incl - own;
       // the selected bin lies in the first lane whose inclusive count reaches krem
       if (excl < krem && incl >= krem) {
-        int cum = excl, sel = 255 - 4 * l;
+        int cum = excl, sel = 255 - 4 * l, cnt = 0;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           if (cum + c4[q] >= krem) {
             sel = 255 - 4 * l - q;
+            cnt = c4[q];
             break;
           }
           cum += c4[q];
         }
         sBcast[0] = sel;
         sBcast[1] = krem - cum;
+        sBcast[2] = cnt;  // after the last digit: the number of keys equal to T
       }
     }
     gsync<NT>();
     prefix |= (uint32_t)sBcast[0] << (8 * byte);
     maskhi |= 0xffu << (8 * byte);
     krem = sBcast[1];
+    *eq_out = sBcast[2];
     gsync<NT>();
   }
   *T_out = prefix;
@@ -130,10 +138,15 @@ __device__ void select_top(const float *vals, int len, int K, int *sHist, int *s
     return;
   }
   uint32_t T;
-  int take;
-  radix_select<NT>(vals, len, K, &T, &take, sHist, sBcast);
-  for (int i = gtid<NT>(); i < len; i += NT)
-    if (float_key(vals[i]) > T) emit(i);
+  int take, neq;
+  radix_select<NT>(vals, len, K, &T, &take, &neq, sHist, sBcast);
+  // every key equal to T is taken when there are no more of them than needed (the usual case)
+  const bool all_eq = take == neq;
+  for (int i = gtid<NT>(); i < len; i += NT) {
+    const uint32_t key = float_key(vals[i]);
+    if (key > T || (all_eq && key == T)) emit(i);
+  }
+  if (all_eq) return;
   // equal keys: lowest positions first
   int seen = 0;
   for (int i0 = 0; i0 < len && seen < take; i0 += NT) {
@@ -188,7 +201,7 @@ constexpr int kVsGather = 8192;  // elements of the largest set kept in LDS
 __global__ void __launch_bounds__(1024) vs_select_kernel(const VsArgs a) {
   constexpr int NT = 1024;
   extern __shared__ uint32_t sBits[];  // nwords
-  __shared__ int sHist[256], sBcast[2], sWave[NT / 64];
+  __shared__ int sHist[256 * (NT / 64)], sBcast[3], sWave[NT / 64];
   __shared__ float sVal[kVsGather];
   __shared__ int sPos[kVsGather];
   const int arr = blockIdx.x;
@@ -258,7 +271,7 @@ __global__ void __launch_bounds__(256) bs_select_kernel(const BsArgs a) {
   constexpr int NT = 64;
   constexpr int SP = 256;  // sort capacity (k_max <= 256)
   constexpr int NBW = kMaxN / 64 / 32;
-  __shared__ int sHistA[4][256], sBcastA[4][2], sCntA[4];
+  __shared__ int sHistA[4][256], sBcastA[4][3], sCntA[4];
   __shared__ unsigned long long sKeyA[4][SP];
   __shared__ uint32_t sBA[4][NBW];
   const int w = (int)(threadIdx.x >> 6), l = (int)(threadIdx.x & 63u);
