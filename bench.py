@@ -133,9 +133,9 @@ def tiles_vs(s0, s1, V, D):
 # ---- HBM traffic of the dominant kernel ------------------------------------------------------
 
 def measured_traffic(kernel):
-    """Calibrated HBM bytes per launch from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE runs
-    (profiles/attn_traffic.json), or None when the attention source or the dominant kernel
-    differs from the one measured."""
+    """Calibrated HBM bytes per launch of ``kernel`` from the committed rocprofv3 FETCH_SIZE /
+    WRITE_SIZE runs (profiles/attn_traffic.json, one entry per family launch), or None when the
+    attention source differs from the one measured or the kernel was not measured."""
     import hashlib
     try:
         with open(os.path.join(ROOT, "profiles", "attn_traffic.json")) as f:
@@ -144,9 +144,9 @@ def measured_traffic(kernel):
             sha = hashlib.sha256(f.read()).hexdigest()
     except OSError:
         return None
-    if t.get("attn_hip_sha256") != sha or t.get("kernel") != kernel:
+    if t.get("attn_hip_sha256") != sha:
         return None
-    return t.get("hbm_bytes_per_launch")
+    return (t.get("kernels", {}).get(kernel) or {}).get("hbm_bytes_per_launch")
 
 
 # ---- CPU baseline: the oracle on a bounded sample ------------------------------------------
