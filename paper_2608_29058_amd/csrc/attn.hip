@@ -88,7 +88,11 @@ struct TileRef {
   int tag;   // bit 0: rows of waves 0-1 use it, bit 1: rows of waves 2-3 (block-sparse)
   Win3 wd;   // vertical-slash: diagonal-bitmap words of this lane's row (prefetched)
   Win3 wv;   // vertical-slash: column-bitmap words of the tile (prefetched)
+  int hm;    // 32-key halves of the tile that are copied and may be kept (bit 0: keys 0-31)
 };
+
+// bit 2m of the result: either of bits 2m, 2m + 1 of w (64-key tile m of a word of 32-key halves)
+__device__ __forceinline__ uint32_t tile_bits(uint32_t w) { return (w | (w >> 1)) & 0x55555555u; }
 
 // One work item: query tile `item & 0xffff` of unit `item >> 16` of the launch's unit list.
 // VT: V is read from the transposed copy (tiles of D rows x 64 keys), else from V itself.
@@ -142,7 +146,9 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
   int *sG = nullptr;
 
   if constexpr (PAT == P_VS) {
-    __shared__ uint32_t sTBbuf[kMaxTiles / 32];
+    // sTB: one bit per 32-key half of the key range the block's diagonals touch; a 64-key tile
+    // is in the list when either of its halves is, and only those halves are copied
+    __shared__ uint32_t sTBbuf[kMaxTiles / 16];
     __shared__ int sGbuf[kMaxGather];
     __shared__ int sScan[NW + 1];
     sTB = sTBbuf;
@@ -154,20 +160,20 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
     const int ndc = a.vs_count[vsrow * 2 + 1];
     vbits = a.vs_vbits + vsrow * a.nwords;
     dbits = a.vs_dbits + vsrow * a.nwords;
-    const int nwt = (last_tile >> 5) + 1;
+    const int nwt = ((2 * last_tile + 1) >> 5) + 1;
     for (int w = tid; w < nwt; w += NT) sTB[w] = 0u;
     __syncthreads();
     // diagonal t covers keys [r_lo - t, r_hi - 1 - t] of this tile's rows
     for (int x = tid; x < ndc; x += NT) {
       const int t = dsorted[x];
       if (t < 0 || t > r_hi - 1) continue;
-      const int lo = max(0, r_lo - t) >> 6, hi = (r_hi - 1 - t) >> 6;
-      for (int kt = lo; kt <= hi; ++kt) atomicOr(&sTB[kt >> 5], 1u << (kt & 31));
+      const int lo = max(0, r_lo - t) >> 5, hi = (r_hi - 1 - t) >> 5;
+      for (int kh = lo; kh <= hi; ++kh) atomicOr(&sTB[kh >> 5], 1u << (kh & 31));
     }
     __syncthreads();
     {
       int cnt = 0;
-      for (int w = 0; w < nwt; ++w) cnt += __builtin_popcount(sTB[w]);
+      for (int w = 0; w < nwt; ++w) cnt += __builtin_popcount(tile_bits(sTB[w]));
       n_contig = cnt;
     }
     // vertical columns outside the diagonal tiles are gathered, ascending
@@ -177,8 +183,8 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
       const int j = (x < nvc) ? vsorted[x] : 0x7fffffff;
       bool f = false;
       if (x < nvc && j >= 0 && j <= r_hi - 1) {
-        const int kt = j >> 6;
-        f = !((sTB[kt >> 5] >> (kt & 31)) & 1u);
+        const int kh = j >> 5;
+        f = !((sTB[kh >> 5] >> (kh & 31)) & 1u);
       }
       const uint64_t bal = __ballot(f);
       const int before = __popcll(bal & ((1ull << lane) - 1ull));
@@ -197,8 +203,8 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
     n_gather = min(total, kMaxGather);
     __syncthreads();
     ntiles = n_contig + (n_gather + 63) / 64;
-    st0 = 0;                         // bitmap word of the next contiguous tile
-    st1 = nwt > 0 ? (int)sTB[0] : 0; // remaining bits of that word
+    st0 = 0;                                   // bitmap word of the next contiguous tile
+    st1 = nwt > 0 ? (int)tile_bits(sTB[0]) : 0; // remaining tiles of that word (even bits)
   } else if constexpr (PAT == P_DENSE) {
     ntiles = last_tile + 1;
   } else if constexpr (PAT == P_ASHAPE) {
@@ -235,9 +241,9 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
   auto next_tile = [&]() -> TileRef {
     const int t = t_next++;
     if constexpr (PAT == P_DENSE) {
-      return TileRef{t * 64, 3, {0u, 0u, 0u}, {0u, 0u, 0u}};
+      return TileRef{t * 64, 3, {0u, 0u, 0u}, {0u, 0u, 0u}, 3};
     } else if constexpr (PAT == P_ASHAPE) {
-      return TileRef{(t < st0 ? t : st1 + (t - st0)) * 64, 3, {0u, 0u, 0u}, {0u, 0u, 0u}};
+      return TileRef{(t < st0 ? t : st1 + (t - st0)) * 64, 3, {0u, 0u, 0u}, {0u, 0u, 0u}, 3};
     } else if constexpr (PAT == P_BS) {
       const int va = st0 < bs_na ? bs_a[st0] : 0x7fffffff;
       const int vb = st1 < bs_nb ? bs_b[st1] : 0x7fffffff;
@@ -245,21 +251,21 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
       const int tag = (va == v ? 1 : 0) | (vb == v ? 2 : 0);
       st0 += va == v;
       st1 += vb == v;
-      return TileRef{v * 64, tag, {0u, 0u, 0u}, {0u, 0u, 0u}};
+      return TileRef{v * 64, tag, {0u, 0u, 0u}, {0u, 0u, 0u}, 3};
     } else {
       if (t < n_contig) {
-        while (st1 == 0) st1 = (int)sTB[++st0];
+        while (st1 == 0) st1 = (int)tile_bits(sTB[++st0]);
         const int bit = __builtin_ctz((uint32_t)st1);
         st1 &= st1 - 1;
-        const int key0 = (st0 * 32 + bit) * 64;
-        TileRef tr{key0, 3, {0u, 0u, 0u}, {0u, 0u, 0u}};
+        const int key0 = (st0 * 16 + (bit >> 1)) * 64;
+        TileRef tr{key0, 3, {0u, 0u, 0u}, {0u, 0u, 0u}, (int)((sTB[st0] >> bit) & 3u)};
         // bitmap words of the element mask, fetched with the tile so that their latency
         // hides behind the previous tile's compute
         tr.wd = load_win(dbits, a.nwords, my_row - key0 - 63);
         tr.wv = load_win(vbits, a.nwords, key0);
         return tr;
       }
-      return TileRef{-(1 + (t - n_contig) * 64), 3, {0u, 0u, 0u}, {0u, 0u, 0u}};
+      return TileRef{-(1 + (t - n_contig) * 64), 3, {0u, 0u, 0u}, {0u, 0u, 0u}, 3};
     }
   };
 
@@ -306,7 +312,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
   [[maybe_unused]] const uint32_t voVT =
       (uint32_t)(8 * wave + lane / 8) * bVT + 16u * (uint32_t)((lane % 8) ^ ((4 * (wave & 1) + (lane >> 4)) & 7));
   // one K or V tile (64 key rows) into dst
-  auto issue = [&](bf16 *dst, int key0, bool isV) {
+  auto issue = [&](bf16 *dst, int key0, bool isV, int hm) {
     if constexpr (VT) {
       if (isV) {
         constexpr int LPV = D / 8 / NW;  // 8-row groups per wave
@@ -325,14 +331,17 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
       const __amdgpu_buffer_rsrc_t rs = isV ? rV : rK;
       const uint32_t b = isV ? bV : bK, vo = isV ? voV : voK;
       bf16 *dw = dst + wave * RPI * D;
+      // load i copies tile rows [i NW RPI, (i + 1) NW RPI), inside 32-row half (i NW RPI) / 32
       if (key0 >= 0 && key0 + 64 <= a.n) {  // contiguous rows: offsets are scalar
 #pragma unroll
         for (int i = 0; i < LPT; ++i)
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void *)(dw + i * NW * RPI * D),
-                                                   16, vo, (uint32_t)(key0 + i * NW * RPI) * b, 0, 0);
+          if ((hm >> ((i * NW * RPI) >> 5)) & 1)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void *)(dw + i * NW * RPI * D),
+                                                     16, vo, (uint32_t)(key0 + i * NW * RPI) * b, 0, 0);
       } else {  // gathered rows, or the last tile (rows clamped to the sequence)
 #pragma unroll
         for (int i = 0; i < LPT; ++i) {
+          if (!((hm >> ((i * NW * RPI) >> 5)) & 1)) continue;
           const uint32_t j = (uint32_t)key_of_row(key0, lrow0 + i * NW * RPI);
           __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void *)(dw + i * NW * RPI * D),
                                                    16, j * b + 16u * (uint32_t)lchunk, 0, 0, 0);
@@ -341,6 +350,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
     } else {
 #pragma unroll
       for (int i = 0; i < LPT; ++i) {
+        if (!((hm >> ((i * NW * RPI) >> 5)) & 1)) continue;
         const int row_base = (i * NW + wave) * RPI;
         const int row = row_base + lane / CPR;
         const int cc = (lane % CPR) ^ swz<D>(row);
@@ -411,7 +421,8 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
         const int i = my_row;
         const uint64_t md = __builtin_bitreverse64(win_bits(tr.wd, i - key0 - 63));
         const uint64_t mv = win_bits(tr.wv, key0);
-        p.Mvs = ((md | mv) & prefix_mask(i - key0 + 1)) >> (4 * hh);
+        const uint64_t halves = (tr.hm & 1 ? 0xffffffffull : 0ull) | (tr.hm & 2 ? 0xffffffff00000000ull : 0ull);
+        p.Mvs = ((md | mv) & prefix_mask(i - key0 + 1) & halves) >> (4 * hh);
         p.do0 = __ballot(((uint32_t)p.Mvs & 0x0f0f0f0fu) != 0u) != 0ull;
         p.do1 = __ballot(((uint32_t)(p.Mvs >> 32) & 0x0f0f0f0fu) != 0u) != 0ull;
         p.on = p.do0 || p.do1;
@@ -541,14 +552,14 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
   // On entry sc holds S^T of tile t; K of tile t+1 (in kn) and V of tile t (in vc) are resident
   // after the barrier.  The step copies K of tile t+2 into kc (released by tile t's products)
   // and V of tile t+1 into vn (released by tile t-1's P V).
-  TileRef Tc{0, 0, {0u, 0u, 0u}, {0u, 0u, 0u}}, Tn = Tc;
+  TileRef Tc{0, 0, {0u, 0u, 0u}, {0u, 0u, 0u}, 3}, Tn = Tc;
   Plan Pc = plan_of(Tc, false), Pn = Pc;
   auto step = [&](int t, f32x16 (&sc)[2], f32x16 (&sn)[2], bf16 *kc, bf16 *kn, bf16 *vc, bf16 *vn) {
-    TileRef T2{0, 0, {0u, 0u, 0u}, {0u, 0u, 0u}};
+    TileRef T2{0, 0, {0u, 0u, 0u}, {0u, 0u, 0u}, 3};
     if (t + 2 < ntiles) T2 = next_tile();
     lds_fence_barrier();
-    if (t + 2 < ntiles) issue(kc, T2.key0, false);
-    if (t + 1 < ntiles) issue(vn, Tn.key0, true);
+    if (t + 2 < ntiles) issue(kc, T2.key0, false, T2.hm);
+    if (t + 1 < ntiles) issue(vn, Tn.key0, true, Tn.hm);
     Pn = plan_of(Tn, t + 1 < ntiles);
     bool has_key = true;
     if (kOverlap || Pc.on)
@@ -600,11 +611,11 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
   f32x16 sA[2], sB[2];
   if (ntiles > 0) {
     Tc = next_tile();
-    issue(sK0, Tc.key0, false);
-    issue(sV0, Tc.key0, true);
+    issue(sK0, Tc.key0, false, Tc.hm);
+    issue(sV0, Tc.key0, true, Tc.hm);
     if (ntiles > 1) {
       Tn = next_tile();
-      issue(sK1, Tn.key0, false);
+      issue(sK1, Tn.key0, false, Tn.hm);
     }
     lds_fence_barrier();
     Pc = plan_of(Tc, true);
