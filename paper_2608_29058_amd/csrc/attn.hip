@@ -105,6 +105,10 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
   constexpr int RPI = 64 / CPR;          // rows covered by one wave-wide 16-byte load
   constexpr int LPT = 64 / RPI / NW;     // loads per thread per K (or V) tile
   constexpr int TE = 64 * D;             // elements of one K or V tile
+  // fragment reads in flight ahead of the products (K for QK^T, V for P V); vertical-slash
+  // has no registers left for them (its tile bookkeeping already fills the register file)
+  constexpr int KPF = PAT == P_VS ? 1 : 4;
+  constexpr int VPF = PAT == P_VS ? 1 : 3;
 
   // K and V tiles are double-buffered separately (K runs one tile ahead of V), row-major and
   // swizzled.  Four distinct arrays, addressed with a parity known at compile time, let the
@@ -436,17 +440,42 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
 
   // ---- S^T[64 keys x 32 rows] = K_tile x Q^T ---------------------------------------------
   auto qk = [&](f32x16 (&s)[2], const bf16 *sKt, const Plan &p) {
+    if constexpr (PAT != P_VS) {
+      // fragment f: 32-key block mb = f % 2, k-step ks = f / 2 (the two accumulators
+      // alternate); reads run KPF fragments ahead of their products
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[mb][r] = 0.f;
+      auto kread = [&](int f) -> u32x4 {
+        return *(const u32x4 *)&sKt[(32 * (f & 1) + l32) * D + (((2 * (f >> 1) + hh) ^ kswz) << 3)];
+      };
+      u32x4 kb[KPF];
+#pragma unroll
+      for (int f = 0; f < KPF; ++f) kb[f] = kread(f);
+#pragma unroll
+      for (int f = 0; f < 2 * KS; ++f) {
+        s[f & 1] = mfma32(kb[f % KPF], qf[f >> 1], s[f & 1]);
+        if (f + KPF < 2 * KS) kb[f % KPF] = kread(f + KPF);
+      }
+      return;
+    }
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb) {
       const bool dm = mb ? p.do1 : p.do0;
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[mb][r] = 0.f;
-      if constexpr (PAT == P_VS)
-        if (!dm) continue;
+      if (!dm) continue;
+      auto kread = [&](int ks) -> u32x4 {
+        return *(const u32x4 *)&sKt[(32 * mb + l32) * D + (((2 * ks + hh) ^ kswz) << 3)];
+      };
+      u32x4 kb[KPF];
+#pragma unroll
+      for (int ks = 0; ks < KPF; ++ks) kb[ks] = kread(ks);
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        const u32x4 kf = *(const u32x4 *)&sKt[(32 * mb + l32) * D + (((2 * ks + hh) ^ kswz) << 3)];
-        s[mb] = mfma32(kf, qf[ks], s[mb]);
+        s[mb] = mfma32(kb[ks % KPF], qf[ks], s[mb]);
+        if (ks + KPF < KS) kb[ks % KPF] = kread(ks + KPF);
       }
     }
   };
@@ -519,33 +548,56 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
   [[maybe_unused]] const int vts = (l32 >> 1) & 7;
   auto pv = [&](const bf16 *sVt, const Plan &p) {
     if constexpr (VT) {
+      // fragment f: 16-key group g = f / DB (g = 2 mb + h), 32-dim block db = f % DB, so that
+      // consecutive products accumulate into different blocks; reads run PF fragments ahead
+      constexpr int NF = 4 * DB, PF = 4;
+      auto vread = [&](int f) -> u32x4 {
+        const int g = f / DB, db = f % DB;
+        return *(const u32x4 *)(sVt + (32 * db + l32) * 64 + (((2 * g + hh) ^ vts) << 3));
+      };
+      u32x4 vb[PF];
 #pragma unroll
-      for (int db = 0; db < DB; ++db)
+      for (int f = 0; f < PF; ++f) vb[f] = vread(f);
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
+      for (int f = 0; f < NF; ++f) {
+        const int g = f / DB, db = f % DB;
+        oacc[db] = mfma32(vb[f % PF], pb[g >> 1][g & 1], oacc[db]);
+        if (f + PF < NF) vb[f % PF] = vread(f + PF);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x100, PF, 0);
 #pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const u32x4 vv = *(const u32x4 *)(sVt + (32 * db + l32) * 64 + (((4 * mb + 2 * h + hh) ^ vts) << 3));
-            oacc[db] = mfma32(vv, pb[mb][h], oacc[db]);
-          }
+      for (int f = 0; f < NF - PF; ++f) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, PF, 0);
       return;
     }
+    // per 32-key half mb (skipped by vertical-slash when no row of the wave keeps a key of
+    // it): fragment f = (h, db) = (f / DB, f % DB), consecutive products into different
+    // blocks, reads VPF fragments ahead
 #pragma unroll
-    for (int db = 0; db < DB; ++db)
+    for (int mb = 0; mb < 2; ++mb) {
+      if constexpr (PAT == P_VS)
+        if (!(mb ? p.do1 : p.do0)) continue;
+      auto vread = [&](int f) -> u32x4 {
+        const int h = f / DB, db = f % DB;
+        const bf16 *vp = sVt + voff[db] + (32 * mb + 16 * h) * D;
+        const bf16 *vq = sVt + voff1[db] + (32 * mb + 16 * h) * D;
+        const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16 *)(vp));
+        const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16 *)(vq));
+        const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
+        return u32x4{l2[0], l2[1], h2[0], h2[1]};
+      };
+      u32x4 vb[VPF];
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb) {
-        if constexpr (PAT == P_VS)
-          if (!(mb ? p.do1 : p.do0)) continue;
+      for (int f = 0; f < VPF; ++f) vb[f] = vread(f);
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const bf16 *vp = sVt + voff[db] + (32 * mb + 16 * h) * D;
-          const bf16 *vq = sVt + voff1[db] + (32 * mb + 16 * h) * D;
-          const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16 *)(vp));
-          const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16 *)(vq));
-          const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
-          oacc[db] = mfma32(u32x4{l2[0], l2[1], h2[0], h2[1]}, pb[mb][h], oacc[db]);
-        }
+      for (int f = 0; f < 2 * DB; ++f) {
+        oacc[f % DB] = mfma32(vb[f % VPF], pb[mb][f / DB], oacc[f % DB]);
+        if (f + VPF < 2 * DB) vb[f % VPF] = vread(f + VPF);
       }
+    }
   };
 
   // ---- one pipeline step: tile t's softmax and P V, tile t+1's products -------------------
@@ -564,19 +616,13 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
     bool has_key = true;
     if (kOverlap || Pc.on)
       if (PAT == P_VS || Pc.need_mask) has_key = apply_mask(sc, Tc, Pc);
-    // tile t+1's products beside tile t's softmax
+    // tile t+1's products, then tile t's softmax: the two waves of a SIMD tend to alternate
+    // between product bursts and softmax bursts, so that one's products overlap the other's
+    // vector work (interleaving them within a wave was measured slower)
     if (kOverlap || Pn.on) qk(sn, kn, Pn);
     if (kOverlap || Pc.on) {
       float psum = form_p(sc, (m_run == -INFINITY) ? 0.f : -m_run * c);
       const uint64_t want = __ballot(!(psum <= 256.f) || (m_run == -INFINITY && has_key));
-      if constexpr (kOverlap) {
-#pragma unroll
-        for (int k = 0; k < 16; ++k) {
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // K fragment read
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // product
-          __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);  // softmax
-        }
-      }
       if (want != 0ull) {
         float mx = -INFINITY;
 #pragma unroll
