@@ -75,7 +75,9 @@ typedef short v4i16 __attribute__((ext_vector_type(4)));
 // vmcnt) and LDS accesses are complete.  The explicit vmcnt wait is required: the
 // compiler's LDS release fence does not always wait for the LDS DMA.
 __device__ __forceinline__ void lds_fence_barrier() {
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  // vmcnt(0) through the builtin, which the compiler's wait insertion knows about (it then
+  // treats every earlier load as complete, instead of waiting for them again later)
+  __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
@@ -146,17 +148,15 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
   int bs_na = 0, bs_nb = 0;
   const uint32_t *vbits = nullptr, *dbits = nullptr;
   int n_contig = 0, n_gather = 0;
-  uint32_t *sTB = nullptr;
-  int *sG = nullptr;
+  // vertical-slash: sTB, one bit per 32-key half of the key range the block's diagonals touch
+  // (a 64-key tile is in the list when either of its halves is, and only those halves are
+  // copied); sG, the gathered vertical columns.  Arrays of their own, not pointers, so that
+  // the compiler sees them apart from the tiles being copied.
+  __shared__ uint32_t sTB[PAT == P_VS ? kMaxTiles / 16 : 1];
+  __shared__ int sG[PAT == P_VS ? kMaxGather : 1];
 
   if constexpr (PAT == P_VS) {
-    // sTB: one bit per 32-key half of the key range the block's diagonals touch; a 64-key tile
-    // is in the list when either of its halves is, and only those halves are copied
-    __shared__ uint32_t sTBbuf[kMaxTiles / 16];
-    __shared__ int sGbuf[kMaxGather];
     __shared__ int sScan[NW + 1];
-    sTB = sTBbuf;
-    sG = sGbuf;
     const long long vsrow = (long long)U.slot * a.ncand_vs + U.cl;
     const int *vsorted = a.vs_vsorted + vsrow * a.nv_max;
     const int *dsorted = a.vs_dsorted + vsrow * a.ns_max;
