@@ -144,8 +144,8 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
   // ---- tile enumeration state ----------------------------------------------------------
   int ntiles = 0;
   int st0 = 0, st1 = 0;  // pattern cursors
-  const int *bs_a = nullptr, *bs_b = nullptr;
-  int bs_na = 0, bs_nb = 0;
+  // block-sparse: key blocks selected by query block bq (sBA) and bq + 1 (sBB) as bitmaps
+  __shared__ uint32_t sBA[PAT == P_BS ? kMaxTiles / 32 : 1], sBB[PAT == P_BS ? kMaxTiles / 32 : 1];
   const uint32_t *vbits = nullptr, *dbits = nullptr;
   int n_contig = 0, n_gather = 0;
   // vertical-slash: sTB, one bit per 32-key half of the key range the block's diagonals touch
@@ -218,26 +218,30 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
     st1 = max(wlo, ns);
     ntiles = ns + max(0, last_tile - st1 + 1);
   } else {  // P_BS: query blocks bq = base/64 (waves 0-1) and bq + 1 (waves 2-3)
+    // the two sorted selections are loaded in parallel into key-block bitmaps; the tiles are
+    // their union in ascending order (a tile's tag says which query block selected it)
     const int bq = base >> 6;
     const long long brow = ((long long)head * a.ncand_bs + U.cl) * a.nb + bq;
-    if (r_lo < base + 64) {
-      bs_a = a.bs_sorted + brow * a.k_max;
-      bs_na = a.bs_count[brow];
+    const int na = r_lo < base + 64 ? a.bs_count[brow] : 0;
+    const int nb2 = (r_hi > base + 64 && bq + 1 < a.nb) ? a.bs_count[brow + 1] : 0;
+    const int nwb = ((bq + 1) >> 5) + 1;  // words holding key blocks 0 .. bq + 1
+    for (int w = tid; w < nwb; w += NT) {
+      sBA[w] = 0u;
+      sBB[w] = 0u;
     }
-    if (r_hi > base + 64 && bq + 1 < a.nb) {
-      bs_b = a.bs_sorted + (brow + 1) * a.k_max;
-      bs_nb = a.bs_count[brow + 1];
+    __syncthreads();
+    for (int x = tid; x < na + nb2; x += NT) {
+      const int v = x < na ? a.bs_sorted[brow * a.k_max + x] : a.bs_sorted[(brow + 1) * a.k_max + x - na];
+      atomicOr(x < na ? &sBA[v >> 5] : &sBB[v >> 5], 1u << (v & 31));
     }
-    // size of the merged (union) list
-    int ia = 0, ib = 0, cnt = 0;
-    while (ia < bs_na || ib < bs_nb) {
-      const int va = ia < bs_na ? bs_a[ia] : 0x7fffffff;
-      const int vb = ib < bs_nb ? bs_b[ib] : 0x7fffffff;
-      ia += va <= vb;
-      ib += vb <= va;
-      ++cnt;
-    }
+    __syncthreads();
+    int cnt = 0;  // every wave sums the same words (no further barrier)
+    for (int w = lane; w < nwb; w += 64) cnt += __builtin_popcount(sBA[w] | sBB[w]);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) cnt += __shfl_xor(cnt, o);
     ntiles = cnt;
+    st0 = 0;                                                        // bitmap word of the next tile
+    st1 = __builtin_amdgcn_readfirstlane((int)(sBA[0] | sBB[0]));  // remaining blocks of that word
   }
 
   // next tile in order (t increases by one per call)
@@ -249,13 +253,16 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
     } else if constexpr (PAT == P_ASHAPE) {
       return TileRef{(t < st0 ? t : st1 + (t - st0)) * 64, 3, {0u, 0u, 0u}, {0u, 0u, 0u}, 3};
     } else if constexpr (PAT == P_BS) {
-      const int va = st0 < bs_na ? bs_a[st0] : 0x7fffffff;
-      const int vb = st1 < bs_nb ? bs_b[st1] : 0x7fffffff;
-      const int v = min(va, vb);
-      const int tag = (va == v ? 1 : 0) | (vb == v ? 2 : 0);
-      st0 += va == v;
-      st1 += vb == v;
-      return TileRef{v * 64, tag, {0u, 0u, 0u}, {0u, 0u, 0u}, 3};
+      // the words are the same for every lane: kept in scalar registers
+      while (st1 == 0) {
+        ++st0;
+        st1 = __builtin_amdgcn_readfirstlane((int)(sBA[st0] | sBB[st0]));
+      }
+      const int bit = __builtin_ctz((uint32_t)st1);
+      st1 &= st1 - 1;
+      const int wa = __builtin_amdgcn_readfirstlane((int)sBA[st0]), wb = __builtin_amdgcn_readfirstlane((int)sBB[st0]);
+      const int tag = ((wa >> bit) & 1) | (((wb >> bit) & 1) << 1);
+      return TileRef{(st0 * 32 + bit) * 64, tag, {0u, 0u, 0u}, {0u, 0u, 0u}, 3};
     } else {
       if (t < n_contig) {
         while (st1 == 0) st1 = (int)tile_bits(sTB[++st0]);

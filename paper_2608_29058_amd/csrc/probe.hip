@@ -121,16 +121,6 @@ __device__ __forceinline__ int swz(int r) {
   else return ((r & 3) << 1) | ((r >> 2) & 1);
 }
 
-// Barrier after which every wave's direct-to-LDS copies (global_load_lds, counted by
-// vmcnt) and LDS accesses are complete.  The explicit vmcnt wait is required: the
-// compiler's LDS release fence does not always wait for the LDS DMA.
-__device__ __forceinline__ void lds_fence_barrier() {
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
-
 enum { M_STATS = 0, M_SCORES = 1, M_COVER = 2 };
 
 // s_waitcnt immediate (gfx9 encoding) waiting until at most n vector-memory operations are
