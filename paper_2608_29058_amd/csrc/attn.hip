@@ -208,7 +208,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
     __syncthreads();
     ntiles = n_contig + (n_gather + 63) / 64;
     st0 = 0;                                   // bitmap word of the next contiguous tile
-    st1 = nwt > 0 ? (int)tile_bits(sTB[0]) : 0; // remaining tiles of that word (even bits)
+    st1 = nwt > 0 ? __builtin_amdgcn_readfirstlane((int)tile_bits(sTB[0])) : 0;  // remaining tiles (even bits)
   } else if constexpr (PAT == P_DENSE) {
     ntiles = last_tile + 1;
   } else if constexpr (PAT == P_ASHAPE) {
@@ -265,15 +265,17 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
       return TileRef{(st0 * 32 + bit) * 64, tag, {0u, 0u, 0u}, {0u, 0u, 0u}, 3};
     } else {
       if (t < n_contig) {
-        while (st1 == 0) st1 = (int)tile_bits(sTB[++st0]);
+        // the bitmap words are the same for every lane: kept in scalar registers
+        while (st1 == 0) st1 = __builtin_amdgcn_readfirstlane((int)tile_bits(sTB[++st0]));
         const int bit = __builtin_ctz((uint32_t)st1);
         st1 &= st1 - 1;
         const int key0 = (st0 * 16 + (bit >> 1)) * 64;
-        TileRef tr{key0, 3, {0u, 0u, 0u}, {0u, 0u, 0u}, (int)((sTB[st0] >> bit) & 3u)};
+        const int hm = (__builtin_amdgcn_readfirstlane((int)sTB[st0]) >> bit) & 3;
+        TileRef tr{key0, 3, {0u, 0u, 0u}, {0u, 0u, 0u}, hm};
         // bitmap words of the element mask, fetched with the tile so that their latency
         // hides behind the previous tile's compute
         tr.wd = load_win(dbits, a.nwords, my_row - key0 - 63);
-        tr.wv = load_win(vbits, a.nwords, key0);
+        tr.wv = load_win_uniform(vbits, a.nwords, key0);
         return tr;
       }
       return TileRef{-(1 + (t - n_contig) * 64), 3, {0u, 0u, 0u}, {0u, 0u, 0u}, 3};

@@ -143,6 +143,19 @@ __device__ __forceinline__ Win3 load_win(const uint32_t *bits, int nwords, int p
   return r;
 }
 
+// load_win for a position that is the same in every lane, through the scalar cache (the
+// bitmap is read-only while the kernel runs)
+__device__ __forceinline__ Win3 load_win_uniform(const uint32_t *bits, int nwords, int pos) {
+  typedef const __attribute__((address_space(4))) uint32_t cu32;
+  cu32 *cb = (cu32 *)bits;
+  const int w = pos >> 5;
+  Win3 r;
+  r.x0 = (w >= 0 && w < nwords) ? cb[w] : 0u;
+  r.x1 = (w + 1 >= 0 && w + 1 < nwords) ? cb[w + 1] : 0u;
+  r.x2 = (w + 2 >= 0 && w + 2 < nwords) ? cb[w + 2] : 0u;
+  return r;
+}
+
 // the 64 bits starting at `pos` from a window loaded with load_win(.., pos)
 __device__ __forceinline__ uint64_t win_bits(const Win3 &r, int pos) {
   const int sh = pos & 31;
