@@ -213,3 +213,11 @@ def test_config5_routed_layer_decisions_and_outputs():
         rows = _sample_rows(s0, s1, u, 128)
         out = _masked_rows(qh, kh, vh, rows, s1, mf)
         check_close(o[h][rows], out, f"c5 unit {u} cand {cand}")
+    # the launch configuration the benchmark times: device route, one persistent launch per
+    # family; the same route and bitwise the same output as the grouped launches above
+    o_groups = RL.o.clone()
+    RL.o.fill_(float("nan"))
+    assert RL.run(q, k, v, device_route=True) is None
+    torch.cuda.synchronize()
+    assert RL.rb.choice[:RL.nunits].cpu().tolist() == route["choice"]
+    assert torch.equal(RL.o.view(torch.int16), o_groups.view(torch.int16))

@@ -12,7 +12,7 @@ from oracle import router as RT
 from paper_2608_29058_amd import _rs
 from synth import gen as G
 
-from gpu_helpers import check_close, dev
+from gpu_helpers import check_close, dev, with_vt
 from test_abi_host import GRID, _brank, _random_instance, _t_of
 
 pytestmark = pytest.mark.gpu
@@ -160,15 +160,19 @@ def _layer(n, hq, hkv, d, seed):
     return q, k, v
 
 
-def test_routed_attention_equals_group_launches():
+@pytest.mark.parametrize("vt", [False, True])
+def test_routed_attention_equals_group_launches(vt):
     """Every family and budget in one routed call, against one call per group on the same
     probe-built index sets: O and LSE bitwise equal; a unit with an invalid choice is left
-    untouched; a few rows checked against the oracle's masked attention."""
+    untouched; a few rows checked against the oracle's masked attention (with and without the
+    transposed V operand)."""
     import torch
     n, hq, hkv, d, seg = 4096, 4, 2, 128, 1024
     q, k, v = _layer(n, hq, hkv, d, 5)
     qd, kd, vd = dev(q), dev(k), dev(v)
     qkv = _rs.make_qkv(qd, kd, vd)
+    if vt:
+        qkv, _vt = with_vt(qkv)
     grid = [(0, 0, 0), (1, 64, 256), (1, 64, 1024), (2, 64, 128), (2, 128, 512), (3, 4, 64), (3, 8, 64)]
     g = _rs.make_grid(grid)
     unit_list = [(h, s, s + seg) for s in range(0, n, seg) for h in range(hq)]
