@@ -206,7 +206,10 @@ rs_status rs_probe(const rs_qkv *qkv, const rs_unit *units, int32_t nunits,
  * VS per unit: V = top n_v columns of col over [0, s1); D = {0} + top (n_s - 1) diagonals
  * of diag over [1, s1).  BS per query head and query block bq (nb blocks of 64):
  * Sel(bq) = {bq} + top (k - 1) of L_bs[bq][0..bq).  Fewer candidates than the budget:
- * all are taken.  Needs the probe output of a scores call with the matching flags. */
+ * all are taken.  Needs the probe output of a scores call with the matching flags.  The
+ * grid's vertical-slash (block-sparse) candidates must be those the index set was sized for,
+ * or none: a family left out of the grid keeps its arrays untouched, so the two families may
+ * be built by two calls (for instance on two streams, each after its scores). */
 size_t rs_build_indices_workspace_size(const rs_probe_out *scores, const rs_candidate *grid,
                                        int32_t ncand);
 rs_status rs_build_indices(const rs_probe_out *scores, const rs_unit *units, int32_t nunits,

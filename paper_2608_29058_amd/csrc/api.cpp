@@ -278,7 +278,10 @@ rs_status rs_build_indices(const rs_probe_out *scores, const rs_unit *units, int
   const int nb = (n + 63) / 64;
   if (out->n != n || out->nb != nb || out->nwords != (n + 31) / 32 || out->nbw != (nb + 31) / 32)
     return fail(RS_ERR_INVALID_ARG, "index set dimensions do not match n");
-  if (out->ncand_vs != nvs || out->ncand_bs != nbs) return fail(RS_ERR_INVALID_ARG, "index set family counts");
+  // a grid may leave out a family altogether (its arrays are then untouched), so that the two
+  // families can be built by separate calls
+  if ((nvs > 0 && out->ncand_vs != nvs) || (nbs > 0 && out->ncand_bs != nbs) || nvs + nbs == 0)
+    return fail(RS_ERR_INVALID_ARG, "index set family counts");
   for (int u = 0; u < nunits; ++u)
     if (units[u].s1 < 1 || units[u].s1 > n || units[u].s0 < 0 || units[u].s0 >= units[u].s1)
       return fail(RS_ERR_INVALID_ARG, "bad unit bounds");

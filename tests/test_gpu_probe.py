@@ -136,6 +136,30 @@ def test_indices_bit_exact_on_gpu_scores(tie):
             assert np.array_equal(rank_g[bq, :m], ranks[bq][:m])
 
 
+def test_index_families_built_separately_match():
+    """Vertical-slash and block-sparse sets built by two calls (each with a grid holding one
+    family) equal the sets of one call with the whole grid, bit for bit."""
+    import torch
+    n, hq, hkv, d = 2600, 2, 1, 128
+    q, k, v = _inputs(n, hq, hkv, d, 4)
+    units = [(0, 0, n), (1, 700, 2000)]
+    res = _probe(q, k, v, units, (64, 8, 8), _rs.RS_PROBE_ROWS | _rs.RS_PROBE_BLOCKMEAN)
+    pb = res["pb"]
+    grid = [(_rs.RS_DENSE, 0, 0), (_rs.RS_VSLASH, 30, 100), (_rs.RS_VSLASH, 64, 256), (_rs.RS_BSPARSE, 3, 64),
+            (_rs.RS_BSPARSE, 9, 64)]
+    ws = _rs.workspace(_rs.rs_build_indices_workspace_size(pb, _rs.make_grid(grid), len(grid)))
+    one = _rs.IndexBuffers(len(units), n, hq, grid)
+    _rs.rs_build_indices(pb, res["u"], len(units), _rs.make_grid(grid), len(grid), ws, one)
+    two = _rs.IndexBuffers(len(units), n, hq, grid)
+    for fam in (_rs.RS_VSLASH, _rs.RS_BSPARSE):
+        sub = [g for g in grid if g[0] == fam]
+        _rs.rs_build_indices(pb, res["u"], len(units), _rs.make_grid(sub), len(sub), ws, two)
+    torch.cuda.synchronize()
+    for name in ("vs_vsorted", "vs_dsorted", "vs_count", "vs_vbits", "vs_dbits", "bs_rank", "bs_sorted", "bs_count",
+                 "bs_bits"):
+        assert torch.equal(getattr(one, name), getattr(two, name)), name
+
+
 @pytest.mark.parametrize("rc", [(64, 16, 8), (64, 0, 0)])
 def test_coverage_matches_oracle(rc):
     import torch
