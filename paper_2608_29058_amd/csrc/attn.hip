@@ -108,9 +108,9 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
   constexpr int LPT = 64 / RPI / NW;     // loads per thread per K (or V) tile
   constexpr int TE = 64 * D;             // elements of one K or V tile
   // fragment reads in flight ahead of the products (K for QK^T, V for P V); vertical-slash
-  // has no registers left for them (its tile bookkeeping already fills the register file)
-  constexpr int KPF = PAT == P_VS ? 1 : 4;
-  constexpr int VPF = PAT == P_VS ? 1 : 3;
+  // keeps two (its tile bookkeeping leaves fewer registers; more spill)
+  constexpr int KPF = PAT == P_VS ? 2 : 4;
+  constexpr int VPF = PAT == P_VS ? 2 : 3;
 
   // K and V tiles are double-buffered separately (K runs one tile ahead of V), row-major and
   // swizzled.  Four distinct arrays, addressed with a parity known at compile time, let the
@@ -628,7 +628,12 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
     // tile t+1's products, then tile t's softmax: the two waves of a SIMD tend to alternate
     // between product bursts and softmax bursts, so that one's products overlap the other's
     // vector work (interleaving them within a wave was measured slower)
-    if (kOverlap || Pn.on) qk(sn, kn, Pn);
+    // (vertical-slash, whose products are few, takes tile t+1's products after tile t's P V
+    // instead: the two S tiles are then never live together, which leaves registers for
+    // fragment read-ahead)
+    constexpr bool kLateQK = PAT == P_VS;
+    if constexpr (!kLateQK)
+      if (kOverlap || Pn.on) qk(sn, kn, Pn);
     if (kOverlap || Pc.on) {
       float psum = form_p(sc, (m_run == -INFINITY) ? 0.f : -m_run * c);
       const uint64_t want = __ballot(!(psum <= 256.f) || (m_run == -INFINITY && has_key));
@@ -657,6 +662,8 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
       l_run += psum;
       pv(vc, Pc);
     }
+    if constexpr (kLateQK)
+      if (Pn.on) qk(sn, kn, Pn);
     Tc = Tn;
     Tn = T2;
     Pc = Pn;
