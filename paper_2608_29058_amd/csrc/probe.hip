@@ -28,7 +28,8 @@ constexpr int kRange = 1024;        // keys per workgroup range in the three pas
 constexpr int kMaxCand = 16;
 constexpr int kPrefVs = 3;   // vertical-slash candidates whose bitmap words are prefetched
 constexpr int kPrefBs = 3;   // block-sparse candidates whose selection words are prefetched
-constexpr int kSkew = 98;    // row stride of the skewed probability tile (96 columns + pad)
+constexpr int kSkew = 84;    // row stride of the skewed 16-row probability tile (79 columns + pad;
+                             // row r at bank offset 19 r: the tile's writes are conflict-free)
 
 struct ProbeUnit {
   int head, s0, s1, nrows;  // nrows = sampled rows actually present
@@ -148,12 +149,14 @@ template <int D, typename InT, int MODE, int NCV, bool GEN = true>
 __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) {
   constexpr int KS = D / 16, CPR = D / 8, RPI = 64 / CPR, LPT = 64 / RPI / 4;
   constexpr int TE = 64 * D;
-  // two K tile buffers: the next tile (and, for coverage, its bitmap words) is fetched while
-  // the current one is computed.  The copy is issued once both blocks have read the current
-  // tile (after the second block's products): the compiler makes every LDS read wait for the
+  // K tile buffers: the next tile (and, for coverage, its bitmap words) is fetched while the
+  // current one is computed.  The copy is issued once both blocks have read the current tile
+  // (after the second block's products): the compiler makes every LDS read wait for the
   // LDS-bound copies in flight, so the copy overlaps the second block's softmax and coverage
-  // work.
-  __shared__ __align__(16) bf16 sKb[2][TE];
+  // work.  The scores pass has one buffer (a barrier after the second block's products
+  // releases it), which keeps its LDS within two workgroups per compute unit.
+  constexpr int NKB = MODE == M_SCORES ? 1 : 2;
+  __shared__ __align__(16) bf16 sKb[NKB][TE];
   __shared__ int sRows[2][32];
 
   const int rg = blockIdx.x;
@@ -213,7 +216,7 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
   const int dw = kRange + U0.nR;                // diagonals touched by recent rows in this range
   const int dbase = U0.r0 - (c0 + kRange - 1);  // smallest such diagonal
   if constexpr (MODE == M_SCORES) {
-    __shared__ float sDbuf[4][32][kSkew];
+    __shared__ float sDbuf[4][16][kSkew];
     __shared__ float sColbuf[4][kRange];
     __shared__ float sDgbuf[4][kRange + kProbeMaxRows];
     sD = sDbuf[wave];
@@ -221,7 +224,7 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
     sDg = sDgbuf[wave];
     for (int x = lane; x < kRange; x += 64) sCol[x] = 0.f;
     for (int x = lane; x < dw; x += 64) sDg[x] = 0.f;
-    for (int x = lane; x < 32 * kSkew; x += 64) sD[x / kSkew][x % kSkew] = 0.f;
+    for (int x = lane; x < 16 * kSkew; x += 64) sD[x / kSkew][x % kSkew] = 0.f;
   }
 
   const int kswz = swz<D>(l32);
@@ -418,28 +421,36 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
           }
         if constexpr (MODE == M_SCORES) {
           if (__ballot(isR[s]) == 0ull) return;
-          // skewed tile: row lane r, key kk -> sD[r][kk - r + 31].  Key columns and diagonals
-          // (kk - r constant) of the block are then both plain columns of sD; entries no key
-          // maps to stay zero.  Recent rows are consecutive and end at lane 31, so diagonal
-          // column e holds t = (last row - k0) - e.
+          // skewed tile, one half of the block's rows at a time: row lane r (r = l32 - 16 h in
+          // half h), key kk -> sD[r][kk - r + 15].  Key columns and diagonals (kk - r
+          // constant) of the half are then both plain columns of sD; entries no key maps to
+          // stay zero.  Recent rows are consecutive and end at lane 31, so the last row of
+          // half h is rmx - 16 (1 - h) and diagonal column e holds t = (that row - k0) - e.
+          float cs = 0.f;
 #pragma unroll
-          for (int mb = 0; mb < 2; ++mb)
+          for (int h = 0; h < 2; ++h) {
+            if ((l32 >> 4) == h) {
+              const int r16 = l32 & 15;
 #pragma unroll
-            for (int r = 0; r < 16; ++r) sD[l32][acc_key(mb, r, hh) - l32 + 31] = isR[s] ? x[mb][r] : 0.f;
-          wave_sync();
-          float cs = 0.f, d0 = 0.f, d1 = 0.f;
-          const int e1 = min(64 + lane, kSkew - 1);
+              for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-          for (int rr = 0; rr < 32; ++rr) {
-            cs += sD[rr][lane - rr + 31];
-            d0 += sD[rr][lane];
-            d1 += sD[rr][e1];
+                for (int r = 0; r < 16; ++r) sD[r16][acc_key(mb, r, hh) - r16 + 15] = isR[s] ? x[mb][r] : 0.f;
+            }
+            wave_sync();
+            float d0 = 0.f, d1 = 0.f;
+            const int e1 = min(64 + lane, kSkew - 1);
+#pragma unroll
+            for (int rr = 0; rr < 16; ++rr) {
+              cs += sD[rr][lane - rr + 15];
+              d0 += sD[rr][lane];
+              d1 += sD[rr][e1];
+            }
+            const int tb = rmx - 16 * (1 - h) - k0 - dbase;
+            if (tb - lane >= 0 && tb - lane < dw) sDg[tb - lane] += d0;
+            if (lane < 15 && tb - 64 - lane >= 0 && tb - 64 - lane < dw) sDg[tb - 64 - lane] += d1;
+            wave_sync();
           }
           sCol[k0 - c0 + lane] += cs;
-          const int tb = rmx - k0 - dbase;
-          if (tb - lane >= 0 && tb - lane < dw) sDg[tb - lane] += d0;
-          if (lane < 31 && tb - 64 - lane >= 0 && tb - 64 - lane < dw) sDg[tb - 64 - lane] += d1;
-          wave_sync();
         } else {  // M_COVER
           const float bt = tsum + __shfl_xor(tsum, 32);  // mass of the row in this 64-key block
           if (bt > 0.f) ent[s] += bt * logf(bt);
@@ -510,11 +521,16 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
       const int k0 = c0 + 64 * t;
       f32x16 S[2];
-      qk_block(sKb[t & 1], k0, 0, S);
+      qk_block(sKb[t % NKB], k0, 0, S);
       block_tile(S, k0, 0, fcur);
-      qk_block(sKb[t & 1], k0, 1, S);
+      qk_block(sKb[t % NKB], k0, 1, S);
+      if constexpr (NKB == 1) {  // every wave has read the tile before it is overwritten
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+      }
       if (t + 1 < nt) {
-        issue_tile(sKb[(t + 1) & 1], k0 + 64);
+        issue_tile(sKb[(t + 1) % NKB], k0 + 64);
         fetch(k0 + 64, fnext);
       }
       block_tile(S, k0, 1, fcur);
