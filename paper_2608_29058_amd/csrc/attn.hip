@@ -107,6 +107,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
   constexpr int RPI = 64 / CPR;          // rows covered by one wave-wide 16-byte load
   constexpr int LPT = 64 / RPI / NW;     // loads per thread per K (or V) tile
   constexpr int TE = 64 * D;             // elements of one K or V tile
+  static_assert(LPT % 2 == 0 && LPT <= 4 && LPT * NW * RPI == 64, "K/V copies: two halves of LPT / 2 loads");
   // fragment reads in flight ahead of the products (K for QK^T, V for P V); vertical-slash
   // keeps two (its tile bookkeeping leaves fewer registers; more spill)
   constexpr int KPF = PAT == P_VS ? 2 : 4;
@@ -345,19 +346,27 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
       const uint32_t b = isV ? bV : bK, vo = isV ? voV : voK;
       bf16 *dw = dst + wave * RPI * D;
       // load i copies tile rows [i NW RPI, (i + 1) NW RPI), inside 32-row half (i NW RPI) / 32
+      // loads [h LPT / 2, (h + 1) LPT / 2) fill 32-key half h (one test of hm per half)
       if (key0 >= 0 && key0 + 64 <= a.n) {  // contiguous rows: offsets are scalar
 #pragma unroll
-        for (int i = 0; i < LPT; ++i)
-          if ((hm >> ((i * NW * RPI) >> 5)) & 1)
+        for (int h = 0; h < 2; ++h) {
+          if (!((hm >> h) & 1)) continue;
+#pragma unroll
+          for (int i = h * LPT / 2; i < (h + 1) * LPT / 2; ++i)
             __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void *)(dw + i * NW * RPI * D),
                                                      16, vo, (uint32_t)(key0 + i * NW * RPI) * b, 0, 0);
+        }
       } else {  // gathered rows, or the last tile (rows clamped to the sequence)
+        uint32_t jr[4];  // (LPT <= 4) every row index first: one LDS round trip for a gathered tile
 #pragma unroll
-        for (int i = 0; i < LPT; ++i) {
-          if (!((hm >> ((i * NW * RPI) >> 5)) & 1)) continue;
-          const uint32_t j = (uint32_t)key_of_row(key0, lrow0 + i * NW * RPI);
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void *)(dw + i * NW * RPI * D),
-                                                   16, j * b + 16u * (uint32_t)lchunk, 0, 0, 0);
+        for (int i = 0; i < LPT; ++i) jr[i] = (uint32_t)key_of_row(key0, lrow0 + i * NW * RPI);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          if (!((hm >> h) & 1)) continue;
+#pragma unroll
+          for (int i = h * LPT / 2; i < (h + 1) * LPT / 2; ++i)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void *)(dw + i * NW * RPI * D),
+                                                     16, jr[i] * b + 16u * (uint32_t)lchunk, 0, 0, 0);
         }
       }
     } else {
