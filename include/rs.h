@@ -137,12 +137,13 @@ typedef struct rs_index_set {
   int32_t ncand_vs, ncand_bs, nbw, _pad;
   int32_t *vs_vsorted; /* [nunits][ncand_vs][nv_max] */
   int32_t *vs_dsorted; /* [nunits][ncand_vs][ns_max] */
-  int32_t *vs_count;   /* [nunits][ncand_vs][2]  |V|, |D| */
+  int32_t *vs_count;   /* [nunits][ncand_vs][2]  |V|, |D| (read clamped to [0, nv_max] / [0, ns_max]) */
   uint32_t *vs_vbits;  /* [nunits][ncand_vs][nwords] bit j set iff column j in V */
   uint32_t *vs_dbits;  /* [nunits][ncand_vs][nwords] bit t set iff diagonal t in D */
   int32_t *bs_rank;    /* [hq][nb][k_max]  diagonal block first */
   int32_t *bs_sorted;  /* [hq][ncand_bs][nb][k_max] */
-  int32_t *bs_count;   /* [hq][ncand_bs][nb] */
+  int32_t *bs_count;   /* [hq][ncand_bs][nb] (read clamped to [0, k_max]; entries outside the
+                          causal key blocks are skipped by the attention kernel) */
   uint32_t *bs_bits;   /* [hq][ncand_bs][nb][nbw] bit bk set iff key block bk selected */
 } rs_index_set;
 

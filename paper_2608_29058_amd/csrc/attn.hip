@@ -161,8 +161,9 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
     const long long vsrow = (long long)U.slot * a.ncand_vs + U.cl;
     const int *vsorted = a.vs_vsorted + vsrow * a.nv_max;
     const int *dsorted = a.vs_dsorted + vsrow * a.ns_max;
-    const int nvc = a.vs_count[vsrow * 2 + 0];
-    const int ndc = a.vs_count[vsrow * 2 + 1];
+    // counts are read within [0, nv_max] / [0, ns_max]: a malformed set never reads past its row
+    const int nvc = min(max(a.vs_count[vsrow * 2 + 0], 0), a.nv_max);
+    const int ndc = min(max(a.vs_count[vsrow * 2 + 1], 0), a.ns_max);
     vbits = a.vs_vbits + vsrow * a.nwords;
     dbits = a.vs_dbits + vsrow * a.nwords;
     const int nwt = ((2 * last_tile + 1) >> 5) + 1;
@@ -223,8 +224,10 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
     // their union in ascending order (a tile's tag says which query block selected it)
     const int bq = base >> 6;
     const long long brow = ((long long)head * a.ncand_bs + U.cl) * a.nb + bq;
-    const int na = r_lo < base + 64 ? a.bs_count[brow] : 0;
-    const int nb2 = (r_hi > base + 64 && bq + 1 < a.nb) ? a.bs_count[brow + 1] : 0;
+    // counts within [0, k_max]; entries outside key blocks [0, bq + 1] (pads, malformed sets)
+    // are skipped, so the bitmaps are never written out of range
+    const int na = r_lo < base + 64 ? min(max(a.bs_count[brow], 0), a.k_max) : 0;
+    const int nb2 = (r_hi > base + 64 && bq + 1 < a.nb) ? min(max(a.bs_count[brow + 1], 0), a.k_max) : 0;
     const int nwb = ((bq + 1) >> 5) + 1;  // words holding key blocks 0 .. bq + 1
     for (int w = tid; w < nwb; w += NT) {
       sBA[w] = 0u;
@@ -233,6 +236,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
     __syncthreads();
     for (int x = tid; x < na + nb2; x += NT) {
       const int v = x < na ? a.bs_sorted[brow * a.k_max + x] : a.bs_sorted[(brow + 1) * a.k_max + x - na];
+      if (v < 0 || v > bq + 1) continue;
       atomicOr(x < na ? &sBA[v >> 5] : &sBB[v >> 5], 1u << (v & 31));
     }
     __syncthreads();

@@ -137,7 +137,10 @@ def test_block_sparse_matches_oracle(n, k_blocks, vt):
 
 
 @pytest.mark.parametrize("n,nv,ns,spread", [(3000, 40, 300, "local"), (2048, 64, 256, "scatter"),
-                                            (4100, 200, 1500, "mixed"), (900, 0, 1, "diag_only")])
+                                            (4100, 200, 1500, "mixed"), (900, 0, 1, "diag_only"),
+                                            # the most vertical columns a set may hold (2048), nearly all
+                                            # gathered (only the local diagonals give contiguous tiles)
+                                            (6000, 2048, 4, "local")])
 @pytest.mark.parametrize("vt", [False, True])   # the vertical-slash kernel ignores vt
 def test_vertical_slash_matches_oracle(n, nv, ns, spread, vt):
     hq, hkv, d = 2, 1, 128
@@ -165,6 +168,44 @@ def test_vertical_slash_matches_oracle(n, nv, ns, spread, vt):
         V, D = sets[slot]
         ref, _ = A.masked_attention(q[h], k[0], v[0], rows, P.vs_mask(rows, s1, V, D))
         check_close(o[h, s0:s1], ref, f"vs slot={slot}")
+
+
+def test_index_counts_beyond_their_arrays_are_clamped():
+    """A set whose count runs past its array (vertical-slash: |V|, |D| above nv_max, ns_max;
+    block-sparse: the -1 pads counted, and a count above k_max) gives exactly the output of
+    the well-formed set: counts are read clamped to the arrays and entries outside the causal
+    key blocks are skipped.  Only unit 0 / head 0 is altered, which is not the last row of
+    its buffer, so every read stays inside the allocation either way."""
+    import torch
+    n, hq, hkv, d = 1500, 2, 1, 128
+    q, k, v = _inputs(n, hq, hkv, d, seed=77)
+    r = np.random.default_rng(11)
+
+    grid = [(_rs.RS_DENSE, 0, 0), (_rs.RS_VSLASH, 40, 64)]
+    units = [(0, 0, n, 1, 0), (1, 200, n, 1, 1)]
+    ib = _rs.IndexBuffers(2, n, hq, grid)
+    for slot in range(2):
+        fill_vs(ib, slot, 0, np.sort(r.choice(n, 40, replace=False)), np.arange(64))
+    ref, _ = _run_sparse(q, k, v, units, grid, ib)
+    nvm, nsm = ib.vs_vsorted.shape[2], ib.vs_dsorted.shape[2]
+    ib.vs_count[0, 0] = torch.tensor([nvm + 100, nsm + 100], dtype=torch.int32).cuda()
+    got, _ = _run_sparse(q, k, v, units, grid, ib)
+    assert np.array_equal(got, ref, equal_nan=True), "vertical-slash counts above the arrays"
+
+    nb = (n + 63) // 64
+    grid = [(_rs.RS_DENSE, 0, 0), (_rs.RS_BSPARSE, 6, 64)]
+    ib = _rs.IndexBuffers(hq, n, hq, grid)
+    for h in range(hq):
+        fill_bs(ib, h, 0, [sorted(set(r.permutation(bq)[:3].tolist()) | {bq}) for bq in range(nb)])
+    units = [(h, 0, n, 1) for h in range(hq)]
+    ref, _ = _run_sparse(q, k, v, units, grid, ib)
+    kmax = ib.bs_sorted.shape[3]
+    ib.bs_count[0, 0] = kmax             # the -1 pads after each set counted
+    got, _ = _run_sparse(q, k, v, units, grid, ib)
+    assert np.array_equal(got, ref, equal_nan=True), "block-sparse counts over the pads"
+    ib.bs_count[0, 0] = kmax + 5         # and beyond the array
+    got, _ = _run_sparse(q, k, v, units, grid, ib)
+    assert np.array_equal(got, ref, equal_nan=True), "block-sparse counts above k_max"
 
 
 def test_empty_rows_give_zero_and_minus_inf_lse():
