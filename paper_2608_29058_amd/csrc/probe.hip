@@ -149,6 +149,11 @@ template <int D, typename InT, int MODE, int NCV, bool GEN = true>
 __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) {
   constexpr int KS = D / 16, CPR = D / 8, RPI = 64 / CPR, LPT = 64 / RPI / 4;
   constexpr int TE = 64 * D;
+  // K fragment reads in flight ahead of the products, in a forced order; the coverage variant
+  // for arbitrary grids (GEN) has no registers to spare (the reordered loop spills there) and
+  // keeps the block-by-block loop
+  constexpr bool kForceKpf = !(MODE == M_COVER && GEN);
+  constexpr int KPF = 4;
   // K tile buffers: the next tile (and, for coverage, its bitmap words) is fetched while the
   // current one is computed.  The copy is issued once both blocks have read the current tile
   // (after the second block's products): the compiler makes every LDS read wait for the
@@ -325,15 +330,41 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
       const int rmx = s ? rmax1 : rmax0;
       if (u < 0 || rmx < k0) return;  // block absent or entirely before the tile
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb) {
+      for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) sacc[mb][r] = 0.f;
+      if constexpr (!kForceKpf) {  // block by block, reads as the compiler places them
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const u32x4 kf = *(const u32x4 *)&sK[(32 * mb + l32) * D + (((2 * ks + hh) ^ kswz) << 3)];
-          sacc[mb] = mfma32(kf, qf[s][ks], sacc[mb]);
-        }
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) {
+            const u32x4 kf = *(const u32x4 *)&sK[(32 * mb + l32) * D + (((2 * ks + hh) ^ kswz) << 3)];
+            sacc[mb] = mfma32(kf, qf[s][ks], sacc[mb]);
+          }
+        return;
       }
+      // fragment f: 32-key block mb = f % 2, k-step ks = f / 2 (the two accumulators alternate);
+      // reads run KPF fragments ahead of their products (else each product waits for its read)
+      auto kread = [&](int f) __attribute__((always_inline)) -> u32x4 {
+        return *(const u32x4 *)&sK[(32 * (f & 1) + l32) * D + (((2 * (f >> 1) + hh) ^ kswz) << 3)];
+      };
+      u32x4 kb[KPF];
+#pragma unroll
+      for (int f = 0; f < KPF; ++f) kb[f] = kread(f);
+#pragma unroll
+      for (int f = 0; f < 2 * KS; ++f) {
+        sacc[f & 1] = mfma32(kb[f % KPF], qf[s][f >> 1], sacc[f & 1]);
+        if (f + KPF < 2 * KS) kb[f % KPF] = kread(f + KPF);
+      }
+      // keep that order: under register pressure the scheduler would otherwise put each read
+      // right before its product
+      __builtin_amdgcn_sched_group_barrier(0x100, KPF, 0);
+#pragma unroll
+      for (int f = 0; f < 2 * KS - KPF; ++f) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, KPF, 0);
     };
     auto block_tile = [&](const f32x16 (&sacc)[2], int k0, int s, const Pref &f) __attribute__((always_inline)) {
       const int rmx = s ? rmax1 : rmax0;
