@@ -112,6 +112,9 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
   // keeps two (its tile bookkeeping leaves fewer registers; more spill)
   constexpr int KPF = PAT == P_VS ? 2 : 4;
   constexpr int VPF = PAT == P_VS ? 2 : 3;
+  // the products of the tile-skipping families sit under a branch, where the compiler puts
+  // each K read right before its product unless the order is forced (scheduling groups)
+  constexpr bool kForceOrder = PAT == P_VS || PAT == P_BS;
 
   // K and V tiles are double-buffered separately (K runs one tile ahead of V), row-major and
   // swizzled.  Four distinct arrays, addressed with a parity known at compile time, let the
@@ -480,6 +483,15 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
         s[f & 1] = mfma32(kb[f % KPF], qf[f >> 1], s[f & 1]);
         if (f + KPF < 2 * KS) kb[f % KPF] = kread(f + KPF);
       }
+      if constexpr (kForceOrder) {
+        __builtin_amdgcn_sched_group_barrier(0x100, KPF, 0);
+#pragma unroll
+        for (int f = 0; f < 2 * KS - KPF; ++f) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, KPF, 0);
+      }
       return;
     }
 #pragma unroll
@@ -498,6 +510,15 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
       for (int ks = 0; ks < KS; ++ks) {
         s[mb] = mfma32(kb[ks % KPF], qf[ks], s[mb]);
         if (ks + KPF < KS) kb[ks % KPF] = kread(ks + KPF);
+      }
+      if constexpr (kForceOrder) {
+        __builtin_amdgcn_sched_group_barrier(0x100, KPF, 0);
+#pragma unroll
+        for (int ks = 0; ks < KS - KPF; ++ks) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, KPF, 0);
       }
     }
   };
