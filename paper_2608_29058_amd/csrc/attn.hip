@@ -640,6 +640,15 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
         oacc[f % DB] = mfma32(vb[f % VPF], pb[mb][f / DB], oacc[f % DB]);
         if (f + VPF < 2 * DB) vb[f % VPF] = vread(f + VPF);
       }
+      if constexpr (kForceOrder) {  // two transposing reads per fragment
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * VPF, 0);
+#pragma unroll
+        for (int f = 0; f < 2 * DB - VPF; ++f) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, VPF, 0);
+      }
     }
   };
 
