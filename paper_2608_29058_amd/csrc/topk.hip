@@ -290,21 +290,45 @@ __global__ void __launch_bounds__(256) bs_select_kernel(const BsArgs a) {
     sKey[p] = ((unsigned long long)float_key(vals[i]) << 32) | (unsigned long long)(0xffffffffu - (uint32_t)i);
   });
   gsync<NT>();
-  // bitonic sort, descending
+  // bitonic sort, descending, in registers: element e = 4 l + j is key kr[j] of lane l; pairs
+  // at a distance of 4 or more meet across lanes (lane l ^ stride / 4), closer ones within a
+  // lane.  The keys are distinct (block index in the low word; empty slots are 0), so the
+  // order is the unique descending one.
+  static_assert(SP == 4 * NT, "four keys per lane");
+  unsigned long long kr[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) kr[j] = sKey[4 * l + j];
+#pragma unroll
   for (int size = 2; size <= SP; size <<= 1)
+#pragma unroll
     for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int x = l; x < SP / 2; x += NT) {
-        const int lo = 2 * x - (x & (stride - 1));
-        const int hi = lo + stride;
-        const bool desc = ((lo & size) == 0);
-        const unsigned long long A = sKey[lo], B = sKey[hi];
-        if ((A < B) == desc) {
-          sKey[lo] = B;
-          sKey[hi] = A;
+      if (stride >= 4) {
+        const int lx = stride >> 2;
+        const bool lo = (l & lx) == 0, desc = ((4 * l) & size) == 0;  // size >= 8: j drops out
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t plo = (uint32_t)__shfl_xor((int)(uint32_t)kr[j], lx);
+          const uint32_t phi = (uint32_t)__shfl_xor((int)(uint32_t)(kr[j] >> 32), lx);
+          const unsigned long long p = ((unsigned long long)phi << 32) | plo;
+          const bool keep_max = lo == desc;  // the lower element keeps the larger key when descending
+          kr[j] = keep_max ? (kr[j] > p ? kr[j] : p) : (kr[j] < p ? kr[j] : p);
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (j & stride) continue;
+          const bool desc = ((4 * l + j) & size) == 0;
+          const unsigned long long A = kr[j], B = kr[j | stride];
+          if ((A < B) == desc) {
+            kr[j] = B;
+            kr[j | stride] = A;
+          }
         }
       }
-      gsync<NT>();
     }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) sKey[4 * l + j] = kr[j];
+  gsync<NT>();
   const int nsel = min(K, bq);
   int *rk = a.rank + ((long long)h * a.nb + bq) * a.k_max;
   for (int x = l; x < a.k_max; x += NT) {
