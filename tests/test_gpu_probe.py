@@ -42,7 +42,9 @@ def _inputs(n, hq, hkv, d, seed):
     return q, k, v
 
 
-@pytest.mark.parametrize("rc", [(64, 16, 8), (64, 0, 0)])
+# (100, 16, 8) and (192, 0, 0): more than one pair of 32-row blocks holds recent rows (the
+# scores pass accumulates its column and diagonal sums over the pairs), the first ragged
+@pytest.mark.parametrize("rc", [(64, 16, 8), (64, 0, 0), (100, 16, 8), (192, 0, 0)])
 def test_probe_scores_match_oracle(rc):
     n, hq, hkv, d = 3000, 2, 1, 128
     q, k, v = _inputs(n, hq, hkv, d, 1)
@@ -160,7 +162,7 @@ def test_index_families_built_separately_match():
         assert torch.equal(getattr(one, name), getattr(two, name)), name
 
 
-@pytest.mark.parametrize("rc", [(64, 16, 8), (64, 0, 0)])
+@pytest.mark.parametrize("rc", [(64, 16, 8), (64, 0, 0), (100, 16, 8)])
 def test_coverage_matches_oracle(rc):
     import torch
     n, hq, hkv, d = 2200, 2, 1, 128
