@@ -80,6 +80,46 @@ def test_probe_scores_match_oracle(rc):
         np.testing.assert_allclose(lbs[h], tri, atol=1e-4, rtol=1e-5)
 
 
+def test_block_sparse_ranks_at_the_largest_budget():
+    """k = 256, the largest block-sparse budget: once a query block sees more than 255 key
+    blocks every slot of the selection's sort holds a key.  Head 1 has a zero query, so all
+    its block logits are equal and the order falls to the position rule."""
+    import torch
+    n, hq, hkv, d = 20000, 2, 1, 128
+    q, k, v = _inputs(n, hq, hkv, d, 4)
+    q[1] = 0.0
+    units = [(0, 0, n), (1, 0, n)]
+    res = _probe(q, k, v, units, (64, 0, 0), _rs.RS_PROBE_ROWS | _rs.RS_PROBE_BLOCKMEAN)
+    pb = res["pb"]
+    grid = [(_rs.RS_DENSE, 0, 0), (_rs.RS_BSPARSE, 100, 64), (_rs.RS_BSPARSE, 256, 64)]
+    g = _rs.make_grid(grid)
+    ib = _rs.IndexBuffers(len(units), n, hq, grid)
+    ws = _rs.workspace(_rs.rs_build_indices_workspace_size(pb, g, len(grid)))
+    _rs.rs_build_indices(pb, res["u"], len(units), g, len(grid), ws, ib)
+    torch.cuda.synchronize()
+    lbs = pb.lbs.cpu().numpy().astype(np.float64)
+    nb = (n + 63) // 64
+    for h in range(hq):
+        L = np.full((nb, nb), np.nan)
+        off = 0
+        for bq in range(nb):
+            L[bq, :bq + 1] = lbs[h, off:off + bq + 1]
+            off += bq + 1
+        rank_g = ib.bs_rank[h].cpu().numpy()
+        for cl, (_, kk, _) in enumerate(grid[1:]):
+            sel, _ = IX.bs_indices(L, kk)
+            srt = ib.bs_sorted[h, cl].cpu().numpy()
+            cnt = ib.bs_count[h, cl].cpu().numpy()
+            for bq in range(nb):
+                assert cnt[bq] == sel[bq].size, (h, kk, bq)
+                assert np.array_equal(srt[bq, :cnt[bq]], sel[bq]) and np.all(srt[bq, cnt[bq]:] == -1)
+        _, ranks = IX.bs_indices(L, 256)
+        for bq in range(nb):
+            m = min(256, bq + 1)
+            assert np.array_equal(rank_g[bq, :m], ranks[bq][:m]), (h, bq)
+            assert np.all(rank_g[bq, m:] == -1)
+
+
 def _gpu_vs_sets(ib, slot, cl):
     cnt = ib.vs_count[slot, cl].cpu().numpy()
     V = ib.vs_vsorted[slot, cl].cpu().numpy()
