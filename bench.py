@@ -276,8 +276,8 @@ def main():
     RL.probe_and_index(qkv0)
     torch.cuda.synchronize()
     edges = np.array([SEG * (b + 1) for b in range(N // SEG)], np.int32)
-    # t_ker(p, b, n): per candidate and key-length bucket, the median over key/value groups of
-    # the per-unit time of one launch holding that group's query heads (median of 3 reps)
+    # t_ker(p, b, n): per candidate and key-length bucket, the per-unit time of one launch over
+    # every unit of the bucket (median of 3 reps)
     t_table = RL.profile_latency(qkv0, edges, reps=3)
     for c in range(len(GRID)):
         log(f"t_ker {GRID[c]} (us/unit):", np.round(t_table[c], 1).tolist())

@@ -190,30 +190,29 @@ class RoutedLayer:
     # -- offline calibration (untimed) ---------------------------------------------------
     def profile_latency(self, qkv, edges, reps=3):
         """Kernel latency table t_ker[candidate][bucket] in us per unit: for every candidate
-        and key-length bucket, the median over key/value groups of the per-unit time of one
-        launch holding that group's query heads (each the median of ``reps`` launches)."""
+        and key-length bucket, the time of one launch over every unit of that bucket (all
+        query heads, as the routed launches hold many units) divided by their number; the
+        median of ``reps`` launches.  Launches over one key/value group's heads alone price
+        the families differently from the routed launches (measured: their routes ran ~3%
+        slower and varied from run to run)."""
         import torch
         stream = torch.cuda.current_stream()
-        G = self.hq // self.hkv
         t = np.zeros((self.ncand, len(edges)))
         for c in range(self.ncand):
             for b in range(len(edges)):
-                per_group = []
-                for g in range(self.hkv):
-                    us = [i for i, u in enumerate(self.unit_list) if u[2] == edges[b] and u[0] // G == g]
-                    if not us:
-                        continue
-                    ts = []
-                    for _ in range(reps):
-                        e0 = torch.cuda.Event(enable_timing=True)
-                        e1 = torch.cuda.Event(enable_timing=True)
-                        e0.record(stream)
-                        self.run_group(qkv, c, us)
-                        e1.record(stream)
-                        e1.synchronize()
-                        ts.append(e0.elapsed_time(e1))
-                    per_group.append(float(np.median(ts)) / len(us))
-                t[c, b] = float(np.median(per_group)) * 1e3 if per_group else 0.0
+                us = [i for i, u in enumerate(self.unit_list) if u[2] == edges[b]]
+                if not us:
+                    continue
+                ts = []
+                for _ in range(reps):
+                    e0 = torch.cuda.Event(enable_timing=True)
+                    e1 = torch.cuda.Event(enable_timing=True)
+                    e0.record(stream)
+                    self.run_group(qkv, c, us)
+                    e1.record(stream)
+                    e1.synchronize()
+                    ts.append(e0.elapsed_time(e1))
+                t[c, b] = float(np.median(ts)) / len(us) * 1e3
         return t
 
     def profile_probe(self, qkv, reps=3):
