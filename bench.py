@@ -8,8 +8,8 @@ sparse/dense attention launch per (pattern, budget) group.  Each head is split i
 segments of 16K rows (units).  The reported value is ms per layer (lower is better).
 
 Before timing (offline calibration, untimed): the kernel latency of every candidate is
-profiled per 16K key-length bucket on layer 0 (per-unit time of a launch over one key/value
-group's query heads, median over groups and over 3 reps), the probe/route overhead is
+profiled per 16K key-length bucket on layer 0 (per-unit time of one launch over every unit
+of the bucket, median of 3 reps), the probe/route overhead is
 measured, and the layer budget is T = (dense time of the layer) / 6.5.
 
     python bench.py [--steps K] [--warmup W] [--layers L] [--no-cpu-baseline]
