@@ -8,11 +8,17 @@ sparse/dense attention launch per (pattern, budget) group.  Each head is split i
 segments of 16K rows (units).  The reported value is ms per layer (lower is better).
 
 Before timing (offline calibration, untimed): the kernel latency of every candidate is
-profiled per 16K key-length bucket on layer 0 (per-unit time of one launch over every unit
-of the bucket, median of 3 reps), the probe/route overhead is
-measured, and the layer budget is T = (dense time of the layer) / 6.5.
+profiled per 16K key-length bucket on a held-out layer (per-unit time of one launch over
+every unit of the bucket, median of 5 reps, 0.95 quantile reported), the probe/route
+overhead is measured, delta_q is calibrated on held-out layers, and the layer budget is
+T = (dense time of the layer) / 6.5.
 
-    python bench.py [--steps K] [--warmup W] [--layers L] [--no-cpu-baseline]
+After the timed layers: a per-(pattern, budget) accounting pass over the same layers
+(kept-pair FLOP, tile efficiency, fallbacks, over-budget rate), the dense kernel on a whole
+layer (speedup), the three single-layer workloads (A-shape at 8K, vertical-slash at 32K,
+block-sparse at 128K) timed on their own, and the oracle on a bounded sample (CPU baseline).
+
+    python bench.py [--steps K] [--warmup W] [--layers L] [--no-cpu-baseline] [--no-configs]
 """
 from __future__ import annotations
 
@@ -34,6 +40,7 @@ GRID = [(0, 0, 0), (1, 128, 1024), (1, 128, 4096), (2, 500, 256), (2, 1000, 512)
 FAM_NAME = {0: "dense", 1: "ashape", 2: "vslash", 3: "bsparse"}
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
+PROFILE_LAYER = 100         # held-out layer of the latency-table calibration
 
 
 def log(*a):
@@ -229,6 +236,132 @@ def cpu_baseline(q, k, v, route, t_table, edges, knobs, rows_per_unit=32):
                         "attention_sample": round(t_attn, 2)}}
 
 
+# ---- the single-layer workloads: A-shape at 8K, vertical-slash at 32K, block-sparse at 128K --
+
+def time_configs(reps):
+    """Per-launch timings of the three single-layer workloads (HIP events on the stream,
+    median and 0.95 quantile over ``reps`` launches after one warm-up), with their exact
+    kept-pair counts, TFLOP/s on kept pairs against the bf16 peak and the build's own dense
+    kernel on the same layer."""
+    import torch
+    from paper_2608_29058_amd import _rs
+    from synth import gen as G
+    stream = torch.cuda.current_stream()
+
+    def timed(fn):
+        fn()
+        ts = []
+        for _ in range(reps):
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            b.synchronize()
+            ts.append(a.elapsed_time(b))
+        return float(np.median(ts)), float(np.quantile(ts, 0.95))
+
+    def entry(ms, p95, flops, **kw):
+        tf = flops / (ms * 1e-3) / 1e12
+        return dict(ms=round(ms, 4), ms_p95=round(p95, 4), tflops=round(tf, 1),
+                    frac=round(tf / PEAK_BF16_TFLOPS, 4), **kw)
+
+    def layer(cfg):
+        t = G.make_layer_torch(cfg, 0, device="cuda")
+        q, k, v = t["q"], t["k"], t["v"]
+        vt = torch.empty(_rs.rs_vt_bytes(_rs.make_qkv(q, k, v)), dtype=torch.uint8, device="cuda")
+        qkv = _rs.make_qkv(q, k, v, vt=vt)
+        return q, k, v, vt, qkv
+
+    def dense(qkv, q, heads, o):
+        n = q.shape[1]
+        ud = _rs.make_units([(h, 0, n) for h in heads])
+        ws = _rs.workspace(_rs.rs_attn_workspace_size(qkv, ud, len(heads)))
+        return lambda: _rs.rs_dense_attn_prefill(qkv, ud, len(heads), o, None, ws)
+
+    out = {}
+    # A-shape (128 sinks + 1024 window) on every head, n = 8192
+    q, k, v, vt, qkv = layer(2)
+    n = q.shape[1]
+    o = torch.empty_like(q)
+    grid = [(0, 0, 0), (1, 128, 1024)]
+    units = _rs.make_units([(h, 0, n, 1, h) for h in range(HQ)])
+    ws = _rs.workspace(_rs.rs_attn_workspace_size(qkv, units, HQ))
+    g = _rs.make_grid(grid)
+    ms, p95 = timed(lambda: _rs.rs_sparse_attn_prefill(qkv, units, HQ, g, 2, None, o, None, ws))
+    pairs = pairs_ashape(0, n, 128, 1024)
+    dms, _ = timed(dense(qkv, q, range(HQ), o))
+    out["ashape_8k"] = entry(ms, p95, 4.0 * D * HQ * pairs, pairs_per_head=pairs, dense_ms=round(dms, 4),
+                             speedup_vs_dense=round(dms / ms, 3),
+                             workload="n=8192, GQA 32/8 d128 bf16, A-shape (128 sinks, 1024 window) on all heads")
+    log("timed ashape_8k", out["ashape_8k"])
+    del q, k, v, vt, qkv, o
+    # vertical-slash (1000 columns, 6096 diagonals) on 28 heads + 4 dense heads, n = 32768
+    q, k, v, vt, qkv = layer(3)
+    n = q.shape[1]
+    o = torch.empty_like(q)
+    dense_heads = [0, 5, 10, 15]
+    vs_heads = [h for h in range(HQ) if h not in dense_heads]
+    grid = [(0, 0, 0), (2, 1000, 6096)]
+    g = _rs.make_grid(grid)
+    units = _rs.make_units([(h, 0, n, 1, i) for i, h in enumerate(vs_heads)])
+    cfg = _rs.RsProbeCfg(r_rec=64, r_uni=0, r_bnd=0, bs_block=64, local_w=1024, flags=_rs.RS_PROBE_ROWS)
+    pb = _rs.ProbeBuffers(len(vs_heads), 64, n, HQ)
+    ib = _rs.IndexBuffers(len(vs_heads), n, HQ, grid)
+    ws = _rs.workspace(max(_rs.rs_probe_workspace_size(qkv, units, len(vs_heads), cfg),
+                           _rs.rs_attn_workspace_size(qkv, units, len(vs_heads))))
+    p_ms, _ = timed(lambda: _rs.rs_probe(qkv, units, len(vs_heads), cfg, None, 0, None, ws, pb))
+    i_ms, _ = timed(lambda: _rs.rs_build_indices(pb, units, len(vs_heads), g, 2, ws, ib))
+    ms, p95 = timed(lambda: _rs.rs_sparse_attn_prefill(qkv, units, len(vs_heads), g, 2, ib, o, None, ws))
+    dfn = dense(qkv, q, dense_heads, o)
+    d4_ms, d4_p95 = timed(dfn)
+    cnt = ib.vs_count[:, 0].cpu().numpy()
+    Vs, Ds = ib.vs_vsorted[:, 0].cpu().numpy(), ib.vs_dsorted[:, 0].cpu().numpy()
+    vs_pairs = [pairs_vs(0, n, Vs[i, :cnt[i, 0]], Ds[i, :cnt[i, 1]]) for i in range(len(vs_heads))]
+    vs_tiles = sum(tiles_vs(0, n, Vs[i, :cnt[i, 0]], Ds[i, :cnt[i, 1]]) for i in range(len(vs_heads)))
+    dms, _ = timed(dense(qkv, q, range(HQ), o))
+    out["vslash_32k"] = entry(ms, p95, 4.0 * D * sum(vs_pairs), pairs_total=int(sum(vs_pairs)),
+                              tile_efficiency=round(sum(vs_pairs) / (vs_tiles * 64 * 128), 4),
+                              probe_ms=round(p_ms, 4), indices_ms=round(i_ms, 4),
+                              dense_4_heads=entry(d4_ms, d4_p95, 4.0 * D * 4 * pairs_dense(0, n)),
+                              layer_ms=round(p_ms + i_ms + ms + d4_ms, 4), dense_ms=round(dms, 4),
+                              speedup_vs_dense=round(dms / (p_ms + i_ms + ms + d4_ms), 3),
+                              workload="n=32768, GQA 32/8 d128 bf16, probe on the last 64 queries, vertical-slash "
+                                       "(1000, 6096) on 28 heads, heads 0/5/10/15 dense")
+    log("timed vslash_32k", out["vslash_32k"])
+    del q, k, v, vt, qkv, o, pb, ib, ws
+    # block-sparse (block-mean scores, top-100 of 64-token blocks) on every head, n = 131072
+    q, k, v, vt, qkv = layer(4)
+    n = q.shape[1]
+    o = torch.empty_like(q)
+    grid = [(0, 0, 0), (3, 100, 64)]
+    g = _rs.make_grid(grid)
+    units = _rs.make_units([(h, 0, n, 1, h) for h in range(HQ)])
+    cfg = _rs.RsProbeCfg(r_rec=0, r_uni=0, r_bnd=0, bs_block=64, local_w=1024, flags=_rs.RS_PROBE_BLOCKMEAN)
+    pb = _rs.ProbeBuffers(HQ, 0, n, HQ, blockmean=True)
+    ib = _rs.IndexBuffers(HQ, n, HQ, grid)
+    ws = _rs.workspace(max(_rs.rs_probe_workspace_size(qkv, units, HQ, cfg),
+                           _rs.rs_attn_workspace_size(qkv, units, HQ)))
+    t_ms, _ = timed(lambda: _rs.rs_transpose_v(qkv, vt))
+    p_ms, _ = timed(lambda: _rs.rs_probe(qkv, units, HQ, cfg, None, 0, None, ws, pb))
+    i_ms, _ = timed(lambda: _rs.rs_build_indices(pb, units, HQ, g, 2, ws, ib))
+    ms, p95 = timed(lambda: _rs.rs_sparse_attn_prefill(qkv, units, HQ, g, 2, ib, o, None, ws))
+    counts = ib.bs_count[:, 0].cpu().numpy()
+    pairs = [pairs_bs(0, n, counts[h]) for h in range(HQ)]
+    srt = ib.bs_sorted[:, 0].cpu().numpy()
+    tiles = sum(tiles_bs(0, n, srt[h], counts[h]) for h in range(HQ))
+    dms, _ = timed(dense(qkv, q, range(HQ), o))
+    lay = t_ms + p_ms + i_ms + ms
+    out["bsparse_128k"] = entry(ms, p95, 4.0 * D * sum(pairs), pairs_per_head=sorted(set(pairs)),
+                                tile_efficiency=round(sum(pairs) / (tiles * 64 * 128), 4),
+                                transpose_v_ms=round(t_ms, 4), blockmean_ms=round(p_ms, 4), indices_ms=round(i_ms, 4),
+                                layer_ms=round(lay, 4), dense_ms=round(dms, 4), speedup_vs_dense=round(dms / lay, 3),
+                                workload="n=131072, GQA 32/8 d128 bf16, block-mean scores, top-100 64-token key "
+                                         "blocks per query block on all heads")
+    log("timed bsparse_128k", out["bsparse_128k"])
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -240,6 +373,8 @@ def main():
     ap.add_argument("--route", choices=("device", "host"), default="device",
                     help="routing on the device (no host synchronisation in a layer) or on the host")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true", help="skip the timed single-layer workloads (c2-c4)")
+    ap.add_argument("--config-reps", type=int, default=10)
     ap.add_argument("--json-out", default=None)
     args = ap.parse_args()
     if args.gpus != 1:
@@ -271,18 +406,24 @@ def main():
         return e
 
     # ---- offline calibration: kernel latency table, probe overhead, budget -----------------
-    q0, k0, v0, _ = layers[0]
-    qkv0 = RL.qkv(q0, k0, v0)
-    RL.probe_and_index(qkv0)
+    # the latency table is profiled on a held-out layer (its seed is neither a timed layer's
+    # nor a calibration layer's), so the router's cost model is not fitted on the timed inputs
+    hp = G.make_layer_torch(5, PROFILE_LAYER, device=dev)
+    qp, kp, vp = hp["q"], hp["k"], hp["v"]
+    del hp
+    qkvp = RL.qkv(qp, kp, vp)
+    RL.probe_and_index(qkvp)
     torch.cuda.synchronize()
     edges = np.array([SEG * (b + 1) for b in range(N // SEG)], np.int32)
     # t_ker(p, b, n): per candidate and key-length bucket, the per-unit time of one launch over
-    # every unit of the bucket (median of 3 reps)
-    t_table = RL.profile_latency(qkv0, edges, reps=3)
+    # every unit of the bucket (median of 5 reps; the 0.95 quantile is reported beside it)
+    tail = {}
+    t_table = RL.profile_latency(qkvp, edges, reps=5, tail=tail)
     for c in range(len(GRID)):
         log(f"t_ker {GRID[c]} (us/unit):", np.round(t_table[c], 1).tolist())
     # probe + index + coverage time, and the host routing overhead
-    tp_us = RL.profile_probe(qkv0, reps=3)
+    tp_us = RL.profile_probe(qkvp, reps=3)
+    del qp, kp, vp, qkvp
     RL.t_table, RL.edges = t_table, edges
     t_dense_layer_us = float(sum(t_table[0, int(np.searchsorted(edges, u[2]))] for u in RL.unit_list))
     # delta_q: one-sided 0.95-quantile of m_hat - m_true over every (unit, sparse candidate) of
@@ -322,6 +463,7 @@ def main():
         q, k, v, _ = layers[s % args.layers]
         RL.run(q, k, v, device_route=device)
     torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()
     records = []
     t_wall0 = time.perf_counter()
     e_start = ev()
@@ -337,6 +479,8 @@ def main():
     wall_ms = (time.perf_counter() - t_wall0) * 1e3
     total_ms = e_start.elapsed_time(e_end)
     ms_per_layer = total_ms / args.steps
+    peak_mem = torch.cuda.max_memory_allocated()
+    step_ms = np.array([dict(m)["start"].elapsed_time(dict(m)["attention"]) for _, m, _ in records])
 
     # ---- per-phase / per-family accounting (after the timed region) -------------------------
     cand_units = [0] * len(GRID)
@@ -346,7 +490,8 @@ def main():
     fam_flops = {f: 0.0 for f in FAM_NAME}
     fam_issued = {f: 0.0 for f in FAM_NAME}
     fam_launches = {f: 0 for f in FAM_NAME}
-    ph = {"transpose_v": 0.0, "probe_index_coverage": 0.0, "route": 0.0, "attention": 0.0}
+    ph = {"transpose_v": 0.0, "probe_scores": 0.0, "indices": 0.0, "coverage": 0.0, "route": 0.0,
+          "attention": 0.0}
     # timed per-family launch time (device routing: one persistent launch per family and layer)
     fam_time_timed = {f: 0.0 for f in FAM_NAME}
     for li, marks, fev in records:
@@ -354,7 +499,9 @@ def main():
         at = {m[0]: m[1] for m in marks}
         t0_probe = at.get("transpose_v", at["start"])
         ph["transpose_v"] += at["start"].elapsed_time(t0_probe) if "transpose_v" in at else 0.0
-        ph["probe_index_coverage"] += t0_probe.elapsed_time(at["probe"])
+        ph["probe_scores"] += t0_probe.elapsed_time(at["probe_scores"])
+        ph["indices"] += at["probe_scores"].elapsed_time(at["indices"])
+        ph["coverage"] += at["indices"].elapsed_time(at["probe"])
         ph["route"] += at["probe"].elapsed_time(at["route"])
         ph["attention"] += at["route"].elapsed_time(evs[-1])
         if fev is not None:
@@ -364,6 +511,7 @@ def main():
     # the host (the device route is checked to be identical), one launch per (pattern, budget)
     # group with events around each, weighted by the layer's number of timed steps.
     n_units_fb = 0
+    n_over_budget = 0
     n_units_dense = 0
     routed_flops = 0.0
     route_mismatch = 0
@@ -381,6 +529,7 @@ def main():
             RL.route_device()
             route_mismatch += int(RL.rb.choice[:RL.nunits].cpu().tolist() != route["choice"])
         n_units_fb += w_l * route["n_fallback"]
+        n_over_budget += w_l * int(route["over_budget"])
         ic = dict(bs_count=RL.ib.bs_count.cpu().numpy(), vs_count=RL.ib.vs_count.cpu().numpy(),
                   vs_v=RL.ib.vs_vsorted.cpu().numpy(), vs_d=RL.ib.vs_dsorted.cpu().numpy(), bs_lists={})
         gev = [ev()]
@@ -422,6 +571,7 @@ def main():
             fam_launches[fam] += w_l
             routed_flops += fl
     # dense reference: the whole layer through the dense kernel, same run
+    q0, k0, v0, _ = layers[0]
     qkv_d = RL.qkv(q0, k0, v0)
     ud = _rs.make_units([(h, 0, N, 0, 0) for h in range(HQ)])
     wsd = _rs.workspace(_rs.rs_attn_workspace_size(qkv_d, ud, HQ))
@@ -452,6 +602,16 @@ def main():
                 "kernel": f"{kname}[{FAM_NAME[dom]}]", "avg_launch_ms": round(dom_avg_ms, 4),
                 "launches": nlaunch[dom],
                 "flops_def": "4*d*(kept query-key pairs) per launch"}
+    # the routed-sparse families together (A-shape, vertical-slash, block-sparse), the whole
+    # attention phase, and each family on its own: kept-pair FLOP over launch time
+    sp_fl = sum(fam_flops[f] for f in (1, 2, 3))
+    sp_t = sum(ftime[f] for f in (1, 2, 3))
+    roofline["sparse_frac"] = round(sp_fl / (sp_t * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4) if sp_t else None
+    roofline["sparse_achieved"] = round(sp_fl / (sp_t * 1e-3) / 1e12, 1) if sp_t else None
+    att_t = ph["attention"]
+    roofline["attention_frac"] = round(sum(fam_flops.values()) / (att_t * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)
+    roofline["family_frac"] = {FAM_NAME[f]: (round(fam_flops[f] / (ftime[f] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)
+                                             if ftime[f] else None) for f in FAM_NAME}
     res = {
         "metric": METRIC, "value": round(ms_per_layer, 4), "unit": "ms/layer", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_layer, 4),
@@ -466,6 +626,10 @@ def main():
         "dense_tflops": round(dense_flops / (dense_ms * 1e-3) / 1e12, 1),
         "speedup_vs_dense": round(dense_ms / ms_per_layer, 3),
         "routed_effective_tflops": round(routed_flops / args.steps / (ms_per_layer * 1e-3) / 1e12, 1),
+        "ms_per_layer_median": round(float(np.median(step_ms)), 4),
+        "ms_per_layer_p95": round(float(np.quantile(step_ms, 0.95)), 4),
+        "ms_per_layer_min_max": [round(float(step_ms.min()), 4), round(float(step_ms.max()), 4)],
+        "peak_mem_allocated_gib": round(peak_mem / 2 ** 30, 3),
         "phase_ms_per_layer": {k2: round(v2 / args.steps, 4) for k2, v2 in ph.items()},
         "family_ms_per_layer": {FAM_NAME[f]: round(ftime[f] / args.steps, 4) for f in FAM_NAME},
         "family_tflops": {FAM_NAME[f]: (round(fam_flops[f] / (ftime[f] * 1e-3) / 1e12, 1) if ftime[f] else None)
@@ -481,6 +645,10 @@ def main():
                         "tflops": (round(4.0 * D * cand_pairs[c] / (cand_time[c] * 1e-3) / 1e12, 1)
                                    if cand_time[c] else None)} for c in range(len(GRID))],
         "fallback_units_per_layer": round(n_units_fb / args.steps, 2),
+        "over_budget_rate": round(n_over_budget / args.steps, 4),
+        "latency_table_layer": PROFILE_LAYER,
+        "t_ker_us_median": {str(tuple(GRID[c])): np.round(t_table[c], 1).tolist() for c in range(len(GRID))},
+        "t_ker_us_p95": {str(tuple(GRID[c])): np.round(tail["p95"][c], 1).tolist() for c in range(len(GRID))},
         "dense_units_per_layer": round(n_units_dense / args.steps, 2),
         "wall_ms_timed": round(wall_ms, 1),
         "t_layer_budget_ms": round(RL.knobs.T_layer_us / 1e3, 3),
@@ -489,6 +657,10 @@ def main():
         "device_route_mismatches": route_mismatch if device else None,
         "delta_q": round(delta_q, 5),
     }
+    if not args.no_configs:
+        del layers, od
+        torch.cuda.empty_cache()
+        res["configs"] = time_configs(args.config_reps)
     if not args.no_cpu_baseline:
         try:
             res["cpu_baseline"] = cpu_baseline(q0, k0, v0, routes[records[0][0]], t_table, edges, RL.knobs)

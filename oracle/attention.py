@@ -18,8 +18,8 @@ def logits(q, k, rows, s1, scale=None):
     """l_ij = (q_i . k_j) * scale for i in rows, j in [0, s1)  (Sec. 2.1, Eq. 1)."""
     rows = np.asarray(rows, dtype=np.int64)
     scale = default_scale(q.shape[1]) if scale is None else scale
-    qr = np.asarray(q, dtype=np.float64)[rows]
-    kk = np.asarray(k, dtype=np.float64)[:s1]
+    qr = np.asarray(q)[rows].astype(np.float64)
+    kk = np.asarray(k)[:s1].astype(np.float64)
     return (qr @ kk.T) * scale
 
 
@@ -79,7 +79,36 @@ def dense_attention(q, k, v, rows=None, scale=None, block=512):
 def masked_attention(q, k, v, rows, mask, scale=None):
     """O~_i = softmax over S_i of l_i. times V (Sec. 2.1): the sparse-mask output."""
     p, lse = masked_softmax(q, k, rows, mask, scale)
-    return p @ np.asarray(v, dtype=np.float64)[:p.shape[1]], lse
+    return p @ np.asarray(v)[:p.shape[1]].astype(np.float64), lse
+
+
+def masked_attention_cols(q, k, v, rows, cols, keep, scale=None):
+    """Masked attention (Sec. 2.1) whose kept sets lie among the key positions ``cols``
+    (ascending): S_i = {cols[c] : keep[r, c] and cols[c] <= i}.  The result equals
+    masked_attention with the mask that is ``keep`` on ``cols`` and False elsewhere; only the
+    logits of the listed keys are formed, so sparse sets over long prefixes stay cheap.  The
+    same fp64 steps as masked_softmax, taken with torch CPU operations (multi-threaded).
+
+    Returns (output, lse) as masked_attention does (empty rows: 0 and minus infinity)."""
+    import torch
+    rows = np.asarray(rows, dtype=np.int64)
+    cols = np.asarray(cols, dtype=np.int64)
+    scale = default_scale(q.shape[1]) if scale is None else scale
+    keep = torch.from_numpy(np.asarray(keep, dtype=bool) & (cols[None, :] <= rows[:, None]))
+    qr = torch.from_numpy(np.asarray(q)[rows]).to(torch.float64)
+    kc = torch.from_numpy(np.asarray(k)[cols]).to(torch.float64)
+    vc = torch.from_numpy(np.asarray(v)[cols]).to(torch.float64)
+    lg = (qr @ kc.T) * scale
+    lg = lg.masked_fill(~keep, float("-inf"))
+    empty = ~keep.any(dim=1)
+    zero = torch.zeros((), dtype=torch.float64)
+    mx = torch.where(empty, zero, lg.amax(dim=1) if cols.size else zero)[:, None]
+    e = torch.exp(lg - mx).masked_fill(~keep, 0.0)
+    den = e.sum(dim=1, keepdim=True)
+    p = e / torch.where(den > 0, den, torch.ones_like(den))  # empty rows: e = 0, so p = 0
+    lse = torch.where(empty, float("-inf"), mx[:, 0] + torch.log(torch.where(den[:, 0] > 0, den[:, 0],
+                                                                           torch.ones_like(den[:, 0]))))
+    return (p @ vc).numpy(), lse.numpy()
 
 
 def retained_mass(a, mask):

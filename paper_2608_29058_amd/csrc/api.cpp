@@ -234,11 +234,23 @@ rs_status rs_probe(const rs_qkv *qkv, const rs_unit *units, int32_t nunits, cons
     if ((st = check_grid(grid, ncand)) != RS_OK) return st;
     if (out->ncand != ncand || !out->cov_rows || !out->cov) return fail(RS_ERR_INVALID_ARG, "coverage arrays missing");
     if (idx->nunits != nunits || idx->n != qkv->n) return fail(RS_ERR_INVALID_ARG, "index set does not match");
+    // the kernels index the bitmaps with the grid-local candidate index and the set's strides:
+    // the set must hold every candidate of the grid with the word counts of this n
+    int nvs = 0, nbs = 0;
     for (int c = 0; c < ncand; ++c) {
-      if (grid[c].fam == RS_VSLASH && (!idx->vs_vbits || !idx->vs_dbits))
-        return fail(RS_ERR_INVALID_ARG, "vertical-slash bitmaps missing");
-      if (grid[c].fam == RS_BSPARSE && (!idx->bs_bits || idx->hq != qkv->hq))
-        return fail(RS_ERR_INVALID_ARG, "block-sparse bitmaps missing");
+      nvs += grid[c].fam == RS_VSLASH;
+      nbs += grid[c].fam == RS_BSPARSE;
+    }
+    const int nbk = (qkv->n + 63) / 64;
+    if (nvs > 0) {
+      if (!idx->vs_vbits || !idx->vs_dbits) return fail(RS_ERR_INVALID_ARG, "vertical-slash bitmaps missing");
+      if (idx->ncand_vs < nvs || idx->nwords != (qkv->n + 31) / 32)
+        return fail(RS_ERR_INVALID_ARG, "index set does not match the grid (vertical-slash candidates or nwords)");
+    }
+    if (nbs > 0) {
+      if (!idx->bs_bits || idx->hq != qkv->hq) return fail(RS_ERR_INVALID_ARG, "block-sparse bitmaps missing");
+      if (idx->ncand_bs < nbs || idx->nb != nbk || idx->nbw != (nbk + 31) / 32)
+        return fail(RS_ERR_INVALID_ARG, "index set does not match the grid (block-sparse candidates, nb or nbw)");
     }
   }
   if (nunits == 0) return RS_OK;
@@ -306,9 +318,10 @@ size_t rs_route_layer_device_workspace_size(int32_t nunits, int32_t ncand) {
   return route_dev_ws_bytes(nunits, ncand);
 }
 
-rs_status rs_route_layer_device(const rs_route_in *in, const rs_route_cfg *cfg, const rs_route_dev_out *out,
-                                void *ws, size_t ws_bytes, rs_stream stream) {
-  g_err.clear();
+// Validation shared by the two device-routing entry points: fills the per-candidate family,
+// budget rank and the dense candidate.
+static rs_status check_route_dev(const rs_route_in *in, const rs_route_cfg *cfg, const rs_route_dev_out *out,
+                                 int *fam, int *brank, int *dense_out) {
   if (!in || !cfg || !out) return fail(RS_ERR_INVALID_ARG, "route: NULL argument");
   const int U = in->nunits, C = in->ncand;
   if (U < 0 || C < 1 || C > 16 || !in->grid) return fail(RS_ERR_INVALID_ARG, "route: bad sizes (1 <= ncand <= 16)");
@@ -317,7 +330,7 @@ rs_status rs_route_layer_device(const rs_route_in *in, const rs_route_cfg *cfg, 
   if (!out->choice || !out->group_cand || !out->group_start || !out->group_units || !out->risk || !out->m_lower ||
       !out->status || !out->totals)
     return fail(RS_ERR_INVALID_ARG, "route: missing outputs");
-  int fam[16], brank[16], dense_c = -1;
+  int dense_c = -1;
   for (int c = 0; c < C; ++c) {
     fam[c] = in->grid[c].fam;
     if (fam[c] < RS_DENSE || fam[c] > RS_BSPARSE) return fail(RS_ERR_INVALID_ARG, "route: unknown family");
@@ -325,6 +338,16 @@ rs_status rs_route_layer_device(const rs_route_in *in, const rs_route_cfg *cfg, 
     if (fam[c] == RS_DENSE && dense_c < 0) dense_c = c;
   }
   if (dense_c < 0) return fail(RS_ERR_INVALID_ARG, "route: the grid must contain a dense candidate");
+  *dense_out = dense_c;
+  return RS_OK;
+}
+
+rs_status rs_route_layer_device(const rs_route_in *in, const rs_route_cfg *cfg, const rs_route_dev_out *out,
+                                void *ws, size_t ws_bytes, rs_stream stream) {
+  g_err.clear();
+  int fam[16], brank[16], dense_c = -1;
+  rs_status st = check_route_dev(in, cfg, out, fam, brank, &dense_c);
+  if (st != RS_OK) return st;
   return route_dev_launch(in, cfg, out, fam, brank, dense_c, ws, ws_bytes, (hipStream_t)stream);
 }
 

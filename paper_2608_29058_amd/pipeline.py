@@ -94,10 +94,14 @@ class RoutedLayer:
         return self._ws
 
     # -- steps ---------------------------------------------------------------------------
-    def probe_and_index(self, qkv):
+    def probe_and_index(self, qkv, mark=None):
+        """Scores probe, index construction, coverage probe (``mark(name)`` after each)."""
+        mark = mark or (lambda name: None)
         ws = self.workspace(qkv)
         _rs.rs_probe(qkv, self.units, self.nunits, self.cfg, None, 0, None, ws, self.pb)
+        mark("probe_scores")
         _rs.rs_build_indices(self.pb, self.units, self.nunits, self.g, self.ncand, ws, self.ib)
+        mark("indices")
         _rs.rs_probe(qkv, self.units, self.nunits, self.cfg, self.g, self.ncand, self.ib, ws, self.pb)
 
     def _use_e(self):
@@ -168,7 +172,7 @@ class RoutedLayer:
         qkv = self.qkv(q, k, v)
         if self.vt is not None:
             mark("transpose_v")
-        self.probe_and_index(qkv)
+        self.probe_and_index(qkv, mark)
         mark("probe")
         if device_route:
             self.route_device()
@@ -188,16 +192,18 @@ class RoutedLayer:
         return route
 
     # -- offline calibration (untimed) ---------------------------------------------------
-    def profile_latency(self, qkv, edges, reps=3):
+    def profile_latency(self, qkv, edges, reps=3, tail=None):
         """Kernel latency table t_ker[candidate][bucket] in us per unit: for every candidate
         and key-length bucket, the time of one launch over every unit of that bucket (all
         query heads, as the routed launches hold many units) divided by their number; the
         median of ``reps`` launches.  Launches over one key/value group's heads alone price
         the families differently from the routed launches (measured: their routes ran ~3%
-        slower and varied from run to run)."""
+        slower and varied from run to run).  ``tail`` (optional dict) receives the 0.95
+        quantile of the same launches under key "p95"."""
         import torch
         stream = torch.cuda.current_stream()
         t = np.zeros((self.ncand, len(edges)))
+        t95 = np.zeros((self.ncand, len(edges)))
         for c in range(self.ncand):
             for b in range(len(edges)):
                 us = [i for i, u in enumerate(self.unit_list) if u[2] == edges[b]]
@@ -213,6 +219,9 @@ class RoutedLayer:
                     e1.synchronize()
                     ts.append(e0.elapsed_time(e1))
                 t[c, b] = float(np.median(ts)) / len(us) * 1e3
+                t95[c, b] = float(np.quantile(ts, 0.95)) / len(us) * 1e3
+        if tail is not None:
+            tail["p95"] = t95
         return t
 
     def profile_probe(self, qkv, reps=3):

@@ -237,3 +237,33 @@ def test_device_routing_entries_reject_bad_arguments_without_launch():
     st = L.rs_routed_attn_prefill(C.byref(q), units, 2, grid, len(GRID), None, C.c_void_p(16), C.c_void_p(16),
                                   256 * 128, 128, None, C.c_void_p(16), 1 << 20, None, None)
     assert st == _rs.RS_ERR_INVALID_ARG and b"index set" in L.rs_last_error()
+
+
+def test_probe_coverage_rejects_mismatched_index_set_without_launch():
+    """Coverage mode indexes the index set's bitmaps with grid-local candidate indices and the
+    set's word counts: a set sized for a smaller grid or another n is rejected on the host."""
+    L = _rs.lib()
+    n, hq, hkv = 4096, 2, 1
+    q = _rs.RsQkv(q=16, k=16, v=16, dtype=_rs.RS_BF16, n=n, hq=hq, hkv=hkv, d=128, sq_h=n * 128, sq_t=128,
+                  sk_h=n * 128, sk_t=128, sv_h=n * 128, sv_t=128)
+    units = _rs.make_units([(0, 0, n), (1, 0, n)])
+    cfg = _rs.RsProbeCfg(r_rec=64, r_uni=0, r_bnd=0, bs_block=64, local_w=1024, flags=_rs.RS_PROBE_ROWS)
+    grid = [(RT.DENSE, 0, 0), (RT.VSLASH, 10, 20), (RT.VSLASH, 20, 40), (RT.BSPARSE, 4, 64), (RT.BSPARSE, 8, 64)]
+    g = _rs.make_grid(grid)
+    nb = n // 64
+    out = _rs.RsProbeOut(nunits=2, rmax=64, n=n, nb=nb, ncand=len(grid), hq=hq, rows=16, subset=16, nsub=16,
+                         row_max=16, row_sum=16, col=16, diag=16, entropy=16, local=16, cov_rows=16, cov=16)
+
+    def idx(**kw):
+        d = dict(nunits=2, n=n, nb=nb, hq=hq, nv_max=20, ns_max=40, k_max=8, nwords=n // 32, ncand_vs=2,
+                 ncand_bs=2, nbw=(nb + 31) // 32, vs_vsorted=16, vs_dsorted=16, vs_count=16, vs_vbits=16,
+                 vs_dbits=16, bs_rank=16, bs_sorted=16, bs_count=16, bs_bits=16)
+        d.update(kw)
+        return _rs.RsIndexSet(**d)
+
+    for bad, what in ((dict(ncand_vs=1), b"vertical-slash"), (dict(nwords=n // 32 - 1), b"nwords"),
+                      (dict(ncand_bs=1), b"block-sparse"), (dict(nbw=7), b"nbw"), (dict(nb=nb - 1), b"nb")):
+        st = L.rs_probe(C.byref(q), units, 2, C.byref(cfg), g, len(grid), C.byref(idx(**bad)), C.c_void_p(256),
+                        1 << 40, C.byref(out), None)
+        assert st == _rs.RS_ERR_INVALID_ARG, bad
+        assert what in L.rs_last_error(), (bad, L.rs_last_error())

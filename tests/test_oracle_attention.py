@@ -127,3 +127,44 @@ def test_e_rel_values():
     assert A.e_rel(o, o) == 0.0
     assert abs(A.e_rel(o, np.zeros_like(o)) - 1.0) < 1e-12
     assert abs(A.e_rel(o, 3 * o) - 2.0) < 1e-12
+
+
+def _brute_masked(q, k, v, rows, keep_fn):
+    """Per-element loops: softmax over the kept keys of each row, times V."""
+    n, d = q.shape
+    out = np.zeros((len(rows), v.shape[1]))
+    for r, i in enumerate(rows):
+        S = [j for j in range(i + 1) if keep_fn(r, j)]
+        if not S:
+            continue
+        lg = [sum(q[i, t] * k[j, t] for t in range(d)) / math.sqrt(d) for j in S]
+        mx = max(lg)
+        w = [math.exp(x - mx) for x in lg]
+        s = sum(w)
+        for jj, j in enumerate(S):
+            out[r] += w[jj] / s * v[j]
+    return out
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_masked_cols_matches_brute_force_and_full_mask(seed):
+    """masked_attention_cols over a column subset equals per-element loops and the full-width
+    masked_attention with the mask embedded (columns outside ``cols`` dropped); rows left with
+    no kept key give 0 and minus infinity."""
+    n, d = 50, 8
+    q, k, v = _rand(n, d, 40 + seed)
+    r = np.random.default_rng(seed)
+    rows = np.sort(r.choice(n, 20, replace=False))
+    cols = np.sort(r.choice(n, 23, replace=False))
+    keep = r.random((rows.size, cols.size)) < 0.6
+    keep[0] = False                                   # an empty row
+    got, lse = A.masked_attention_cols(q, k, v, rows, cols, keep)
+    full = np.zeros((rows.size, n), bool)
+    full[:, cols] = keep
+    ref, rl = A.masked_attention(q, k, v, rows, full)
+    colpos = {int(c): x for x, c in enumerate(cols)}
+    brute = _brute_masked(q, k, v, rows, lambda rr, j: j in colpos and keep[rr, colpos[j]])
+    np.testing.assert_allclose(got, brute, atol=1e-12, rtol=0)
+    np.testing.assert_allclose(got, ref, atol=1e-13, rtol=0)
+    assert np.isneginf(lse[0]) and np.all(got[0] == 0)
+    np.testing.assert_allclose(lse[1:], rl[1:], atol=1e-12)

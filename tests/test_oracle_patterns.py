@@ -80,3 +80,22 @@ def test_workload_pair_counts():
     m = P.bs_mask(np.arange(n2), n2, B2, lambda bq: range(max(0, bq - k2 + 1), bq + 1))
     tot2 = sum((min(bq + 1, k2) - 1) * B2 * B2 + B2 * (B2 + 1) // 2 for bq in range(n2 // B2))
     assert m.sum() == tot2
+
+
+def test_masks_on_column_subsets_equal_full_mask_columns():
+    """Evaluating a pattern on a subset of key positions gives exactly those columns of the
+    full mask, for every family (used to check long prefixes on the kept keys only)."""
+    r = np.random.default_rng(9)
+    s1 = 700
+    rows = np.sort(r.choice(s1, 60, replace=False))
+    cols = np.sort(r.choice(s1, 250, replace=False))
+    V = r.choice(s1, 40, replace=False)
+    D = np.concatenate([[0], r.choice(s1, 30, replace=False)])
+    sel = {b: sorted(set(r.choice(b + 1, min(b + 1, 4), replace=False).tolist()) | {b}) for b in range(11)}
+    cases = [(P.dense_mask, ()), (P.ashape_mask, (64, 100)), (P.vs_mask, (V, D)),
+             (P.bs_mask, (64, lambda b: sel[b]))]
+    for fn, args in cases:
+        full = fn(rows, s1, *args)
+        sub = fn(rows, s1, *args, cols=cols)
+        assert sub.shape == (rows.size, cols.size)
+        assert np.array_equal(sub, full[:, cols]), fn.__name__
