@@ -15,7 +15,8 @@
  *    until the work queued on `stream` has finished.  Host pointers are read before the
  *    call returns.
  *  - The library allocates no device memory: calls that need scratch space take a
- *    caller-provided workspace whose size a *_workspace_size() query returns.
+ *    caller-provided workspace whose size a *_workspace_size() query returns (the one
+ *    exception, rs_route_layer_device_noalloc, uses a fixed static device array instead).
  *  - GPU calls are asynchronous on `stream` (a hipStream_t; NULL = the null stream).
  *    rs_route_layer is host-only, synchronous and pure.
  *  - Every call returns an rs_status; on failure nothing has been launched and
@@ -264,6 +265,20 @@ size_t rs_route_layer_device_workspace_size(int32_t nunits, int32_t ncand);
 rs_status rs_route_layer_device(const rs_route_in *in, const rs_route_cfg *cfg,
                                 const rs_route_dev_out *out, void *ws, size_t ws_bytes,
                                 rs_stream stream);
+
+/* ---- device routing without a workspace ---------------------------------------------------
+ * For callers that cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): rs_route_layer_device with the same arguments,
+ * validation and results (bit for bit), except that the router's scratch lives in a fixed
+ * library-owned device array of 96 KiB per GPU (one copy per device the library runs on,
+ * held until the process ends) instead of a caller workspace.  The call allocates nothing.
+ * Every call on one GPU shares that GPU's array, and the kernel writes every scratch element
+ * before reading it, so consecutive calls need no clearing; calls that overlap on one GPU
+ * (concurrent streams, several threads) race on the array and must be serialised by the
+ * caller.  Limits: nunits <= 2048 and nunits * (ncand - 1) <= 4096, the largest sizes the
+ * array holds; beyond them RS_ERR_UNSUPPORTED, with nothing launched. */
+rs_status rs_route_layer_device_noalloc(const rs_route_in *in, const rs_route_cfg *cfg,
+                                        const rs_route_dev_out *out, rs_stream stream);
 
 /* ---- routed attention from a device route (Sec. 3.4 grouping, inference step 6) ---------
  * Runs every unit u with candidate choice[u] (device int32 [nunits], e.g.

@@ -21,7 +21,7 @@ RS_PROBE_ROWS, RS_PROBE_BLOCKMEAN = 1, 2
 EXPORTS = ["rs_probe_workspace_size", "rs_probe", "rs_build_indices_workspace_size",
            "rs_build_indices", "rs_route_layer", "rs_attn_workspace_size",
            "rs_sparse_attn_prefill", "rs_dense_attn_prefill", "rs_error_predict",
-           "rs_route_layer_device_workspace_size", "rs_route_layer_device",
+           "rs_route_layer_device_workspace_size", "rs_route_layer_device", "rs_route_layer_device_noalloc",
            "rs_routed_attn_workspace_size", "rs_routed_attn_prefill", "rs_vt_bytes", "rs_transpose_v",
            "rs_last_error", "rs_version"]
 
@@ -130,12 +130,15 @@ def lib():
         L.rs_route_layer_device_workspace_size.argtypes = [I32, I32]
         L.rs_route_layer_device.argtypes = [C.POINTER(RsRouteIn), C.POINTER(RsRouteCfg), C.POINTER(RsRouteDevOut),
                                             P, C.c_size_t, P]
+        L.rs_route_layer_device_noalloc.argtypes = [C.POINTER(RsRouteIn), C.POINTER(RsRouteCfg),
+                                                    C.POINTER(RsRouteDevOut), P]
         L.rs_routed_attn_workspace_size.argtypes = [C.POINTER(RsQkv), C.POINTER(RsUnit), I32]
         L.rs_routed_attn_prefill.argtypes = [C.POINTER(RsQkv), C.POINTER(RsUnit), I32, C.POINTER(RsCandidate),
                                              I32, C.POINTER(RsIndexSet), P, P, I64, I64, P, P, C.c_size_t,
                                              C.POINTER(P), P]
         for name in ("rs_probe", "rs_build_indices", "rs_route_layer", "rs_sparse_attn_prefill",
                      "rs_dense_attn_prefill", "rs_error_predict", "rs_route_layer_device",
+                     "rs_route_layer_device_noalloc",
                      "rs_routed_attn_prefill", "rs_transpose_v"):
             getattr(L, name).restype = C.c_int
         _lib = L
@@ -419,6 +422,17 @@ def rs_route_layer_device(rb, cov, nsub, t_probe_us, T_layer_us, tau, alpha, bet
     cfg = RsRouteCfg(T_layer_us=T_layer_us, tau=tau, alpha=alpha, beta=beta, delta_q=delta_q)
     return _check(lib().rs_route_layer_device(C.byref(rin), C.byref(cfg), C.byref(rb.out), _ptr(rb.ws),
                                               rb.ws.numel(), _stream(stream)))
+
+
+def rs_route_layer_device_noalloc(rb, cov, nsub, t_probe_us, T_layer_us, tau, alpha, beta, delta_q, e=None,
+                                  stream=None):
+    """As rs_route_layer_device, with the library's fixed scratch instead of rb.ws."""
+    rin = RsRouteIn(nunits=rb.U, ncand=rb.C, grid=C.cast(rb.grid, P), cov=cov.data_ptr(), nsub=nsub.data_ptr(),
+                    e=e.data_ptr() if e is not None else None, s1=rb.s1.data_ptr(),
+                    t_table=rb.t_table.data_ptr(), bucket_edge=rb.bucket_edge.data_ptr(), nbucket=rb.nbucket,
+                    t_probe_us=t_probe_us)
+    cfg = RsRouteCfg(T_layer_us=T_layer_us, tau=tau, alpha=alpha, beta=beta, delta_q=delta_q)
+    return _check(lib().rs_route_layer_device_noalloc(C.byref(rin), C.byref(cfg), C.byref(rb.out), _stream(stream)))
 
 
 def rs_routed_attn_workspace_size(qkv, units, nunits):

@@ -111,6 +111,8 @@ size_t route_dev_ws_bytes(int32_t nunits, int32_t ncand);
 rs_status route_dev_launch(const rs_route_in *in, const rs_route_cfg *cfg, const rs_route_dev_out *out,
                            const int *fam, const int *brank, int dense_c, void *ws, size_t ws_bytes,
                            hipStream_t st);
+rs_status route_dev_launch_noalloc(const rs_route_in *in, const rs_route_cfg *cfg, const rs_route_dev_out *out,
+                                   const int *fam, const int *brank, int dense_c, hipStream_t st);
 rs_status error_predict_launch(const rs_probe_out *p, const rs_candidate *grid, int32_t ncand,
                                const rs_error_model *m, float *e, hipStream_t st);
 size_t routed_attn_ws_bytes(const rs_unit *units, int32_t nunits);
@@ -349,6 +351,15 @@ rs_status rs_route_layer_device(const rs_route_in *in, const rs_route_cfg *cfg, 
   rs_status st = check_route_dev(in, cfg, out, fam, brank, &dense_c);
   if (st != RS_OK) return st;
   return route_dev_launch(in, cfg, out, fam, brank, dense_c, ws, ws_bytes, (hipStream_t)stream);
+}
+
+rs_status rs_route_layer_device_noalloc(const rs_route_in *in, const rs_route_cfg *cfg,
+                                        const rs_route_dev_out *out, rs_stream stream) {
+  g_err.clear();
+  int fam[16], brank[16], dense_c = -1;
+  rs_status st = check_route_dev(in, cfg, out, fam, brank, &dense_c);
+  if (st != RS_OK) return st;
+  return route_dev_launch_noalloc(in, cfg, out, fam, brank, dense_c, (hipStream_t)stream);
 }
 
 rs_status rs_error_predict(const rs_probe_out *probe, const rs_candidate *grid, int32_t ncand,

@@ -24,6 +24,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -462,6 +463,54 @@ size_t route_dev_ws_bytes(int32_t nunits, int32_t ncand) {
   ar.take<int>((size_t)nunits * (ncand > 1 ? ncand - 1 : 1));
   ar.take<int>((size_t)nunits);
   return ar.off + 256;
+}
+
+// ---- allocation-free device routing ------------------------------------------------------
+// The router's scratch (per-(unit, candidate) latency, the units' greedy paths and the merged
+// order's ranks) in a fixed device array instead of a caller workspace.  Every element the
+// kernel reads it has written earlier in the same launch, so nothing needs clearing between
+// calls.  The largest workspace the limits allow (nunits <= 2048, nunits * (ncand - 1) <=
+// 4096, ncand <= 16) is 16 U (C - 1) + 12 U <= 90112 bytes plus alignment: 96 KiB holds it.
+constexpr size_t kRouteScratchBytes = 96 * 1024;
+static __device__ __align__(256) char scratch[kRouteScratchBytes];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void *g_scratch_ptr[kMaxDevices];  // device address of `scratch` on each GPU, once known
+
+// Device address of this GPU's copy of the scratch array (the host symbol is only a
+// stand-in): looked up once per device, with that device current.
+static rs_status route_scratch(void **ptr) {
+  int dev = 0;
+  RS_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(RS_ERR_UNSUPPORTED, "device index beyond the scratch table");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    RS_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(RS_ERR_HIP, "hipGetSymbolAddress returned no address for the routing scratch");
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return RS_OK;
+}
+
+rs_status route_dev_launch(const rs_route_in *in, const rs_route_cfg *cfg, const rs_route_dev_out *out,
+                           const int *fam, const int *brank, int dense_c, void *ws, size_t ws_bytes,
+                           hipStream_t st);
+
+rs_status route_dev_launch_noalloc(const rs_route_in *in, const rs_route_cfg *cfg, const rs_route_dev_out *out,
+                                   const int *fam, const int *brank, int dense_c, hipStream_t st) {
+  const int U = in->nunits, C = in->ncand;
+  if (U > kRouteMaxUnits || U * (C - 1) > kRouteMaxMoves)
+    return fail(RS_ERR_UNSUPPORTED, "device routing supports nunits <= 2048 and nunits * (ncand - 1) <= 4096");
+  if (route_dev_ws_bytes(U, C) > kRouteScratchBytes)
+    return fail(RS_ERR_UNSUPPORTED, "routing scratch needs " + std::to_string(route_dev_ws_bytes(U, C)) +
+                                        " bytes, more than the fixed " + std::to_string(kRouteScratchBytes));
+  void *ptr = nullptr;
+  rs_status s = route_scratch(&ptr);
+  if (s != RS_OK) return s;
+  return route_dev_launch(in, cfg, out, fam, brank, dense_c, ptr, kRouteScratchBytes, st);
 }
 
 rs_status route_dev_launch(const rs_route_in *in, const rs_route_cfg *cfg, const rs_route_dev_out *out,
