@@ -298,8 +298,9 @@ def main():
     torch.cuda.synchronize()
     log(f"generated {len(calib) + len(evl)} layers ({time.perf_counter() - t0:.1f}s)")
 
-    # hardware latency table, probe time and budget, measured on the first evaluation layer
-    q0, k0, v0 = evl[0]
+    # hardware latency table, probe time and budget, measured on a held-out layer (neither a
+    # calibration nor an evaluation layer)
+    q0, k0, v0 = gen(100)
     qkv0 = RL.qkv(q0, k0, v0)
     RL.probe_and_index(qkv0)
     RL.t_table, RL.edges = RL.profile_latency(qkv0, edges, reps=3), edges
@@ -313,7 +314,8 @@ def main():
            "calibration": {"layers": [64 + i for i in range(args.calib_layers)], "q": args.q, "delta_q": dq,
                            "residuals": int(resid.size), "residual_mean": float(resid.mean()),
                            "residual_max": float(resid.max()), "per_family": per_fam},
-           "eval_layers": list(range(args.eval_layers)), "T_layer_us": T, "t_probe_us": RL.t_probe_us,
+           "eval_layers": list(range(args.eval_layers)), "latency_table_layer": 100,
+           "T_layer_us": T, "t_probe_us": RL.t_probe_us,
            "dense_layer_us": t_dense}
     kn = RouteKnobs(T_layer_us=T, tau=0.95, alpha=1.0, beta=0.0, delta_q=dq)
     res["routed"] = evaluate(RL, ref, evl, kn, log, label=f"routed delta_q={dq:.4f}")
