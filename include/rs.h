@@ -42,6 +42,7 @@ extern "C" {
 #endif
 
 typedef void *rs_stream; /* hipStream_t */
+struct rs_unit_table;
 
 typedef enum {
   RS_OK = 0,
@@ -71,7 +72,25 @@ typedef struct rs_qkv {
   const void *vt;            /* optional (device): V in the transposed layout written by
                                 rs_transpose_v, or NULL.  When set, the dense, A-shape and
                                 block-sparse kernels read it in place of v. */
+  const struct rs_unit_table *tables; /* optional (host struct): the unit tables of the call's
+                                unit list (rs_unit_table_init), or NULL; read by rs_probe and
+                                rs_routed_attn_prefill in place of per-call uploads */
 } rs_qkv;
+
+/* Unit tables: everything derived from a layer's unit list alone (the list itself, each
+ * unit's sampled probe rows with their subsets, the probe's unit groups), built once on the
+ * host and uploaded once into caller-owned device memory by rs_unit_table_init.  Calls given
+ * a table (rs_qkv.tables, rs_probe_out.tables) read it instead of rebuilding these arrays and
+ * copying them to the device on every call, so a layer's calls issue no host-to-device copy.
+ * The library fills the struct; the caller keeps it and its device memory unchanged while
+ * calls use it.  A call whose unit list (or probe configuration) differs from the table's is
+ * rejected with RS_ERR_INVALID_ARG before anything is launched. */
+typedef struct rs_unit_table {
+  void *dev;                 /* device memory holding the tables (caller-owned) */
+  uint64_t key_units;        /* hash of n, hq, hkv and every unit's (head, s0, s1, slot) */
+  uint64_t key_cfg;          /* hash of the probe configuration's sampled-row counts */
+  int32_t nunits, rmax, ngroups, n, hq, hkv;
+} rs_unit_table;
 
 /* One unit: rows [s0, s1) of query head `head`; `cand` indexes the candidate grid.
  * `slot` is the unit's position in the unit list given to rs_probe / rs_build_indices,
@@ -125,6 +144,8 @@ typedef struct rs_probe_out {
   float *lbs;        /* [hq][nb*(nb+1)/2] pooled logits, row bq at bq*(bq+1)/2, or NULL */
   float *cov_rows;   /* [nunits][ncand][rmax] m_i(c): mass of row i kept by candidate c */
   float *cov;        /* [nunits][ncand][4] m_hat, m_R, m_U, m_B (subset means; 0 if empty) */
+  const struct rs_unit_table *tables; /* optional: unit tables of the probe's unit list (read
+                        by rs_build_indices in place of a per-call upload), or NULL */
 } rs_probe_out;
 
 /* Index sets built from probe scores (Sec. 3.1), device arrays allocated by the caller.
@@ -183,6 +204,14 @@ typedef struct rs_route_out {
   int32_t ngroups, n_fallback, over_budget, infeasible;
   double total_us, total_risk;
 } rs_route_out;
+
+/* ---- unit tables (set-up, once per unit list) -------------------------------------------
+ * rs_unit_table_size: bytes of device memory the tables of this unit list need (cfg may be
+ * NULL: no probe rows).  rs_unit_table_init: builds them on the host, copies them into `dev`
+ * on `stream` and synchronises the stream (a set-up call, not part of a layer); fills *out. */
+size_t rs_unit_table_size(const rs_qkv *qkv, const rs_unit *units, int32_t nunits, const rs_probe_cfg *cfg);
+rs_status rs_unit_table_init(const rs_qkv *qkv, const rs_unit *units, int32_t nunits, const rs_probe_cfg *cfg,
+                             void *dev, size_t bytes, rs_unit_table *out, rs_stream stream);
 
 /* ---- probe (Sec. 3.2, Eq. 3; coverage of Sec. 3.2-3.3) -------------------------------
  * Scores mode (idx == NULL): for each unit, samples rows as in rs_probe_cfg, computes

@@ -18,7 +18,8 @@ RS_BF16, RS_F32 = 0, 1
 RS_DENSE, RS_ASHAPE, RS_VSLASH, RS_BSPARSE = 0, 1, 2, 3
 RS_PROBE_ROWS, RS_PROBE_BLOCKMEAN = 1, 2
 
-EXPORTS = ["rs_probe_workspace_size", "rs_probe", "rs_build_indices_workspace_size",
+EXPORTS = ["rs_unit_table_size", "rs_unit_table_init",
+           "rs_probe_workspace_size", "rs_probe", "rs_build_indices_workspace_size",
            "rs_build_indices", "rs_route_layer", "rs_attn_workspace_size",
            "rs_sparse_attn_prefill", "rs_dense_attn_prefill", "rs_error_predict",
            "rs_route_layer_device_workspace_size", "rs_route_layer_device", "rs_route_layer_device_noalloc",
@@ -34,7 +35,7 @@ class RsQkv(C.Structure):
     _fields_ = [("q", P), ("k", P), ("v", P), ("dtype", I32), ("n", I32), ("hq", I32),
                 ("hkv", I32), ("d", I32), ("_pad0", I32), ("sq_h", I64), ("sq_t", I64),
                 ("sk_h", I64), ("sk_t", I64), ("sv_h", I64), ("sv_t", I64),
-                ("scale", C.c_float), ("_pad1", I32), ("vt", P)]
+                ("scale", C.c_float), ("_pad1", I32), ("vt", P), ("tables", P)]
 
 
 class RsUnit(C.Structure):
@@ -55,7 +56,12 @@ class RsProbeOut(C.Structure):
     _fields_ = [("nunits", I32), ("rmax", I32), ("n", I32), ("nb", I32), ("ncand", I32),
                 ("hq", I32), ("rows", P), ("subset", P), ("nsub", P), ("row_max", P),
                 ("row_sum", P), ("col", P), ("diag", P), ("entropy", P), ("local", P),
-                ("lbs", P), ("cov_rows", P), ("cov", P)]
+                ("lbs", P), ("cov_rows", P), ("cov", P), ("tables", P)]
+
+
+class RsUnitTable(C.Structure):
+    _fields_ = [("dev", P), ("key_units", C.c_uint64), ("key_cfg", C.c_uint64), ("nunits", I32), ("rmax", I32),
+                ("ngroups", I32), ("n", I32), ("hq", I32), ("hkv", I32)]
 
 
 class RsIndexSet(C.Structure):
@@ -106,10 +112,13 @@ def lib():
         L = C.CDLL(LIB_PATH)
         L.rs_last_error.restype = C.c_char_p
         L.rs_version.restype = C.c_char_p
-        for name in ("rs_probe_workspace_size", "rs_build_indices_workspace_size",
+        for name in ("rs_unit_table_size", "rs_probe_workspace_size", "rs_build_indices_workspace_size",
                      "rs_attn_workspace_size", "rs_route_layer_device_workspace_size",
                      "rs_routed_attn_workspace_size", "rs_vt_bytes"):
             getattr(L, name).restype = C.c_size_t
+        L.rs_unit_table_size.argtypes = [C.POINTER(RsQkv), C.POINTER(RsUnit), I32, C.POINTER(RsProbeCfg)]
+        L.rs_unit_table_init.argtypes = [C.POINTER(RsQkv), C.POINTER(RsUnit), I32, C.POINTER(RsProbeCfg), P,
+                                         C.c_size_t, C.POINTER(RsUnitTable), P]
         L.rs_vt_bytes.argtypes = [C.POINTER(RsQkv)]
         L.rs_transpose_v.argtypes = [C.POINTER(RsQkv), P, P]
         L.rs_probe_workspace_size.argtypes = [C.POINTER(RsQkv), C.POINTER(RsUnit), I32, C.POINTER(RsProbeCfg)]
@@ -136,7 +145,7 @@ def lib():
         L.rs_routed_attn_prefill.argtypes = [C.POINTER(RsQkv), C.POINTER(RsUnit), I32, C.POINTER(RsCandidate),
                                              I32, C.POINTER(RsIndexSet), P, P, I64, I64, P, P, C.c_size_t,
                                              C.POINTER(P), P]
-        for name in ("rs_probe", "rs_build_indices", "rs_route_layer", "rs_sparse_attn_prefill",
+        for name in ("rs_unit_table_init", "rs_probe", "rs_build_indices", "rs_route_layer", "rs_sparse_attn_prefill",
                      "rs_dense_attn_prefill", "rs_error_predict", "rs_route_layer_device",
                      "rs_route_layer_device_noalloc",
                      "rs_routed_attn_prefill", "rs_transpose_v"):
@@ -189,6 +198,24 @@ def rs_vt_bytes(qkv) -> int:
 def rs_transpose_v(qkv, vt, stream=None):
     """vt: uint8 device tensor of rs_vt_bytes(qkv) bytes (or more)."""
     return _check(lib().rs_transpose_v(C.byref(qkv), _ptr(vt), _stream(stream)))
+
+
+class UnitTable:
+    """Device unit tables of one unit list (rs_unit_table_init): set ``qkv.tables`` and the
+    probe output's ``tables`` to ``ptr`` so the layer's calls read them instead of uploading."""
+
+    def __init__(self, qkv, units, nunits, cfg=None, device="cuda", stream=None):
+        import torch
+        cp = C.byref(cfg) if cfg is not None else None
+        nbytes = lib().rs_unit_table_size(C.byref(qkv), units, nunits, cp)
+        self.dev = torch.empty(max(256, int(nbytes)), dtype=torch.uint8, device=device)
+        self.c = RsUnitTable()
+        _check(lib().rs_unit_table_init(C.byref(qkv), units, nunits, cp, _ptr(self.dev), self.dev.numel(),
+                                        C.byref(self.c), _stream(stream)))
+
+    @property
+    def ptr(self):
+        return C.cast(C.pointer(self.c), P).value
 
 
 def make_units(units) -> C.Array:

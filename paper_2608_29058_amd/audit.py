@@ -360,9 +360,10 @@ def main():
         ab["one_fixed_budget"] = evaluate(R1, ref, evl, kn, log, label="one budget per family")
         del R1
         Rr = RoutedLayer(N, HQ, HKV, D, SEG, GRID, r_uni=0, r_bnd=0)
-        Rr.probe_and_index(qkv0)
+        qkv_r = Rr.qkv(q0, k0, v0)
+        Rr.probe_and_index(qkv_r)
         Rr.t_table, Rr.edges = measured, edges
-        Rr.t_probe_us = Rr.profile_probe(qkv0, reps=3)
+        Rr.t_probe_us = Rr.profile_probe(qkv_r, reps=3)
         ab["recent_queries_only"] = evaluate(Rr, ref, evl, kn, log, label="recent queries only")
         res["ablations"] = ab
     res["wall_s"] = round(time.perf_counter() - t0, 1)

@@ -70,11 +70,52 @@ rs_status check_units(const rs_qkv *qkv, const rs_unit *units, int32_t nunits) {
   return RS_OK;
 }
 
+static uint64_t fnv(uint64_t h, uint64_t v) {
+  for (int b = 0; b < 8; ++b) {
+    h ^= (v >> (8 * b)) & 0xffu;
+    h *= 0x100000001b3ull;
+  }
+  return h;
+}
+
+uint64_t unit_list_key(const rs_qkv *qkv, const rs_unit *units, int32_t nunits) {
+  uint64_t h = 0xcbf29ce484222325ull;
+  h = fnv(h, (uint64_t)qkv->n);
+  h = fnv(h, ((uint64_t)qkv->hq << 32) | (uint32_t)qkv->hkv);
+  h = fnv(h, (uint64_t)nunits);
+  for (int i = 0; i < nunits; ++i) {
+    h = fnv(h, ((uint64_t)(uint32_t)units[i].head << 32) | (uint32_t)units[i].s0);
+    h = fnv(h, ((uint64_t)(uint32_t)units[i].s1 << 32) | (uint32_t)units[i].slot);
+  }
+  return h;
+}
+
+uint64_t probe_cfg_key(const rs_probe_cfg *cfg) {
+  uint64_t h = 0x84222325cbf29ce4ull;
+  if (!cfg) return h;
+  h = fnv(h, ((uint64_t)(uint32_t)cfg->r_rec << 32) | (uint32_t)cfg->r_uni);
+  return fnv(h, (uint64_t)(uint32_t)cfg->r_bnd | (1ull << 40));
+}
+
+rs_status check_unit_table(const rs_unit_table *t, const rs_qkv *qkv, const rs_unit *units, int32_t nunits,
+                           const rs_probe_cfg *cfg) {
+  if (!t->dev) return fail(RS_ERR_INVALID_ARG, "unit table without device memory");
+  if (t->nunits != nunits || t->n != qkv->n || t->hq != qkv->hq || t->hkv != qkv->hkv ||
+      t->key_units != unit_list_key(qkv, units, nunits))
+    return fail(RS_ERR_INVALID_ARG, "unit table built for another unit list");
+  if (cfg && (t->key_cfg != probe_cfg_key(cfg) || t->rmax != cfg->r_rec + cfg->r_uni + cfg->r_bnd))
+    return fail(RS_ERR_INVALID_ARG, "unit table built for another probe configuration");
+  return RS_OK;
+}
+
 // defined in the .hip translation units
 size_t attn_ws_bytes(const rs_unit *units, int32_t nunits);
 rs_status attn_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int32_t nunits, int fam,
                       const rs_candidate *cand, int cand_local, const rs_index_set *idx, void *o, int64_t so_h,
                       int64_t so_t, float *lse, void *ws, size_t ws_bytes, hipStream_t st);
+size_t unit_table_bytes(int32_t nunits, const rs_probe_cfg *cfg);
+rs_status unit_table_init(const rs_qkv *qkv, const rs_unit *units, int32_t nunits, const rs_probe_cfg *cfg,
+                          void *dev, size_t bytes, rs_unit_table *out, hipStream_t st);
 size_t probe_ws_bytes(const rs_qkv *qkv, int32_t nunits, const rs_probe_cfg *cfg);
 rs_status probe_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int32_t nunits,
                        const rs_probe_cfg *cfg, const rs_candidate *grid, int32_t ncand, const rs_index_set *idx,
@@ -201,6 +242,28 @@ rs_status rs_sparse_attn_prefill(const rs_qkv *qkv, const rs_unit *units, int32_
                      (hipStream_t)stream);
 }
 
+size_t rs_unit_table_size(const rs_qkv *qkv, const rs_unit *units, int32_t nunits, const rs_probe_cfg *cfg) {
+  (void)qkv;
+  (void)units;
+  if (nunits < 0) return 0;
+  return unit_table_bytes(nunits, cfg);
+}
+
+rs_status rs_unit_table_init(const rs_qkv *qkv, const rs_unit *units, int32_t nunits, const rs_probe_cfg *cfg,
+                             void *dev, size_t bytes, rs_unit_table *out, rs_stream stream) {
+  g_err.clear();
+  float scale;
+  rs_status st;
+  if ((st = check_qkv(qkv, &scale)) != RS_OK) return st;
+  if ((st = check_units(qkv, units, nunits)) != RS_OK) return st;
+  if (!out) return fail(RS_ERR_INVALID_ARG, "out is NULL");
+  if (cfg && (cfg->r_rec < 0 || cfg->r_uni < 0 || cfg->r_bnd < 0 || cfg->r_rec + cfg->r_uni + cfg->r_bnd > 256))
+    return fail(RS_ERR_INVALID_ARG, "sampled rows must be in [0, 256]");
+  if (!dev || bytes < unit_table_bytes(nunits, cfg))
+    return fail(RS_ERR_WORKSPACE, "unit table memory too small: need " + std::to_string(unit_table_bytes(nunits, cfg)));
+  return unit_table_init(qkv, units, nunits, cfg, dev, bytes, out, (hipStream_t)stream);
+}
+
 size_t rs_probe_workspace_size(const rs_qkv *qkv, const rs_unit *units, int32_t nunits, const rs_probe_cfg *cfg) {
   (void)units;
   if (!qkv || !cfg || nunits < 0) return 0;
@@ -255,6 +318,7 @@ rs_status rs_probe(const rs_qkv *qkv, const rs_unit *units, int32_t nunits, cons
         return fail(RS_ERR_INVALID_ARG, "index set does not match the grid (block-sparse candidates, nb or nbw)");
     }
   }
+  if (qkv->tables && (st = check_unit_table(qkv->tables, qkv, units, nunits, cfg)) != RS_OK) return st;
   if (nunits == 0) return RS_OK;
   return probe_launch(qkv, scale, units, nunits, cfg, grid, ncand, idx, ws, ws_bytes, out, (hipStream_t)stream);
 }
@@ -310,6 +374,13 @@ rs_status rs_build_indices(const rs_probe_out *scores, const rs_unit *units, int
     if (!scores->lbs || out->hq != scores->hq) return fail(RS_ERR_INVALID_ARG, "block-mean scores missing");
     if (!out->bs_rank || !out->bs_sorted || !out->bs_count || !out->bs_bits)
       return fail(RS_ERR_INVALID_ARG, "block-sparse arrays missing");
+  }
+  if (scores->tables) {
+    rs_qkv shape{};  // the key covers n, hq and hkv: those the table recorded
+    shape.n = n;
+    shape.hq = scores->tables->hq;
+    shape.hkv = scores->tables->hkv;
+    if ((st = check_unit_table(scores->tables, &shape, units, nunits, nullptr)) != RS_OK) return st;
   }
   if (nunits == 0 && nbs == 0) return RS_OK;
   return build_indices_launch(scores, units, nunits, grid, ncand, out, (hipStream_t)stream, ws, ws_bytes);
@@ -428,6 +499,7 @@ rs_status rs_routed_attn_prefill(const rs_qkv *qkv, const rs_unit *units, int32_
     if (nbs > idx->ncand_bs || idx->nb != (qkv->n + 63) / 64 || idx->hq != qkv->hq)
       return fail(RS_ERR_INVALID_ARG, "index set does not match the grid");
   }
+  if (qkv->tables && (st = check_unit_table(qkv->tables, qkv, units, nunits, nullptr)) != RS_OK) return st;
   return routed_attn_launch(qkv, scale, units, nunits, grid, ncand, idx, choice, o, so_h, so_t, lse, ws, ws_bytes,
                             events, (hipStream_t)stream);
 }

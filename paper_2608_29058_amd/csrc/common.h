@@ -33,6 +33,16 @@ rs_status hip_check(hipError_t e, const char *what);
     if (_e != hipSuccess) return ::rs::hip_check(_e, #call);           \
   } while (0)
 
+// Keys of a unit table (FNV-1a over the fields that define it).
+uint64_t unit_list_key(const rs_qkv *qkv, const rs_unit *units, int32_t nunits);
+uint64_t probe_cfg_key(const rs_probe_cfg *cfg);
+// Device arrays of a unit table (probe.hip lays the table out).
+const rs_unit *unit_tab_units(const rs_unit_table *t);
+const int *unit_tab_s1(const rs_unit_table *t);
+// Checks that `t` was built for this unit list (and, with cfg, this probe configuration).
+rs_status check_unit_table(const rs_unit_table *t, const rs_qkv *qkv, const rs_unit *units, int32_t nunits,
+                           const rs_probe_cfg *cfg);
+
 // Validate rs_qkv; fills scale.  Returns RS_OK or an error (message set).
 rs_status check_qkv(const rs_qkv *qkv, float *scale);
 rs_status check_units(const rs_qkv *qkv, const rs_unit *units, int32_t nunits);

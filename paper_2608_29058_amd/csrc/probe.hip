@@ -68,6 +68,9 @@ struct ProbeArgs {
   const uint32_t *bs_bits;
   int nb, nbw, ncand_bs;
   float *cov_part;
+  // scores call with a unit table: the table's sampled rows are copied to the probe output
+  int *rows_out, *subset_out, *nsub_out;
+  const int *nsub_tab;
 };
 
 // Orders this wave's LDS writes before its following LDS reads by other lanes.  The LDS
@@ -124,6 +127,26 @@ __device__ __forceinline__ int swz(int r) {
 
 enum { M_STATS = 0, M_SCORES = 1, M_COVER = 2 };
 
+// Three bitmap words around a bit position, loaded from clamped indices with no condition on
+// the loaded values (a select right after a load makes the compiler wait for it, and with it
+// for every copy issued before); win_fix zeroes the words outside the bitmap where they are used.
+__device__ __forceinline__ Win3 load_win_raw(const uint32_t *bits, int nwords, int pos) {
+  const int w = pos >> 5;
+  const int last = nwords - 1;
+  Win3 r;
+  r.x0 = bits[min(max(w, 0), last)];
+  r.x1 = bits[min(max(w + 1, 0), last)];
+  r.x2 = bits[min(max(w + 2, 0), last)];
+  return r;
+}
+__device__ __forceinline__ Win3 win_fix(Win3 r, int nwords, int pos) {
+  const int w = pos >> 5;
+  r.x0 = (w >= 0 && w < nwords) ? r.x0 : 0u;
+  r.x1 = (w + 1 >= 0 && w + 1 < nwords) ? r.x1 : 0u;
+  r.x2 = (w + 2 >= 0 && w + 2 < nwords) ? r.x2 : 0u;
+  return r;
+}
+
 // s_waitcnt immediate (gfx9 encoding) waiting until at most n vector-memory operations are
 // outstanding, with no wait on the other counters
 constexpr int vm_wait_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
@@ -161,7 +184,11 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
   // work.  The scores pass has one buffer (a barrier after the second block's products
   // releases it), which keeps its LDS within two workgroups per compute unit.
   constexpr int NKB = MODE == M_SCORES ? 1 : 2;
-  __shared__ __align__(16) bf16 sKb[NKB][TE];
+  // two K buffers as arrays of their own (tile parity known at compile time): the compiler then
+  // sees that the copy into one never overlaps the fragment reads of the other, and the next
+  // tile's copy can be issued at the start of the current tile
+  __shared__ __align__(16) bf16 sK0[TE];
+  __shared__ __align__(16) bf16 sK1[NKB == 2 ? TE : 8];
   __shared__ int sRows[2][32];
 
   const int rg = blockIdx.x;
@@ -233,7 +260,8 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
   }
 
   const int kswz = swz<D>(l32);
-  const InT *Qp = u >= 0 ? (const InT *)a.q + (long long)a.units[u].head * a.sq_h : nullptr;
+  const int uhead = u >= 0 ? a.units[u].head : 0;  // loaded once: no dependent load inside the tile loop
+  const InT *Qp = u >= 0 ? (const InT *)a.q + (long long)uhead * a.sq_h : nullptr;
   const float c = a.c;
 
   for (int pr = p_lo; pr < p_hi; ++pr) {
@@ -290,35 +318,41 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
 
     // coverage pass: diagonal-bitmap windows (vertical-slash) and block-selection words
     // (block-sparse) of each row, fetched together with the K copy of the tile they serve
+    // Only raw words are loaded here (combined where they are used, in the next tile): a use
+    // right after the loads would make the compiler wait for them, and with them for the
+    // tile copy issued just before.
     struct Pref {
       Win3 wd[2][kPrefVs];
-      uint64_t mv[kPrefVs];  // column bits of the tile's keys
+      uint32_t mv[kPrefVs][2];  // column-bitmap words of the tile's 64 keys (k0 is a multiple of 64)
       uint32_t bw[2][kPrefBs];
     };
     auto fetch = [&](int k0, Pref &f) __attribute__((always_inline)) {
       if constexpr (MODE == M_COVER) {
         const int kt = k0 >> 6;
+        const int w0 = k0 >> 5;
 #pragma unroll
         for (int k = 0; k < kPrefVs; ++k) {
-          f.mv[k] = 0ull;
-          if (k < a.nvs_pref && u >= 0)
-            f.mv[k] = bits64_at(a.vs_vbits + ((long long)u * a.ncand_vs + a.vs_pref_cl[k]) * a.nwords, a.nwords, k0);
+          f.mv[k][0] = f.mv[k][1] = 0u;
+          if (k < a.nvs_pref && u >= 0) {
+            const uint32_t *vb = a.vs_vbits + ((long long)u * a.ncand_vs + a.vs_pref_cl[k]) * a.nwords;
+            f.mv[k][0] = vb[w0];                        // k0 < n: in the bitmap
+            f.mv[k][1] = vb[min(w0 + 1, a.nwords - 1)];  // zeroed at use when past it
+          }
         }
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
-          const bool ok = u >= 0 && row[s] >= 0;
 #pragma unroll
           for (int k = 0; k < kPrefVs; ++k) {
             f.wd[s][k] = Win3{0u, 0u, 0u};
-            if (k < a.nvs_pref && ok)
-              f.wd[s][k] = load_win(a.vs_dbits + ((long long)u * a.ncand_vs + a.vs_pref_cl[k]) * a.nwords, a.nwords,
-                                    row[s] - k0 - 63);
+            if (k < a.nvs_pref && u >= 0)
+              f.wd[s][k] = load_win_raw(a.vs_dbits + ((long long)u * a.ncand_vs + a.vs_pref_cl[k]) * a.nwords,
+                                        a.nwords, max(row[s], 0) - k0 - 63);
           }
 #pragma unroll
           for (int k = 0; k < kPrefBs; ++k) {
             f.bw[s][k] = 0u;
-            if (k < a.nbs_pref && ok)
-              f.bw[s][k] = a.bs_bits[(((long long)a.units[u].head * a.ncand_bs + a.bs_pref_cl[k]) * a.nb + (row[s] >> 6)) *
+            if (k < a.nbs_pref && u >= 0)  // rows of absent lanes (row -1) read row 0's words, unused
+              f.bw[s][k] = a.bs_bits[(((long long)uhead * a.ncand_bs + a.bs_pref_cl[k]) * a.nb + (max(row[s], 0) >> 6)) *
                                          a.nbw + (kt >> 5)];
           }
         }
@@ -506,8 +540,11 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
 #pragma unroll
           for (int k = 0; k < kPrefVs; ++k) {
             if (k >= a.nvs_pref) break;
-            const uint64_t md = __builtin_bitreverse64(win_bits(f.wd[s][k], i - k0 - 63));
-            const uint64_t m = (md | f.mv[k]) >> (4 * hh);
+            const int dpos = max(i, 0) - k0 - 63;
+            const uint64_t md = __builtin_bitreverse64(win_bits(win_fix(f.wd[s][k], a.nwords, dpos), dpos));
+            const uint32_t mv1 = (k0 >> 5) + 1 < a.nwords ? f.mv[k][1] : 0u;
+            const uint64_t mv = (uint64_t)f.mv[k][0] | ((uint64_t)mv1 << 32);
+            const uint64_t m = (md | mv) >> (4 * hh);
             if (__ballot(m != 0ull) != 0ull) covv[s][k] += masked(m);  // wave-uniform skip
           }
 #pragma unroll
@@ -530,7 +567,7 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
               const uint64_t mv = bits64_at(a.vs_vbits + vr, a.nwords, k0);
               cov[s][q] += masked((md | mv) >> (4 * hh));
             } else if (cd.fam == RS_BSPARSE) {
-              const long long br = (((long long)a.units[u].head * a.ncand_bs + cd.cl) * a.nb + (max(i, 0) >> 6)) * a.nbw;
+              const long long br = (((long long)uhead * a.ncand_bs + cd.cl) * a.nb + (max(i, 0) >> 6)) * a.nbw;
               if ((a.bs_bits[br + (kt >> 5)] >> (kt & 31)) & 1u) cov[s][q] += tsum;
             }
           }
@@ -543,29 +580,51 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
     // no wait for them lands inside the tile loop (where it would drain the tile copies).
     __builtin_amdgcn_s_waitcnt(vm_wait_imm(0));
     Pref fcur, fnext;
-    issue_tile(sKb[0], c0);
+    issue_tile(sK0, c0);
     fetch(c0, fcur);
-    for (int t = 0; t < nt; ++t) {
-      __builtin_amdgcn_s_waitcnt(vm_wait_imm(0));  // tile t (and its bitmap words) landed
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-      __builtin_amdgcn_s_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-      const int k0 = c0 + 64 * t;
-      f32x16 S[2];
-      qk_block(sKb[t % NKB], k0, 0, S);
-      block_tile(S, k0, 0, fcur);
-      qk_block(sKb[t % NKB], k0, 1, S);
-      if constexpr (NKB == 1) {  // every wave has read the tile before it is overwritten
+    if constexpr (NKB == 1) {
+      for (int t = 0; t < nt; ++t) {
+        __builtin_amdgcn_s_waitcnt(vm_wait_imm(0));  // tile t landed
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
         __builtin_amdgcn_s_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+        const int k0 = c0 + 64 * t;
+        f32x16 S[2];
+        qk_block(sK0, k0, 0, S);
+        block_tile(S, k0, 0, fcur);
+        qk_block(sK0, k0, 1, S);
+        // every wave has read the tile before it is overwritten
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+        if (t + 1 < nt) issue_tile(sK0, k0 + 64);
+        block_tile(S, k0, 1, fcur);
       }
-      if (t + 1 < nt) {
-        issue_tile(sKb[(t + 1) % NKB], k0 + 64);
-        fetch(k0 + 64, fnext);
+    } else {
+      // tile t in `cur`; after the barrier every wave is done with tile t - 1 (in `nxt`), so
+      // tile t + 1 (and its bitmap words) is fetched into `nxt` before tile t's products
+      auto tile = [&](int t, const bf16 *cur, bf16 *nxt) __attribute__((always_inline)) {
+        __builtin_amdgcn_s_waitcnt(vm_wait_imm(0));  // tile t (and its bitmap words) landed
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+        const int k0 = c0 + 64 * t;
+        if (t + 1 < nt) {
+          issue_tile(nxt, k0 + 64);
+          fetch(k0 + 64, fnext);
+        }
+        f32x16 S[2];
+        qk_block(cur, k0, 0, S);
+        block_tile(S, k0, 0, fcur);
+        qk_block(cur, k0, 1, S);
+        block_tile(S, k0, 1, fcur);
+        fcur = fnext;
+      };
+      for (int t = 0; t < nt; t += 2) {
+        tile(t, sK0, sK1);
+        if (t + 1 >= nt) break;
+        tile(t + 1, sK1, sK0);
       }
-      block_tile(S, k0, 1, fcur);
-      fcur = fnext;
     }
 
     // ---- per-row partials of this range ------------------------------------------------------
@@ -679,6 +738,11 @@ __global__ void probe_finish_kernel(const ProbeArgs a, float *diag, float *entro
     }
     diag[(long long)u * a.n + x] = v;
     if (x >= U.s1) a.col[(long long)u * a.n + x] = 0.f;
+  }
+  if (a.rows_out && x < a.rmax) {
+    a.rows_out[(long long)u * a.rmax + x] = a.rows[(long long)u * a.rmax + x];
+    a.subset_out[(long long)u * a.rmax + x] = a.subset[(long long)u * a.rmax + x];
+    if (x < 3) a.nsub_out[u * 3 + x] = a.nsub_tab[u * 3 + x];
   }
 }
 
@@ -899,6 +963,136 @@ static void sample_rows(int s0, int s1, const rs_probe_cfg &cfg, std::vector<int
 
 static int rmax_of(const rs_probe_cfg *cfg) { return cfg->r_rec + cfg->r_uni + cfg->r_bnd; }
 
+// Host form of the per-unit probe tables: sampled rows, subsets and subset sizes, the units'
+// ProbeUnit records and the unit groups (the query heads of one key/value head over one
+// segment, up to 4).
+struct ProbeHost {
+  std::vector<ProbeUnit> units;
+  std::vector<int4> groups;
+  std::vector<int> rows, subset, nsub;
+};
+
+static void build_probe_host(const rs_unit *units, int32_t nunits, const rs_probe_cfg *cfg, int group,
+                             ProbeHost &h) {
+  const int rmax = rmax_of(cfg);
+  h.units.assign(nunits, ProbeUnit{});
+  h.rows.assign((size_t)nunits * rmax, -1);
+  h.subset.assign((size_t)nunits * rmax, -1);
+  h.nsub.assign((size_t)nunits * 3, 0);
+  for (int u = 0; u < nunits; ++u) {
+    std::vector<int> rows, lab;
+    int r0;
+    sample_rows(units[u].s0, units[u].s1, *cfg, rows, lab, r0);
+    h.units[u] = ProbeUnit{units[u].head, units[u].s0, units[u].s1, (int)rows.size(), r0, units[u].s1 - r0, 0, 0};
+    for (size_t x = 0; x < rows.size(); ++x) {
+      h.rows[(size_t)u * rmax + x] = rows[x];
+      h.subset[(size_t)u * rmax + x] = lab[x];
+      h.nsub[(size_t)u * 3 + lab[x]]++;
+    }
+  }
+  std::vector<std::vector<int>> open_lists;
+  std::vector<long long> keys;
+  for (int u = 0; u < nunits; ++u) {
+    const long long key = ((long long)(units[u].head / group) * (kMaxN + 1) + units[u].s0) * (kMaxN + 1) + units[u].s1;
+    int slot = -1;
+    for (size_t k = 0; k < keys.size(); ++k)
+      if (keys[k] == key && open_lists[k].size() < 4) {
+        slot = (int)k;
+        break;
+      }
+    if (slot < 0) {
+      keys.push_back(key);
+      open_lists.push_back({});
+      slot = (int)keys.size() - 1;
+    }
+    open_lists[slot].push_back(u);
+  }
+  h.groups.clear();
+  for (auto &l : open_lists) {
+    int4 g{-1, -1, -1, -1};
+    g.x = l[0];
+    if (l.size() > 1) g.y = l[1];
+    if (l.size() > 2) g.z = l[2];
+    if (l.size() > 3) g.w = l[3];
+    h.groups.push_back(g);
+  }
+}
+
+// Device layout of a unit table: [rs_unit x U][s1 x U][ProbeUnit x U][int4 x U][rows][subset][nsub],
+// each array 256-byte aligned; the probe arrays only with a probe configuration.
+struct UnitTab {
+  rs_unit *units;
+  int *s1;
+  ProbeUnit *punits;
+  int4 *groups;
+  int *rows, *subset, *nsub;
+  size_t bytes;
+};
+
+static UnitTab unit_tab_layout(void *dev, int32_t nunits, int rmax, bool probe) {
+  Arena ar(dev, ~size_t(0));
+  UnitTab t{};
+  t.units = ar.take<rs_unit>(nunits);
+  t.s1 = ar.take<int>(nunits);
+  if (probe) {
+    t.punits = ar.take<ProbeUnit>(nunits);
+    t.groups = ar.take<int4>(nunits);
+    t.rows = ar.take<int>((size_t)nunits * rmax);
+    t.subset = ar.take<int>((size_t)nunits * rmax);
+    t.nsub = ar.take<int>((size_t)nunits * 3);
+  }
+  t.bytes = ar.off + 256;
+  return t;
+}
+
+static UnitTab unit_tab_of(const rs_unit_table *t) {
+  return unit_tab_layout(t->dev, t->nunits, t->rmax, t->key_cfg != probe_cfg_key(nullptr));
+}
+
+const rs_unit *unit_tab_units(const rs_unit_table *t) { return unit_tab_of(t).units; }
+const int *unit_tab_s1(const rs_unit_table *t) { return unit_tab_of(t).s1; }
+
+size_t unit_table_bytes(int32_t nunits, const rs_probe_cfg *cfg) {
+  return unit_tab_layout(nullptr, nunits, cfg ? rmax_of(cfg) : 0, cfg != nullptr).bytes;
+}
+
+rs_status unit_table_init(const rs_qkv *qkv, const rs_unit *units, int32_t nunits, const rs_probe_cfg *cfg,
+                          void *dev, size_t bytes, rs_unit_table *out, hipStream_t st) {
+  const int rmax = cfg ? rmax_of(cfg) : 0;
+  const UnitTab t = unit_tab_layout(dev, nunits, rmax, cfg != nullptr);
+  if (bytes < t.bytes) return fail(RS_ERR_WORKSPACE, "unit table memory too small");
+  // the whole table is staged in one host image and copied once
+  std::vector<char> img(t.bytes, 0);
+  auto at = [&](const void *p) { return img.data() + ((const char *)p - (const char *)dev); };
+  std::vector<int> s1(nunits);
+  for (int u = 0; u < nunits; ++u) s1[u] = units[u].s1;
+  memcpy(at(t.units), units, (size_t)nunits * sizeof(rs_unit));
+  memcpy(at(t.s1), s1.data(), s1.size() * sizeof(int));
+  int ngroups = 0;
+  if (cfg) {
+    ProbeHost h;
+    build_probe_host(units, nunits, cfg, qkv->hq / qkv->hkv, h);
+    ngroups = (int)h.groups.size();
+    memcpy(at(t.punits), h.units.data(), h.units.size() * sizeof(ProbeUnit));
+    memcpy(at(t.groups), h.groups.data(), h.groups.size() * sizeof(int4));
+    memcpy(at(t.rows), h.rows.data(), h.rows.size() * sizeof(int));
+    memcpy(at(t.subset), h.subset.data(), h.subset.size() * sizeof(int));
+    memcpy(at(t.nsub), h.nsub.data(), h.nsub.size() * sizeof(int));
+  }
+  RS_HIP(hipMemcpyAsync(dev, img.data(), img.size(), hipMemcpyHostToDevice, st));
+  RS_HIP(hipStreamSynchronize(st));  // set-up call: the host image is released on return
+  out->dev = dev;
+  out->key_units = unit_list_key(qkv, units, nunits);
+  out->key_cfg = probe_cfg_key(cfg);
+  out->nunits = nunits;
+  out->rmax = rmax;
+  out->ngroups = cfg ? ngroups : 0;
+  out->n = qkv->n;
+  out->hq = qkv->hq;
+  out->hkv = qkv->hkv;
+  return RS_OK;
+}
+
 size_t probe_ws_bytes(const rs_qkv *qkv, int32_t nunits, const rs_probe_cfg *cfg) {
   const int rmax = rmax_of(cfg);
   const long long nchunks = (qkv->n + kRange - 1) / kRange;
@@ -968,58 +1162,34 @@ rs_status probe_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int
     qbar = ar.take<float>((size_t)qkv->hq * nb * qkv->d);
     kbar = ar.take<float>((size_t)qkv->hkv * nb * qkv->d);
   }
-  // sampled rows are computed here and uploaded (scores mode), or re-derived (coverage)
-  std::vector<ProbeUnit> hu(nunits);
-  std::vector<int> hrows((size_t)nunits * rmax, -1), hsub((size_t)nunits * rmax, -1), hn((size_t)nunits * 3, 0);
-  for (int u = 0; u < nunits; ++u) {
-    std::vector<int> rows, lab;
-    int r0;
-    sample_rows(units[u].s0, units[u].s1, *cfg, rows, lab, r0);
-    hu[u] = ProbeUnit{units[u].head, units[u].s0, units[u].s1, (int)rows.size(), r0, units[u].s1 - r0, 0, 0};
-    for (size_t x = 0; x < rows.size(); ++x) {
-      hrows[(size_t)u * rmax + x] = rows[x];
-      hsub[(size_t)u * rmax + x] = lab[x];
-      hn[(size_t)u * 3 + lab[x]]++;
-    }
-  }
-  RS_HIP(hipMemcpyAsync(d_units, hu.data(), hu.size() * sizeof(ProbeUnit), hipMemcpyHostToDevice, st));
-  // unit groups: the query heads of one key/value head over the same segment, up to 4
-  std::vector<int4> hg;
-  {
-    const int G = qkv->hq / qkv->hkv;
-    std::vector<std::vector<int>> open_lists;
-    std::vector<long long> keys;
-    for (int u = 0; u < nunits; ++u) {
-      const long long key = ((long long)(units[u].head / G) * (kMaxN + 1) + units[u].s0) * (kMaxN + 1) + units[u].s1;
-      int slot = -1;
-      for (size_t k = 0; k < keys.size(); ++k)
-        if (keys[k] == key && open_lists[k].size() < 4) {
-          slot = (int)k;
-          break;
-        }
-      if (slot < 0) {
-        keys.push_back(key);
-        open_lists.push_back({});
-        slot = (int)keys.size() - 1;
-      }
-      open_lists[slot].push_back(u);
-    }
-    for (auto &l : open_lists) {
-      int4 g{-1, -1, -1, -1};
-      g.x = l[0];
-      if (l.size() > 1) g.y = l[1];
-      if (l.size() > 2) g.z = l[2];
-      if (l.size() > 3) g.w = l[3];
-      hg.push_back(g);
-    }
-  }
-  const int ngroups = (int)hg.size();
-  RS_HIP(hipMemcpyAsync(d_groups, hg.data(), hg.size() * sizeof(int4), hipMemcpyHostToDevice, st));
+  // per-unit tables: read from the caller's unit table, or built here and uploaded into the
+  // workspace (sampled rows to the probe output in scores mode)
   const bool cover = idx != nullptr;
-  if (!cover && (cfg->flags & RS_PROBE_ROWS)) {
-    RS_HIP(hipMemcpyAsync(out->rows, hrows.data(), hrows.size() * 4, hipMemcpyHostToDevice, st));
-    RS_HIP(hipMemcpyAsync(out->subset, hsub.data(), hsub.size() * 4, hipMemcpyHostToDevice, st));
-    RS_HIP(hipMemcpyAsync(out->nsub, hn.data(), hn.size() * 4, hipMemcpyHostToDevice, st));
+  const rs_unit_table *tab = qkv->tables;
+  const ProbeUnit *pu_dev = d_units;
+  const int4 *grp_dev = d_groups;
+  const int *rows_dev = out->rows, *subset_dev = out->subset, *nsub_tab = nullptr;
+  int ngroups = 0;
+  if (tab) {
+    const UnitTab t = unit_tab_of(tab);
+    pu_dev = t.punits;
+    grp_dev = t.groups;
+    rows_dev = t.rows;
+    subset_dev = t.subset;
+    nsub_tab = t.nsub;
+    ngroups = tab->ngroups;
+  } else {
+    ProbeHost h;
+    build_probe_host(units, nunits, cfg, qkv->hq / qkv->hkv, h);
+    ngroups = (int)h.groups.size();
+    RS_HIP(hipMemcpyAsync(d_units, h.units.data(), h.units.size() * sizeof(ProbeUnit), hipMemcpyHostToDevice, st));
+    RS_HIP(hipMemcpyAsync(d_groups, h.groups.data(), h.groups.size() * sizeof(int4), hipMemcpyHostToDevice, st));
+    if (!cover && (cfg->flags & RS_PROBE_ROWS)) {
+      RS_HIP(hipMemcpyAsync(out->rows, h.rows.data(), h.rows.size() * 4, hipMemcpyHostToDevice, st));
+      RS_HIP(hipMemcpyAsync(out->subset, h.subset.data(), h.subset.size() * 4, hipMemcpyHostToDevice, st));
+      RS_HIP(hipMemcpyAsync(out->nsub, h.nsub.data(), h.nsub.size() * 4, hipMemcpyHostToDevice, st));
+    }
+    // the pageable host vectors are copied before hipMemcpyAsync returns
   }
   ProbeArgs pa{};
   pa.q = qkv->q; pa.k = qkv->k;
@@ -1027,7 +1197,13 @@ rs_status probe_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int
   pa.n = qkv->n; pa.group = qkv->hq / qkv->hkv; pa.rmax = rmax; pa.nchunks = nchunks;
   pa.c = scale * kLog2e; pa.scale = scale; pa.local_w = cfg->local_w;
   pa.stats_rows = (cfg->r_rec + 63) / 64 * 64;
-  pa.units = d_units; pa.groups = d_groups; pa.rows = out->rows; pa.subset = out->subset;
+  pa.units = pu_dev; pa.groups = grp_dev; pa.rows = rows_dev; pa.subset = subset_dev;
+  if (tab && !cover && (cfg->flags & RS_PROBE_ROWS)) {
+    pa.rows_out = out->rows;
+    pa.subset_out = out->subset;
+    pa.nsub_out = out->nsub;
+    pa.nsub_tab = nsub_tab;
+  }
   pa.row_max = out->row_max; pa.row_sum = out->row_sum;
   pa.col = out->col; pa.diag_part = diag_part; pa.ent_part = ent_part; pa.loc_part = loc_part;
   pa.max_part = max_part; pa.sum_part = sum_part;

@@ -608,7 +608,12 @@ rs_status routed_attn_launch(const rs_qkv *qkv, float scale, const rs_unit *unit
   p.qsize = d_q;
   p.qoff = d_q + 32;
   p.qcount = d_q + 64;
-  RS_HIP(hipMemcpyAsync(d_units, units, (size_t)nunits * sizeof(rs_unit), hipMemcpyHostToDevice, st));
+  // the unit list: from the caller's unit table, else copied into the workspace (from the
+  // caller's array, which the copy reads before hipMemcpyAsync returns)
+  if (qkv->tables)
+    p.units = unit_tab_units(qkv->tables);
+  else
+    RS_HIP(hipMemcpyAsync(d_units, units, (size_t)nunits * sizeof(rs_unit), hipMemcpyHostToDevice, st));
   hipLaunchKernelGGL(plan_kernel, dim3(4), dim3(1024), 0, st, p);
   RS_HIP(hipGetLastError());
   // persistent grids: two workgroups per compute unit (the kernel's occupancy), a multiple of 8

@@ -370,13 +370,20 @@ rs_status build_indices_launch(const rs_probe_out *sc, const rs_unit *units, int
     }
   }
   if (nvs > 0) {
-    // unit key lengths go to the workspace
-    Arena ar(ws, ws_bytes);
-    int *d_s1 = ar.take<int>(nunits);
-    if (!ws || !ar.ok()) return fail(RS_ERR_WORKSPACE, "index workspace too small");
-    std::vector<int> hs1(nunits);
-    for (int u = 0; u < nunits; ++u) hs1[u] = units[u].s1;
-    RS_HIP(hipMemcpyAsync(d_s1, hs1.data(), nunits * sizeof(int), hipMemcpyHostToDevice, st));
+    // unit key lengths: from the probe's unit table, else uploaded into the workspace
+    const int *d_s1 = nullptr;
+    if (sc->tables) {
+      d_s1 = unit_tab_s1(sc->tables);
+    } else {
+      Arena ar(ws, ws_bytes);
+      int *w_s1 = ar.take<int>(nunits);
+      if (!ws || !ar.ok()) return fail(RS_ERR_WORKSPACE, "index workspace too small");
+      std::vector<int> hs1(nunits);
+      for (int u = 0; u < nunits; ++u) hs1[u] = units[u].s1;
+      // the pageable host vector is copied before hipMemcpyAsync returns
+      RS_HIP(hipMemcpyAsync(w_s1, hs1.data(), nunits * sizeof(int), hipMemcpyHostToDevice, st));
+      d_s1 = w_s1;
+    }
     va.col = sc->col; va.diag = sc->diag; va.n = sc->n; va.nunits = nunits; va.ncand_vs = nvs;
     va.s1 = d_s1; va.nv_max = out->nv_max; va.ns_max = out->ns_max; va.nwords = out->nwords;
     va.vsorted = out->vs_vsorted; va.dsorted = out->vs_dsorted; va.count = out->vs_count;

@@ -41,7 +41,7 @@ class RoutedLayer:
     """Buffers and call order of one routed layer for fixed shapes."""
 
     def __init__(self, n, hq, hkv, d, seg_len, grid, r_rec=64, r_uni=64, r_bnd=32, local_w=1024,
-                 device="cuda", use_vt=True):
+                 device="cuda", use_vt=True, use_tables=True):
         import torch
         self.n, self.hq, self.hkv, self.d = n, hq, hkv, d
         self.grid = list(grid)
@@ -67,6 +67,8 @@ class RoutedLayer:
         self.e_host = torch.empty((self.nunits, self.ncand), dtype=torch.float32, pin_memory=True)
         self.rb = None
         self._rb_table = None
+        self.tables = None   # device unit tables (rs_unit_table_init), built with the first qkv()
+        self.use_tables = use_tables
         self._ws = None
         self._ws_routed = None
         self.t_table = None
@@ -77,10 +79,16 @@ class RoutedLayer:
     def qkv(self, q, k, v):
         """The layer's rs_qkv.  With the transposed-V layout on, this also (re)writes V^T of this
         layer into self.vt on the stream (rs_transpose_v): the returned descriptor is valid until
-        the next qkv() call."""
-        if self.vt is None:
-            return _rs.make_qkv(q, k, v)
+        the next qkv() call.  The descriptor carries the unit tables of the layer's unit list
+        (built once, on the first call), so the layer's calls upload nothing."""
         qkv = _rs.make_qkv(q, k, v, vt=self.vt)
+        if self.use_tables:
+            if self.tables is None:
+                self.tables = _rs.UnitTable(qkv, self.units, self.nunits, self.cfg)
+                self.pb.c.tables = self.tables.ptr
+            qkv.tables = self.tables.ptr
+        if self.vt is None:
+            return qkv
         assert _rs.rs_vt_bytes(qkv) == self.vt.numel()
         _rs.rs_transpose_v(qkv, self.vt)
         return qkv

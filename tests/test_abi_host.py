@@ -40,7 +40,8 @@ def test_struct_layouts_match_the_c_compiler(tmp_path):
                "rs_probe_cfg": _rs.RsProbeCfg, "rs_probe_out": _rs.RsProbeOut,
                "rs_index_set": _rs.RsIndexSet, "rs_route_in": _rs.RsRouteIn,
                "rs_route_cfg": _rs.RsRouteCfg, "rs_route_out": _rs.RsRouteOut,
-               "rs_error_model": _rs.RsErrorModel, "rs_route_dev_out": _rs.RsRouteDevOut}
+               "rs_error_model": _rs.RsErrorModel, "rs_route_dev_out": _rs.RsRouteDevOut,
+               "rs_unit_table": _rs.RsUnitTable}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "rs.h"', 'int main(void) {']
     for cname, py in structs.items():
         lines.append(f'printf("{cname} size %zu\\n", sizeof({cname}));')
@@ -267,3 +268,29 @@ def test_probe_coverage_rejects_mismatched_index_set_without_launch():
                         1 << 40, C.byref(out), None)
         assert st == _rs.RS_ERR_INVALID_ARG, bad
         assert what in L.rs_last_error(), (bad, L.rs_last_error())
+
+
+def test_unit_table_of_another_unit_list_rejected_without_launch():
+    """A unit table is only read by calls with the unit list (and probe configuration) it was
+    built for: any other list is rejected on the host before a launch."""
+    L = _rs.lib()
+    n = 4096
+    q = _rs.RsQkv(q=16, k=16, v=16, dtype=_rs.RS_BF16, n=n, hq=2, hkv=1, d=128, sq_h=n * 128, sq_t=128,
+                  sk_h=n * 128, sk_t=128, sv_h=n * 128, sv_t=128)
+    units = _rs.make_units([(0, 0, n), (1, 0, n)])
+    cfg = _rs.RsProbeCfg(r_rec=64, r_uni=0, r_bnd=0, bs_block=64, local_w=1024, flags=_rs.RS_PROBE_ROWS)
+    tab = _rs.RsUnitTable(dev=256, key_units=12345, key_cfg=1, nunits=2, rmax=64, ngroups=1, n=n, hq=2, hkv=1)
+    q.tables = C.cast(C.pointer(tab), C.c_void_p).value
+    out = _rs.RsProbeOut(nunits=2, rmax=64, n=n, nb=n // 64, ncand=0, hq=2, rows=16, subset=16, nsub=16,
+                         row_max=16, row_sum=16, col=16, diag=16, entropy=16, local=16)
+    st = L.rs_probe(C.byref(q), units, 2, C.byref(cfg), None, 0, None, C.c_void_p(256), 1 << 40, C.byref(out), None)
+    assert st == _rs.RS_ERR_INVALID_ARG and b"unit table" in L.rs_last_error()
+    grid = _rs.make_grid([(0, 0, 0), (2, 10, 20)])
+    out.tables = q.tables
+    ib = _rs.RsIndexSet(nunits=2, n=n, nb=n // 64, hq=2, nv_max=10, ns_max=20, k_max=0, nwords=n // 32, ncand_vs=1,
+                        ncand_bs=0, nbw=2, vs_vsorted=16, vs_dsorted=16, vs_count=16, vs_vbits=16, vs_dbits=16)
+    st = L.rs_build_indices(C.byref(out), units, 2, grid, 2, C.c_void_p(256), 1 << 20, C.byref(ib), None)
+    assert st == _rs.RS_ERR_INVALID_ARG and b"unit table" in L.rs_last_error()
+    st = L.rs_routed_attn_prefill(C.byref(q), units, 2, grid, 2, C.byref(ib), C.c_void_p(16), C.c_void_p(16), n * 128,
+                                  128, None, C.c_void_p(256), 1 << 20, None, None)
+    assert st == _rs.RS_ERR_INVALID_ARG and b"unit table" in L.rs_last_error()

@@ -236,3 +236,39 @@ def test_routed_attention_equals_group_launches(vt):
             mask = P.bs_mask(rows, s1, 64, lambda bq: srt[bq, :cnt[bq]])
         ref, _ = A.masked_attention(q[h], k[h // grp], v[h // grp], rows, mask)
         check_close(a2[h, rows], ref, f"routed unit {i}")
+
+
+def test_unit_tables_give_the_same_layer_bit_for_bit():
+    """A routed layer whose calls read the unit tables (no per-call uploads) gives bitwise the
+    same probe scores, indices, coverage, device route and attention output as the same layer
+    with the tables built and uploaded per call."""
+    import torch
+    from paper_2608_29058_amd.pipeline import RoutedLayer, RouteKnobs
+    n, hq, hkv, d, seg = 4096, 4, 2, 128, 1024
+    q, k, v = _layer(n, hq, hkv, d, 9)
+    qd, kd, vd = dev(q), dev(k), dev(v)
+    grid = [(0, 0, 0), (1, 64, 256), (2, 64, 128), (2, 128, 512), (3, 4, 64), (3, 8, 64)]
+    edges = np.array([seg * (b + 1) for b in range(n // seg)], np.int32)
+    tt = np.array([[e / 1000.0 * (1.0 if g[0] == 0 else 0.2 + 0.03 * c) for e in edges] for c, g in enumerate(grid)])
+    snaps = []
+    for use_tables in (True, False):
+        RL = RoutedLayer(n, hq, hkv, d, seg, grid, r_rec=64, r_uni=16, r_bnd=8, use_tables=use_tables)
+        RL.t_table, RL.edges, RL.t_probe_us = tt, edges, 3.0
+        RL.knobs = RouteKnobs(T_layer_us=float(tt[0].sum()) * hq / 5, tau=0.9)
+        RL.o.fill_(float("nan"))
+        assert RL.run(qd, kd, vd, device_route=True) is None
+        torch.cuda.synchronize()
+        assert (RL.tables is not None) == use_tables
+        snap = {"o": RL.o.view(torch.int16).clone(), "choice": RL.rb.choice.clone()}
+        for name in ("rows", "subset", "nsub", "row_max", "row_sum", "col", "diag", "lbs", "cov_rows", "cov", "entropy",
+                     "local"):
+            snap["pb_" + name] = getattr(RL.pb, name).clone()
+        for name in ("vs_vsorted", "vs_dsorted", "vs_count", "vs_vbits", "vs_dbits", "bs_rank", "bs_sorted",
+                     "bs_count", "bs_bits"):
+            snap["ib_" + name] = getattr(RL.ib, name).clone()
+        snaps.append(snap)
+    for name, a in snaps[0].items():
+        b = snaps[1][name]
+        if a.is_floating_point():
+            a, b = a.view(torch.int32), b.view(torch.int32)
+        assert torch.equal(a, b), name
