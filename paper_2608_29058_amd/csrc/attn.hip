@@ -283,7 +283,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
         // bitmap words of the element mask, fetched with the tile so that their latency
         // hides behind the previous tile's compute
         tr.wd = load_win(dbits, a.nwords, my_row - key0 - 63);
-        tr.wv = load_win_uniform(vbits, a.nwords, key0);
+        tr.wv = load_win(vbits, a.nwords, key0);
         return tr;
       }
       return TileRef{-(1 + (t - n_contig) * 64), 3, {0u, 0u, 0u}, {0u, 0u, 0u}, 3};
@@ -659,9 +659,11 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
   TileRef Tc{0, 0, {0u, 0u, 0u}, {0u, 0u, 0u}, 3}, Tn = Tc;
   Plan Pc = plan_of(Tc, false), Pn = Pc;
   auto step = [&](int t, f32x16 (&sc)[2], f32x16 (&sn)[2], bf16 *kc, bf16 *kn, bf16 *vc, bf16 *vn) {
+    // the next tile is taken after the barrier: the barrier waits for every load in flight,
+    // and the vertical-slash mask words that next_tile fetches are only needed a step later
+    lds_fence_barrier();
     TileRef T2{0, 0, {0u, 0u, 0u}, {0u, 0u, 0u}, 3};
     if (t + 2 < ntiles) T2 = next_tile();
-    lds_fence_barrier();
     if (t + 2 < ntiles) issue(kc, T2.key0, false, T2.hm);
     if (t + 1 < ntiles) issue(vn, Tn.key0, true, Tn.hm);
     Pn = plan_of(Tn, t + 1 < ntiles);

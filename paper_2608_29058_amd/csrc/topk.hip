@@ -190,6 +190,7 @@ struct VsArgs {
   const int *s1;  // [nunits]
   int nv[kMaxCandFam], ns[kMaxCandFam];
   int nv_max, ns_max, nwords;
+  int gcap;  // capacity of the LDS gather of the largest set
   int *vsorted, *dsorted, *count;
   uint32_t *vbits, *dbits;
 };
@@ -197,13 +198,17 @@ struct VsArgs {
 // grid: (2, nunits); blockIdx.x = array (0: V from col, 1: D from diag).  Budgets of the family
 // are nested prefixes of one ranking, so the largest budget is selected from the whole array
 // and every smaller one from the largest set (gathered, in ascending position, into LDS).
-constexpr int kVsGather = 8192;  // elements of the largest set kept in LDS
-__global__ void __launch_bounds__(1024) vs_select_kernel(const VsArgs a) {
+constexpr int kVsGather = 8192;  // elements of the largest set kept in LDS, at most
+// Dynamic LDS: [nwords bitmap words][gcap values][gcap positions], gcap = the largest budget
+// selected from the whole array (at most kVsGather): the LDS of a workgroup is then sized
+// for the grid's budgets, and two workgroups share a compute unit for budgets up to ~8K.
+__global__ void __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(8, 8))) vs_select_kernel(const VsArgs a) {
   constexpr int NT = 1024;
-  extern __shared__ uint32_t sBits[];  // nwords
+  extern __shared__ uint32_t sDyn[];
+  uint32_t *sBits = sDyn;
+  float *sVal = (float *)(sDyn + a.nwords);
+  int *sPos = (int *)(sVal + a.gcap);
   __shared__ int sHist[256 * (NT / 64)], sBcast[3], sWave[NT / 64];
-  __shared__ float sVal[kVsGather];
-  __shared__ int sPos[kVsGather];
   const int arr = blockIdx.x;
   const int u = blockIdx.y;
   const int s1 = a.s1[u];
@@ -217,7 +222,7 @@ __global__ void __launch_bounds__(1024) vs_select_kernel(const VsArgs a) {
   const int kmax = budget(cmax);
   // largest set: bitmap, then its members in ascending position with their values (when it
   // fits in LDS; otherwise every budget is selected from the whole array)
-  const bool gather = kmax <= kVsGather;
+  const bool gather = kmax <= a.gcap;
   int nmax = 0;
   if (gather) {
     for (int w = threadIdx.x; w < a.nwords; w += NT) sBits[w] = 0u;
@@ -225,7 +230,7 @@ __global__ void __launch_bounds__(1024) vs_select_kernel(const VsArgs a) {
     select_top<NT>(vals, len, kmax, sHist, sBcast, sWave,
                    [&](int i) { atomicOr(&sBits[(i + off) >> 5], 1u << ((i + off) & 31)); });
     __syncthreads();
-    nmax = bits_to_list<NT>(sBits, a.nwords, sPos, kVsGather, sWave);
+    nmax = bits_to_list<NT>(sBits, a.nwords, sPos, a.gcap, sWave);
     __syncthreads();
     for (int x = threadIdx.x; x < nmax; x += NT) sVal[x] = vals[sPos[x] - off];
     __syncthreads();
@@ -388,7 +393,10 @@ rs_status build_indices_launch(const rs_probe_out *sc, const rs_unit *units, int
     va.s1 = d_s1; va.nv_max = out->nv_max; va.ns_max = out->ns_max; va.nwords = out->nwords;
     va.vsorted = out->vs_vsorted; va.dsorted = out->vs_dsorted; va.count = out->vs_count;
     va.vbits = out->vs_vbits; va.dbits = out->vs_dbits;
-    const size_t lds = (size_t)out->nwords * sizeof(uint32_t);
+    int kbig = 0;  // the largest budget selected from a whole array (columns: n_v, diagonals: n_s - 1)
+    for (int c = 0; c < nvs; ++c) kbig = std::max(kbig, std::max(va.nv[c], va.ns[c] - 1));
+    va.gcap = std::min(kVsGather, std::max(kbig, 1));
+    const size_t lds = (size_t)out->nwords * sizeof(uint32_t) + (size_t)va.gcap * (sizeof(float) + sizeof(int));
     hipLaunchKernelGGL(vs_select_kernel, dim3(2, nunits), dim3(1024), lds, st, va);
     RS_HIP(hipGetLastError());
   }
