@@ -45,6 +45,7 @@ struct ProbeArgs {
   const void *q, *k;
   long long sq_h, sq_t, sk_h, sk_t;
   int n, group, rmax, nchunks;
+  int lg_groups, lg_pairs;  // task grid of a range pass: unit groups x row-block pairs per range
   float c, scale;
   int local_w;
   const ProbeUnit *units;
@@ -151,8 +152,28 @@ __device__ __forceinline__ Win3 win_fix(Win3 r, int nwords, int pos) {
 // outstanding, with no wait on the other counters
 constexpr int vm_wait_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 
+// Task of a range-pass workgroup.  The grid is one-dimensional, and workgroups are dealt to
+// the 8 XCDs in turn (workgroup b on XCD b % 8).  XCD x takes the key ranges x, x + 8, ...
+// and, per range, every (unit group, row-block pair) task in turn: the groups of one
+// key/value head (its segments and query heads) and the pairs of a group read the same K
+// range, and they then run at about the same time on one L2.  Ranges are dealt in turn so
+// that the XCDs get a similar mix of early ranges (seen by every segment) and late ones.
+struct RangeTask {
+  int rg, gy, pz;
+};
+__device__ __forceinline__ RangeTask range_task(const ProbeArgs &a) {
+  const int per = a.lg_groups * a.lg_pairs;
+  const int b = (int)blockIdx.x, j = b >> 3;
+  const int rem = j % per;
+  return RangeTask{(b & 7) + 8 * (j / per), rem / a.lg_pairs, rem % a.lg_pairs};
+}
+// workgroups of a range pass over (ranges, groups, pairs)
+static inline dim3 range_grid(int nchunks, int ngroups, int npairs) {
+  return dim3((unsigned)(8 * ((nchunks + 7) / 8) * ngroups * npairs));
+}
+
 // ---- the three passes over one key range ------------------------------------------------
-// grid: (key range, unit group, row-block pair).  A group holds the units of up to 4 query
+// tasks: (key range, unit group, row-block pair), in the XCD-aware order of range_task.  A group holds the units of up to 4 query
 // heads that share a key/value head and a segment, hence the same sampled rows and keys; wave
 // w computes unit w.  Sampled rows are split into 32-row blocks aligned at the end of the
 // (ascending) row list, so the recent rows fill the last blocks, and blocks are paired from
@@ -191,8 +212,10 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
   __shared__ __align__(16) bf16 sK1[NKB == 2 ? TE : 8];
   __shared__ int sRows[2][32];
 
-  const int rg = blockIdx.x;
-  const int4 grp = a.groups[blockIdx.y];
+  const RangeTask task = range_task(a);
+  const int rg = task.rg;
+  if (rg >= a.nchunks) return;
+  const int4 grp = a.groups[task.gy];
   const ProbeUnit U0 = a.units[grp.x];
   const int c0 = rg * kRange;
   if (c0 >= U0.s1) return;
@@ -204,7 +227,7 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
     p_lo = 0;
     p_hi = (U0.nR - 1) / 64 + 1;
   } else {
-    p_lo = blockIdx.z;
+    p_lo = task.pz;
     p_hi = p_lo + 1;
     if (2 * p_lo >= nrb) return;
   }
@@ -1114,25 +1137,31 @@ template <int D, typename InT>
 static hipError_t launch_rows(const ProbeArgs &pa, int nunits, int ngroups, int mode, float *diag, float *ent, float *loc,
                               float *cov_rows, float *cov, hipStream_t st) {
   const int npairs = ((pa.rmax + 31) / 32 + 1) / 2;  // row-block pairs of the fullest unit
+  ProbeArgs ra = pa;  // with the task grid of each range pass
+  ra.lg_groups = ngroups;
   if (mode == 0) {
     // statistics of the row pairs holding recent rows (pairs are taken from the end of the
     // ascending row list, where the recent rows are); the coverage pass normalises online
     const int spairs = std::min(npairs, pa.stats_rows / 64);
     if (spairs > 0) {
-      hipLaunchKernelGGL((probe_range_kernel<D, InT, M_STATS, 1>), dim3(pa.nchunks, ngroups, spairs), dim3(256), 0, st, pa);
+      ra.lg_pairs = spairs;
+      hipLaunchKernelGGL((probe_range_kernel<D, InT, M_STATS, 1>), range_grid(pa.nchunks, ngroups, spairs), dim3(256), 0, st, ra);
       hipLaunchKernelGGL(probe_stats_combine_kernel, dim3((pa.rmax + 3) / 4, nunits), dim3(256), 0, st, pa);
     }
-    hipLaunchKernelGGL((probe_range_kernel<D, InT, M_SCORES, 1>), dim3(pa.nchunks, ngroups), dim3(256), 0, st, pa);
+    ra.lg_pairs = 1;
+    hipLaunchKernelGGL((probe_range_kernel<D, InT, M_SCORES, 1>), range_grid(pa.nchunks, ngroups, 1), dim3(256), 0, st, ra);
     hipLaunchKernelGGL(probe_finish_kernel, dim3((pa.n + 255) / 256, nunits), dim3(256), 0, st, pa, diag, ent, loc);
   } else {
     bool ashape_only = true;
     for (int q = 0; q < pa.ncov; ++q) ashape_only = ashape_only && pa.cand[pa.cov_cand[q]].fam == RS_ASHAPE;
+    ra.lg_pairs = npairs;
+    const dim3 grid = range_grid(pa.nchunks, ngroups, npairs);
     if (ashape_only && pa.ncov <= 2)
-      hipLaunchKernelGGL((probe_range_kernel<D, InT, M_COVER, 2, false>), dim3(pa.nchunks, ngroups, npairs), dim3(256), 0, st, pa);
+      hipLaunchKernelGGL((probe_range_kernel<D, InT, M_COVER, 2, false>), grid, dim3(256), 0, st, ra);
     else if (pa.ncov <= 4)
-      hipLaunchKernelGGL((probe_range_kernel<D, InT, M_COVER, 4>), dim3(pa.nchunks, ngroups, npairs), dim3(256), 0, st, pa);
+      hipLaunchKernelGGL((probe_range_kernel<D, InT, M_COVER, 4>), grid, dim3(256), 0, st, ra);
     else
-      hipLaunchKernelGGL((probe_range_kernel<D, InT, M_COVER, kMaxCand>), dim3(pa.nchunks, ngroups, npairs), dim3(256), 0, st, pa);
+      hipLaunchKernelGGL((probe_range_kernel<D, InT, M_COVER, kMaxCand>), grid, dim3(256), 0, st, ra);
     hipLaunchKernelGGL(cover_combine_kernel, dim3((pa.rmax + 3) / 4, nunits), dim3(256), 0, st, pa, ent, loc, cov_rows);
     hipLaunchKernelGGL(cover_means_kernel, dim3(pa.ncand, nunits), dim3(64), 0, st, pa, cov_rows, cov);
   }
