@@ -3,8 +3,9 @@
 Workload: 32 layers of a Llama-3.1-8B-shaped attention layer (GQA 32/8, d = 128, bf16,
 n = 131072 tokens), per-layer seeds and mixed head regimes (synthetic, see synth/gen.py).
 One step = one layer through the whole hot path: probe (sampled rows + block-mean),
-index construction, coverage, host routing under the latency budget, and one grouped
-sparse/dense attention launch per (pattern, budget) group.  Each head is split into 8
+index construction, coverage, routing under the latency budget (on the device by default,
+`--route host` for the host router), and one persistent attention launch per pattern family
+(the host route launches one per (pattern, budget) group).  Each head is split into 8
 segments of 16K rows (units).  The reported value is ms per layer (lower is better).
 
 Before timing (offline calibration, untimed): the kernel latency of every candidate is
@@ -373,7 +374,7 @@ def main():
     ap.add_argument("--route", choices=("device", "host"), default="device",
                     help="routing on the device (no host synchronisation in a layer) or on the host")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-configs", action="store_true", help="skip the timed single-layer workloads (c2-c4)")
+    ap.add_argument("--no-configs", action="store_true", help="skip the timed single-layer workloads (A-shape 8K, vertical-slash 32K, block-sparse 128K)")
     ap.add_argument("--config-reps", type=int, default=10)
     ap.add_argument("--json-out", default=None)
     args = ap.parse_args()
@@ -421,7 +422,7 @@ def main():
     t_table = RL.profile_latency(qkvp, edges, reps=5, tail=tail)
     for c in range(len(GRID)):
         log(f"t_ker {GRID[c]} (us/unit):", np.round(t_table[c], 1).tolist())
-    # probe + index + coverage time, and the host routing overhead
+    # probe + index + coverage time, and the routing overhead
     tp_us = RL.profile_probe(qkvp, reps=3)
     del qp, kp, vp, qkvp
     RL.t_table, RL.edges = t_table, edges

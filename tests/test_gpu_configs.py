@@ -104,7 +104,7 @@ def test_config2_ashape_all_heads():
         rows = _sample_rows(0, n, h)
         ref = _masked_rows(_host(q, h), _host(k, h // 4), _host(v, h // 4), rows, n,
                            lambda rb, s1, cols: P.ashape_mask(rb, s1, 128, 1024, cols=cols), _cols_ashape(128, 1024))
-        check_close(_host(o, h)[rows], ref, f"c2 h={h}")
+        check_close(_host(o, h)[rows], ref, f"A-shape 8K h={h}")
 
 
 @pytest.mark.timeout(900)
@@ -148,12 +148,12 @@ def test_config3_probe_vs_and_forced_dense():
         rows = _sample_rows(0, n, h)
         out = _masked_rows(qh, kh, vh, rows, n, lambda rb, s1, cols: P.vs_mask(rb, s1, V, D, cols=cols),
                            _cols_vs(V, D))
-        check_close(_host(o, h)[rows], out, f"c3 vs h={h}")
+        check_close(_host(o, h)[rows], out, f"vertical-slash 32K h={h}")
     for h in dense_heads:
         rows = _sample_rows(0, n, h)
         ref = _masked_rows(_host(q, h), _host(k, h // 4), _host(v, h // 4), rows, n,
                            lambda rb, s1, cols: P.dense_mask(rb, s1, cols=cols), _cols_dense)
-        check_close(_host(o, h)[rows], ref, f"c3 dense h={h}")
+        check_close(_host(o, h)[rows], ref, f"dense 32K h={h}")
 
 
 def _config4_layer():
@@ -213,7 +213,7 @@ def test_config4_block_sparse_128k():
         out = _masked_rows(qh, kh, vh, rows, n,
                            lambda rb, s1, cols: P.bs_mask(rb, s1, 64, lambda b: sel[b], cols=cols),
                            _cols_bs(lambda b: sel[b]))
-        check_close(_host(o, h)[rows], out, f"c4 h={h}")
+        check_close(_host(o, h)[rows], out, f"block-sparse 128K h={h}")
 
 
 @pytest.mark.timeout(900)
@@ -231,7 +231,7 @@ def test_config4_whole_head_every_row():
     out = _masked_rows(qh, kh, vh, np.arange(n), n,
                        lambda rb, s1, cols: P.bs_mask(rb, s1, 64, lambda b: sel[b], cols=cols),
                        _cols_bs(lambda b: sel[b]), block=64)
-    check_close(got, out, f"c4 head {h}, all rows")
+    check_close(got, out, f"block-sparse 128K head {h}, all rows")
 
 
 @pytest.mark.timeout(900)
@@ -292,7 +292,7 @@ def test_config5_routed_layer_decisions_and_outputs():
                 mf, cf = (lambda rb, e1, cols: P.bs_mask(rb, e1, 64, sf, cols=cols)), _cols_bs(sf)
             rows = _sample_rows(s0, s1, u, 64, 2)
             out = _masked_rows(qh, kh, vh, rows, s1, mf, cf)
-            check_close(oh[rows], out, f"c5 unit {u} cand {cand}")
+            check_close(oh[rows], out, f"routed 128K unit {u} cand {cand}")
     # the launch configuration the benchmark times: device route, one persistent launch per
     # family; the same route and bitwise the same output as the grouped launches above
     o_groups = RL.o.clone()
