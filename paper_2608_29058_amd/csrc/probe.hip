@@ -211,6 +211,10 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
   __shared__ __align__(16) bf16 sK0[TE];
   __shared__ __align__(16) bf16 sK1[NKB == 2 ? TE : 8];
   __shared__ int sRows[2][32];
+  // coverage pass: per wave (unit) and prefetched vertical-slash candidate, the diagonal-bitmap
+  // words that the windows of this row-block pair and key range read (staged when they fit)
+  constexpr int kDCap = MODE == M_COVER ? 576 : 1;
+  __shared__ uint32_t sDW[4][kPrefVs][kDCap];
 
   const RangeTask task = range_task(a);
   const int rg = task.rg;
@@ -339,44 +343,67 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
       for (int k = 0; k < kPrefBs; ++k) covb[s][k] = 0.f;
     }
 
+    // coverage pass, per range: the block-sparse selection word of each row's query block (the
+    // range's 16 key blocks share one word), the range's 32 column-bitmap words (lane w holds
+    // word c0 / 32 + w) and, when they fit in sDW, the diagonal-bitmap words of every window
+    // the rows read here: window positions i - k0 - 63 lie in [r_lo - c0 - 1023, r_hi - c0 - 63]
+    // for the pair's rows [r_lo, r_hi], and a window reads its word and the next two
+    uint32_t bwr[2][kPrefBs], vmv[kPrefVs];
+    int rlo = 0, dw0 = 0;
+    bool stage = false;
+    if constexpr (MODE == M_COVER) {
+      rlo = 0x7fffffff;
+#pragma unroll
+      for (int s = 0; s < 2; ++s)
+        if (row[s] >= 0) rlo = min(rlo, row[s]);
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) rlo = min(rlo, __shfl_xor(rlo, o));  // the last block has rows
+      dw0 = (rlo - c0 - (kRange - 1)) >> 5;
+      const int nspan = ((rmax1 - c0 - 63) >> 5) + 3 - dw0;
+      stage = nspan <= kDCap;  // the same rows for every wave
+#pragma unroll
+      for (int s = 0; s < 2; ++s)
+#pragma unroll
+        for (int k = 0; k < kPrefBs; ++k) {
+          bwr[s][k] = 0u;
+          if (k < a.nbs_pref && u >= 0)  // absent rows (-1) read row 0's word, unused
+            bwr[s][k] = a.bs_bits[(((long long)uhead * a.ncand_bs + a.bs_pref_cl[k]) * a.nb + (max(row[s], 0) >> 6)) *
+                                      a.nbw + (c0 >> 11)];
+        }
+#pragma unroll
+      for (int k = 0; k < kPrefVs; ++k) {
+        vmv[k] = 0u;
+        if (k >= a.nvs_pref || u < 0) continue;
+        const long long vr = ((long long)u * a.ncand_vs + a.vs_pref_cl[k]) * a.nwords;
+        const int wv = (c0 >> 5) + lane;
+        if (lane < 32 && wv < a.nwords) vmv[k] = a.vs_vbits[vr + wv];
+        if (stage)
+          for (int x = lane; x < nspan; x += 64) {
+            const int w = dw0 + x;
+            sDW[wave][k][x] = (w >= 0 && w < a.nwords) ? a.vs_dbits[vr + w] : 0u;
+          }
+      }
+      wave_sync();  // sDW is written and read by the lanes of one wave
+    }
+
     // coverage pass: diagonal-bitmap windows (vertical-slash) and block-selection words
     // (block-sparse) of each row, fetched together with the K copy of the tile they serve
     // Only raw words are loaded here (combined where they are used, in the next tile): a use
     // right after the loads would make the compiler wait for them, and with them for the
     // tile copy issued just before.
     struct Pref {
-      Win3 wd[2][kPrefVs];
-      uint32_t mv[kPrefVs][2];  // column-bitmap words of the tile's 64 keys (k0 is a multiple of 64)
-      uint32_t bw[2][kPrefBs];
+      Win3 wd[2][kPrefVs];  // diagonal windows when they are not staged in sDW
     };
     auto fetch = [&](int k0, Pref &f) __attribute__((always_inline)) {
       if constexpr (MODE == M_COVER) {
-        const int kt = k0 >> 6;
-        const int w0 = k0 >> 5;
-#pragma unroll
-        for (int k = 0; k < kPrefVs; ++k) {
-          f.mv[k][0] = f.mv[k][1] = 0u;
-          if (k < a.nvs_pref && u >= 0) {
-            const uint32_t *vb = a.vs_vbits + ((long long)u * a.ncand_vs + a.vs_pref_cl[k]) * a.nwords;
-            f.mv[k][0] = vb[w0];                        // k0 < n: in the bitmap
-            f.mv[k][1] = vb[min(w0 + 1, a.nwords - 1)];  // zeroed at use when past it
-          }
-        }
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
 #pragma unroll
           for (int k = 0; k < kPrefVs; ++k) {
             f.wd[s][k] = Win3{0u, 0u, 0u};
-            if (k < a.nvs_pref && u >= 0)
+            if (!stage && k < a.nvs_pref && u >= 0)
               f.wd[s][k] = load_win_raw(a.vs_dbits + ((long long)u * a.ncand_vs + a.vs_pref_cl[k]) * a.nwords,
                                         a.nwords, max(row[s], 0) - k0 - 63);
-          }
-#pragma unroll
-          for (int k = 0; k < kPrefBs; ++k) {
-            f.bw[s][k] = 0u;
-            if (k < a.nbs_pref && u >= 0)  // rows of absent lanes (row -1) read row 0's words, unused
-              f.bw[s][k] = a.bs_bits[(((long long)uhead * a.ncand_bs + a.bs_pref_cl[k]) * a.nb + (max(row[s], 0) >> 6)) *
-                                         a.nbw + (kt >> 5)];
           }
         }
       }
@@ -560,20 +587,29 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
           };
           loc[s] += from(i - a.local_w + 1);
           const int kt = k0 >> 6;
+          const int tl = (k0 - c0) >> 5;  // column word of the tile within the range
 #pragma unroll
           for (int k = 0; k < kPrefVs; ++k) {
             if (k >= a.nvs_pref) break;
-            const int dpos = max(i, 0) - k0 - 63;
-            const uint64_t md = __builtin_bitreverse64(win_bits(win_fix(f.wd[s][k], a.nwords, dpos), dpos));
-            const uint32_t mv1 = (k0 >> 5) + 1 < a.nwords ? f.mv[k][1] : 0u;
-            const uint64_t mv = (uint64_t)f.mv[k][0] | ((uint64_t)mv1 << 32);
+            uint64_t md;
+            if (stage) {  // absent rows (-1) read the first row's window, unused
+              const int dpos = (i >= 0 ? i : rlo) - k0 - 63;
+              const uint32_t *dw = &sDW[wave][k][(dpos >> 5) - dw0];
+              md = __builtin_bitreverse64(win_bits(Win3{dw[0], dw[1], dw[2]}, dpos));
+            } else {
+              const int dpos = max(i, 0) - k0 - 63;
+              md = __builtin_bitreverse64(win_bits(win_fix(f.wd[s][k], a.nwords, dpos), dpos));
+            }
+            const uint32_t mv0 = (uint32_t)__builtin_amdgcn_readlane((int)vmv[k], tl);
+            const uint32_t mv1 = (uint32_t)__builtin_amdgcn_readlane((int)vmv[k], tl + 1);
+            const uint64_t mv = (uint64_t)mv0 | ((uint64_t)mv1 << 32);
             const uint64_t m = (md | mv) >> (4 * hh);
             if (__ballot(m != 0ull) != 0ull) covv[s][k] += masked(m);  // wave-uniform skip
           }
 #pragma unroll
           for (int k = 0; k < kPrefBs; ++k) {
             if (k >= a.nbs_pref) break;
-            if ((f.bw[s][k] >> (kt & 31)) & 1u) covb[s][k] += tsum;
+            if ((bwr[s][k] >> (kt & 31)) & 1u) covb[s][k] += tsum;
           }
 #pragma unroll
           for (int q = 0; q < NCV; ++q) {
