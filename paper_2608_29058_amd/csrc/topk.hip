@@ -262,6 +262,84 @@ __global__ void __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(8, 8)
   }
 }
 
+// select_top for one wave whose elements are held in registers: key[c] is the key of element
+// c * 64 + lane (elements >= len are ignored); emit(i, key) for each selected element.  The
+// same selection as select_top<64> over the same keys: radix select over 8-bit digits with
+// one 256-bin histogram, then the lowest positions among keys equal to the threshold.
+template <int NV, typename F>
+__device__ void select_top_regs(const uint32_t (&key)[NV], int len, int K, int *sHist, int *sBcast, F emit) {
+  const int l = (int)(threadIdx.x & 63u);
+  if (K <= 0) return;
+  if (len <= K) {
+#pragma unroll
+    for (int c = 0; c < NV; ++c)
+      if (c * 64 + l < len) emit(c * 64 + l, key[c]);
+    return;
+  }
+  uint32_t prefix = 0, maskhi = 0;
+  int krem = K, neq = 0;
+  for (int byte = 3; byte >= 0; --byte) {
+    for (int b = l; b < 256; b += 64) sHist[b] = 0;
+    gsync<64>();
+#pragma unroll
+    for (int c = 0; c < NV; ++c)
+      if (c * 64 + l < len && (key[c] & maskhi) == prefix) atomicAdd(&sHist[(key[c] >> (8 * byte)) & 255u], 1);
+    gsync<64>();
+    // lane l owns bins 255-4l .. 252-4l (descending); inclusive scan of the counts
+    int c4[4], own = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      c4[q] = sHist[255 - 4 * l - q];
+      own += c4[q];
+    }
+    int incl = own;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(incl, o);
+      if (l >= o) incl += y;
+    }
+    const int excl = incl - own;
+    if (excl < krem && incl >= krem) {
+      int cum = excl, sel = 255 - 4 * l, cnt = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (cum + c4[q] >= krem) {
+          sel = 255 - 4 * l - q;
+          cnt = c4[q];
+          break;
+        }
+        cum += c4[q];
+      }
+      sBcast[0] = sel;
+      sBcast[1] = krem - cum;
+      sBcast[2] = cnt;
+    }
+    gsync<64>();
+    prefix |= (uint32_t)sBcast[0] << (8 * byte);
+    maskhi |= 0xffu << (8 * byte);
+    krem = sBcast[1];
+    neq = sBcast[2];
+    gsync<64>();
+  }
+  const uint32_t T = prefix;
+  const int take = krem;
+  const bool all_eq = take == neq;
+#pragma unroll
+  for (int c = 0; c < NV; ++c)
+    if (c * 64 + l < len && (key[c] > T || (all_eq && key[c] == T))) emit(c * 64 + l, key[c]);
+  if (all_eq) return;
+  int seen = 0;
+#pragma unroll
+  for (int c = 0; c < NV; ++c) {
+    if (c * 64 >= len || seen >= take) break;
+    const int f = (c * 64 + l < len && key[c] == T) ? 1 : 0;
+    int tot;
+    const int in = block_incl_scan<64>(f, nullptr, &tot);
+    if (f && seen + in - 1 < take) emit(c * 64 + l, key[c]);
+    seen += tot;
+  }
+}
+
 struct BsArgs {
   const float *lbs;
   int nb, hq, ncand_bs, k_max, nbw;
@@ -271,7 +349,9 @@ struct BsArgs {
 };
 
 // grid: (ceil(nb / 4), hq), 256 threads; one query block per wave (waves synchronise only
-// themselves: each has its own LDS)
+// themselves: each has its own LDS).  The wave's pooled scores are read once into registers
+// (NV per lane, NV * 64 >= nb - 1).
+template <int NV>
 __global__ void __launch_bounds__(256) bs_select_kernel(const BsArgs a) {
   constexpr int NT = 64;
   constexpr int SP = 256;  // sort capacity (k_max <= 256)
@@ -290,9 +370,12 @@ __global__ void __launch_bounds__(256) bs_select_kernel(const BsArgs a) {
   if (l == 0) sCntA[w] = 0;
   gsync<NT>();
   const int K = a.k_max - 1;
-  select_top<NT>(vals, bq, K, sHist, sBcast, nullptr, [&](int i) {
+  uint32_t key[NV];
+#pragma unroll
+  for (int c = 0; c < NV; ++c) key[c] = c * 64 + l < bq ? float_key(vals[c * 64 + l]) : 0u;
+  select_top_regs<NV>(key, bq, K, sHist, sBcast, [&](int i, uint32_t kv) {
     const int p = atomicAdd(&sCntA[w], 1);
-    sKey[p] = ((unsigned long long)float_key(vals[i]) << 32) | (unsigned long long)(0xffffffffu - (uint32_t)i);
+    sKey[p] = ((unsigned long long)kv << 32) | (unsigned long long)(0xffffffffu - (uint32_t)i);
   });
   gsync<NT>();
   // bitonic sort, descending, in registers: element e = 4 l + j is key kr[j] of lane l; pairs
@@ -403,7 +486,10 @@ rs_status build_indices_launch(const rs_probe_out *sc, const rs_unit *units, int
   if (nbs > 0) {
     ba.lbs = sc->lbs; ba.nb = out->nb; ba.hq = out->hq; ba.ncand_bs = nbs; ba.k_max = out->k_max; ba.nbw = out->nbw;
     ba.rank = out->bs_rank; ba.sorted = out->bs_sorted; ba.count = out->bs_count; ba.bits = out->bs_bits;
-    hipLaunchKernelGGL(bs_select_kernel, dim3((out->nb + 3) / 4, out->hq), dim3(256), 0, st, ba);
+    if (out->nb - 1 <= 32 * 64)
+      hipLaunchKernelGGL(bs_select_kernel<32>, dim3((out->nb + 3) / 4, out->hq), dim3(256), 0, st, ba);
+    else
+      hipLaunchKernelGGL(bs_select_kernel<kMaxN / 64 / 64>, dim3((out->nb + 3) / 4, out->hq), dim3(256), 0, st, ba);
     RS_HIP(hipGetLastError());
   }
   return RS_OK;
