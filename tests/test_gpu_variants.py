@@ -240,6 +240,22 @@ def test_coverage_general_grids_match_oracle(grid, rcfg):
     _check_coverage(q, k, units, grid, rcfg, ib, pc, hq // hkv)
 
 
+def test_coverage_staged_and_fetched_bitmap_words():
+    """The coverage pass stages a pair's diagonal-bitmap words in LDS when they fit (rows spread
+    over at most ~17K positions) and fetches them with each tile otherwise: a 24K-row unit
+    (fetched) and a 16K-row unit (staged) in one call, three prefetched vertical-slash
+    candidates, against the oracle."""
+    n, hq, hkv, d = 24576, 2, 1, 128
+    q, k, v = _inputs(n, hq, hkv, d, seed=11, kscale=1.5)
+    rcfg = (64, 64, 32)
+    units = [(0, 0, n), (1, 8192, n)]
+    res = _probe_scores(q, k, v, units, rcfg, "bf16")
+    grid = [(DENSE, 0, 0), (ASHAPE, 64, 256), (VSLASH, 40, 120), (VSLASH, 80, 300), (VSLASH, 200, 900),
+            (BSPARSE, 5, 64)]
+    ib, pc = _coverage(res, units, grid, rcfg)
+    _check_coverage(q, k, units, grid, rcfg, ib, pc, hq // hkv)
+
+
 def test_coverage_general_grid_on_128k_segments():
     """The 16-candidate coverage variant over 16K-row segments of a 128K prefix (the last
     segment sees every key) on the 32-layer workload's synthetic layer."""
