@@ -79,7 +79,18 @@ __device__ void radix_select(const float *vals, int len, int K, uint32_t *T_out,
   for (int byte = 3; byte >= 0; --byte) {
     for (int b = gtid<NT>(); b < 256 * NWV; b += NT) sHist[b] = 0;
     gsync<NT>();
-    for (int i = gtid<NT>(); i < len; i += NT) {
+    // four loads in flight per thread before their histogram updates (counts do not depend
+    // on the order of the adds)
+    int i = gtid<NT>();
+    for (; i + 3 * NT < len; i += 4 * NT) {
+      uint32_t k4[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) k4[j] = float_key(vals[i + j * NT]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if ((k4[j] & maskhi) == prefix) atomicAdd(&myHist[(k4[j] >> (8 * byte)) & 255u], 1);
+    }
+    for (; i < len; i += NT) {
       const uint32_t key = float_key(vals[i]);
       if ((key & maskhi) == prefix) atomicAdd(&myHist[(key >> (8 * byte)) & 255u], 1);
     }
@@ -142,9 +153,18 @@ __device__ void select_top(const float *vals, int len, int K, int *sHist, int *s
   radix_select<NT>(vals, len, K, &T, &take, &neq, sHist, sBcast);
   // every key equal to T is taken when there are no more of them than needed (the usual case)
   const bool all_eq = take == neq;
-  for (int i = gtid<NT>(); i < len; i += NT) {
-    const uint32_t key = float_key(vals[i]);
-    if (key > T || (all_eq && key == T)) emit(i);
+  int ie = gtid<NT>();
+  for (; ie + 3 * NT < len; ie += 4 * NT) {
+    uint32_t k4[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) k4[j] = float_key(vals[ie + j * NT]);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (k4[j] > T || (all_eq && k4[j] == T)) emit(ie + j * NT);
+  }
+  for (; ie < len; ie += NT) {
+    const uint32_t key = float_key(vals[ie]);
+    if (key > T || (all_eq && key == T)) emit(ie);
   }
   if (all_eq) return;
   // equal keys: lowest positions first
