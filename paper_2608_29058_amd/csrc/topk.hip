@@ -79,15 +79,15 @@ __device__ void radix_select(const float *vals, int len, int K, uint32_t *T_out,
   for (int byte = 3; byte >= 0; --byte) {
     for (int b = gtid<NT>(); b < 256 * NWV; b += NT) sHist[b] = 0;
     gsync<NT>();
-    // four loads in flight per thread before their histogram updates (counts do not depend
+    // eight loads in flight per thread before their histogram updates (counts do not depend
     // on the order of the adds)
     int i = gtid<NT>();
-    for (; i + 3 * NT < len; i += 4 * NT) {
-      uint32_t k4[4];
+    for (; i + 7 * NT < len; i += 8 * NT) {
+      uint32_t k4[8];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) k4[j] = float_key(vals[i + j * NT]);
+      for (int j = 0; j < 8; ++j) k4[j] = float_key(vals[i + j * NT]);
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < 8; ++j)
         if ((k4[j] & maskhi) == prefix) atomicAdd(&myHist[(k4[j] >> (8 * byte)) & 255u], 1);
     }
     for (; i < len; i += NT) {
@@ -154,12 +154,12 @@ __device__ void select_top(const float *vals, int len, int K, int *sHist, int *s
   // every key equal to T is taken when there are no more of them than needed (the usual case)
   const bool all_eq = take == neq;
   int ie = gtid<NT>();
-  for (; ie + 3 * NT < len; ie += 4 * NT) {
-    uint32_t k4[4];
+  for (; ie + 7 * NT < len; ie += 8 * NT) {
+    uint32_t k4[8];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) k4[j] = float_key(vals[ie + j * NT]);
+    for (int j = 0; j < 8; ++j) k4[j] = float_key(vals[ie + j * NT]);
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < 8; ++j)
       if (k4[j] > T || (all_eq && k4[j] == T)) emit(ie + j * NT);
   }
   for (; ie < len; ie += NT) {
