@@ -379,7 +379,7 @@ def main():
     ap.add_argument("--json-out", default=None)
     args = ap.parse_args()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        print(json.dumps({"error": "this benchmark runs the layer on one GPU; --gpus must be 1"}))
         sys.exit(2)
 
     import torch
