@@ -173,9 +173,10 @@ static inline dim3 range_grid(int nchunks, int ngroups, int npairs) {
 }
 
 // ---- the three passes over one key range ------------------------------------------------
-// tasks: (key range, unit group, row-block pair), in the XCD-aware order of range_task.  A group holds the units of up to 4 query
-// heads that share a key/value head and a segment, hence the same sampled rows and keys; wave
-// w computes unit w.  Sampled rows are split into 32-row blocks aligned at the end of the
+// tasks: (key range, unit group, row-block pair), in the XCD-aware order of range_task.  A
+// group holds the units of up to 4 query heads that share a key/value head and a segment,
+// hence the same sampled rows and keys; wave w computes unit w.  Sampled rows are split into
+// 32-row blocks aligned at the end of the
 // (ascending) row list, so the recent rows fill the last blocks, and blocks are paired from
 // the end.  A workgroup streams the 64-key tiles of its range through two LDS buffers (direct
 // buffer-to-LDS copies, one barrier per tile) and keeps the Q fragments of its block pair in
@@ -386,11 +387,10 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
       wave_sync();  // sDW is written and read by the lanes of one wave
     }
 
-    // coverage pass: diagonal-bitmap windows (vertical-slash) and block-selection words
-    // (block-sparse) of each row, fetched together with the K copy of the tile they serve
-    // Only raw words are loaded here (combined where they are used, in the next tile): a use
-    // right after the loads would make the compiler wait for them, and with them for the
-    // tile copy issued just before.
+    // coverage pass, when the diagonal-bitmap words are not staged: each row's windows,
+    // fetched together with the K copy of the tile they serve.  Only raw words are loaded here
+    // (combined where they are used, in the next tile): a use right after the loads would make
+    // the compiler wait for them, and with them for the tile copy issued just before.
     struct Pref {
       Win3 wd[2][kPrefVs];  // diagonal windows when they are not staged in sDW
     };
