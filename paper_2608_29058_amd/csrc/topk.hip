@@ -83,12 +83,12 @@ __device__ void radix_select(const float *vals, int len, int K, uint32_t *T_out,
     // on the order of the adds)
     int i = gtid<NT>();
     for (; i + 7 * NT < len; i += 8 * NT) {
-      uint32_t k4[8];
+      uint32_t k8[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) k4[j] = float_key(vals[i + j * NT]);
+      for (int j = 0; j < 8; ++j) k8[j] = float_key(vals[i + j * NT]);
 #pragma unroll
       for (int j = 0; j < 8; ++j)
-        if ((k4[j] & maskhi) == prefix) atomicAdd(&myHist[(k4[j] >> (8 * byte)) & 255u], 1);
+        if ((k8[j] & maskhi) == prefix) atomicAdd(&myHist[(k8[j] >> (8 * byte)) & 255u], 1);
     }
     for (; i < len; i += NT) {
       const uint32_t key = float_key(vals[i]);
@@ -155,12 +155,12 @@ __device__ void select_top(const float *vals, int len, int K, int *sHist, int *s
   const bool all_eq = take == neq;
   int ie = gtid<NT>();
   for (; ie + 7 * NT < len; ie += 8 * NT) {
-    uint32_t k4[8];
+    uint32_t k8[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) k4[j] = float_key(vals[ie + j * NT]);
+    for (int j = 0; j < 8; ++j) k8[j] = float_key(vals[ie + j * NT]);
 #pragma unroll
     for (int j = 0; j < 8; ++j)
-      if (k4[j] > T || (all_eq && k4[j] == T)) emit(ie + j * NT);
+      if (k8[j] > T || (all_eq && k8[j] == T)) emit(ie + j * NT);
   }
   for (; ie < len; ie += NT) {
     const uint32_t key = float_key(vals[ie]);
@@ -221,7 +221,8 @@ struct VsArgs {
 constexpr int kVsGather = 8192;  // elements of the largest set kept in LDS, at most
 // Dynamic LDS: [nwords bitmap words][gcap values][gcap positions], gcap = the largest budget
 // selected from the whole array (at most kVsGather): the LDS of a workgroup is then sized
-// for the grid's budgets, and two workgroups share a compute unit for budgets up to ~8K.
+// for the grid's budgets (two workgroups share a compute unit for budgets up to about 6K at
+// n = 128K, where the bitmap takes 16 KB).
 __global__ void __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(8, 8))) vs_select_kernel(const VsArgs a) {
   constexpr int NT = 1024;
   extern __shared__ uint32_t sDyn[];
