@@ -577,11 +577,12 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
             masked_add16(cs, (uint32_t)(M >> 32), x[1]);
             return cs;
           };
-          // mass of the keys j >= lo: whole tile, none, or element-wise (wave-uniform choice)
+          // mass of the keys j >= lo: whole tile, none, or element-wise.  The element-wise sums
+          // run only when some lane's boundary lies inside the tile (rows spread over a
+          // segment mostly split into whole-tile and empty lanes).
           auto from = [&](int lo) __attribute__((always_inline)) -> float {
             const bool all = lo <= k0, nil = lo > k0 + 63;
-            if (__ballot(all) == ~0ull) return tsum;
-            if (__ballot(nil) == ~0ull) return 0.f;
+            if (__ballot(!all && !nil) == 0ull) return all ? tsum : 0.f;
             const float m = masked(~prefix_mask(lo - k0) >> (4 * hh));
             return all ? tsum : nil ? 0.f : m;
           };

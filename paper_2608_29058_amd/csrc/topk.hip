@@ -284,11 +284,15 @@ __global__ void __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(8, 8)
 }
 
 // select_top for one wave whose elements are held in registers: key[c] is the key of element
-// c * 64 + lane (elements >= len are ignored); emit(i, key) for each selected element.  The
-// same selection as select_top<64> over the same keys: radix select over 8-bit digits with
-// one 256-bin histogram, then the lowest positions among keys equal to the threshold.
+// c * 64 + lane (elements >= len are ignored); emit(i, key) for each selected element.  Radix
+// select over 8-bit digits with one 256-bin histogram, then the lowest positions among keys
+// equal to the threshold.  With cap > K the caller orders what it gets and keeps the first K:
+// the passes then stop as soon as the elements above the digit bin holding the K-th key and
+// that bin together number at most cap, and every one of them is emitted (the top K and the
+// rest of that bin; at most cap calls of emit).  With cap = K it emits exactly the top K.
 template <int NV, typename F>
-__device__ void select_top_regs(const uint32_t (&key)[NV], int len, int K, int *sHist, int *sBcast, F emit) {
+__device__ void select_top_regs(const uint32_t (&key)[NV], int len, int K, int cap, int *sHist, int *sBcast,
+                                F emit) {
   const int l = (int)(threadIdx.x & 63u);
   if (K <= 0) return;
   if (len <= K) {
@@ -341,6 +345,15 @@ __device__ void select_top_regs(const uint32_t (&key)[NV], int len, int K, int *
     krem = sBcast[1];
     neq = sBcast[2];
     gsync<64>();
+    // K - krem elements lie in higher bins, neq in the bin of the K-th key: when they fit in
+    // cap, they are all the keys whose leading digits are at least prefix's (key >= prefix,
+    // the lower digits of prefix being zero)
+    if (byte > 0 && K - krem + neq <= cap) {
+#pragma unroll
+      for (int c = 0; c < NV; ++c)
+        if (c * 64 + l < len && key[c] >= prefix) emit(c * 64 + l, key[c]);
+      return;
+    }
   }
   const uint32_t T = prefix;
   const int take = krem;
@@ -394,7 +407,8 @@ __global__ void __launch_bounds__(256) bs_select_kernel(const BsArgs a) {
   uint32_t key[NV];
 #pragma unroll
   for (int c = 0; c < NV; ++c) key[c] = c * 64 + l < bq ? float_key(vals[c * 64 + l]) : 0u;
-  select_top_regs<NV>(key, bq, K, sHist, sBcast, [&](int i, uint32_t kv) {
+  // up to SP candidates are emitted; the sort below orders them and the first K are kept
+  select_top_regs<NV>(key, bq, K, SP, sHist, sBcast, [&](int i, uint32_t kv) {
     const int p = atomicAdd(&sCntA[w], 1);
     sKey[p] = ((unsigned long long)kv << 32) | (unsigned long long)(0xffffffffu - (uint32_t)i);
   });
