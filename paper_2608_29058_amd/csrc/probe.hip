@@ -9,8 +9,9 @@
 //   pass 3  (coverage) for every sampled row, with its own running max (online
 //           normalisation): the row statistics, m_i(c) = sum_{j in S_i(c)} a_ij for every
 //           candidate c, the 64-key block entropy and the local-band mass.
-// Logit tiles are bf16 MFMA products (S^T = K_tile x Q_rows^T, one lane per sampled row),
-// statistics fp32.  Every cross-workgroup reduction goes through per-chunk partials
+// Logit tiles are bf16 MFMA products, statistics fp32: S^T = K_tile x Q_rows^T (a lane per
+// sampled row) in passes 1 and 3, S = Q_rows x K_tile^T (a lane per key) in pass 2, whose
+// column sums are then in-lane adds.  Every cross-workgroup reduction goes through per-chunk partials
 // summed in a fixed order, so results are deterministic.
 //
 // Block-mean estimator: qbar/kbar = means of 64-row blocks (last block over its actual
@@ -28,8 +29,8 @@ constexpr int kRange = 1024;        // keys per workgroup range in the three pas
 constexpr int kMaxCand = 16;
 constexpr int kPrefVs = 3;   // vertical-slash candidates whose bitmap words are prefetched
 constexpr int kPrefBs = 3;   // block-sparse candidates whose selection words are prefetched
-constexpr int kSkew = 84;    // row stride of the skewed 16-row probability tile (79 columns + pad;
-                             // row r at bank offset 19 r: the tile's writes are conflict-free)
+constexpr int kSkew = 89;    // row stride of the skewed 16-row probability tile (79 columns + pad;
+                             // rows r and r + 4, written by the two lane halves, 32 banks apart)
 
 struct ProbeUnit {
   int head, s0, s1, nrows;  // nrows = sampled rows actually present
@@ -309,26 +310,38 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
 
     int xr[2], row[2];
     u32x4 qf[2][KS];
-    float nmc[2];
-    bool isR[2];
+    // scores pass: the logit tile is S = Q K^T (a lane holds one key and the 16 rows
+    // 8 (r / 4) + 4 hh + r % 4 of its accumulator), with per element the row's constant
+    // -(row_max log2 e + log2 row_sum), -inf for rows that are absent or not recent
+    float nmv[2][16];
+    bool anyR[2];
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
       const int b = s ? b1 : b0;
       xr[s] = nrows - 32 * (nrb - b) + l32;
       row[s] = sRows[s][l32];
       const bool ok = u >= 0 && row[s] >= 0;
-      const long long rofs = (long long)u * a.rmax + xr[s];
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         qf[s][ks] = u32x4{0u, 0u, 0u, 0u};
         if (ok) qf[s][ks] = load8<InT>(Qp + (long long)row[s] * a.sq_t + 16 * ks + 8 * hh);
       }
-      nmc[s] = -INFINITY;
-      isR[s] = false;
       if constexpr (MODE == M_SCORES) {
-        // a_ij = exp2(l_ij * c - (row_max * log2 e + log2 row_sum))
-        if (ok) nmc[s] = -a.row_max[rofs] * kLog2e - __builtin_amdgcn_logf(a.row_sum[rofs]);
-        isR[s] = ok && xr[s] >= nrows - U0.nR;
+        // a_ij = exp2(l_ij * c - (row_max * log2 e + log2 row_sum)); recent rows are the last
+        // ones of the list, so the block holds one when its last row is recent
+        const int xb = nrows - 32 * (nrb - b);
+        anyR[s] = u >= 0 && b >= 0 && xb + 31 >= nrows - U0.nR;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int rho = 8 * (r >> 2) + 4 * hh + (r & 3);
+          const int rw = sRows[s][rho];
+          float v = -INFINITY;
+          if (u >= 0 && rw >= 0 && xb + rho >= nrows - U0.nR) {
+            const long long o = (long long)u * a.rmax + xb + rho;
+            v = -a.row_max[o] * kLog2e - __builtin_amdgcn_logf(a.row_sum[o]);
+          }
+          nmv[s][r] = v;
+        }
       }
     }
     float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
@@ -437,7 +450,10 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
       for (int f = 0; f < KPF; ++f) kb[f] = kread(f);
 #pragma unroll
       for (int f = 0; f < 2 * KS; ++f) {
-        sacc[f & 1] = mfma32(kb[f % KPF], qf[s][f >> 1], sacc[f & 1]);
+        if constexpr (MODE == M_SCORES)  // S = Q K^T
+          sacc[f & 1] = mfma32(qf[s][f >> 1], kb[f % KPF], sacc[f & 1]);
+        else  // S^T = K Q^T
+          sacc[f & 1] = mfma32(kb[f % KPF], qf[s][f >> 1], sacc[f & 1]);
         if (f + KPF < 2 * KS) kb[f % KPF] = kread(f + KPF);
       }
       // keep that order: under register pressure the scheduler would otherwise put each read
@@ -453,6 +469,67 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
     auto block_tile = [&](const f32x16 (&sacc)[2], int k0, int s, const Pref &f) __attribute__((always_inline)) {
       const int rmx = s ? rmax1 : rmax0;
       if (u < 0 || rmx < k0) return;  // block absent or entirely before the tile
+      if constexpr (MODE == M_SCORES) {
+        if (!anyR[s]) return;
+        // element (mb, r): row rho = 8 (r / 4) + 4 hh + r % 4 of the block, key k0 + 32 mb + l32
+        float x[2][16];
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) x[mb][r] = sacc[mb][r];
+        // keys after a row: only where the block's first recent row (at least rmx - 31; recent
+        // rows are consecutive and end at the block's last row) lies before the tile's end
+        if (rmx - 31 < k0 + 63) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int ir = sRows[s][8 * (r >> 2) + 4 * hh + (r & 3)];
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb)
+              if (k0 + 32 * mb + l32 > ir) x[mb][r] = -INFINITY;
+          }
+        }
+        float cA[2] = {0.f, 0.f};  // this lane's rows of key columns l32 and 32 + l32
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            x[mb][r] = __builtin_amdgcn_exp2f(fmaf(x[mb][r], c, nmv[s][r]));
+            cA[mb] += x[mb][r];
+          }
+        // column sums: lane half 0 completes key l32, half 1 key 32 + l32, with the other
+        // half's 16 rows of that key
+        const float give = hh ? cA[0] : cA[1];
+        const float cs = (hh ? cA[1] : cA[0]) + __shfl_xor(give, 32);
+        sCol[k0 - c0 + 32 * hh + l32] += cs;
+        // diagonals through the skewed tile, 16 rows at a time: row rho' = rho - 16 h, key kk
+        // -> sD[rho'][kk - rho' + 15], so that a diagonal (kk - rho' constant) is a column of
+        // sD; entries no key maps to stay zero.  Recent rows are consecutive and end at row
+        // 31, so the last row of half h is rmx - 16 (1 - h) and column e holds diagonal
+        // t = (that row - k0) - e.  Elements r in [8 h, 8 h + 8) are the lane's rows of half h.
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+#pragma unroll
+          for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+            for (int r = 8 * h; r < 8 * h + 8; ++r) {
+              const int rp = 8 * ((r >> 2) & 1) + 4 * hh + (r & 3);
+              sD[rp][32 * mb + l32 - rp + 15] = x[mb][r];
+            }
+          wave_sync();
+          float d0 = 0.f, d1 = 0.f;
+          const int e1 = min(64 + lane, kSkew - 1);
+#pragma unroll
+          for (int rr = 0; rr < 16; ++rr) {
+            d0 += sD[rr][lane];
+            d1 += sD[rr][e1];
+          }
+          const int tb = rmx - 16 * (1 - h) - k0 - dbase;
+          if (tb - lane >= 0 && tb - lane < dw) sDg[tb - lane] += d0;
+          if (lane < 15 && tb - 64 - lane >= 0 && tb - 64 - lane < dw) sDg[tb - 64 - lane] += d1;
+          wave_sync();
+        }
+        return;
+      }
       const int i = row[s];
       // keys after the row: a row before the tile sees none of it; a row inside the tile
       // (some lane of the wave) masks element-wise
@@ -492,40 +569,37 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
           for (int r = 0; r < 16; ++r) ps += __builtin_amdgcn_exp2f(fmaf(x[mb][r], c, nm));
         l_run[s] = l_run[s] * __builtin_amdgcn_exp2f((m_run[s] - m_use) * c) + ps;
         m_run[s] = m_new;
-      } else {
-        float nm = none ? -INFINITY : nmc[s];
-        if constexpr (MODE == M_COVER) {
-          // online normalisation: the row's running max over this range (both halves of the
-          // row see the same max); raising it rescales every accumulator of the row, and
-          // S = sum B log B becomes alpha (S + log(alpha) Z) for alpha = exp(m_old - m_new)
-          float mx = -INFINITY;
+      } else {  // M_COVER
+        // online normalisation: the row's running max over this range (both halves of the
+        // row see the same max); raising it rescales every accumulator of the row, and
+        // S = sum B log B becomes alpha (S + log(alpha) Z) for alpha = exp(m_old - m_new)
+        float mx = -INFINITY;
 #pragma unroll
-          for (int mb = 0; mb < 2; ++mb)
+        for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, x[mb][r]);
-          if (none) mx = -INFINITY;
-          mx = fmaxf(mx, __shfl_xor(mx, 32));
-          if (__ballot(mx > m_run[s]) != 0ull) {
-            const float zt = l_run[s] + __shfl_xor(l_run[s], 32);
-            if (mx > m_run[s]) {
-              if (m_run[s] != -INFINITY) {  // else every accumulator is still zero
-                const float la = (m_run[s] - mx) * c;  // log2 alpha
-                const float al = __builtin_amdgcn_exp2f(la);
-                ent[s] = al * (ent[s] + la * kLn2 * zt);
-                l_run[s] *= al;
-                loc[s] *= al;
+          for (int r = 0; r < 16; ++r) mx = fmaxf(mx, x[mb][r]);
+        if (none) mx = -INFINITY;
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        if (__ballot(mx > m_run[s]) != 0ull) {
+          const float zt = l_run[s] + __shfl_xor(l_run[s], 32);
+          if (mx > m_run[s]) {
+            if (m_run[s] != -INFINITY) {  // else every accumulator is still zero
+              const float la = (m_run[s] - mx) * c;  // log2 alpha
+              const float al = __builtin_amdgcn_exp2f(la);
+              ent[s] = al * (ent[s] + la * kLn2 * zt);
+              l_run[s] *= al;
+              loc[s] *= al;
 #pragma unroll
-                for (int q = 0; q < NCV; ++q) cov[s][q] *= al;
+              for (int q = 0; q < NCV; ++q) cov[s][q] *= al;
 #pragma unroll
-                for (int k = 0; k < kPrefVs; ++k) covv[s][k] *= al;
+              for (int k = 0; k < kPrefVs; ++k) covv[s][k] *= al;
 #pragma unroll
-                for (int k = 0; k < kPrefBs; ++k) covb[s][k] *= al;
-              }
-              m_run[s] = mx;
+              for (int k = 0; k < kPrefBs; ++k) covb[s][k] *= al;
             }
+            m_run[s] = mx;
           }
-          nm = none ? -INFINITY : -m_run[s] * c;
         }
+        const float nm = none ? -INFINITY : -m_run[s] * c;
         float tsum = 0.f;
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb)
@@ -534,102 +608,68 @@ __global__ void __launch_bounds__(256, 2) probe_range_kernel(const ProbeArgs a) 
             x[mb][r] = __builtin_amdgcn_exp2f(fmaf(x[mb][r], c, nm));
             tsum += x[mb][r];
           }
-        if constexpr (MODE == M_SCORES) {
-          if (__ballot(isR[s]) == 0ull) return;
-          // skewed tile, one half of the block's rows at a time: row lane r (r = l32 - 16 h in
-          // half h), key kk -> sD[r][kk - r + 15].  Key columns and diagonals (kk - r
-          // constant) of the half are then both plain columns of sD; entries no key maps to
-          // stay zero.  Recent rows are consecutive and end at lane 31, so the last row of
-          // half h is rmx - 16 (1 - h) and diagonal column e holds t = (that row - k0) - e.
+        const float bt = tsum + __shfl_xor(tsum, 32);  // mass of the row in this 64-key block
+        if (bt > 0.f) ent[s] += bt * logf(bt);
+        l_run[s] += tsum;
+        // kept mass of a 64-bit key mask (bits of this lane's keys after the half shift)
+        auto masked = [&](uint64_t M) __attribute__((always_inline)) -> float {
           float cs = 0.f;
+          masked_add16(cs, (uint32_t)M, x[0]);
+          masked_add16(cs, (uint32_t)(M >> 32), x[1]);
+          return cs;
+        };
+        // mass of the keys j >= lo: whole tile, none, or element-wise.  The element-wise sums
+        // run only when some lane's boundary lies inside the tile (rows spread over a
+        // segment mostly split into whole-tile and empty lanes).
+        auto from = [&](int lo) __attribute__((always_inline)) -> float {
+          const bool all = lo <= k0, nil = lo > k0 + 63;
+          if (__ballot(!all && !nil) == 0ull) return all ? tsum : 0.f;
+          const float m = masked(~prefix_mask(lo - k0) >> (4 * hh));
+          return all ? tsum : nil ? 0.f : m;
+        };
+        loc[s] += from(i - a.local_w + 1);
+        const int kt = k0 >> 6;
+        const int tl = (k0 - c0) >> 5;  // column word of the tile within the range
 #pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            if ((l32 >> 4) == h) {
-              const int r16 = l32 & 15;
-#pragma unroll
-              for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) sD[r16][acc_key(mb, r, hh) - r16 + 15] = isR[s] ? x[mb][r] : 0.f;
-            }
-            wave_sync();
-            float d0 = 0.f, d1 = 0.f;
-            const int e1 = min(64 + lane, kSkew - 1);
-#pragma unroll
-            for (int rr = 0; rr < 16; ++rr) {
-              cs += sD[rr][lane - rr + 15];
-              d0 += sD[rr][lane];
-              d1 += sD[rr][e1];
-            }
-            const int tb = rmx - 16 * (1 - h) - k0 - dbase;
-            if (tb - lane >= 0 && tb - lane < dw) sDg[tb - lane] += d0;
-            if (lane < 15 && tb - 64 - lane >= 0 && tb - 64 - lane < dw) sDg[tb - 64 - lane] += d1;
-            wave_sync();
+        for (int k = 0; k < kPrefVs; ++k) {
+          if (k >= a.nvs_pref) break;
+          uint64_t md;
+          if (stage) {  // absent rows (-1) read the first row's window, unused
+            const int dpos = (i >= 0 ? i : rlo) - k0 - 63;
+            const uint32_t *dw = &sDW[wave][k][(dpos >> 5) - dw0];
+            md = __builtin_bitreverse64(win_bits(Win3{dw[0], dw[1], dw[2]}, dpos));
+          } else {
+            const int dpos = max(i, 0) - k0 - 63;
+            md = __builtin_bitreverse64(win_bits(win_fix(f.wd[s][k], a.nwords, dpos), dpos));
           }
-          sCol[k0 - c0 + lane] += cs;
-        } else {  // M_COVER
-          const float bt = tsum + __shfl_xor(tsum, 32);  // mass of the row in this 64-key block
-          if (bt > 0.f) ent[s] += bt * logf(bt);
-          l_run[s] += tsum;
-          // kept mass of a 64-bit key mask (bits of this lane's keys after the half shift)
-          auto masked = [&](uint64_t M) __attribute__((always_inline)) -> float {
-            float cs = 0.f;
-            masked_add16(cs, (uint32_t)M, x[0]);
-            masked_add16(cs, (uint32_t)(M >> 32), x[1]);
-            return cs;
-          };
-          // mass of the keys j >= lo: whole tile, none, or element-wise.  The element-wise sums
-          // run only when some lane's boundary lies inside the tile (rows spread over a
-          // segment mostly split into whole-tile and empty lanes).
-          auto from = [&](int lo) __attribute__((always_inline)) -> float {
-            const bool all = lo <= k0, nil = lo > k0 + 63;
-            if (__ballot(!all && !nil) == 0ull) return all ? tsum : 0.f;
-            const float m = masked(~prefix_mask(lo - k0) >> (4 * hh));
-            return all ? tsum : nil ? 0.f : m;
-          };
-          loc[s] += from(i - a.local_w + 1);
-          const int kt = k0 >> 6;
-          const int tl = (k0 - c0) >> 5;  // column word of the tile within the range
+          const uint32_t mv0 = (uint32_t)__builtin_amdgcn_readlane((int)vmv[k], tl);
+          const uint32_t mv1 = (uint32_t)__builtin_amdgcn_readlane((int)vmv[k], tl + 1);
+          const uint64_t mv = (uint64_t)mv0 | ((uint64_t)mv1 << 32);
+          const uint64_t m = (md | mv) >> (4 * hh);
+          if (__ballot(m != 0ull) != 0ull) covv[s][k] += masked(m);  // wave-uniform skip
+        }
 #pragma unroll
-          for (int k = 0; k < kPrefVs; ++k) {
-            if (k >= a.nvs_pref) break;
-            uint64_t md;
-            if (stage) {  // absent rows (-1) read the first row's window, unused
-              const int dpos = (i >= 0 ? i : rlo) - k0 - 63;
-              const uint32_t *dw = &sDW[wave][k][(dpos >> 5) - dw0];
-              md = __builtin_bitreverse64(win_bits(Win3{dw[0], dw[1], dw[2]}, dpos));
-            } else {
-              const int dpos = max(i, 0) - k0 - 63;
-              md = __builtin_bitreverse64(win_bits(win_fix(f.wd[s][k], a.nwords, dpos), dpos));
-            }
-            const uint32_t mv0 = (uint32_t)__builtin_amdgcn_readlane((int)vmv[k], tl);
-            const uint32_t mv1 = (uint32_t)__builtin_amdgcn_readlane((int)vmv[k], tl + 1);
-            const uint64_t mv = (uint64_t)mv0 | ((uint64_t)mv1 << 32);
-            const uint64_t m = (md | mv) >> (4 * hh);
-            if (__ballot(m != 0ull) != 0ull) covv[s][k] += masked(m);  // wave-uniform skip
-          }
+        for (int k = 0; k < kPrefBs; ++k) {
+          if (k >= a.nbs_pref) break;
+          if ((bwr[s][k] >> (kt & 31)) & 1u) covb[s][k] += tsum;
+        }
 #pragma unroll
-          for (int k = 0; k < kPrefBs; ++k) {
-            if (k >= a.nbs_pref) break;
-            if ((bwr[s][k] >> (kt & 31)) & 1u) covb[s][k] += tsum;
-          }
-#pragma unroll
-          for (int q = 0; q < NCV; ++q) {
-            if (q >= a.ncov) break;
-            const CandDev cd = a.cand[a.cov_cand[q]];
-            if (cd.fam == RS_ASHAPE) {
-              const float sink = k0 + 63 < cd.a ? tsum : k0 >= cd.a ? 0.f : masked(prefix_mask(cd.a - k0) >> (4 * hh));
-              // window keys j >= i - b + 1 that are not sink keys
-              cov[s][q] += sink + from(max(i - cd.b + 1, cd.a));
-            } else if (!GEN) {
-            } else if (cd.fam == RS_VSLASH) {
-              const long long vr = ((long long)u * a.ncand_vs + cd.cl) * a.nwords;
-              const uint64_t md = __builtin_bitreverse64(bits64_at(a.vs_dbits + vr, a.nwords, i - k0 - 63));
-              const uint64_t mv = bits64_at(a.vs_vbits + vr, a.nwords, k0);
-              cov[s][q] += masked((md | mv) >> (4 * hh));
-            } else if (cd.fam == RS_BSPARSE) {
-              const long long br = (((long long)uhead * a.ncand_bs + cd.cl) * a.nb + (max(i, 0) >> 6)) * a.nbw;
-              if ((a.bs_bits[br + (kt >> 5)] >> (kt & 31)) & 1u) cov[s][q] += tsum;
-            }
+        for (int q = 0; q < NCV; ++q) {
+          if (q >= a.ncov) break;
+          const CandDev cd = a.cand[a.cov_cand[q]];
+          if (cd.fam == RS_ASHAPE) {
+            const float sink = k0 + 63 < cd.a ? tsum : k0 >= cd.a ? 0.f : masked(prefix_mask(cd.a - k0) >> (4 * hh));
+            // window keys j >= i - b + 1 that are not sink keys
+            cov[s][q] += sink + from(max(i - cd.b + 1, cd.a));
+          } else if (!GEN) {
+          } else if (cd.fam == RS_VSLASH) {
+            const long long vr = ((long long)u * a.ncand_vs + cd.cl) * a.nwords;
+            const uint64_t md = __builtin_bitreverse64(bits64_at(a.vs_dbits + vr, a.nwords, i - k0 - 63));
+            const uint64_t mv = bits64_at(a.vs_vbits + vr, a.nwords, k0);
+            cov[s][q] += masked((md | mv) >> (4 * hh));
+          } else if (cd.fam == RS_BSPARSE) {
+            const long long br = (((long long)uhead * a.ncand_bs + cd.cl) * a.nb + (max(i, 0) >> 6)) * a.nbw;
+            if ((a.bs_bits[br + (kt >> 5)] >> (kt & 31)) & 1u) cov[s][q] += tsum;
           }
         }
       }
