@@ -957,13 +957,15 @@ __global__ void __launch_bounds__(256) block_pool_kernel(const InT *x, long long
 }
 
 // L[h][bq][bk] = qbar . kbar * scale for bk <= bq; 128 x 128 output tiles, each wave a 64 x 64
-// quarter as 2 x 2 fp32 MFMA blocks (v_mfma_f32_32x32x2_f32: fp32 products, fp32 sums).  The
-// head dimension goes through LDS in chunks of 32; within a group of 8 dims, lanes 0-31 take
-// dims 0-3 and lanes 32-63 dims 4-7 over four k-steps (any assignment of dims to k-steps is
-// the same sum, as long as A and B use the same one).
+// quarter as 2 x 2 bf16 MFMA blocks (v_mfma_f32_32x32x16_bf16).  Each fp32 mean x is split into
+// hi = bf16(x) and lo = bf16(x - hi) as it is staged in LDS, and a product takes
+// hi.hi + hi.lo + lo.hi with fp32 sums: the dropped lo.lo and the rounding of lo are below
+// 2^-16 of |q_d k_d|, so the result is within ~1e-5 of the fp64 dot product on logits of a few
+// units, at three bf16 products per k-step instead of eight fp32 ones.  The head dimension
+// goes through LDS in chunks of 32.
 __global__ void __launch_bounds__(256) block_logits_kernel(const float *qbar, const float *kbar, int nb, int d,
                                                            int group, float scale, float *lbs) {
-  constexpr int TB = 128, KC = 32, LD = KC + 4;
+  constexpr int TB = 128, KC = 32, LD = KC + 8;  // bf16 row of a chunk, padded to 80 bytes
   const int h = blockIdx.y;
   // decode lower-triangular tile index
   int tq = 0;
@@ -973,7 +975,7 @@ __global__ void __launch_bounds__(256) block_logits_kernel(const float *qbar, co
     ++tq;
   }
   const int tk = t;
-  __shared__ __align__(16) float sq[TB][LD], sk[TB][LD];
+  __shared__ __align__(16) bf16 sqh[TB][LD], sql[TB][LD], skh[TB][LD], skl[TB][LD];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wr = (wave >> 1) * 64, wc = (wave & 1) * 64;  // this wave's quarter
   const int l32 = lane & 31, hh = lane >> 5;
@@ -986,31 +988,68 @@ __global__ void __launch_bounds__(256) block_logits_kernel(const float *qbar, co
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
   const float *qb = qbar + (long long)h * nb * d;
   const float *kb = kbar + (long long)(h / group) * nb * d;
-  for (int d0 = 0; d0 < d; d0 += KC) {
-    // 128 rows x 32 dims of each operand: 1024 float4, 4 per thread
+  // four floats -> their hi and lo bf16 parts (two dwords each)
+  auto split4 = [](f32x4 v, u32x2 &hi, u32x2 &lo) {
+    hi[0] = pack_bf16x2(v[0], v[1]);
+    hi[1] = pack_bf16x2(v[2], v[3]);
+    f32x4 r;
+    r[0] = v[0] - __builtin_bit_cast(float, hi[0] << 16);
+    r[1] = v[1] - __builtin_bit_cast(float, hi[0] & 0xffff0000u);
+    r[2] = v[2] - __builtin_bit_cast(float, hi[1] << 16);
+    r[3] = v[3] - __builtin_bit_cast(float, hi[1] & 0xffff0000u);
+    lo[0] = pack_bf16x2(r[0], r[1]);
+    lo[1] = pack_bf16x2(r[2], r[3]);
+  };
+  // 128 rows x 32 dims of each operand per chunk: 1024 float4, 4 per thread; the next chunk is
+  // loaded into registers while the current one is multiplied
+  f32x4 vq[4], vk[4];
+  auto load_chunk = [&](int d0) {
 #pragma unroll
-    for (int x0 = 0; x0 < TB * KC / 4; x0 += 256) {
-      const int x = x0 + tid, r = x / (KC / 4), c4 = x % (KC / 4);
+    for (int e = 0; e < 4; ++e) {
+      const int x = 256 * e + tid, r = x / (KC / 4), c4 = x % (KC / 4);
       const int bq = tq * TB + r, bk = tk * TB + r;
-      const f32x4 zq = {0.f, 0.f, 0.f, 0.f};
-      *(f32x4 *)&sq[r][4 * c4] = bq < nb ? *(const f32x4 *)&qb[(long long)bq * d + d0 + 4 * c4] : zq;
-      *(f32x4 *)&sk[r][4 * c4] = bk < nb ? *(const f32x4 *)&kb[(long long)bk * d + d0 + 4 * c4] : zq;
+      const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+      vq[e] = bq < nb ? *(const f32x4 *)&qb[(long long)bq * d + d0 + 4 * c4] : z;
+      vk[e] = bk < nb ? *(const f32x4 *)&kb[(long long)bk * d + d0 + 4 * c4] : z;
+    }
+  };
+  static_assert(TB * KC / 4 == 4 * 256, "four float4 of each operand per thread");
+  load_chunk(0);
+  for (int d0 = 0; d0 < d; d0 += KC) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int x = 256 * e + tid, r = x / (KC / 4), c4 = x % (KC / 4);
+      u32x2 hq, lq, hk, lk;
+      split4(vq[e], hq, lq);
+      split4(vk[e], hk, lk);
+      *(u32x2 *)&sqh[r][4 * c4] = hq;
+      *(u32x2 *)&sql[r][4 * c4] = lq;
+      *(u32x2 *)&skh[r][4 * c4] = hk;
+      *(u32x2 *)&skl[r][4 * c4] = lk;
     }
     __syncthreads();
+    if (d0 + KC < d) load_chunk(d0 + KC);
 #pragma unroll
-    for (int g = 0; g < KC / 8; ++g) {
-      f32x4 a4[2], b4[2];
+    for (int ks = 0; ks < KC / 16; ++ks) {
+      u32x4 ah[2], al[2], bh[2], bl[2];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) a4[i] = *(const f32x4 *)&sq[wr + 32 * i + l32][8 * g + 4 * hh];
+      for (int i = 0; i < 2; ++i) {
+        ah[i] = *(const u32x4 *)&sqh[wr + 32 * i + l32][16 * ks + 8 * hh];
+        al[i] = *(const u32x4 *)&sql[wr + 32 * i + l32][16 * ks + 8 * hh];
+      }
 #pragma unroll
-      for (int j = 0; j < 2; ++j) b4[j] = *(const f32x4 *)&sk[wc + 32 * j + l32][8 * g + 4 * hh];
+      for (int j = 0; j < 2; ++j) {
+        bh[j] = *(const u32x4 *)&skh[wc + 32 * j + l32][16 * ks + 8 * hh];
+        bl[j] = *(const u32x4 *)&skl[wc + 32 * j + l32][16 * ks + 8 * hh];
+      }
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
+      for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-          for (int j = 0; j < 2; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4[i][e], b4[j][e], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < 2; ++j) {
+          acc[i][j] = mfma32(al[i], bh[j], acc[i][j]);
+          acc[i][j] = mfma32(ah[i], bl[j], acc[i][j]);
+          acc[i][j] = mfma32(ah[i], bh[j], acc[i][j]);
+        }
     }
     __syncthreads();
   }
