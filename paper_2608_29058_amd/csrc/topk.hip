@@ -69,9 +69,12 @@ __device__ int block_incl_scan(int v, int *sWave, int *tot) {
 // how many elements equal to T are taken and how many there are.  Requires len > K >= 1.
 // sHist holds one 256-bin histogram per wave of the group (values of similar magnitude share
 // their leading digits: one histogram for all waves would serialise their atomics).
+// Returns true when it stopped early instead: the elements above the digit bin holding the
+// K-th key and that bin together number at most cap, and T is then the bin's leading digits
+// with zero lower digits (they are exactly the keys >= T).
 template <int NT>
-__device__ void radix_select(const float *vals, int len, int K, uint32_t *T_out, int *take_out, int *eq_out,
-                             int *sHist, int *sBcast) {
+__device__ bool radix_select(const float *vals, int len, int K, int cap, uint32_t *T_out, int *take_out,
+                             int *eq_out, int *sHist, int *sBcast) {
   constexpr int NWV = NT / 64;
   uint32_t prefix = 0, maskhi = 0;
   int krem = K;
@@ -135,14 +138,24 @@ __device__ void radix_select(const float *vals, int len, int K, uint32_t *T_out,
     krem = sBcast[1];
     *eq_out = sBcast[2];
     gsync<NT>();
+    if (byte > 0 && K - krem + *eq_out <= cap) {
+      *T_out = prefix;
+      *take_out = krem;
+      return true;
+    }
   }
   *T_out = prefix;
   *take_out = krem;
+  return false;
 }
 
 // Calls emit(i) for each selected element index of vals[0, len) (top K in the total order).
+// With cap > K the radix passes may stop early: emit is then called for every element whose
+// key shares the leading digits of the K-th key or is above them (at most cap elements, the
+// top K among them), and the caller selects the top K from those.
 template <int NT, typename F>
-__device__ void select_top(const float *vals, int len, int K, int *sHist, int *sBcast, int *sWave, F emit) {
+__device__ void select_top(const float *vals, int len, int K, int *sHist, int *sBcast, int *sWave, F emit,
+                           int cap = 0) {
   if (K <= 0) return;
   if (len <= K) {
     for (int i = gtid<NT>(); i < len; i += NT) emit(i);
@@ -150,7 +163,20 @@ __device__ void select_top(const float *vals, int len, int K, int *sHist, int *s
   }
   uint32_t T;
   int take, neq;
-  radix_select<NT>(vals, len, K, &T, &take, &neq, sHist, sBcast);
+  if (radix_select<NT>(vals, len, K, max(cap, K), &T, &take, &neq, sHist, sBcast)) {
+    int ie = gtid<NT>();
+    for (; ie + 7 * NT < len; ie += 8 * NT) {
+      uint32_t k8[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) k8[j] = float_key(vals[ie + j * NT]);
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (k8[j] >= T) emit(ie + j * NT);
+    }
+    for (; ie < len; ie += NT)
+      if (float_key(vals[ie]) >= T) emit(ie);
+    return;
+  }
   // every key equal to T is taken when there are no more of them than needed (the usual case)
   const bool all_eq = take == neq;
   int ie = gtid<NT>();
@@ -216,13 +242,15 @@ struct VsArgs {
 };
 
 // grid: (2, nunits); blockIdx.x = array (0: V from col, 1: D from diag).  Budgets of the family
-// are nested prefixes of one ranking, so the largest budget is selected from the whole array
-// and every smaller one from the largest set (gathered, in ascending position, into LDS).
-constexpr int kVsGather = 8192;  // elements of the largest set kept in LDS, at most
-// Dynamic LDS: [nwords bitmap words][gcap values][gcap positions], gcap = the largest budget
-// selected from the whole array (at most kVsGather): the LDS of a workgroup is then sized
-// for the grid's budgets (two workgroups share a compute unit for budgets up to about 6K at
-// n = 128K, where the bitmap takes 16 KB).
+// are nested prefixes of one ranking: a superset of the largest set is taken from the whole
+// array (the radix passes stop once the keys sharing the leading digits of its last key fit
+// the gather, usually after two of the four passes), gathered in ascending position into LDS,
+// and every budget is selected from it.
+constexpr int kVsGather = 8192;  // elements kept in LDS, at most
+// Dynamic LDS: [nwords bitmap words][gcap values][gcap positions], gcap = twice the largest
+// budget selected from the whole array (at most kVsGather): the LDS of a workgroup is then
+// sized for the grid's budgets (two workgroups share a compute unit for budgets up to about
+// 3K at n = 128K, where the bitmap takes 16 KB).
 __global__ void __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(8, 8))) vs_select_kernel(const VsArgs a) {
   constexpr int NT = 1024;
   extern __shared__ uint32_t sDyn[];
@@ -241,15 +269,17 @@ __global__ void __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(8, 8)
   for (int c = 1; c < a.ncand_vs; ++c)
     if (budget(c) > budget(cmax)) cmax = c;
   const int kmax = budget(cmax);
-  // largest set: bitmap, then its members in ascending position with their values (when it
-  // fits in LDS; otherwise every budget is selected from the whole array)
+  // a superset of the largest set (at most gcap elements): bitmap, then its members in
+  // ascending position with their values (when the largest set fits in LDS; otherwise every
+  // budget is selected from the whole array)
   const bool gather = kmax <= a.gcap;
   int nmax = 0;
   if (gather) {
     for (int w = threadIdx.x; w < a.nwords; w += NT) sBits[w] = 0u;
     __syncthreads();
-    select_top<NT>(vals, len, kmax, sHist, sBcast, sWave,
-                   [&](int i) { atomicOr(&sBits[(i + off) >> 5], 1u << ((i + off) & 31)); });
+    select_top<NT>(
+        vals, len, kmax, sHist, sBcast, sWave, [&](int i) { atomicOr(&sBits[(i + off) >> 5], 1u << ((i + off) & 31)); },
+        a.gcap);
     __syncthreads();
     nmax = bits_to_list<NT>(sBits, a.nwords, sPos, a.gcap, sWave);
     __syncthreads();
@@ -263,7 +293,7 @@ __global__ void __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(8, 8)
     if (!gather) {
       select_top<NT>(vals, len, budget(c), sHist, sBcast, sWave,
                      [&](int i) { atomicOr(&sBits[(i + off) >> 5], 1u << ((i + off) & 31)); });
-    } else if (c == cmax) {
+    } else if (nmax <= budget(c)) {  // the whole gathered set (the largest set itself)
       for (int x = threadIdx.x; x < nmax; x += NT) atomicOr(&sBits[sPos[x] >> 5], 1u << (sPos[x] & 31));
     } else {
       select_top<NT>(sVal, nmax, budget(c), sHist, sBcast, sWave, [&](int x) {
@@ -284,12 +314,14 @@ __global__ void __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(8, 8)
 }
 
 // select_top for one wave whose elements are held in registers: key[c] is the key of element
-// c * 64 + lane (elements >= len are ignored); emit(i, key) for each selected element.  Radix
+// c * 64 + lane (elements >= len are ignored).  emit(c, take) is called by the whole wave, once
+// per register c and step (take: this lane's element c * 64 + lane is selected there), so that
+// it can place the selected elements with a ballot instead of an LDS counter.  Radix
 // select over 8-bit digits with one 256-bin histogram, then the lowest positions among keys
 // equal to the threshold.  With cap > K the caller orders what it gets and keeps the first K:
 // the passes then stop as soon as the elements above the digit bin holding the K-th key and
 // that bin together number at most cap, and every one of them is emitted (the top K and the
-// rest of that bin; at most cap calls of emit).  With cap = K it emits exactly the top K.
+// rest of that bin; at most cap taken).  With cap = K it takes exactly the top K.
 template <int NV, typename F>
 __device__ void select_top_regs(const uint32_t (&key)[NV], int len, int K, int cap, int *sHist, int *sBcast,
                                 F emit) {
@@ -297,8 +329,7 @@ __device__ void select_top_regs(const uint32_t (&key)[NV], int len, int K, int c
   if (K <= 0) return;
   if (len <= K) {
 #pragma unroll
-    for (int c = 0; c < NV; ++c)
-      if (c * 64 + l < len) emit(c * 64 + l, key[c]);
+    for (int c = 0; c < NV; ++c) emit(c, c * 64 + l < len);
     return;
   }
   uint32_t prefix = 0, maskhi = 0;
@@ -350,8 +381,7 @@ __device__ void select_top_regs(const uint32_t (&key)[NV], int len, int K, int c
     // the lower digits of prefix being zero)
     if (byte > 0 && K - krem + neq <= cap) {
 #pragma unroll
-      for (int c = 0; c < NV; ++c)
-        if (c * 64 + l < len && key[c] >= prefix) emit(c * 64 + l, key[c]);
+      for (int c = 0; c < NV; ++c) emit(c, c * 64 + l < len && key[c] >= prefix);
       return;
     }
   }
@@ -359,8 +389,7 @@ __device__ void select_top_regs(const uint32_t (&key)[NV], int len, int K, int c
   const int take = krem;
   const bool all_eq = take == neq;
 #pragma unroll
-  for (int c = 0; c < NV; ++c)
-    if (c * 64 + l < len && (key[c] > T || (all_eq && key[c] == T))) emit(c * 64 + l, key[c]);
+  for (int c = 0; c < NV; ++c) emit(c, c * 64 + l < len && (key[c] > T || (all_eq && key[c] == T)));
   if (all_eq) return;
   int seen = 0;
 #pragma unroll
@@ -369,7 +398,7 @@ __device__ void select_top_regs(const uint32_t (&key)[NV], int len, int K, int c
     const int f = (c * 64 + l < len && key[c] == T) ? 1 : 0;
     int tot;
     const int in = block_incl_scan<64>(f, nullptr, &tot);
-    if (f && seen + in - 1 < take) emit(c * 64 + l, key[c]);
+    emit(c, f && seen + in - 1 < take);
     seen += tot;
   }
 }
@@ -390,7 +419,7 @@ __global__ void __launch_bounds__(256) bs_select_kernel(const BsArgs a) {
   constexpr int NT = 64;
   constexpr int SP = 256;  // sort capacity (k_max <= 256)
   constexpr int NBW = kMaxN / 64 / 32;
-  __shared__ int sHistA[4][256], sBcastA[4][3], sCntA[4];
+  __shared__ int sHistA[4][256], sBcastA[4][3];
   __shared__ unsigned long long sKeyA[4][SP];
   __shared__ uint32_t sBA[4][NBW];
   const int w = (int)(threadIdx.x >> 6), l = (int)(threadIdx.x & 63u);
@@ -401,16 +430,21 @@ __global__ void __launch_bounds__(256) bs_select_kernel(const BsArgs a) {
   uint32_t *sB = sBA[w];
   const float *vals = a.lbs + (long long)h * ((long long)a.nb * (a.nb + 1) / 2) + (long long)bq * (bq + 1) / 2;
   for (int x = l; x < SP; x += NT) sKey[x] = 0ull;
-  if (l == 0) sCntA[w] = 0;
   gsync<NT>();
   const int K = a.k_max - 1;
   uint32_t key[NV];
 #pragma unroll
   for (int c = 0; c < NV; ++c) key[c] = c * 64 + l < bq ? float_key(vals[c * 64 + l]) : 0u;
-  // up to SP candidates are emitted; the sort below orders them and the first K are kept
-  select_top_regs<NV>(key, bq, K, SP, sHist, sBcast, [&](int i, uint32_t kv) {
-    const int p = atomicAdd(&sCntA[w], 1);
-    sKey[p] = ((unsigned long long)kv << 32) | (unsigned long long)(0xffffffffu - (uint32_t)i);
+  // up to SP candidates are taken, in slots given by a ballot (nsel, the same in every lane,
+  // counts the slots used); the sort below orders them and the first K are kept
+  int nsel_t = 0;
+  select_top_regs<NV>(key, bq, K, SP, sHist, sBcast, [&](int c, bool take) {
+    const uint64_t m = __ballot(take);
+    if (take) {
+      const int p = nsel_t + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+      sKey[p] = ((unsigned long long)key[c] << 32) | (unsigned long long)(0xffffffffu - (uint32_t)(c * 64 + l));
+    }
+    nsel_t += __popcll(m);
   });
   gsync<NT>();
   // bitonic sort, descending, in registers: element e = 4 l + j is key kr[j] of lane l; pairs
@@ -513,7 +547,7 @@ rs_status build_indices_launch(const rs_probe_out *sc, const rs_unit *units, int
     va.vbits = out->vs_vbits; va.dbits = out->vs_dbits;
     int kbig = 0;  // the largest budget selected from a whole array (columns: n_v, diagonals: n_s - 1)
     for (int c = 0; c < nvs; ++c) kbig = std::max(kbig, std::max(va.nv[c], va.ns[c] - 1));
-    va.gcap = std::min(kVsGather, std::max(kbig, 1));
+    va.gcap = std::min(kVsGather, 2 * std::max(kbig, 1));
     const size_t lds = (size_t)out->nwords * sizeof(uint32_t) + (size_t)va.gcap * (sizeof(float) + sizeof(int));
     hipLaunchKernelGGL(vs_select_kernel, dim3(2, nunits), dim3(1024), lds, st, va);
     RS_HIP(hipGetLastError());
