@@ -218,7 +218,9 @@ rs_status rs_unit_table_init(const rs_qkv *qkv, const rs_unit *units, int32_t nu
  * exact softmax statistics over keys [0, s1) of the last ceil(r_rec / 64) * 64 sampled rows
  * (the recent rows among them), the recent-row column and diagonal scores (flag
  * RS_PROBE_ROWS), and the block-mean pooled logits L_bs of every query head (flag
- * RS_PROBE_BLOCKMEAN).
+ * RS_PROBE_BLOCKMEAN; fp32 block means, their dot products taken as hi.hi + hi.lo + lo.hi
+ * of bf16 parts hi = bf16(x), lo = bf16(x - hi): within about 2^-16 of sum_d |q_d k_d| x
+ * scale of the exact product).
  * Coverage mode (idx != NULL, after a scores call on the same `out`; reads its sampled
  * rows): for each unit, candidate and sampled row, m_i(c) = sum of a_ij over the
  * candidate's key set, the subset means, the per-row descriptors (entropy, local mass) and
