@@ -178,6 +178,76 @@ def test_indices_bit_exact_on_gpu_scores(tie):
             assert np.array_equal(rank_g[bq, :m], ranks[bq][:m])
 
 
+@pytest.mark.parametrize("kind", ["few_values", "near_equal", "signed_zeros"])
+def test_selections_on_tied_and_near_equal_scores(kind):
+    """Index sets (Sec. 3.1 rules) built from scores written straight into the probe output:
+    heavy ties, keys that differ only in their last digits, and +0.0 / -0.0 with tiny values.
+    The radix selections stop at every digit on these (early, with the superset ordered or
+    re-selected, or after the last digit with the ordered tie scan); bit-exact against the
+    oracle's rule on the same scores."""
+    import torch
+    n, hq, hkv, d = 65536, 2, 1, 64
+    q, k, v = _inputs(n, hq, hkv, d, 3)
+    units = [(0, 0, n), (1, 0, 40000)]
+    res = _probe(q, k, v, units, (64, 0, 0), _rs.RS_PROBE_ROWS | _rs.RS_PROBE_BLOCKMEAN)
+    pb = res["pb"]
+    r = np.random.default_rng({"few_values": 11, "near_equal": 12, "signed_zeros": 13}[kind])
+
+    def scores(shape):
+        if kind == "few_values":
+            x = r.integers(-4, 5, size=shape) * 0.25
+        elif kind == "near_equal":
+            x = 1.0 + r.integers(0, 400, size=shape) * 2.0 ** -23
+        else:
+            x = r.choice(np.array([0.0, -0.0, 1e-30, -1e-30, 3.0, 2.5]), size=shape, p=[0.4, 0.4, 0.08, 0.08, 0.02, 0.02])
+        return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(pb.col.device)
+
+    pb.col.copy_(scores(tuple(pb.col.shape)))
+    pb.diag.copy_(scores(tuple(pb.diag.shape)))
+    pb.lbs.copy_(scores(tuple(pb.lbs.shape)))
+    grid = [(_rs.RS_DENSE, 0, 0), (_rs.RS_VSLASH, 30, 100), (_rs.RS_VSLASH, 400, 1500), (_rs.RS_VSLASH, 2000, 2048),
+            (_rs.RS_BSPARSE, 3, 64), (_rs.RS_BSPARSE, 100, 64), (_rs.RS_BSPARSE, 200, 64)]
+    g = _rs.make_grid(grid)
+    ib = _rs.IndexBuffers(len(units), n, hq, grid)
+    ws = _rs.workspace(_rs.rs_build_indices_workspace_size(pb, g, len(grid)))
+    _rs.rs_build_indices(pb, res["u"], len(units), g, len(grid), ws, ib)
+    torch.cuda.synchronize()
+    col, diag = pb.col.cpu().numpy().astype(np.float64), pb.diag.cpu().numpy().astype(np.float64)
+    nw = (n + 31) // 32
+    from gpu_helpers import words_of
+    for ui, (h, s0, s1) in enumerate(units):
+        for cl, (_, nv, ns) in enumerate(grid[1:4]):
+            Vr, Dr, _, _ = IX.vs_indices(col[ui], diag[ui], s1, nv, ns)
+            V, D, Vpad, Dpad = _gpu_vs_sets(ib, ui, cl)
+            assert np.array_equal(V, Vr) and np.array_equal(D, Dr), (kind, ui, cl)
+            assert np.all(Vpad == -1) and np.all(Dpad == -1)
+            assert np.array_equal(ib.vs_vbits[ui, cl].cpu().numpy(), words_of(Vr, nw))
+            assert np.array_equal(ib.vs_dbits[ui, cl].cpu().numpy(), words_of(Dr, nw))
+    lbs = pb.lbs.cpu().numpy().astype(np.float64)
+    nb = n // 64
+    for h in range(hq):
+        L = np.full((nb, nb), np.nan)
+        off = 0
+        for bq in range(nb):
+            L[bq, :bq + 1] = lbs[h, off:off + bq + 1]
+            off += bq + 1
+        for cl, (_, kk, _) in enumerate(grid[4:]):
+            sel, _ = IX.bs_indices(L, kk)
+            srt = ib.bs_sorted[h, cl].cpu().numpy()
+            cnt = ib.bs_count[h, cl].cpu().numpy()
+            bits = ib.bs_bits[h, cl].cpu().numpy()
+            for bq in range(nb):
+                assert cnt[bq] == sel[bq].size, (kind, h, kk, bq)
+                assert np.array_equal(srt[bq, :cnt[bq]], sel[bq]) and np.all(srt[bq, cnt[bq]:] == -1), (kind, h, kk, bq)
+                assert np.array_equal(bits[bq], words_of(sel[bq], bits.shape[1])), (kind, h, kk, bq)
+        rank_g = ib.bs_rank[h].cpu().numpy()
+        _, ranks = IX.bs_indices(L, 200)
+        for bq in range(nb):
+            m = min(200, bq + 1)
+            assert np.array_equal(rank_g[bq, :m], ranks[bq][:m]), (kind, h, bq)
+            assert np.all(rank_g[bq, m:] == -1)
+
+
 def test_index_families_built_separately_match():
     """Vertical-slash and block-sparse sets built by two calls (each with a grid holding one
     family) equal the sets of one call with the whole grid, bit for bit."""
