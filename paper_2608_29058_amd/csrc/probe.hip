@@ -867,7 +867,13 @@ __global__ void cover_combine_kernel(const ProbeArgs a, float *entropy, float *l
   M = wave_max(M);
   // a range with no visible key has z = 0 (and m = -inf): it contributes nothing
   auto lw = [&](int ch) { return pz[ch] > 0.f ? (pm[ch] - M) * a.c : -INFINITY; };  // log2 w
-  float Z = 0.f, S = 0.f, L = 0.f;
+  // every sum of the row in one pass over its ranges, then one butterfly for all of them
+  // (the same per-lane order and butterfly as a separate reduction per sum)
+  float Z = 0.f, S = 0.f, L = 0.f, acc[kMaxCand];
+#pragma unroll
+  for (int c = 0; c < kMaxCand; ++c) acc[c] = 0.f;
+  const float *pc0 = a.cov_part + ((long long)u * a.ncand * a.rmax + x) * a.nchunks;
+  const long long cstride = (long long)a.rmax * a.nchunks;  // from one candidate to the next
   for (int ch = lane; ch < nch; ch += 64) {
     const float l2 = lw(ch);
     if (l2 == -INFINITY) continue;
@@ -875,24 +881,24 @@ __global__ void cover_combine_kernel(const ProbeArgs a, float *entropy, float *l
     Z += w * pz[ch];
     S += w * (pe[ch] + l2 * kLn2 * pz[ch]);
     L += w * pl[ch];
+#pragma unroll
+    for (int c = 0; c < kMaxCand; ++c)
+      if (c < a.ncand && a.cand[c].fam != RS_DENSE) acc[c] += w * pc0[c * cstride + ch];
   }
-  Z = wave_sum(Z);
-  S = wave_sum(S);
-  L = wave_sum(L);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    Z += __shfl_xor(Z, o);
+    S += __shfl_xor(S, o);
+    L += __shfl_xor(L, o);
+#pragma unroll
+    for (int c = 0; c < kMaxCand; ++c)
+      if (c < a.ncand) acc[c] += __shfl_xor(acc[c], o);
+  }
   const float inv = Z > 0.f ? 1.f / Z : 0.f;
-  for (int c = 0; c < a.ncand; ++c) {
-    float m = 1.f;
-    if (a.cand[c].fam != RS_DENSE) {
-      const float *pc = a.cov_part + (((long long)u * a.ncand + c) * a.rmax + x) * a.nchunks;
-      float acc = 0.f;
-      for (int ch = lane; ch < nch; ch += 64) {
-        const float l2 = lw(ch);
-        if (l2 != -INFINITY) acc += __builtin_amdgcn_exp2f(l2) * pc[ch];
-      }
-      m = wave_sum(acc) * inv;
-    }
-    if (lane == 0) cov_rows[((long long)u * a.ncand + c) * a.rmax + x] = m;
-  }
+  if (lane == 0)
+#pragma unroll
+    for (int c = 0; c < kMaxCand; ++c)
+      if (c < a.ncand) cov_rows[((long long)u * a.ncand + c) * a.rmax + x] = a.cand[c].fam != RS_DENSE ? acc[c] * inv : 1.f;
   if (lane == 0) {
     const long long o = (long long)u * a.rmax + x;
     a.row_max[o] = M * a.scale;
