@@ -26,6 +26,8 @@
 // lists; each pair of waves computes only the blocks its own query block selected.
 #include <algorithm>
 #include <cstring>
+#include <map>
+#include <tuple>
 #include <vector>
 
 #include "common.h"
@@ -133,15 +135,21 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
   const int qt = item & 0xffff;
   const int head = U.head, s0 = U.s0, s1 = U.s1;
   const int kvh = head / a.group;
-  const int base = (s0 / BM + qt) * BM;
-  const int r_lo = max(s0, base), r_hi = min(s1, base + BM);  // valid rows [r_lo, r_hi)
-  const int wbase = base + 32 * wave;
+  // A block-sparse unit with a mate runs 64-row items: waves 0-1 take its rows of query block
+  // qt, waves 2-3 the same rows of the mate head (same key/value head, so the key blocks the
+  // two selections share are copied once); otherwise an item is a 128-row query tile.
+  const bool paired = PAT == P_BS && U.mate > 0;
+  const int IM = paired ? 64 : BM;  // rows of an item
+  const int base = (s0 / IM + qt) * IM;
+  const int r_lo = max(s0, base), r_hi = min(s1, base + IM);  // valid rows [r_lo, r_hi)
+  const int wbase = base + 32 * (paired ? (wave & 1) : wave);
+  const int whead = paired && wave >= 2 ? U.mate - 1 : head;  // this wave's query head
   const int w_lo = max(r_lo, wbase), w_hi = min(r_hi, wbase + 32) - 1;
   const bool wave_active = w_lo <= w_hi;
   const int my_row = wbase + l32;
   const int last_tile = (r_hi - 1) >> 6;
 
-  const InT *Qp = (const InT *)a.q + (long long)head * a.sq_h;
+  const InT *Qp = (const InT *)a.q + (long long)whead * a.sq_h;
   const InT *Kp = (const InT *)a.k + (long long)kvh * a.sk_h;
   const InT *Vp = (const InT *)a.v + (long long)kvh * a.sv_h;
 
@@ -222,15 +230,17 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
     st0 = ns;
     st1 = max(wlo, ns);
     ntiles = ns + max(0, last_tile - st1 + 1);
-  } else {  // P_BS: query blocks bq = base/64 (waves 0-1) and bq + 1 (waves 2-3)
+  } else {  // P_BS: query blocks bq = base/64 (waves 0-1) and bq + 1 (waves 2-3), or block bq
+    // of this head (waves 0-1) and of the mate head (waves 2-3)
     // the two sorted selections are loaded in parallel into key-block bitmaps; the tiles are
-    // their union in ascending order (a tile's tag says which query block selected it)
+    // their union in ascending order (a tile's tag says which selection holds it)
     const int bq = base >> 6;
     const long long brow = ((long long)head * a.ncand_bs + U.cl) * a.nb + bq;
+    const long long brow2 = paired ? ((long long)(U.mate - 1) * a.ncand_bs + U.mate_cl) * a.nb + bq : brow + 1;
     // counts within [0, k_max]; entries outside key blocks [0, bq + 1] (pads, malformed sets)
     // are skipped, so the bitmaps are never written out of range
     const int na = r_lo < base + 64 ? min(max(a.bs_count[brow], 0), a.k_max) : 0;
-    const int nb2 = (r_hi > base + 64 && bq + 1 < a.nb) ? min(max(a.bs_count[brow + 1], 0), a.k_max) : 0;
+    const int nb2 = (paired || (r_hi > base + 64 && bq + 1 < a.nb)) ? min(max(a.bs_count[brow2], 0), a.k_max) : 0;
     const int nwb = ((bq + 1) >> 5) + 1;  // words holding key blocks 0 .. bq + 1
     for (int w = tid; w < nwb; w += NT) {
       sBA[w] = 0u;
@@ -238,7 +248,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
     }
     __syncthreads();
     for (int x = tid; x < na + nb2; x += NT) {
-      const int v = x < na ? a.bs_sorted[brow * a.k_max + x] : a.bs_sorted[(brow + 1) * a.k_max + x - na];
+      const int v = x < na ? a.bs_sorted[brow * a.k_max + x] : a.bs_sorted[brow2 * a.k_max + x - na];
       if (v < 0 || v > bq + 1) continue;
       atomicOr(x < na ? &sBA[v >> 5] : &sBB[v >> 5], 1u << (v & 31));
     }
@@ -740,7 +750,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
   const int i = my_row;
   if (i < r_lo || i >= r_hi) return;
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  bf16 *op = a.o + (long long)head * a.so_h + (long long)i * a.so_t;
+  bf16 *op = a.o + (long long)whead * a.so_h + (long long)i * a.so_t;
 #pragma unroll
   for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -751,7 +761,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
       *(u32x2 *)(op + 32 * db + 8 * ii + 4 * hh) = w;
     }
   if (a.lse && hh == 0)
-    a.lse[(long long)head * a.n + i] = l_tot > 0.f ? m_run * a.scale + logf(l_tot) : -INFINITY;
+    a.lse[(long long)whead * a.n + i] = l_tot > 0.f ? m_run * a.scale + logf(l_tot) : -INFINITY;
 }
 
 // attn_fwd_kernel: workgroup b runs item order[b].  attn_fwd_queue_kernel: the grid is
@@ -855,6 +865,7 @@ static int family_bm(int) { return 128; }
 
 static int tiles_of(const rs_unit &u, int bm) { return (u.s1 - 1) / bm - u.s0 / bm + 1; }
 
+// (a unit with a mate has at most twice its 128-row tiles in 64-row blocks, and its mate none)
 size_t attn_ws_bytes(const rs_unit *units, int32_t nunits) {
   size_t items = 0;
   for (int i = 0; i < nunits; ++i) items += (size_t)tiles_of(units[i], 128);
@@ -864,16 +875,38 @@ size_t attn_ws_bytes(const rs_unit *units, int32_t nunits) {
   return ar.off + 256;
 }
 
+// Block-sparse mates: a unit of an even head takes along the unit of the next head with the
+// same rows when both heads read the same key/value head (their items then run the two
+// heads' selections of one 64-row query block side by side).  mate[u]: the unit taken along
+// by u, -2 for a unit taken along, -1 otherwise.
+static void pair_units(const rs_unit *units, int nunits, int group, std::vector<int> &mate) {
+  mate.assign(nunits, -1);
+  std::map<std::tuple<int, int, int>, int> at;  // (head, s0, s1) -> first unit
+  for (int u = 0; u < nunits; ++u) at.emplace(std::make_tuple(units[u].head, units[u].s0, units[u].s1), u);
+  for (int u = 0; u < nunits; ++u) {
+    const int h = units[u].head;
+    if ((h & 1) || mate[u] != -1 || (h + 1) / group != h / group) continue;
+    const auto it = at.find(std::make_tuple(h + 1, units[u].s0, units[u].s1));
+    if (it == at.end() || mate[it->second] != -1) continue;
+    mate[u] = it->second;
+    mate[it->second] = -2;
+  }
+}
+
 // Build the dispatch order: items bucketed by key/value head (round-robin workgroup
 // dispatch places workgroup b on XCD b % 8, so the query heads sharing one K/V stream
-// share one XCD's L2), longest query tiles first within a bucket.
-static void build_order(const rs_unit *units, int nunits, int group, int bm,
+// share one XCD's L2), longest query tiles first within a bucket.  Items of a unit with a
+// mate are 64-row query blocks, others bm-row query tiles (bm = 128); units taken along by a
+// mate have none.
+static void build_order(const rs_unit *units, int nunits, int group, int bm, const std::vector<int> &mate,
                         std::vector<int> &order) {
-  std::vector<std::vector<std::pair<int, int>>> buckets(8);  // (neg cost, item)
+  std::vector<std::vector<std::pair<int, int>>> buckets(8);  // (-first row / 64, item)
   for (int u = 0; u < nunits; ++u) {
-    const int t0 = units[u].s0 / bm, nt = tiles_of(units[u], bm);
+    if (mate[u] == -2) continue;
+    const int im = mate[u] >= 0 ? 64 : bm;
+    const int t0 = units[u].s0 / im, nt = tiles_of(units[u], im);
     const int b = (units[u].head / group) & 7;
-    for (int t = 0; t < nt; ++t) buckets[b].push_back({-(t0 + t), (u << 16) | t});
+    for (int t = 0; t < nt; ++t) buckets[b].push_back({-((t0 + t) * (im / 64)), (u << 16) | t});
   }
   size_t mx = 0;
   for (auto &b : buckets) {
@@ -968,8 +1001,9 @@ rs_status attn_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int3
   if (nunits == 0) return RS_OK;
   const int bm = family_bm(fam);
   const int group = qkv->hq / qkv->hkv;
-  std::vector<int> order;
-  build_order(units, nunits, group, bm, order);
+  std::vector<int> mate(nunits, -1), order;
+  if (fam == RS_BSPARSE) pair_units(units, nunits, group, mate);
+  build_order(units, nunits, group, bm, mate, order);
   const size_t need = attn_ws_bytes(units, nunits);
   if (!ws || ws_bytes < need)
     return fail(RS_ERR_WORKSPACE, "attention workspace too small: need " + std::to_string(need) +
@@ -983,7 +1017,8 @@ rs_status attn_launch(const rs_qkv *qkv, float scale, const rs_unit *units, int3
   DevUnit *h_units = (DevUnit *)stage.data();
   for (int u = 0; u < nunits; ++u) {
     h_units[u] = DevUnit{units[u].head, units[u].s0, units[u].s1, cand_local, units[u].slot,
-                         fam == RS_ASHAPE ? cand->a : 0, fam == RS_ASHAPE ? cand->b : 0, 0};
+                         fam == RS_ASHAPE ? cand->a : 0, fam == RS_ASHAPE ? cand->b : 0,
+                         mate[u] >= 0 ? units[mate[u]].head + 1 : 0, cand_local};
   }
   memcpy(stage.data() + off_order, order.data(), order.size() * sizeof(int));
   RS_HIP(hipMemcpyAsync(ws, stage.data(), stage.size(), hipMemcpyHostToDevice, st));

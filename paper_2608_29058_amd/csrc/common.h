@@ -51,7 +51,9 @@ rs_status check_units(const rs_qkv *qkv, const rs_unit *units, int32_t nunits);
 struct DevUnit {
   int head, s0, s1, cl, slot;  // cl: index of the unit's candidate among its family's
   int sink, window;            // A-shape candidate of the unit
-  int pad;
+  // block-sparse: head + 1 of a second unit (same rows, same key/value head) whose query
+  // blocks this unit's items also run, and that unit's cl; 0: none (items of 128 rows)
+  int mate, mate_cl;
 };
 
 // Device work queues of a persistent attention launch: per key/value bucket b (8), the items

@@ -8,7 +8,8 @@
 //                         one workgroup
 //   plan_kernel           per family, the work queues of the attention launch (query tiles of
 //                         the units routed to the family, one queue per key/value bucket, longest
-//                         first), one workgroup per family
+//                         first; block-sparse units of two heads with the same rows and key/value
+//                         head share 64-row items), one workgroup per family
 //
 // Greedy on the device.  The host solve repeatedly applies the (unit, candidate)
 // substitution of minimum ratio rho = (R(c) - R(cur)) / (t(cur) - t(c)) over strictly cheaper
@@ -354,17 +355,54 @@ __global__ void __launch_bounds__(1024) plan_kernel(const PlanArgs a) {
   __shared__ int sLu2u[kRouteMaxUnits];   // local unit -> unit
   __shared__ int sOff[kRouteMaxUnits + 1];  // local unit -> first flat item
   __shared__ int sBl[kRouteMaxUnits];     // units of each bucket, ascending
-  __shared__ int sK0[kRouteMaxUnits], sK1[kRouteMaxUnits];  // first and last query tile of a unit
+  // items of a unit: n of them, the j-th starting at row 64 (k0 + g j); g = 2 for 128-row
+  // query tiles, 1 for the 64-row query blocks of a block-sparse unit with a mate
+  __shared__ int sK0[kRouteMaxUnits], sN[kRouteMaxUnits], sG[kRouteMaxUnits];
   __shared__ int sBk[kRouteMaxUnits];     // bucket of a unit, -1 when routed to another family
+  __shared__ int sMate[kRouteMaxUnits];   // unit taken along (block-sparse), -2 taken along, -1
   __shared__ int sBs[9], sSize[8], sNl;
   const int U = a.U, bm = a.bm;
-  // per unit, in parallel: tiles, bucket and whether the unit is routed to this family
+  // per unit, in parallel: bucket and whether the unit is routed to this family
   for (int u = tid; u < U; u += NT) {
     const rs_unit un = a.units[u];
     const int c = a.choice[u];
-    sK0[u] = un.s0 / bm;
-    sK1[u] = (un.s1 - 1) / bm;
     sBk[u] = (c >= 0 && c < a.C && a.fam[c] == f) ? (un.head / a.group) & 7 : -1;
+    sMate[u] = -1;
+  }
+  __syncthreads();
+  // block-sparse mates: the first unit of an even head h takes along the first unit of head
+  // h + 1 with the same rows when both are routed here and read the same key/value head
+  if (f == RS_BSPARSE) {
+    for (int u = tid; u < U; u += NT) {
+      const rs_unit un = a.units[u];
+      const int h = un.head;
+      if (sBk[u] < 0 || (h & 1) || (h + 1) / a.group != h / a.group) continue;
+      int v = -1;
+      bool first = true;
+      for (int w = 0; w < U && first; ++w) {
+        const rs_unit x = a.units[w];
+        if (sBk[w] < 0 || x.s0 != un.s0 || x.s1 != un.s1) continue;
+        if (x.head == h && w < u) first = false;
+        if (x.head == h + 1 && v < 0) v = w;
+      }
+      if (first && v >= 0) {
+        sMate[u] = v;
+        sMate[v] = -2;
+      }
+    }
+    __syncthreads();
+  }
+  for (int u = tid; u < U; u += NT) {
+    const rs_unit un = a.units[u];
+    if (sMate[u] >= 0) {
+      sK0[u] = un.s0 / 64;
+      sN[u] = (un.s1 - 1) / 64 - un.s0 / 64 + 1;
+      sG[u] = 1;
+    } else {
+      sK0[u] = 2 * (un.s0 / bm);
+      sN[u] = sMate[u] == -2 ? 0 : (un.s1 - 1) / bm - un.s0 / bm + 1;
+      sG[u] = 2;
+    }
   }
   __syncthreads();
   if (tid == 0) {
@@ -373,8 +411,8 @@ __global__ void __launch_bounds__(1024) plan_kernel(const PlanArgs a) {
     sOff[0] = 0;
     for (int u = 0; u < U; ++u) {
       const int b = sBk[u];
-      if (b < 0) continue;
-      const int nt = sK1[u] - sK0[u] + 1;
+      if (b < 0 || sMate[u] == -2) continue;
+      const int nt = sN[u];
       sLu2u[nl] = u;
       sOff[nl + 1] = sOff[nl] + nt;
       sSize[b] += nt;
@@ -406,8 +444,10 @@ __global__ void __launch_bounds__(1024) plan_kernel(const PlanArgs a) {
     const int u = sLu2u[l];
     const rs_unit &un = a.units[u];
     const int c = a.choice[u];
+    const int m = sMate[u];
     dunits[l] = DevUnit{un.head, un.s0, un.s1, a.cl[c], un.slot, f == RS_ASHAPE ? a.ca[c] : 0,
-                             f == RS_ASHAPE ? a.cb[c] : 0, 0};
+                        f == RS_ASHAPE ? a.cb[c] : 0, m >= 0 ? a.units[m].head + 1 : 0,
+                        m >= 0 ? a.cl[a.choice[m]] : 0};
   }
   for (int i = tid; i < total; i += NT) {
     int lo = 0, hi = nl - 1;  // local unit holding flat item i
@@ -417,15 +457,16 @@ __global__ void __launch_bounds__(1024) plan_kernel(const PlanArgs a) {
       else hi = mid - 1;
     }
     const int u = sLu2u[lo], t = i - sOff[lo];
-    const int key = sK0[u] + t;
+    const int key = sK0[u] + sG[u] * t;  // first row / 64
     const int b = sBk[u];
-    // rank in the bucket: longer query tiles (larger key) first, then units ascending
+    // rank in the bucket: later query rows first, then units ascending
     int r = 0;
     for (int x = sBs[b]; x < sBs[b + 1]; ++x) {
       const int v = sBl[x];
-      const int k0 = sK0[v], k1 = sK1[v];
-      r += max(0, k1 - max(key + 1, k0) + 1);
-      r += (v < u && k0 <= key && key <= k1) ? 1 : 0;
+      const int k0 = sK0[v], g = sG[v], n = sN[v];
+      const int below = key < k0 ? 0 : min(n, (key - k0) / g + 1);  // items of v starting at or before key
+      r += n - below;
+      r += (v < u && key >= k0 && (key - k0) % g == 0 && (key - k0) / g < n) ? 1 : 0;
     }
     int off = 0;
     for (int bb = 0; bb < b; ++bb) off += sSize[bb];

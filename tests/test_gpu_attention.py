@@ -136,6 +136,44 @@ def test_block_sparse_matches_oracle(n, k_blocks, vt):
         check_close(o[h, s0:s1], ref, f"bs h={h}")
 
 
+@pytest.mark.parametrize("n,s0,k_blocks", [(2000, 0, 7), (2600, 96, 30), (4160, 640, 64)])
+@pytest.mark.parametrize("vt", [False, True])
+def test_block_sparse_mates_match_single_units(n, s0, k_blocks, vt):
+    """Block-sparse units of heads 2m and 2m + 1 with the same rows and key/value head run as
+    mates (64-row items, one selection per wave pair): every row's output and LSE equal, bit
+    for bit, those of the same units launched one by one (128-row items), and the oracle's
+    masked attention (Sec. 3.1 block-sparse mask)."""
+    hq, hkv, d = 4, 2, 128
+    q, k, v = _inputs(n, hq, hkv, d, seed=n + s0)
+    nb = (n + 63) // 64
+    grid = [(_rs.RS_DENSE, 0, 0), (_rs.RS_BSPARSE, k_blocks, 64)]
+    ib = _rs.IndexBuffers(hq, n, hq, grid)
+    r = np.random.default_rng(n)
+    sels = {}
+    for h in range(hq):
+        # head 1 shares part of head 0's selections, heads 2 and 3 are independent
+        sel = []
+        for bq in range(nb):
+            others = r.permutation(bq)[:k_blocks - 1]
+            if h == 1 and bq < len(sels[0]):
+                keep = [b for b in sels[0][bq] if b != bq][: (k_blocks - 1) // 2]
+                others = np.array(sorted(set(keep) | set(others.tolist()[: k_blocks - 1 - len(keep)])), dtype=np.int64)
+            sel.append(sorted(set(others.tolist()) | {bq}))
+        sels[h] = sel
+        fill_bs(ib, h, 0, sel)
+    units = [(h, s0, n, 1) for h in range(hq)]
+    o, lse = _run_sparse(q, k, v, units, grid, ib, vt=vt)
+    g = hq // hkv
+    for h in range(hq):
+        o1, lse1 = _run_sparse(q, k, v, [units[h]], grid, ib, vt=vt)
+        assert np.array_equal(o[h, s0:n], o1[h, s0:n]) and np.array_equal(lse[h, s0:n], lse1[h, s0:n]), h
+        rows = np.arange(s0, n)
+        mask = P.bs_mask(rows, n, 64, lambda bq, h=h: sels[h][bq])
+        ref, rl = A.masked_attention(q[h], k[h // g], v[h // g], rows, mask)
+        check_close(o[h, s0:n], ref, f"bs mates h={h}")
+        np.testing.assert_allclose(lse[h, s0:n], rl, atol=2e-3, rtol=1e-4)
+
+
 @pytest.mark.parametrize("n,nv,ns,spread", [(3000, 40, 300, "local"), (2048, 64, 256, "scatter"),
                                             (4100, 200, 1500, "mixed"), (900, 0, 1, "diag_only"),
                                             # the most vertical columns a set may hold (2048), nearly all
