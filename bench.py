@@ -117,6 +117,46 @@ def tiles_bs(s0, s1, lists, counts):
     return tot
 
 
+def bs_mates(units, group):
+    """Block-sparse mates as the attention planners form them: the first unit of an even head
+    h takes along the first unit of head h + 1 with the same rows when both heads read the
+    same key/value head.  ``units``: (h, s0, s1, ...) in unit order; returns {leader: mate}."""
+    first = {}
+    for i, u in enumerate(units):
+        first.setdefault(tuple(u[:3]), i)
+    mates, taken = {}, set()
+    for i, u in enumerate(units):
+        h, s0, s1 = u[:3]
+        if h % 2 or first[(h, s0, s1)] != i or (h + 1) // group != h // group:
+            continue
+        j = first.get((h + 1, s0, s1))
+        if j is not None and j not in taken:
+            mates[i] = j
+            taken.add(j)
+    return mates
+
+
+def tiles_bs_units(units, group, lists_of, counts_of):
+    """Tiles the block-sparse launch schedules for ``units`` (h, s0, s1, cl): a pair of mates
+    runs 64-row items over the union of the two heads' selections of each query block, any
+    other unit 128-row items over the union of two consecutive blocks' selections."""
+    mates = bs_mates(units, group)
+    follow = set(mates.values())
+    tot = 0
+    for i, (h, s0, s1, cl) in enumerate(units):
+        if i in follow:
+            continue
+        la, ca = lists_of(h, cl), counts_of(h, cl)
+        if i in mates:
+            h2, _, _, cl2 = units[mates[i]]
+            lb, cb = lists_of(h2, cl2), counts_of(h2, cl2)
+            for bq in range(s0 // 64, (s1 - 1) // 64 + 1):
+                tot += len(np.union1d(la[bq, :ca[bq]], lb[bq, :cb[bq]]))
+        else:
+            tot += tiles_bs(s0, s1, la, ca)
+    return tot
+
+
 def tiles_vs(s0, s1, V, D):
     """Diagonal tiles (64-key tiles any selected diagonal crosses for the query tile's rows)
     plus gathered tiles of the vertical columns outside them."""
@@ -350,7 +390,7 @@ def time_configs(reps):
     counts = ib.bs_count[:, 0].cpu().numpy()
     pairs = [pairs_bs(0, n, counts[h]) for h in range(HQ)]
     srt = ib.bs_sorted[:, 0].cpu().numpy()
-    tiles = sum(tiles_bs(0, n, srt[h], counts[h]) for h in range(HQ))
+    tiles = tiles_bs_units([(h, 0, n, 0) for h in range(HQ)], HQ // HKV, lambda h, cl: srt[h], lambda h, cl: counts[h])
     dms, _ = timed(dense(qkv, q, range(HQ), o))
     lay = t_ms + p_ms + i_ms + ms
     out["bsparse_128k"] = entry(ms, p95, 4.0 * D * sum(pairs), pairs_per_head=sorted(set(pairs)),
@@ -538,6 +578,7 @@ def main():
             RL.run_group(qkv_l, cand, us)
             gev.append(ev())
         torch.cuda.synchronize()
+        bs_units = []
         for gi, (cand, us) in enumerate(route["groups"]):
             fam, a_, b_ = GRID[cand]
             dt = w_l * gev[gi].elapsed_time(gev[gi + 1])
@@ -555,9 +596,7 @@ def main():
                     tiles += tiles_ashape(s0, s1, a_, b_)
                 elif fam == 3:
                     pairs += pairs_bs(s0, s1, ic["bs_count"][h, cl])
-                    if (h, cl) not in ic["bs_lists"]:
-                        ic["bs_lists"][(h, cl)] = RL.ib.bs_sorted[h, cl].cpu().numpy()
-                    tiles += tiles_bs(s0, s1, ic["bs_lists"][(h, cl)], ic["bs_count"][h, cl])
+                    bs_units.append((u, h, s0, s1, cl))
                 else:
                     cv, cdn = ic["vs_count"][u, cl]
                     pairs += pairs_vs(s0, s1, ic["vs_v"][u, cl, :cv], ic["vs_d"][u, cl, :cdn])
@@ -571,6 +610,17 @@ def main():
             fam_flops[fam] += fl
             fam_launches[fam] += w_l
             routed_flops += fl
+        # block-sparse tiles: device routing runs every block-sparse unit of the layer in one
+        # launch (mates across budgets), host routing one launch per (pattern, budget) group
+        def lists_of(h, cl):
+            if (h, cl) not in ic["bs_lists"]:
+                ic["bs_lists"][(h, cl)] = RL.ib.bs_sorted[h, cl].cpu().numpy()
+            return ic["bs_lists"][(h, cl)]
+        batches = [sorted(bs_units)] if device else [[x for x in bs_units if x[4] == c] for c in
+                                                     sorted({x[4] for x in bs_units})]
+        for bt in batches:
+            fam_issued[3] += w_l * 4.0 * D * 64 * 128 * tiles_bs_units(
+                [x[1:] for x in bt], HQ // HKV, lists_of, lambda h, cl: ic["bs_count"][h, cl])
     # dense reference: the whole layer through the dense kernel, same run
     q0, k0, v0, _ = layers[0]
     qkv_d = RL.qkv(q0, k0, v0)
