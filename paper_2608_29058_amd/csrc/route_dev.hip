@@ -380,8 +380,9 @@ __global__ void __launch_bounds__(1024) plan_kernel(const PlanArgs a) {
       int v = -1;
       bool first = true;
       for (int w = 0; w < U && first; ++w) {
+        if (sBk[w] != sBk[u]) continue;  // a mate reads the same key/value head: same bucket
         const rs_unit x = a.units[w];
-        if (sBk[w] < 0 || x.s0 != un.s0 || x.s1 != un.s1) continue;
+        if (x.s0 != un.s0 || x.s1 != un.s1) continue;
         if (x.head == h && w < u) first = false;
         if (x.head == h + 1 && v < 0) v = w;
       }
