@@ -683,10 +683,11 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
     // tile t+1's products, then tile t's softmax: the two waves of a SIMD tend to alternate
     // between product bursts and softmax bursts, so that one's products overlap the other's
     // vector work (interleaving them within a wave was measured slower)
-    // (vertical-slash and dense take tile t+1's products after tile t's P V instead: the two
-    // S tiles are then never live together, which leaves registers for fragment read-ahead;
-    // 1-2% faster for dense, slower for block-sparse)
-    constexpr bool kLateQK = PAT == P_VS || PAT == P_DENSE;
+    // (vertical-slash, dense and block-sparse take tile t+1's products after tile t's P V
+    // instead: the two S tiles are then never live together, which leaves registers for
+    // fragment read-ahead; 1-2% faster for dense and for block-sparse with mates, not for
+    // A-shape, whose short items keep the early products)
+    constexpr bool kLateQK = PAT == P_VS || PAT == P_DENSE || PAT == P_BS;
     if constexpr (!kLateQK)
       if (kOverlap || Pn.on) qk(sn, kn, Pn);
     if (kOverlap || Pc.on) {
