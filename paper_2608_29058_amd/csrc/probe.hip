@@ -909,22 +909,35 @@ __global__ void cover_combine_kernel(const ProbeArgs a, float *entropy, float *l
   }
 }
 
-// subset means of the per-row coverage; grid (ncand, nunits)
+// subset means of the per-row coverage; grid (ncand, nunits), one wave: lane l sums rows
+// l, l + 64, ... in order, then a fixed xor-butterfly combines the lanes (deterministic)
 __global__ void cover_means_kernel(const ProbeArgs a, const float *cov_rows, float *cov) {
-  const int u = blockIdx.y, c = blockIdx.x;
+  const int u = blockIdx.y, c = blockIdx.x, lane = threadIdx.x & 63;
   const ProbeUnit U = a.units[u];
-  if (threadIdx.x != 0) return;
   float tot = 0.f, sub[3] = {0.f, 0.f, 0.f};
   int cnt[3] = {0, 0, 0};
   const float *m = cov_rows + ((long long)u * a.ncand + c) * a.rmax;
-  for (int r = 0; r < U.nrows; ++r) {
+  for (int r = lane; r < U.nrows; r += 64) {
     const int s = a.subset[(long long)u * a.rmax + r];
-    tot += m[r];
-    if (s >= 0 && s < 3) {
-      sub[s] += m[r];
-      cnt[s]++;
+    const float x = m[r];
+    tot += x;
+#pragma unroll
+    for (int s2 = 0; s2 < 3; ++s2)
+      if (s == s2) {
+        sub[s2] += x;
+        cnt[s2]++;
+      }
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    tot += __shfl_xor(tot, o);
+#pragma unroll
+    for (int s2 = 0; s2 < 3; ++s2) {
+      sub[s2] += __shfl_xor(sub[s2], o);
+      cnt[s2] += __shfl_xor(cnt[s2], o);
     }
   }
+  if (lane != 0) return;
   float *o = cov + ((long long)u * a.ncand + c) * 4;
   o[0] = U.nrows ? tot / U.nrows : 0.f;
   for (int s2 = 0; s2 < 3; ++s2) o[1 + s2] = cnt[s2] ? sub[s2] / cnt[s2] : 0.f;
