@@ -23,7 +23,10 @@
 // Online softmax in the exp2 domain (logit * scale * log2 e), fp32 statistics; the running
 // max is raised only when it grows by more than 2^8, so the O rescale is rare.
 // Block-sparse: the workgroup's two 64-row query blocks walk the union of their block
-// lists; each pair of waves computes only the blocks its own query block selected.
+// lists; each pair of waves computes only the blocks its own query block selected.  The two
+// blocks are the same rows of two heads that read one key/value head when both heads' units
+// are block-sparse (their selections overlap far more than two consecutive blocks of one
+// head do), else consecutive blocks of one head.
 #include <algorithm>
 #include <cstring>
 #include <map>
