@@ -136,14 +136,16 @@ def test_block_sparse_matches_oracle(n, k_blocks, vt):
         check_close(o[h, s0:s1], ref, f"bs h={h}")
 
 
-@pytest.mark.parametrize("n,s0,k_blocks", [(2000, 0, 7), (2600, 96, 30), (4160, 640, 64)])
+@pytest.mark.parametrize("n,s0,k_blocks,hq,hkv", [(2000, 0, 7, 4, 2), (2600, 96, 30, 4, 2), (4160, 640, 64, 4, 2),
+                                                  (2600, 96, 30, 6, 2)])
 @pytest.mark.parametrize("vt", [False, True])
-def test_block_sparse_mates_match_single_units(n, s0, k_blocks, vt):
+def test_block_sparse_mates_match_single_units(n, s0, k_blocks, hq, hkv, vt):
     """Block-sparse units of heads 2m and 2m + 1 with the same rows and key/value head run as
     mates (64-row items, one selection per wave pair): every row's output and LSE equal, bit
     for bit, those of the same units launched one by one (128-row items), and the oracle's
-    masked attention (Sec. 3.1 block-sparse mask)."""
-    hq, hkv, d = 4, 2, 128
+    masked attention (Sec. 3.1 block-sparse mask).  With three heads per key/value head,
+    heads 2 and 3 read different key/value heads and stay unpaired."""
+    d = 128
     q, k, v = _inputs(n, hq, hkv, d, seed=n + s0)
     nb = (n + 63) // 64
     grid = [(_rs.RS_DENSE, 0, 0), (_rs.RS_BSPARSE, k_blocks, 64)]
