@@ -818,12 +818,14 @@ __global__ void probe_stats_combine_kernel(const ProbeArgs a) {
   }
 }
 
-// diagonals from their chunk partials, zero tails of col/diag: one thread per position
-__global__ void probe_finish_kernel(const ProbeArgs a, float *diag, float *entropy, float *local) {
+// diagonals from their chunk partials, zero tails of col/diag: with vec, one thread per 4
+// positions and 16-byte stores (n a multiple of 4, both arrays 16-byte aligned), else one
+// thread per position
+__global__ void probe_finish_kernel(const ProbeArgs a, float *diag, float *entropy, float *local, int vec) {
   const int u = blockIdx.y;
   const ProbeUnit U = a.units[u];
-  const int x = blockIdx.x * blockDim.x + threadIdx.x;
-  if (x < a.n) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  auto diag_at = [&](int x) -> float {
     float v = 0.f;
     if (x < U.s1 && U.nR > 0) {
       // chunks whose diagonal range [r0 - c0 - (kRange-1), r0 + nR - 1 - c0] holds t = x
@@ -836,14 +838,30 @@ __global__ void probe_finish_kernel(const ProbeArgs a, float *diag, float *entro
         if (xi >= 0 && xi < kRange + U.nR) v += a.diag_part[((long long)u * a.nchunks + ch) * a.diag_w + xi];
       }
     }
-    diag[(long long)u * a.n + x] = v;
-    if (x >= U.s1) a.col[(long long)u * a.n + x] = 0.f;
+    return v;
+  };
+  float *drow = diag + (long long)u * a.n, *crow = a.col + (long long)u * a.n;
+  if (vec) {
+    const int x = 4 * t;
+    if (x < a.n) {
+      const f32x4 v = {diag_at(x), diag_at(x + 1), diag_at(x + 2), diag_at(x + 3)};
+      *(f32x4 *)(drow + x) = v;
+      if (x >= U.s1) {
+        *(f32x4 *)(crow + x) = f32x4{0.f, 0.f, 0.f, 0.f};
+      } else {
+        for (int e = max(U.s1 - x, 0); e < 4; ++e) crow[x + e] = 0.f;
+      }
+    }
+  } else if (t < a.n) {
+    drow[t] = diag_at(t);
+    if (t >= U.s1) crow[t] = 0.f;
   }
-  if (a.rows_out && x < a.rmax) {
-    a.rows_out[(long long)u * a.rmax + x] = a.rows[(long long)u * a.rmax + x];
-    a.subset_out[(long long)u * a.rmax + x] = a.subset[(long long)u * a.rmax + x];
-    if (x < 3) a.nsub_out[u * 3 + x] = a.nsub_tab[u * 3 + x];
-  }
+  if (a.rows_out)
+    for (int x = t; x < a.rmax; x += gridDim.x * blockDim.x) {
+      a.rows_out[(long long)u * a.rmax + x] = a.rows[(long long)u * a.rmax + x];
+      a.subset_out[(long long)u * a.rmax + x] = a.subset[(long long)u * a.rmax + x];
+      if (x < 3) a.nsub_out[u * 3 + x] = a.nsub_tab[u * 3 + x];
+    }
 }
 
 // coverage pass partials of each sampled row combined over its ranges (one wave per row):
@@ -1285,7 +1303,10 @@ static hipError_t launch_rows(const ProbeArgs &pa, int nunits, int ngroups, int 
     }
     ra.lg_pairs = 1;
     hipLaunchKernelGGL((probe_range_kernel<D, InT, M_SCORES, 1>), range_grid(pa.nchunks, ngroups, 1), dim3(256), 0, st, ra);
-    hipLaunchKernelGGL(probe_finish_kernel, dim3((pa.n + 255) / 256, nunits), dim3(256), 0, st, pa, diag, ent, loc);
+    const int vec = (pa.n & 3) == 0 && ((uintptr_t)diag & 15) == 0 && ((uintptr_t)pa.col & 15) == 0;
+    const int fin_threads = vec ? pa.n / 4 : pa.n;
+    hipLaunchKernelGGL(probe_finish_kernel, dim3((fin_threads + 255) / 256, nunits), dim3(256), 0, st, pa, diag, ent,
+                       loc, vec);
   } else {
     bool ashape_only = true;
     for (int q = 0; q < pa.ncov; ++q) ashape_only = ashape_only && pa.cand[pa.cov_cand[q]].fam == RS_ASHAPE;
