@@ -78,10 +78,10 @@ def greedy(R, t, choice, t_probe, T_layer):
 
 def expand_or_fallback(choice, fam, brank, ML, tau, dense_c, t):
     """A sparse choice whose lower mass is below tau first expands its budget: the smallest
-    larger budget of the same family with m_lower >= tau.  If none passes, the router
-    switches to dense only "if no sparse candidate satisfies the threshold" (Sec. 3.4): the
-    cheapest sparse candidate of any family with m_lower >= tau (lowest time, then lowest
-    candidate index), else the dense candidate."""
+    larger budget of the same family with m_lower >= tau.  If none passes, dense is taken
+    only when no sparse candidate at all reaches tau (Sec. 3.4): first the cheapest sparse
+    candidate of any family with m_lower >= tau (lowest time, then lowest candidate index),
+    else the dense candidate."""
     out = list(choice)
     C = len(fam)
     nfb = 0

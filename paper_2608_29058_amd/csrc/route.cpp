@@ -152,7 +152,7 @@ extern "C" rs_status rs_route_layer(const rs_route_in *in, const rs_route_cfg *c
     for (i >>= 1; i >= 1; i >>= 1) tree[i] = win(tree[2 * i], tree[2 * i + 1]);
   }
   // expand or fall back: larger budgets of the family first, then the cheapest passing
-  // sparse candidate of any family ("dense if no sparse candidate satisfies tau")
+  // sparse candidate of any family, dense only when no sparse candidate reaches tau
   int nfb = 0;
   for (int u = 0; u < U; ++u) {
     const int c = choice[u];
