@@ -864,25 +864,28 @@ __global__ void probe_finish_kernel(const ProbeArgs a, float *diag, float *entro
     }
 }
 
-// coverage pass partials of each sampled row combined over its ranges (one wave per row):
+// coverage pass partials of each sampled row combined over its ranges:
 // with M the row's max, a range's partials (relative to its own max m) are weighted by
 // w = exp(m - M); Z = sum w z, m_i(c) = sum w cov(c) / Z, local mass likewise, and with
 // S = sum over 64-key blocks of B log B (B relative to M) = sum w (s + log(w) z), the block
 // entropy is log Z - S / Z.  Writes row_max / row_sum, the descriptors and m_i(c).
 // grid (ceil(rmax / 4), nunits), 256 threads
+// sixteen lanes per row (a row has at most n / 1024 ranges): four rows per wave, more loads
+// in flight per lane than one row per wave; the sixteen lanes reduce with a fixed butterfly
 __global__ void cover_combine_kernel(const ProbeArgs a, float *entropy, float *local, float *cov_rows) {
   const int u = blockIdx.y;
   const ProbeUnit U = a.units[u];
-  const int x = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (x >= U.nrows) return;
+  const int x = blockIdx.x * 16 + (threadIdx.x >> 4), lane = threadIdx.x & 15;
+  if (x >= U.nrows) return;  // the sixteen lanes of a row leave together
   const int row = a.rows[(long long)u * a.rmax + x];
   const int nch = row / kRange + 1;
   const long long base = ((long long)u * a.rmax + x) * a.nchunks;
   const float *pm = a.max_part + base, *pz = a.sum_part + base;
   const float *pe = a.ent_part + base, *pl = a.loc_part + base;
   float M = -INFINITY;
-  for (int ch = lane; ch < nch; ch += 64) M = fmaxf(M, pm[ch]);
-  M = wave_max(M);
+  for (int ch = lane; ch < nch; ch += 16) M = fmaxf(M, pm[ch]);
+#pragma unroll
+  for (int o = 8; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
   // a range with no visible key has z = 0 (and m = -inf): it contributes nothing
   auto lw = [&](int ch) { return pz[ch] > 0.f ? (pm[ch] - M) * a.c : -INFINITY; };  // log2 w
   // every sum of the row in one pass over its ranges, then one butterfly for all of them
@@ -892,7 +895,7 @@ __global__ void cover_combine_kernel(const ProbeArgs a, float *entropy, float *l
   for (int c = 0; c < kMaxCand; ++c) acc[c] = 0.f;
   const float *pc0 = a.cov_part + ((long long)u * a.ncand * a.rmax + x) * a.nchunks;
   const long long cstride = (long long)a.rmax * a.nchunks;  // from one candidate to the next
-  for (int ch = lane; ch < nch; ch += 64) {
+  for (int ch = lane; ch < nch; ch += 16) {
     const float l2 = lw(ch);
     if (l2 == -INFINITY) continue;
     const float w = __builtin_amdgcn_exp2f(l2);
@@ -904,7 +907,7 @@ __global__ void cover_combine_kernel(const ProbeArgs a, float *entropy, float *l
       if (c < a.ncand && a.cand[c].fam != RS_DENSE) acc[c] += w * pc0[c * cstride + ch];
   }
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
+  for (int o = 8; o >= 1; o >>= 1) {
     Z += __shfl_xor(Z, o);
     S += __shfl_xor(S, o);
     L += __shfl_xor(L, o);
@@ -1318,7 +1321,7 @@ static hipError_t launch_rows(const ProbeArgs &pa, int nunits, int ngroups, int 
       hipLaunchKernelGGL((probe_range_kernel<D, InT, M_COVER, 4>), grid, dim3(256), 0, st, ra);
     else
       hipLaunchKernelGGL((probe_range_kernel<D, InT, M_COVER, kMaxCand>), grid, dim3(256), 0, st, ra);
-    hipLaunchKernelGGL(cover_combine_kernel, dim3((pa.rmax + 3) / 4, nunits), dim3(256), 0, st, pa, ent, loc, cov_rows);
+    hipLaunchKernelGGL(cover_combine_kernel, dim3((pa.rmax + 15) / 16, nunits), dim3(256), 0, st, pa, ent, loc, cov_rows);
     hipLaunchKernelGGL(cover_means_kernel, dim3(pa.ncand, nunits), dim3(64), 0, st, pa, cov_rows, cov);
   }
   return hipGetLastError();
