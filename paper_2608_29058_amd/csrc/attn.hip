@@ -23,10 +23,13 @@
 // Online softmax in the exp2 domain (logit * scale * log2 e), fp32 statistics; the running
 // max is raised only when it grows by more than 2^8, so the O rescale is rare.
 // Block-sparse: the workgroup's two 64-row query blocks walk the union of their block
-// lists; each pair of waves computes only the blocks its own query block selected.  The two
-// blocks are the same rows of two heads that read one key/value head when both heads' units
-// are block-sparse (their selections overlap far more than two consecutive blocks of one
-// head do), else consecutive blocks of one head.
+// lists from the diagonal block down; each pair of waves computes only the blocks its own
+// query block selected.  The two blocks are the same rows of two heads that read one
+// key/value head when both heads' units are block-sparse (their selections overlap far more
+// than two consecutive blocks of one head do), else consecutive blocks of one head.
+// Vertical-slash takes its diagonal-band tiles from the diagonal down as well, then the
+// gathered columns.  (Items that start together share their blocks near the diagonal; taken
+// first, those are still in L2 when the neighbours reach them.)
 #include <algorithm>
 #include <cstring>
 #include <map>
@@ -223,8 +226,9 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
     n_gather = min(total, kMaxGather);
     __syncthreads();
     ntiles = n_contig + (n_gather + 63) / 64;
-    st0 = 0;                                   // bitmap word of the next contiguous tile
-    st1 = nwt > 0 ? __builtin_amdgcn_readfirstlane((int)tile_bits(sTB[0])) : 0;  // remaining tiles (even bits)
+    // contiguous tiles are taken from the diagonal down (descending keys)
+    st0 = nwt - 1;                                                            // bitmap word of the next contiguous tile
+    st1 = __builtin_amdgcn_readfirstlane((int)tile_bits(sTB[st0]));           // remaining tiles (even bits)
   } else if constexpr (PAT == P_DENSE) {
     ntiles = last_tile + 1;
   } else if constexpr (PAT == P_ASHAPE) {
@@ -236,7 +240,8 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
   } else {  // P_BS: query blocks bq = base/64 (waves 0-1) and bq + 1 (waves 2-3), or block bq
     // of this head (waves 0-1) and of the mate head (waves 2-3)
     // the two sorted selections are loaded in parallel into key-block bitmaps; the tiles are
-    // their union in ascending order (a tile's tag says which selection holds it)
+    // their union, walked from the highest key block down (a tile's tag says which selection
+    // holds it)
     const int bq = base >> 6;
     const long long brow = ((long long)head * a.ncand_bs + U.cl) * a.nb + bq;
     const long long brow2 = paired ? ((long long)(U.mate - 1) * a.ncand_bs + U.mate_cl) * a.nb + bq : brow + 1;
@@ -261,8 +266,9 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) cnt += __shfl_xor(cnt, o);
     ntiles = cnt;
-    st0 = 0;                                                        // bitmap word of the next tile
-    st1 = __builtin_amdgcn_readfirstlane((int)(sBA[0] | sBB[0]));  // remaining blocks of that word
+    // the union is walked from the diagonal block down (descending key blocks)
+    st0 = nwb - 1;                                                      // bitmap word of the next tile
+    st1 = __builtin_amdgcn_readfirstlane((int)(sBA[st0] | sBB[st0]));  // remaining blocks of that word
   }
 
   // next tile in order (t increases by one per call)
@@ -276,20 +282,20 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
     } else if constexpr (PAT == P_BS) {
       // the words are the same for every lane: kept in scalar registers
       while (st1 == 0) {
-        ++st0;
+        --st0;
         st1 = __builtin_amdgcn_readfirstlane((int)(sBA[st0] | sBB[st0]));
       }
-      const int bit = __builtin_ctz((uint32_t)st1);
-      st1 &= st1 - 1;
+      const int bit = 31 - __builtin_clz((uint32_t)st1);
+      st1 &= ~(1u << bit);
       const int wa = __builtin_amdgcn_readfirstlane((int)sBA[st0]), wb = __builtin_amdgcn_readfirstlane((int)sBB[st0]);
       const int tag = ((wa >> bit) & 1) | (((wb >> bit) & 1) << 1);
       return TileRef{(st0 * 32 + bit) * 64, tag, {0u, 0u, 0u}, {0u, 0u, 0u}, 3};
     } else {
       if (t < n_contig) {
         // the bitmap words are the same for every lane: kept in scalar registers
-        while (st1 == 0) st1 = __builtin_amdgcn_readfirstlane((int)tile_bits(sTB[++st0]));
-        const int bit = __builtin_ctz((uint32_t)st1);
-        st1 &= st1 - 1;
+        while (st1 == 0) st1 = __builtin_amdgcn_readfirstlane((int)tile_bits(sTB[--st0]));
+        const int bit = 31 - __builtin_clz((uint32_t)st1);
+        st1 &= ~(1u << bit);
         const int key0 = (st0 * 16 + (bit >> 1)) * 64;
         const int hm = (__builtin_amdgcn_readfirstlane((int)sTB[st0]) >> bit) & 3;
         TileRef tr{key0, 3, {0u, 0u, 0u}, {0u, 0u, 0u}, hm};
