@@ -162,8 +162,10 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const int item) {
   // ---- tile enumeration state ----------------------------------------------------------
   int ntiles = 0;
   int st0 = 0, st1 = 0;  // pattern cursors
-  // block-sparse: key blocks selected by query block bq (sBA) and bq + 1 (sBB) as bitmaps
-  __shared__ uint32_t sBA[PAT == P_BS ? kMaxTiles / 32 : 1], sBB[PAT == P_BS ? kMaxTiles / 32 : 1];
+  // block-sparse: key blocks selected by query block bq (sBA) and bq + 1 (sBB) as bitmaps;
+  // words for key blocks 0 .. bq + 1, where bq + 1 reaches kMaxTiles for the last 64-row item
+  // of a sequence of the maximum length
+  __shared__ uint32_t sBA[PAT == P_BS ? kMaxTiles / 32 + 1 : 1], sBB[PAT == P_BS ? kMaxTiles / 32 + 1 : 1];
   const uint32_t *vbits = nullptr, *dbits = nullptr;
   int n_contig = 0, n_gather = 0;
   // vertical-slash: sTB, one bit per 32-key half of the key range the block's diagonals touch

@@ -176,6 +176,36 @@ def test_block_sparse_mates_match_single_units(n, s0, k_blocks, hq, hkv, vt):
         np.testing.assert_allclose(lse[h, s0:n], rl, atol=2e-3, rtol=1e-4)
 
 
+def test_block_sparse_mates_at_the_maximum_length():
+    """The last 64-row query blocks of a sequence of the maximum length (262144 tokens, 4096
+    key blocks) run as mates: their key-block bitmaps reach block 4096 (one past the last),
+    and the rows match the same units launched one by one and the oracle."""
+    n, hq, hkv, d, kb = 262144, 2, 1, 128, 5
+    q, k, v = _inputs(n, hq, hkv, d, seed=11)
+    nb = n // 64
+    grid = [(_rs.RS_DENSE, 0, 0), (_rs.RS_BSPARSE, kb, 64)]
+    ib = _rs.IndexBuffers(hq, n, hq, grid)
+    r = np.random.default_rng(3)
+    sels = {}
+    for h in range(hq):
+        sel = [[bq] for bq in range(nb)]
+        for bq in (nb - 2, nb - 1):
+            sel[bq] = sorted({bq, 0, *r.choice(bq, kb - 2, replace=False).tolist()})
+        sels[h] = sel
+        fill_bs(ib, h, 0, sel)
+    s0 = n - 128
+    units = [(h, s0, n, 1) for h in range(hq)]
+    o, lse = _run_sparse(q, k, v, units, grid, ib, vt=True)
+    for h in range(hq):
+        o1, lse1 = _run_sparse(q, k, v, [units[h]], grid, ib, vt=True)
+        assert np.array_equal(o[h, s0:n], o1[h, s0:n]) and np.array_equal(lse[h, s0:n], lse1[h, s0:n]), h
+        rows = np.arange(s0, n)
+        mask = P.bs_mask(rows, n, 64, lambda bq, h=h: sels[h][bq])
+        ref, rl = A.masked_attention(q[h], k[0], v[0], rows, mask)
+        check_close(o[h, s0:n], ref, f"bs mates max length h={h}")
+        np.testing.assert_allclose(lse[h, s0:n], rl, atol=2e-3, rtol=1e-4)
+
+
 @pytest.mark.parametrize("n,nv,ns,spread", [(3000, 40, 300, "local"), (2048, 64, 256, "scatter"),
                                             (4100, 200, 1500, "mixed"), (900, 0, 1, "diag_only"),
                                             # the most vertical columns a set may hold (2048), nearly all
